@@ -1,0 +1,637 @@
+/*
+ * repops_ref.c -- CPU oracle for the RepOps operators (Verde, arXiv 2502.19405,
+ * Section 3 "Reproducible Operations (RepOps) library").
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg; never by the GPU library or its binding.
+ *
+ * Every function below is the plain statement of one operator as a fixed
+ * sequence of IEEE-754 binary32 operations, written for a reader to check
+ * against the paper by eye: no blocking, fusion or reordering beyond what the
+ * definition states.  Threads only split independent outputs (rows), never the
+ * operation sequence of one output.
+ *
+ * Build (strict IEEE on the host): gcc -std=c11 -O2 -ffp-contract=off
+ * -fno-fast-math -mfma -fexcess-precision=standard.  -ffp-contract=off keeps
+ * every a*b+c written below as two rounded operations; fmaf() is the single
+ * rounding fused multiply-add.
+ *
+ * Where the paper fixes the order (the matrix-multiplication listing of
+ * Section 3.2) the code follows it; where the paper is silent (block constant,
+ * row reductions, exp, GELU, softmax, LayerNorm) the chosen reading is stated
+ * at the definition.
+ */
+#define _GNU_SOURCE
+#include "repops_ref.h"
+
+#include <fenv.h>
+#include <float.h>
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+/* ------------------------------------------------------------------------- */
+/* Floating-point environment                                                */
+/* ------------------------------------------------------------------------- */
+
+/* Section 3.3: RepOps assumes IEEE-754 binary32 arithmetic.  On x86-64 that
+ * means SSE scalar arithmetic (no x87 excess precision), round-to-nearest-even,
+ * and gradual underflow (MXCSR FTZ/DAZ clear).  Each worker thread installs the
+ * default environment, which clears FTZ/DAZ a foreign library may have set. */
+static void install_ieee_env(void) { fesetenv(FE_DFL_ENV); }
+
+static float bits_to_float(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+int repops_ref_env_check(void)
+{
+    fenv_t saved;
+    fegetenv(&saved);
+    install_ieee_env();
+    int bad = 0;
+    /* A case where fused and unfused results differ: a = b = 1 + 2^-12 and
+     * c = -(1 + 2^-11).  a*b = 1 + 2^-11 + 2^-24 exactly, so the fused result
+     * is 2^-24 while RN(a*b) = 1 + 2^-11 cancels c to 0. */
+    volatile float a = bits_to_float(0x3f800800u); /* 1 + 2^-12 */
+    volatile float c = bits_to_float(0xbf801000u); /* -(1 + 2^-11) */
+    if (fmaf(a, a, c) != bits_to_float(0x33800000u)) bad |= 1; /* 2^-24 */
+    volatile float tiny = FLT_MIN;                   /* 2^-126 */
+    volatile float half = 0.5f;
+    if (tiny * half == 0.0f) bad |= 2;
+    if (fegetround() != FE_TONEAREST) bad |= 4;
+    if (FLT_EVAL_METHOD != 0) bad |= 8;
+    fesetenv(&saved);
+    return bad;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Thread helper: split [0, count) into contiguous chunks                    */
+/* ------------------------------------------------------------------------- */
+
+typedef void (*range_fn)(void *ctx, int64_t begin, int64_t end);
+
+typedef struct {
+    range_fn fn;
+    void *ctx;
+    int64_t begin, end;
+} range_job;
+
+static void *range_worker(void *arg)
+{
+    range_job *job = (range_job *)arg;
+    install_ieee_env();
+    job->fn(job->ctx, job->begin, job->end);
+    return NULL;
+}
+
+int repops_ref_default_threads(void)
+{
+    long n = sysconf(_SC_NPROCESSORS_ONLN);
+    return n > 0 ? (int)n : 1;
+}
+
+static void parallel_for(int nthreads, int64_t count, range_fn fn, void *ctx)
+{
+    if (count <= 0) return;
+    if (nthreads <= 0) nthreads = repops_ref_default_threads();
+    if (nthreads > 256) nthreads = 256;
+    if ((int64_t)nthreads > count) nthreads = (int)count;
+    fenv_t saved;
+    fegetenv(&saved);
+    if (nthreads == 1) {
+        install_ieee_env();
+        fn(ctx, 0, count);
+        fesetenv(&saved);
+        return;
+    }
+    pthread_t tid[256];
+    range_job job[256];
+    int started = 0;
+    for (int t = 0; t < nthreads; ++t) {
+        job[t].fn = fn;
+        job[t].ctx = ctx;
+        job[t].begin = count * t / nthreads;
+        job[t].end = count * (t + 1) / nthreads;
+        if (pthread_create(&tid[t], NULL, range_worker, &job[t]) == 0) {
+            ++started;
+        } else {
+            /* Could not start a thread: run its share here. */
+            tid[t] = 0;
+            install_ieee_env();
+            fn(ctx, job[t].begin, job[t].end);
+        }
+    }
+    for (int t = 0; t < nthreads; ++t)
+        if (tid[t]) pthread_join(tid[t], NULL);
+    (void)started;
+    fesetenv(&saved);
+}
+
+/* ------------------------------------------------------------------------- */
+/* c1: the canonical contraction                                             */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Section 3.2, matrix-multiplication listing: the two output loops (i, j) may
+ * run in any order; the contraction loop over k runs in one fixed order,
+ * starting from sum = 0 and adding a*b term by term.
+ *
+ * Reading used here (the paper gives no block constant): the k range is cut
+ * into consecutive blocks of k_block indices, the last one possibly shorter.
+ * Each block's partial starts at +0 and takes its terms in ascending k; the
+ * partials are then added left to right, in ascending block order, into an
+ * accumulator that starts at +0.  k_block = 0 means a single block covering the
+ * whole range, which is the listing itself.  The term update is a fused
+ * multiply-add (k_inner = 0) or a rounded product followed by a rounded add
+ * (k_inner = 1): the listing's "sum = sum + a*b" admits both.
+ */
+float repops_ref_dot(int64_t k_block, int k_inner, int64_t K,
+                     const float *a, int64_t inc_a, const float *b, int64_t inc_b)
+{
+    const int64_t blk = (k_block > 0) ? k_block : K;
+    float acc = 0.0f;
+    for (int64_t k0 = 0; k0 < K; k0 += blk) {
+        const int64_t k1 = (k0 + blk < K) ? k0 + blk : K;
+        float p = 0.0f;
+        for (int64_t k = k0; k < k1; ++k) {
+            const float x = a[k * inc_a];
+            const float y = b[k * inc_b];
+            if (k_inner == REF_INNER_FMA) {
+                p = fmaf(x, y, p);
+            } else {
+                const float prod = x * y;
+                p = p + prod;
+            }
+        }
+        acc = acc + p;
+    }
+    return acc;
+}
+
+static int check_order_k(int64_t k_block, int k_inner)
+{
+    if (k_block < 0) return -1;
+    if (k_inner != REF_INNER_FMA && k_inner != REF_INNER_MUL_ADD) return -1;
+    return 0;
+}
+
+/* Logical element A[i][k] / B[k][j] and the stride that walks k. */
+static const float *row_of_a(const float *A, int64_t lda, int trans_a, int64_t i, int64_t *inc)
+{
+    if (trans_a) { *inc = lda; return A + i; }
+    *inc = 1;
+    return A + i * lda;
+}
+
+static const float *col_of_b(const float *B, int64_t ldb, int trans_b, int64_t j, int64_t *inc)
+{
+    if (trans_b) { *inc = 1; return B + j * ldb; }
+    *inc = ldb;
+    return B + j;
+}
+
+/* Epilogue (paper silent; reading used here): the scale alpha multiplies the
+ * finished contraction, then the bias is added, each one rounding. */
+typedef struct {
+    int64_t k_block;
+    int k_inner;
+    int64_t n, k;
+    const float *A; int64_t lda; int trans_a;
+    const float *B; int64_t ldb; int trans_b;
+    const float *bias;
+    float *C; int64_t ldc;
+} matmul_ctx;
+
+static void matmul_rows(void *vctx, int64_t i0, int64_t i1)
+{
+    const matmul_ctx *c = (const matmul_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) {
+        for (int64_t j = 0; j < c->n; ++j) {
+            int64_t ia, ib;
+            const float *a = row_of_a(c->A, c->lda, c->trans_a, i, &ia);
+            const float *b = col_of_b(c->B, c->ldb, c->trans_b, j, &ib);
+            float v = repops_ref_dot(c->k_block, c->k_inner, c->k, a, ia, b, ib);
+            if (c->bias) v = v + c->bias[j];
+            c->C[i * c->ldc + j] = v;
+        }
+    }
+}
+
+int repops_ref_matmul(int64_t k_block, int k_inner, int64_t m, int64_t n, int64_t k,
+                      const float *A, int64_t lda, int trans_a,
+                      const float *B, int64_t ldb, int trans_b,
+                      const float *bias, float *C, int64_t ldc, int nthreads)
+{
+    if (check_order_k(k_block, k_inner) || m < 0 || n < 0 || k < 0) return -1;
+    if (m == 0 || n == 0) return 0;
+    if (!C || (k > 0 && (!A || !B))) return -2;
+    matmul_ctx c = {k_block, k_inner, n, k, A, lda, trans_a, B, ldb, trans_b, bias, C, ldc};
+    parallel_for(nthreads, m, matmul_rows, &c);
+    return 0;
+}
+
+int repops_ref_matmul_at(int64_t k_block, int k_inner, int64_t m, int64_t n, int64_t k,
+                         const float *A, int64_t lda, int trans_a,
+                         const float *B, int64_t ldb, int trans_b,
+                         const float *bias, int64_t npts, const int64_t *rows,
+                         const int64_t *cols, float *out)
+{
+    if (check_order_k(k_block, k_inner) || m < 0 || n < 0 || k < 0 || npts < 0) return -1;
+    fenv_t saved;
+    fegetenv(&saved);
+    install_ieee_env();
+    for (int64_t p = 0; p < npts; ++p) {
+        const int64_t i = rows[p], j = cols[p];
+        if (i < 0 || i >= m || j < 0 || j >= n) { fesetenv(&saved); return -3; }
+        int64_t ia, ib;
+        const float *a = row_of_a(A, lda, trans_a, i, &ia);
+        const float *b = col_of_b(B, ldb, trans_b, j, &ib);
+        float v = repops_ref_dot(k_block, k_inner, k, a, ia, b, ib);
+        if (bias) v = v + bias[j];
+        out[p] = v;
+    }
+    fesetenv(&saved);
+    return 0;
+}
+
+/* Batched product (Section 2.2 names the attention key-query product as an
+ * operator that decomposes into independent matrix products): every batch
+ * element is one matrix product with the same per-output order, followed by
+ * one rounded multiplication by alpha. */
+typedef struct {
+    int64_t k_block;
+    int k_inner;
+    int64_t batch1, m, n, k;
+    const float *A; int64_t sa0, sa1, lda; int trans_a;
+    const float *B; int64_t sb0, sb1, ldb; int trans_b;
+    float alpha;
+    float *C; int64_t sc0, sc1, ldc;
+} bmm_ctx;
+
+static float bmm_one(const bmm_ctx *c, int64_t b0, int64_t b1, int64_t i, int64_t j)
+{
+    const float *Ab = c->A + b0 * c->sa0 + b1 * c->sa1;
+    const float *Bb = c->B + b0 * c->sb0 + b1 * c->sb1;
+    int64_t ia, ib;
+    const float *a = row_of_a(Ab, c->lda, c->trans_a, i, &ia);
+    const float *b = col_of_b(Bb, c->ldb, c->trans_b, j, &ib);
+    const float v = repops_ref_dot(c->k_block, c->k_inner, c->k, a, ia, b, ib);
+    return v * c->alpha;
+}
+
+static void bmm_rows(void *vctx, int64_t r0, int64_t r1)
+{
+    const bmm_ctx *c = (const bmm_ctx *)vctx;
+    for (int64_t r = r0; r < r1; ++r) {
+        /* r enumerates (b0, b1, i) */
+        const int64_t i = r % c->m;
+        const int64_t b = r / c->m;
+        const int64_t b1 = b % c->batch1, b0 = b / c->batch1;
+        float *Cb = c->C + b0 * c->sc0 + b1 * c->sc1;
+        for (int64_t j = 0; j < c->n; ++j) Cb[i * c->ldc + j] = bmm_one(c, b0, b1, i, j);
+    }
+}
+
+int repops_ref_bmm(int64_t k_block, int k_inner, int64_t batch0, int64_t batch1,
+                   int64_t m, int64_t n, int64_t k,
+                   const float *A, int64_t sa0, int64_t sa1, int64_t lda, int trans_a,
+                   const float *B, int64_t sb0, int64_t sb1, int64_t ldb, int trans_b,
+                   float alpha, float *C, int64_t sc0, int64_t sc1, int64_t ldc, int nthreads)
+{
+    if (check_order_k(k_block, k_inner) || batch0 < 0 || batch1 < 0 || m < 0 || n < 0 || k < 0)
+        return -1;
+    if (batch0 == 0 || batch1 == 0 || m == 0 || n == 0) return 0;
+    bmm_ctx c = {k_block, k_inner, batch1, m, n, k, A, sa0, sa1, lda, trans_a,
+                 B, sb0, sb1, ldb, trans_b, alpha, C, sc0, sc1, ldc};
+    parallel_for(nthreads, batch0 * batch1 * m, bmm_rows, &c);
+    return 0;
+}
+
+int repops_ref_bmm_at(int64_t k_block, int k_inner, int64_t batch0, int64_t batch1,
+                      int64_t m, int64_t n, int64_t k,
+                      const float *A, int64_t sa0, int64_t sa1, int64_t lda, int trans_a,
+                      const float *B, int64_t sb0, int64_t sb1, int64_t ldb, int trans_b,
+                      float alpha, int64_t npts, const int64_t *b0, const int64_t *b1,
+                      const int64_t *rows, const int64_t *cols, float *out)
+{
+    if (check_order_k(k_block, k_inner) || batch0 < 0 || batch1 < 0 || m < 0 || n < 0 || k < 0)
+        return -1;
+    bmm_ctx c = {k_block, k_inner, batch1, m, n, k, A, sa0, sa1, lda, trans_a,
+                 B, sb0, sb1, ldb, trans_b, alpha, NULL, 0, 0, 0};
+    fenv_t saved;
+    fegetenv(&saved);
+    install_ieee_env();
+    for (int64_t p = 0; p < npts; ++p) {
+        if (b0[p] < 0 || b0[p] >= batch0 || b1[p] < 0 || b1[p] >= batch1 || rows[p] < 0 ||
+            rows[p] >= m || cols[p] < 0 || cols[p] >= n) {
+            fesetenv(&saved);
+            return -3;
+        }
+        out[p] = bmm_one(&c, b0[p], b1[p], rows[p], cols[p]);
+    }
+    fesetenv(&saved);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* c2: fixed-order row reduction                                             */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * The paper fixes no order for row reductions; Section 3.2 only asks that the
+ * order-critical dimension be serialised or synchronised in a fixed way.
+ * Reading used here, a function of the row length n and the constant W only:
+ *
+ *   strided tree (row_combine 0): W partials q[l] start at +0; element x[j]
+ *   is added to q[j mod W] in ascending j; then for s = W/2, W/4, ..., 1 each
+ *   q[l] with l < s becomes q[l] + q[l+s]; the result is q[0].
+ *
+ *   blocked left-to-right (row_combine 1): the c1 rule with addition, blocks of
+ *   W consecutive elements, block partials added left to right.
+ *
+ * For a sum of squares the term update is q = fma(x, x, q) instead of q + x.
+ */
+static float term_update(float q, float x, int squares)
+{
+    return squares ? fmaf(x, x, q) : q + x;
+}
+
+float repops_ref_rowsum(int row_width, int row_combine, int64_t n, const float *x, int squares)
+{
+    const int64_t W = row_width;
+    if (row_combine == REF_ROW_BLOCKED) {
+        float acc = 0.0f;
+        for (int64_t j0 = 0; j0 < n; j0 += W) {
+            float p = 0.0f;
+            for (int64_t j = j0; j < j0 + W && j < n; ++j) p = term_update(p, x[j], squares);
+            acc = acc + p;
+        }
+        return acc;
+    }
+    float q[1024];
+    for (int64_t l = 0; l < W; ++l) q[l] = 0.0f;
+    for (int64_t j = 0; j < n; ++j) q[j % W] = term_update(q[j % W], x[j], squares);
+    for (int64_t s = W / 2; s >= 1; s /= 2)
+        for (int64_t l = 0; l < s; ++l) q[l] = q[l] + q[l + s];
+    return q[0];
+}
+
+static int check_order_rows(int row_width, int row_combine)
+{
+    if (row_width < 1 || row_width > 1024 || (row_width & (row_width - 1))) return -1;
+    if (row_combine != REF_ROW_TREE && row_combine != REF_ROW_BLOCKED) return -1;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* c4: reproducible exp                                                      */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Section 3.1: RepOps rebuilds exp (and the other math functions) so that the
+ * operation order is controlled.  The paper gives no algorithm; the one used
+ * here is Cody and Waite's additive argument reduction followed by the degree-7
+ * Taylor polynomial of exp, evaluated by Horner's rule with fused multiply-adds:
+ *
+ *   n = rint(x * log2 e)                (nearest integer, ties to even)
+ *   r = (x - n*ln2_hi) - n*ln2_lo       (two fused steps)
+ *   p = sum_{i<=7} r^i / i!             (Horner, highest coefficient first)
+ *   exp(x) = p * 2^n, applied as (p * 2^floor(n/2)) * 2^(n - floor(n/2))
+ *
+ * The split scaling keeps both powers of two normal, so the first product is
+ * exact and the second rounds once, giving correctly handled overflow and
+ * subnormal results.  Constants are the binary32 values nearest their
+ * definitions: log2 e; ln2_hi = RN(ln 2); ln2_lo = RN(ln 2 - ln2_hi);
+ * coefficients RN(1/i!).
+ */
+static const float EXP_LOG2E = 0x1.715476p+0f;
+static const float EXP_LN2_HI = 0x1.62e43p-1f;
+static const float EXP_LN2_LO = -0x1.05c61p-29f;
+static const float EXP_C[8] = {
+    0x1p+0f,        /* 1/0! */
+    0x1p+0f,        /* 1/1! */
+    0x1p-1f,        /* 1/2! */
+    0x1.555556p-3f, /* 1/3! */
+    0x1.555556p-5f, /* 1/4! */
+    0x1.111112p-7f, /* 1/5! */
+    0x1.6c16c2p-10f,/* 1/6! */
+    0x1.a01a02p-13f /* 1/7! */
+};
+
+/* 2^e for an integer e in [-126, 127], built from the exponent field. */
+static float pow2i(int e)
+{
+    return bits_to_float((uint32_t)(e + 127) << 23);
+}
+
+float repops_ref_exp1(float x)
+{
+    if (isnan(x)) return x;
+    const float t = x * EXP_LOG2E;
+    const float nf = rintf(t);
+    if (nf > 128.0f) return INFINITY;
+    if (nf < -151.0f) return 0.0f;
+    float r = fmaf(nf, -EXP_LN2_HI, x);
+    r = fmaf(nf, -EXP_LN2_LO, r);
+    float p = EXP_C[7];
+    for (int i = 6; i >= 0; --i) p = fmaf(p, r, EXP_C[i]);
+    const int n = (int)nf;
+    const int n1 = (n >= 0) ? n / 2 : -((-n + 1) / 2); /* floor(n / 2) */
+    const int n2 = n - n1;
+    const float y = p * pow2i(n1);
+    return y * pow2i(n2);
+}
+
+/* ------------------------------------------------------------------------- */
+/* c5: tanh-form GELU                                                        */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * GELU appears among the DistilBERT operators of Section 4.2.  The tanh form
+ * 0.5*x*(1 + tanh(z)), z = sqrt(2/pi)*(x + 0.044715*x^3), is rewritten with the
+ * identity 0.5*(1 + tanh z) = 1 / (1 + exp(-2z)), which avoids the cancellation
+ * in 1 + tanh z for negative z:
+ *
+ *   u = (x*x)*x;  z = fma(0.044715, u, x) * sqrt(2/pi);  w = -2*z (exact)
+ *   y = x / (1 + exp_rep(w))
+ *
+ * Constants: RN(0.044715) and RN(sqrt(2/pi)).
+ */
+static const float GELU_C = 0x1.6e4e26p-5f;
+static const float GELU_SQ = 0x1.988454p-1f;
+
+float repops_ref_gelu1(float x)
+{
+    float u = x * x;
+    u = u * x;
+    float z = fmaf(GELU_C, u, x);
+    z = z * GELU_SQ;
+    const float w = z * -2.0f;
+    const float e = repops_ref_exp1(w);
+    const float d = 1.0f + e;
+    return x / d;
+}
+
+typedef struct {
+    const float *x;
+    float *y;
+    int which; /* 0 = exp, 1 = gelu */
+} ew_ctx;
+
+static void ew_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const ew_ctx *c = (const ew_ctx *)vctx;
+    if (c->which == 0)
+        for (int64_t i = i0; i < i1; ++i) c->y[i] = repops_ref_exp1(c->x[i]);
+    else
+        for (int64_t i = i0; i < i1; ++i) c->y[i] = repops_ref_gelu1(c->x[i]);
+}
+
+int repops_ref_exp(int64_t n, const float *x, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    ew_ctx c = {x, y, 0};
+    parallel_for(nthreads, n, ew_range, &c);
+    return 0;
+}
+
+int repops_ref_gelu(int64_t n, const float *x, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    ew_ctx c = {x, y, 1};
+    parallel_for(nthreads, n, ew_range, &c);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* c6: row softmax                                                           */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Softmax is not named in the paper; it is one of the operators needed to run
+ * the DistilBERT and Llama programs of Section 4.2.  Reading used here:
+ *
+ *   m   = maximum of the unmasked entries (first maximum kept on ties);
+ *   e_j = exp_rep(x_j - m) for unmasked j, +0 for masked j;
+ *   s   = fixed-order row sum of e (c2, masked terms included as +0);
+ *   r   = 1 / s, once per row;  y_j = e_j * r.
+ *
+ * The causal mask of row i keeps columns j <= i mod causal_period.
+ */
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *X; int64_t ldx;
+    float *Y; int64_t ldy;
+    int64_t period;
+} softmax_ctx;
+
+static void softmax_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const softmax_ctx *c = (const softmax_ctx *)vctx;
+    float *e = (float *)malloc(sizeof(float) * (size_t)(c->cols > 0 ? c->cols : 1));
+    if (!e) abort();
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *x = c->X + r * c->ldx;
+        float *y = c->Y + r * c->ldy;
+        const int64_t valid = (c->period > 0) ? (r % c->period) + 1 : c->cols;
+        const int64_t nv = valid < c->cols ? valid : c->cols;
+        float m = -INFINITY;
+        for (int64_t j = 0; j < nv; ++j) m = (x[j] > m) ? x[j] : m;
+        for (int64_t j = 0; j < c->cols; ++j) {
+            if (j < nv) {
+                const float d = x[j] - m;
+                e[j] = repops_ref_exp1(d);
+            } else {
+                e[j] = 0.0f;
+            }
+        }
+        const float s = repops_ref_rowsum(c->W, c->combine, c->cols, e, 0);
+        const float rs = 1.0f / s;
+        for (int64_t j = 0; j < c->cols; ++j) y[j] = e[j] * rs;
+    }
+    free(e);
+}
+
+int repops_ref_softmax_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                            const float *X, int64_t ldx, float *Y, int64_t ldy,
+                            int64_t causal_period, int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || rows < 0 || cols < 0 || causal_period < 0)
+        return -1;
+    softmax_ctx c = {row_width, row_combine, cols, X, ldx, Y, ldy, causal_period};
+    parallel_for(nthreads, rows, softmax_range, &c);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* c7: row LayerNorm                                                         */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * LayerNorm is named among the DistilBERT operators of Section 4.2; the paper
+ * gives no formula or order.  Reading used here (biased variance, as in the
+ * usual LayerNorm definition):
+ *
+ *   mean = rowsum(x) / n;  d_j = x_j - mean;
+ *   var  = rowsum of fma(d, d, .) / n;
+ *   rstd = 1 / sqrt(var + eps)   (correctly rounded sqrt and division);
+ *   t_j  = d_j * rstd;  y_j = fma(t_j, gamma_j, beta_j).
+ *
+ * A missing gamma or beta skips its operation: y = t, t + beta or t * gamma.
+ */
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *X; int64_t ldx;
+    const float *gamma, *beta;
+    float eps;
+    float *Y; int64_t ldy;
+    float *mean_out, *rstd_out;
+} ln_ctx;
+
+static void ln_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const ln_ctx *c = (const ln_ctx *)vctx;
+    float *d = (float *)malloc(sizeof(float) * (size_t)(c->cols > 0 ? c->cols : 1));
+    if (!d) abort();
+    const float nf = (float)c->cols;
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *x = c->X + r * c->ldx;
+        float *y = c->Y + r * c->ldy;
+        const float s = repops_ref_rowsum(c->W, c->combine, c->cols, x, 0);
+        const float mean = s / nf;
+        for (int64_t j = 0; j < c->cols; ++j) d[j] = x[j] - mean;
+        const float q = repops_ref_rowsum(c->W, c->combine, c->cols, d, 1);
+        const float var = q / nf;
+        const float ve = var + c->eps;
+        const float sd = sqrtf(ve);
+        const float rstd = 1.0f / sd;
+        for (int64_t j = 0; j < c->cols; ++j) {
+            const float t = d[j] * rstd;
+            float v;
+            if (c->gamma && c->beta) v = fmaf(t, c->gamma[j], c->beta[j]);
+            else if (c->gamma) v = t * c->gamma[j];
+            else if (c->beta) v = t + c->beta[j];
+            else v = t;
+            y[j] = v;
+        }
+        if (c->mean_out) c->mean_out[r] = mean;
+        if (c->rstd_out) c->rstd_out[r] = rstd;
+    }
+    free(d);
+}
+
+int repops_ref_layernorm_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                              const float *X, int64_t ldx, const float *gamma,
+                              const float *beta, float eps, float *Y, int64_t ldy,
+                              float *mean_out, float *rstd_out, int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || rows < 0 || cols < 0) return -1;
+    if (rows > 0 && cols == 0) return -1; /* mean of an empty row is undefined */
+    ln_ctx c = {row_width, row_combine, cols, X, ldx, gamma, beta, eps, Y, ldy, mean_out, rstd_out};
+    parallel_for(nthreads, rows, ln_range, &c);
+    return 0;
+}

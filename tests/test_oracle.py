@@ -1,0 +1,485 @@
+"""Pins for the CPU oracle (no GPU).
+
+The oracle is checked against facts that do not come from itself: hand-derived
+order witnesses, integer closed forms, exact rational brute force, error bounds
+against high-precision references, special values and closed-form rows, and
+independence from the host compiler's optimisation level.  Each test names the
+passage or reading it pins.
+"""
+import json
+import math
+import os
+import re
+import tempfile
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import exactfp
+import oracle
+from bitcmp import assert_bits_equal
+from paper_2502_19405_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "order_witnesses.json")
+U = 2.0 ** -24  # unit roundoff of binary32
+
+
+def hexf(s):
+    return np.float32(float.fromhex(s))
+
+
+def _witness(name):
+    for w in json.load(open(GOLDEN))["witnesses"]:
+        if w["name"] == name:
+            return w
+    raise KeyError(name)
+
+
+def _expand(spec, n):
+    v = np.zeros(n, np.float32)
+    for key, val in spec.items():
+        if ":" in key:
+            lo, hi = map(int, key.split(":"))
+            v[lo:hi] = hexf(val)
+        else:
+            v[int(key)] = hexf(val)
+    return v
+
+
+def test_host_environment_is_strict_ieee(ref):
+    assert oracle.env_check(ref) == 0
+
+
+# --------------------------------------------------------------------------
+# c1: canonical contraction (Section 3.2 listing + block reading)
+# --------------------------------------------------------------------------
+
+def test_witness_w1_blocked_vs_sequential(ref):
+    w = _witness("W1_blocked_vs_sequential")
+    a = _expand(w["a_nonzero"], w["K"])
+    b = np.ones(w["K"], np.float32)
+    got = oracle.dot(a, b, k_block=w["k_block"], k_inner=w["k_inner"], lib=ref)
+    assert got == hexf(w["expect"])
+    # planted mistake: the unblocked order must give the other value
+    wrong = oracle.dot(a, b, k_block=w["wrong_order"]["k_block"], lib=ref)
+    assert wrong == hexf(w["wrong_order"]["expect"]) and wrong != got
+
+
+def test_witness_w2_left_to_right_combine(ref):
+    w = _witness("W2_left_to_right_vs_pairwise")
+    a = _expand(w["a_nonzero"], w["K"])
+    b = np.ones(w["K"], np.float32)
+    got = oracle.dot(a, b, k_block=w["k_block"], k_inner=w["k_inner"], lib=ref)
+    assert got == hexf(w["expect"])
+    assert got != hexf(w["pairwise_block_tree"])
+
+
+def test_witness_w3_fused_vs_unfused(ref):
+    w = _witness("W3_fused_vs_unfused")
+    a = np.array([hexf(s) for s in w["a"]], np.float32)
+    b = np.array([hexf(s) for s in w["b"]], np.float32)
+    fused = oracle.dot(a, b, k_block=w["k_block"], k_inner=0, lib=ref)
+    unfused = oracle.dot(a, b, k_block=w["k_block"], k_inner=1, lib=ref)
+    assert fused.view(np.uint32) == hexf(w["expect_fma"]).view(np.uint32)
+    assert unfused.view(np.uint32) == hexf(w["expect_mul_add"]).view(np.uint32)
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (7, 5, 3), (33, 17, 64), (19, 23, 65), (40, 9, 300)])
+@pytest.mark.parametrize("trans_a,trans_b", [(0, 0), (1, 0), (0, 1), (1, 1)])
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (16, 1), (7, 0)])
+def test_matmul_integer_closed_form(ref, shape, trans_a, trans_b, k_block, k_inner):
+    """Integers in [-8, 8] keep every partial below 2^24, so every order of
+    operations gives the exact integer product: pins values and indexing."""
+    m, n, k = shape
+    g = inputs.rng(m * 1000 + n * 10 + k)
+    A = inputs.integers(g, (m, k))
+    B = inputs.integers(g, (k, n))
+    bias = inputs.integers(g, (n,))
+    exact = A.astype(np.int64) @ B.astype(np.int64) + bias.astype(np.int64)
+    Ain = np.ascontiguousarray(A.T) if trans_a else A
+    Bin = np.ascontiguousarray(B.T) if trans_b else B
+    C = oracle.matmul(Ain, Bin, bias, trans_a=trans_a, trans_b=trans_b, k_block=k_block,
+                      k_inner=k_inner, lib=ref)
+    assert np.array_equal(C.astype(np.int64), exact)
+
+
+def test_matmul_int2048_workload_sample(ref):
+    """The integer 2048^3 workload, sampled: exact integers at every sampled output."""
+    d = inputs.gemm2048_int()
+    rows, cols = inputs.sample_indices(2, 256, 2048, 2048)
+    got = oracle.matmul_at(d["A"], d["B"], rows, cols, bias=d["bias"], lib=ref)
+    exact = np.einsum("pk,kp->p", d["A"][rows].astype(np.int64), d["B"][:, cols].astype(np.int64))
+    exact = exact + d["bias"][cols].astype(np.int64)
+    assert np.array_equal(got.astype(np.int64), exact)
+
+
+@pytest.mark.parametrize("k", [1, 3, 63, 64, 65, 130])
+@pytest.mark.parametrize("k_block,fused", [(64, True), (0, True), (5, True), (64, False)])
+def test_matmul_exact_rational_brute_force(ref, k, k_block, fused):
+    """Every step of the canonical order carried out in exact rationals with one
+    round-to-nearest-even per step (an independent model of binary32): the C
+    oracle must agree bit for bit, which pins contraction, excess precision and
+    block boundaries."""
+    g = inputs.rng(k * 7 + k_block)
+    m, n = 3, 4
+    A = inputs.normal(g, (m, k))
+    B = inputs.normal(g, (k, n))
+    C = oracle.matmul(A, B, k_block=k_block, k_inner=0 if fused else 1, lib=ref)
+    for i in range(m):
+        for j in range(n):
+            want = exactfp.canonical_dot([float(v) for v in A[i]], [float(v) for v in B[:, j]],
+                                         k_block, fused)
+            assert C[i, j] == np.float32(want), (i, j)
+
+
+@pytest.mark.parametrize("k,k_block", [(200, 64), (1000, 64), (2048, 64), (777, 0)])
+def test_matmul_error_bound(ref, k, k_block):
+    """|C - C*| <= gamma_n (sum|a_k b_k| + |bias|) with n = B + ceil(K/B) + 1,
+    gamma_n = n u / (1 - n u), against exactly summed products: catches dropped
+    terms, wrong indices and transposed operands."""
+    g = inputs.rng(k)
+    m, n = 9, 11
+    A = inputs.uniform(g, (m, k), -1, 1)
+    B = inputs.uniform(g, (k, n), -1, 1)
+    bias = inputs.uniform(g, (n,), -0.1, 0.1)
+    C = oracle.matmul(A, B, bias, k_block=k_block, lib=ref)
+    blk = k_block if k_block > 0 else k
+    nn = blk + math.ceil(k / blk) + 1
+    gamma = nn * U / (1 - nn * U)
+    A64, B64 = A.astype(np.float64), B.astype(np.float64)
+    for i in range(m):
+        for j in range(n):
+            prods = A64[i] * B64[:, j]  # exact in double
+            exact = math.fsum(list(prods) + [float(bias[j])])
+            bound = gamma * (np.abs(prods).sum() + abs(float(bias[j])))
+            assert abs(float(C[i, j]) - exact) <= bound, (i, j)
+
+
+def test_matmul_layout_invariance(ref):
+    """Section 3.1: strides must not change the order.  Transposed storage and
+    padded leading dimensions give identical bits."""
+    g = inputs.rng(11)
+    m, n, k = 37, 29, 150
+    A = inputs.normal(g, (m, k))
+    B = inputs.normal(g, (k, n))
+    base = oracle.matmul(A, B, lib=ref)
+    assert_bits_equal(oracle.matmul(np.ascontiguousarray(A.T), B, trans_a=True, lib=ref), base, "trans_a")
+    assert_bits_equal(oracle.matmul(A, np.ascontiguousarray(B.T), trans_b=True, lib=ref), base, "trans_b")
+    # padded leading dimensions through the raw batched entry (batch 1x1)
+    lda, ldb, ldc = k + 5, n + 3, n + 7
+    Ap = np.zeros((m, lda), np.float32); Ap[:, :k] = A
+    Bp = np.zeros((k, ldb), np.float32); Bp[:, :n] = B
+    Cp = np.full((m, ldc), np.nan, np.float32)
+    oracle.bmm_raw(1, 1, m, n, k, Ap, 0, 0, lda, 0, Bp, 0, 0, ldb, 0, 1.0, Cp, 0, 0, ldc, lib=ref)
+    assert_bits_equal(Cp[:, :n], base, "padded")
+    assert np.isnan(Cp[:, n:]).all()
+
+
+def test_bmm_is_matmul_per_batch(ref):
+    """bmm applies the same per-output order to every batch element, then one
+    rounded multiplication by alpha."""
+    g = inputs.rng(12)
+    A = inputs.normal(g, (2, 3, 20, 70))
+    B = inputs.normal(g, (2, 3, 70, 15))
+    alpha = np.float32(1 / math.sqrt(128))
+    C = oracle.bmm(A, B, alpha=alpha, lib=ref)
+    for b0 in range(2):
+        for b1 in range(3):
+            want = oracle.matmul(np.ascontiguousarray(A[b0, b1]), np.ascontiguousarray(B[b0, b1]),
+                                 lib=ref) * alpha
+            assert_bits_equal(C[b0, b1], want, f"batch {b0},{b1}")
+    # sampled entry point agrees with the full one
+    b0, b1, r, c = inputs.sample_indices(3, 50, 2, 3, 20, 15)
+    flatA, flatB = A.ravel(), B.ravel()
+    got = oracle.bmm_at_raw(2, 3, 20, 15, 70, flatA, 3 * 1400, 1400, 70, 0, flatB, 3 * 1050, 1050,
+                            15, 0, alpha, b0, b1, r, c, lib=ref)
+    assert_bits_equal(got, C[b0, b1, r, c], "bmm_at")
+
+
+def test_kblock_at_least_k_is_the_listing(ref):
+    """A block at least as long as K leaves one block: the paper's listing
+    (sum from 0, one term at a time) taken literally."""
+    g = inputs.rng(13)
+    a = inputs.normal(g, (100,))
+    b = inputs.normal(g, (100,))
+    lit = np.float32(0.0)
+    for x, y in zip(a, b):
+        lit = np.float32(exactfp.fma(float(x), float(y), float(lit)))
+    for kb in (0, 100, 128, 4096):
+        assert oracle.dot(a, b, k_block=kb, lib=ref) == lit
+
+
+def test_optimisation_level_does_not_change_bits(ref):
+    """The -O0 and -O2 builds of the oracle agree bit for bit on every operator."""
+    with tempfile.TemporaryDirectory() as tmp:
+        lib0 = oracle.load(oracle.build(opt="-O0", out=os.path.join(tmp, "ref_O0.so")))
+        g = inputs.rng(14)
+        A = inputs.normal(g, (31, 200)); B = inputs.normal(g, (200, 17))
+        assert_bits_equal(oracle.matmul(A, B, lib=lib0), oracle.matmul(A, B, lib=ref), "matmul")
+        X = inputs.normal(g, (9, 333), var=4.0)
+        assert_bits_equal(oracle.softmax_rows(X, lib=lib0), oracle.softmax_rows(X, lib=ref), "softmax")
+        gam = inputs.uniform(g, (333,), 0.9, 1.1); bet = inputs.uniform(g, (333,), -0.1, 0.1)
+        assert_bits_equal(oracle.layernorm_rows(X, gam, bet, lib=lib0),
+                          oracle.layernorm_rows(X, gam, bet, lib=ref), "layernorm")
+        x = inputs.uniform(g, (100000,), -100, 100)
+        assert_bits_equal(oracle.exp(x, lib=lib0), oracle.exp(x, lib=ref), "exp")
+        assert_bits_equal(oracle.gelu(x, lib=lib0), oracle.gelu(x, lib=ref), "gelu")
+
+
+def test_threads_do_not_change_bits(ref):
+    g = inputs.rng(15)
+    A = inputs.normal(g, (64, 300)); B = inputs.normal(g, (300, 50))
+    assert_bits_equal(oracle.matmul(A, B, nthreads=1, lib=ref),
+                      oracle.matmul(A, B, nthreads=7, lib=ref), "threads")
+
+
+# --------------------------------------------------------------------------
+# c2: fixed row reduction
+# --------------------------------------------------------------------------
+
+def test_witness_w4_strided_tree(ref):
+    w = _witness("W4_strided_tree_vs_blocked")
+    x = _expand(w["x_nonzero"], w["n"])
+    assert oracle.rowsum(x, w["row_width"], oracle.ROW_TREE, lib=ref) == hexf(w["expect_tree"])
+    assert oracle.rowsum(x, w["row_width"], oracle.ROW_BLOCKED, lib=ref) == hexf(w["expect_blocked"])
+
+
+@pytest.mark.parametrize("n", [1, 5, 64, 100, 1024, 3000])
+@pytest.mark.parametrize("W,combine", [(64, 0), (1, 0), (256, 0), (64, 1), (8, 1)])
+def test_rowsum_integers_exact(ref, n, W, combine):
+    g = inputs.rng(n + W)
+    x = inputs.integers(g, (n,), -1000, 1000)
+    assert oracle.rowsum(x, W, combine, lib=ref) == np.float32(x.astype(np.int64).sum())
+    x2 = inputs.integers(g, (n,), -60, 60)  # 3000 * 60^2 < 2^24: every partial exact
+    assert oracle.rowsum(x2, W, combine, squares=True, lib=ref) == np.float32(
+        (x2.astype(np.int64) ** 2).sum())
+
+
+@pytest.mark.parametrize("n", [7, 100, 1000])
+def test_rowsum_sequential_special_cases(ref, n):
+    """W = 1 (strided) and a single block (blocked, W >= n) both reduce to the
+    plain left-to-right sum, here numpy's sequential float32 cumulative sum."""
+    g = inputs.rng(n)
+    x = inputs.normal(g, (n,))
+    seq = np.cumsum(x, dtype=np.float32)[-1]
+    assert oracle.rowsum(x, 1, oracle.ROW_TREE, lib=ref) == seq
+    assert oracle.rowsum(x, 1024, oracle.ROW_BLOCKED, lib=ref) == seq
+
+
+def test_rowsum_bound(ref):
+    g = inputs.rng(21)
+    for n in (50, 768, 1024, 5000):
+        x = inputs.normal(g, (n,))
+        got = oracle.rowsum(x, lib=ref)
+        nn = math.ceil(n / 64) + 6
+        assert abs(float(got) - math.fsum(x.astype(np.float64))) <= nn * U / (1 - nn * U) * np.abs(
+            x.astype(np.float64)).sum()
+
+
+# --------------------------------------------------------------------------
+# c4 / c5: exp and GELU
+# --------------------------------------------------------------------------
+
+def check_constants(src):
+    """The binary32 constants in the oracle source are the nearest values to
+    their mathematical definitions, computed here at 200-bit precision."""
+    import mpmath
+    mpmath.mp.prec = 200
+
+    def rn(v):
+        return exactfp.rn32(Fraction(mpmath.nstr(v, 60)))
+
+    ln2_hi = rn(mpmath.log(2))
+    want = {
+        "EXP_LOG2E": rn(1 / mpmath.log(2)), "EXP_LN2_HI": ln2_hi,
+        "EXP_LN2_LO": rn(mpmath.log(2) - mpmath.mpf(ln2_hi)),
+        "GELU_C": rn(mpmath.mpf("0.044715")), "GELU_SQ": rn(mpmath.sqrt(2 / mpmath.pi)),
+    }
+    for name, v in want.items():
+        line = [l for l in src.splitlines() if f" {name} =" in l][0]
+        lit = line.split("=")[1].strip().rstrip(";").rstrip("f")
+        assert float.fromhex(lit) == v, name
+    body = src[src.index("EXP_C[8]"):]
+    lits = [re.match(r"\s*([-+0-9a-fA-Fx.p]+?)f\b", l).group(1) for l in body.splitlines()[1:9]]
+    for i, lit in enumerate(lits):
+        assert float.fromhex(lit) == rn(mpmath.mpf(1) / mpmath.factorial(i)), f"C{i}"
+
+
+def test_exp_constants_match_definitions():
+    check_constants(open(os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")).read())
+
+
+def test_exp_special_values(ref):
+    assert oracle.exp1(0.0, lib=ref) == 1.0
+    assert oracle.exp1(-0.0, lib=ref) == 1.0
+    assert oracle.exp1(np.inf, lib=ref) == np.inf
+    z = oracle.exp1(-np.inf, lib=ref)
+    assert z == 0 and not np.signbit(z)
+    assert np.isnan(oracle.exp1(np.nan, lib=ref))
+    assert oracle.exp1(1.0, lib=ref) == np.float32(math.e)
+    # largest finite result and first overflow
+    assert np.isfinite(oracle.exp1(88.72283, lib=ref))
+    assert oracle.exp1(88.7229, lib=ref) == np.inf
+    # deep underflow gives +0, the smallest subnormal region is reached
+    assert oracle.exp1(-104.0, lib=ref) == 0.0
+    assert oracle.exp1(-103.0, lib=ref) > 0.0
+
+
+def _ulp_err(y, t):
+    t = np.asarray(t, np.float64)
+    _, e = np.frexp(np.abs(t))
+    ulp = np.ldexp(1.0, np.maximum(e - 1, -126) - 23)
+    return np.abs(np.asarray(y, np.float64) - t) / ulp
+
+
+def test_exp_accuracy_under_one_ulp(ref):
+    """Cody-Waite + degree-7 Taylor: error under 1 ulp against float64 exp on
+    every 211th binary32 pattern with a finite, nonzero result (measured maximum
+    on a denser sweep: 0.915 ulp)."""
+    u = np.arange(0, 2 ** 32, 211, dtype=np.uint64).astype(np.uint32)
+    x = u.view(np.float32)
+    x = x[np.isfinite(x) & (np.abs(x) < 110)]
+    y = oracle.exp(x, lib=ref)
+    t = np.exp(x.astype(np.float64))
+    ok = (t > 0) & (t <= float(np.finfo(np.float32).max))
+    err = _ulp_err(y[ok], t[ok])
+    assert err.max() < 1.0, (err.max(), x[ok][err.argmax()])
+
+
+def test_gelu_special_values(ref):
+    z = oracle.gelu1(0.0, lib=ref)
+    assert z == 0 and not np.signbit(z)
+    for x in (20.0, 50.0, 1e6):
+        assert oracle.gelu1(x, lib=ref) == np.float32(x)
+    for x in (-20.0, -100.0, -1e6):
+        y = oracle.gelu1(x, lib=ref)
+        assert y == 0 and np.signbit(y)
+    assert np.isnan(oracle.gelu1(np.nan, lib=ref))
+
+
+def test_gelu_accuracy_bound(ref):
+    """Against the same formula in float64 (with the binary32 constants):
+    error <= 4 + 4|w| ulp, w = -2z, while exp(w) is finite; once exp(w)
+    overflows the result is -0 and the true value is below 2^-121."""
+    g = inputs.rng(31)
+    x = np.concatenate([inputs.uniform(g, (400000,), -12, 12), inputs.normal(g, (400000,))])
+    y = oracle.gelu(x, lib=ref)
+    x64 = x.astype(np.float64)
+    gc = float(np.float32(0.044715))
+    sq = float(np.float32(math.sqrt(2 / math.pi)))
+    w = -2 * sq * (x64 + gc * x64 ** 3)
+    with np.errstate(over="ignore"):
+        t = x64 / (1 + np.exp(w))
+    fin = w < 88.5
+    err = _ulp_err(y[fin], t[fin])
+    assert (err <= 4 + 4 * np.abs(w[fin])).all(), err.max()
+    over = w > 88.8
+    assert over.any()
+    assert (y[over] == 0).all() and np.signbit(y[over]).all()
+    assert (np.abs(t[over]) < 2.0 ** -121).all()
+
+
+# --------------------------------------------------------------------------
+# c6: softmax rows
+# --------------------------------------------------------------------------
+
+def test_softmax_constant_row_is_reciprocal(ref):
+    for n in (1, 3, 256, 1000):
+        X = np.full((2, n), 1.75, np.float32)
+        Y = oracle.softmax_rows(X, lib=ref)
+        assert (Y == np.float32(1.0) / np.float32(n)).all()
+
+
+def test_softmax_closed_form_rows(ref):
+    X = np.full((1, 256), -200.0, np.float32)
+    X[0, 0] = 0.0
+    Y = oracle.softmax_rows(X, lib=ref)
+    assert Y[0, 0] == 1.0 and (Y[0, 1:] == 0).all()
+    # causal: row r keeps columns j <= r % period; masked outputs are +0
+    g = inputs.rng(41)
+    S = inputs.normal(g, (12, 8), var=4.0)
+    Yc = oracle.softmax_rows(S, causal_period=4, lib=ref)
+    for r in range(12):
+        keep = r % 4
+        assert (Yc[r, keep + 1:].view(np.uint32) == 0).all()
+        if keep == 0:
+            assert Yc[r, 0] == 1.0
+        # unmasked part equals the plain softmax of the kept prefix
+        pre = oracle.softmax_rows(np.ascontiguousarray(S[r:r + 1, :keep + 1]), lib=ref)
+        if keep + 1 <= 64:  # same partial structure when the prefix fits one stride
+            assert_bits_equal(Yc[r, :keep + 1], pre[0], f"row {r}")
+
+
+@pytest.mark.parametrize("W,combine", [(64, 0), (16, 0), (64, 1)])
+def test_softmax_bound(ref, W, combine):
+    """|y - y*| <= y* u (|x - m| + n/W + log2 W + 8) + 2^-149 against float64."""
+    d = inputs.gemm256_softmax256()
+    S = d["S"]
+    Y = oracle.softmax_rows(S, row_width=W, row_combine=combine, lib=ref)
+    S64 = S.astype(np.float64)
+    m = S64.max(axis=1, keepdims=True)
+    e = np.exp(S64 - m)
+    t = e / e.sum(axis=1, keepdims=True)
+    n = S.shape[1]
+    bound = t * U * (np.abs(S64 - m) + n / W + math.log2(W) + 8) + 2.0 ** -149
+    assert (np.abs(Y - t) <= bound).all()
+    assert (np.abs(Y.astype(np.float64).sum(axis=1) - 1) <= (n + 2) * U * 4).all()
+
+
+# --------------------------------------------------------------------------
+# c7: LayerNorm rows
+# --------------------------------------------------------------------------
+
+def test_layernorm_constant_row_gives_beta(ref):
+    g = inputs.rng(51)
+    beta = inputs.uniform(g, (768,), -0.1, 0.1)
+    gamma = inputs.uniform(g, (768,), 0.9, 1.1)
+    X = np.full((3, 768), 2.5, np.float32)
+    Y = oracle.layernorm_rows(X, gamma, beta, lib=ref)
+    assert_bits_equal(Y, np.broadcast_to(beta, Y.shape), "beta")
+    Y0 = oracle.layernorm_rows(X, lib=ref)
+    assert (Y0.view(np.uint32) == 0).all()  # d = +0 exactly, no affine
+
+
+@pytest.mark.parametrize("a", [1.0, 3.0])
+def test_layernorm_alternating_row_closed_form(ref, a):
+    """x = (+a, -a, +a, ...): the strided partials cancel exactly, so mean = +0,
+    var = a^2 exactly, rstd = RN(1/RN(sqrt(RN(a^2 + eps)))), y = RN(+-a * rstd)."""
+    n = 768
+    x = np.where(np.arange(n) % 2 == 0, a, -a).astype(np.float32)[None, :]
+    eps = np.float32(1e-5)
+    Y, mean, rstd = oracle.layernorm_rows(x, eps=eps, lib=ref, with_stats=True)
+    assert mean[0] == 0 and not np.signbit(mean[0])
+    want_rstd = np.float32(1.0) / np.sqrt(np.float32(a * a) + eps)
+    assert rstd[0] == want_rstd
+    assert_bits_equal(Y[0], x[0] * want_rstd, "alternating")
+
+
+def test_layernorm_affine_variants(ref):
+    g = inputs.rng(52)
+    X = inputs.normal(g, (4, 300))
+    gamma = inputs.uniform(g, (300,), 0.9, 1.1)
+    beta = inputs.uniform(g, (300,), -0.1, 0.1)
+    t = oracle.layernorm_rows(X, lib=ref)
+    assert_bits_equal(oracle.layernorm_rows(X, None, beta, lib=ref), t + beta, "beta only")
+    assert_bits_equal(oracle.layernorm_rows(X, gamma, None, lib=ref), t * gamma, "gamma only")
+    full = oracle.layernorm_rows(X, gamma, beta, lib=ref)
+    want = np.array([[exactfp.fma(float(tv), float(gv), float(bv)) for tv, gv, bv in
+                      zip(t[r], gamma, beta)] for r in range(4)], np.float32)
+    assert_bits_equal(full, want, "fma affine")
+
+
+@pytest.mark.parametrize("scale", [1.0, 3e-3])
+def test_layernorm_bound(ref, scale):
+    """Against float64 LayerNorm (biased variance, eps inside the root):
+    |y - y*| <= 64 u (1 + |y*|).  The small-scale rows have variance near eps,
+    which exposes eps placement; n - 1 instead of n would miss by 1/(2n)."""
+    d = inputs.distilbert_mlp(tokens=64)
+    X = (d["X"] * np.float32(scale)).astype(np.float32)
+    Y = oracle.layernorm_rows(X, d["gamma"], d["beta"], eps=1e-5, lib=ref)
+    X64 = X.astype(np.float64)
+    mu = X64.mean(axis=1, keepdims=True)
+    var = ((X64 - mu) ** 2).mean(axis=1, keepdims=True)
+    t = (X64 - mu) / np.sqrt(var + float(np.float32(1e-5))) * d["gamma"] + d["beta"]
+    assert (np.abs(Y - t) <= 64 * U * (1 + np.abs(t))).all()

@@ -1,0 +1,101 @@
+"""Planted mistakes in the oracle must fail its pins (CPU only).
+
+Each case copies the oracle source, plants one plausible mistake by a text
+substitution, compiles the copy into a temporary library and runs the pin tests
+against it: at least one of the named pins has to fail.  The committed oracle is
+never modified.
+"""
+import os
+import tempfile
+
+import pytest
+
+import oracle
+import test_oracle as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")
+
+MUTATIONS = {
+    # c1: unblocked contraction instead of 64-blocks
+    "no_k_blocks": ("const int64_t blk = (k_block > 0) ? k_block : K;", "const int64_t blk = K;",
+                    ["w1"]),
+    # c1: rounded product then add, in place of the fused update
+    "unfused_inner": ("p = fmaf(x, y, p);", "p = p + x * y;", ["w3"]),
+    # c1: last term of every block dropped
+    "dropped_term": ("for (int64_t k = k0; k < k1; ++k) {", "for (int64_t k = k0; k + 1 < k1; ++k) {",
+                     ["int", "bound"]),
+    # c1: A read with its transpose's stride
+    "transposed_a": ("*inc = 1;\n    return A + i * lda;", "*inc = lda;\n    return A + i;",
+                     ["int", "bound"]),
+    # c1: block partial not reset between blocks
+    "partial_not_reset": ("        float p = 0.0f;\n        for (int64_t k = k0;",
+                          "        static __thread float p; if (k0 == 0) p = 0.0f;\n        for (int64_t k = k0;",
+                          ["w1", "int", "bound"]),
+    # c2: tree partner index off by one
+    "tree_index": ("q[l] = q[l] + q[l + s];", "q[l] = q[l] + q[l + s - (s > 1)];", ["w4", "rowint"]),
+    # c4: sign of the low part of ln 2 flipped
+    "ln2_lo_sign": ("r = fmaf(nf, -EXP_LN2_LO, r);", "r = fmaf(nf, EXP_LN2_LO, r);", ["exp"]),
+    # c4: a Taylor coefficient with the wrong exponent (1/12 for 1/24)
+    "taylor_coeff": ("0x1.555556p-5f, /* 1/4! */", "0x1.555556p-4f, /* 1/4! */", ["exp"]),
+    # c4: a coefficient one ulp off: invisible to accuracy, caught by the
+    # constants-against-definitions check
+    "taylor_coeff_ulp": ("0x1.555556p-5f, /* 1/4! */", "0x1.555554p-5f, /* 1/4! */", ["const"]),
+    # c5: cubic coefficient applied to x^2
+    "gelu_power": ("    u = u * x;\n    float z", "    float z", ["gelu"]),
+    # c6: max not subtracted (scale-invariant pins still catch it via bits)
+    "softmax_no_max": ("const float d = x[j] - m;", "const float d = x[j];", ["softmax_const"]),
+    # c7: unbiased variance
+    "ln_unbiased": ("const float var = q / nf;", "const float var = q / (nf - 1.0f);", ["ln"]),
+    # c7: eps outside the square root
+    "ln_eps_outside": ("const float sd = sqrtf(ve);", "const float sd = sqrtf(var) + c->eps;", ["ln"]),
+}
+
+CHECKS = {
+    "const": lambda lib: pins.check_constants(open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
+    "w1": lambda lib: pins.test_witness_w1_blocked_vs_sequential(lib),
+    "w3": lambda lib: pins.test_witness_w3_fused_vs_unfused(lib),
+    "w4": lambda lib: pins.test_witness_w4_strided_tree(lib),
+    "int": lambda lib: pins.test_matmul_integer_closed_form(lib, (19, 23, 65), 0, 0, 64, 0),
+    "bound": lambda lib: pins.test_matmul_error_bound(lib, 200, 64),
+    "rowint": lambda lib: pins.test_rowsum_integers_exact(lib, 100, 64, 0),
+    "exp": lambda lib: pins.test_exp_accuracy_under_one_ulp(lib),
+    "gelu": lambda lib: pins.test_gelu_accuracy_bound(lib),
+    "softmax_const": lambda lib: pins.test_softmax_constant_row_is_reciprocal(lib),
+    "ln": lambda lib: pins.test_layernorm_bound(lib, 3e-3),
+}
+
+
+def _build_mutant(tmp, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    path = os.path.join(tmp, "repops_ref.c")
+    with open(path, "w") as f:
+        f.write(src.replace(old, new))
+    hdr = os.path.join(os.path.dirname(SRC), "repops_ref.h")
+    with open(os.path.join(tmp, "repops_ref.h"), "w") as f:
+        f.write(open(hdr).read())
+    import subprocess
+    out = os.path.join(tmp, "mutant.so")
+    subprocess.run(["gcc", *oracle.CFLAGS, "-o", out, path, "-lm", "-lpthread"], check=True)
+    return oracle.load(out)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name):
+    old, new, checks = MUTATIONS[name]
+    with tempfile.TemporaryDirectory() as tmp:
+        lib = _build_mutant(tmp, old, new)
+        caught = []
+        for c in checks:
+            try:
+                CHECKS[c](lib)
+            except AssertionError:
+                caught.append(c)
+        assert caught, f"mutation {name} passed every pin in {checks}"
+
+
+def test_unmutated_copy_passes_the_same_checks():
+    with tempfile.TemporaryDirectory() as tmp:
+        lib = _build_mutant(tmp, "#include <fenv.h>", "#include <fenv.h>")
+        for fn in CHECKS.values():
+            fn(lib)
