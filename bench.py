@@ -1,0 +1,202 @@
+"""Benchmark of the reproducible fp32 operators on one MI355X.
+
+One step is one reproducible GEMM C = A.B + bias of the 2048^3 workload
+(A, B ~ U(-1,1), bias ~ U(-0.1,0.1), canonical 64-block k order), timed
+with HIP events on the stream the kernel runs on.  The same run also times the
+row reductions and GELU at their model shapes (secondary figures) and the CPU
+oracle on a bounded sample of the GEMM (cpu_baseline).  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--launch tiled:1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X published dense fp32 vector peak
+HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
+METRIC = "bit-exact reproducible fp32 GEMM GFLOP/s (% fp32 vector peak); softmax/LN GB/s"
+
+
+def parse_launch(spec, repops):
+    if spec in (None, "", "auto"):
+        return None
+    kind, _, idx = spec.partition(":")
+    kinds = {"simple": repops.LAUNCH_GEMM_SIMPLE, "tiled": repops.LAUNCH_GEMM_TILED,
+             "mfma": repops.LAUNCH_GEMM_MFMA}
+    if kind == "simple":
+        return repops.Launch(kinds[kind])
+    return repops.Launch(kinds[kind], (int(idx or 0),))
+
+
+def event_time_ms(fn, reps, warmup=2):
+    """Average duration of fn() over reps launches, HIP events on the current
+    stream (the stream the library launches on)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        fn()
+    stop.record()
+    stop.synchronize()
+    return start.elapsed_time(stop) / reps
+
+
+def cpu_baseline(d, flops_per_row_unit, target_s=12.0):
+    """The oracle, as it stands, on a bounded row sample of the same GEMM."""
+    import numpy as np
+    import oracle
+
+    threads = oracle.default_threads()
+    A, B, bias = d["A"], d["B"], d["bias"]
+    rows = 8
+    while True:
+        t0 = time.perf_counter()
+        oracle.matmul(np.ascontiguousarray(A[:rows]), B, bias, nthreads=threads)
+        dt = time.perf_counter() - t0
+        if dt > 1.0 or rows >= A.shape[0]:
+            break
+        rows *= 2
+    if dt < target_s and rows < A.shape[0]:
+        rows = int(min(A.shape[0], max(rows, rows * target_s / max(dt, 1e-3))))
+        t0 = time.perf_counter()
+        oracle.matmul(np.ascontiguousarray(A[:rows]), B, bias, nthreads=threads)
+        dt = time.perf_counter() - t0
+    gflops = rows * flops_per_row_unit / dt / 1e9
+    return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of 2048 output rows of the 2048^3 GEMM (+bias), "
+                      f"{dt:.2f} s wall on {threads} threads"}
+
+
+def secondary(repops, steps):
+    """Row reductions and GELU at their model shapes: GB/s of algorithmic
+    bytes (each element read once and written once; causal softmax reads only
+    the unmasked part)."""
+    import numpy as np
+    import torch
+    from paper_2502_19405_amd import inputs
+
+    out = {}
+    g = inputs.rng(4)
+    # causal softmax, Llama attention scores: 4 x 32 heads x 1024 rows of 1024
+    T, rows = 1024, 4 * 32 * 1024
+    S = torch.from_numpy(inputs.normal(g, (rows, T), var=4.0)).cuda()
+    P = torch.empty_like(S)
+    ms = event_time_ms(lambda: repops.softmax_rows(S, causal_period=T, out=P), steps)
+    nbytes = 4 * (rows // T) * (T * (T + 1) // 2 + T * T)
+    out["softmax_causal_131072x1024"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+                                         "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    ms = event_time_ms(lambda: repops.softmax_rows(S, out=P), steps)
+    nbytes = 4 * rows * T * 2
+    out["softmax_dense_131072x1024"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+                                        "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    del S, P
+    d = inputs.distilbert_mlp()
+    for name, shape in (("layernorm_4096x768", (4096, 768)), ("layernorm_65536x768", (65536, 768))):
+        Z = torch.from_numpy(inputs.normal(g, shape, var=0.5)).cuda()
+        Y = torch.empty_like(Z)
+        gam, bet = torch.from_numpy(d["gamma"]).cuda(), torch.from_numpy(d["beta"]).cuda()
+        ms = event_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y), steps)
+        nbytes = 4 * Z.numel() * 2
+        out[name] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+                     "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    H = torch.from_numpy(inputs.normal(g, (4096, 3072), var=0.31)).cuda()
+    G = torch.empty_like(H)
+    ms = event_time_ms(lambda: repops.gelu(H, out=G), steps)
+    nbytes = 4 * H.numel() * 2
+    out["gelu_4096x3072"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+                             "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--launch", default=None, help="auto | simple | tiled:I | mfma:I")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the reproducible operators shard without any "
+              "exchange along their order-free dimensions, so a multi-GPU figure adds nothing "
+              "here; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2502_19405_amd import inputs, repops
+
+    repops.load()
+    dev = torch.device("cuda:0")
+    d = inputs.gemm2048_bias()
+    M = N = K = 2048
+    A = torch.from_numpy(d["A"]).to(dev)
+    B = torch.from_numpy(d["B"]).to(dev)
+    bias = torch.from_numpy(d["bias"]).to(dev)
+    C = torch.empty((M, N), device=dev)
+    launch = parse_launch(args.launch, repops)
+
+    def step():
+        repops.matmul(A, B, bias, launch=launch, out=C)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    kernel_ms = start.elapsed_time(stop) / args.steps
+    flops = 2.0 * M * N * K
+    gflops = flops / (kernel_ms * 1e-3) / 1e9
+    achieved_tflops = gflops / 1e3
+
+    # which kernel ran (for the roofline bound)
+    mfma = launch is not None and launch.kind == repops.LAUNCH_GEMM_MFMA
+    result = {
+        "metric": METRIC,
+        "value": round(gflops, 1),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(kernel_ms, 5),
+        "wall_ms_per_step": round(wall_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "gemm2048_bias: C = A.B + bias, M=N=K=2048, A,B ~ U(-1,1), "
+                               "bias ~ U(-0.1,0.1), k_block 64, fma, left-to-right",
+                   "launch": args.launch or "auto", "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma" if mfma else "alu", "achieved": round(achieved_tflops, 3),
+                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved_tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_secondary:
+        result["secondary"] = secondary(repops, 20)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(d, 2.0 * N * K)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

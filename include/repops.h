@@ -1,0 +1,224 @@
+/*
+ * repops.h -- C ABI of librepops, bitwise-reproducible fp32 operators for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operators are those of RepOps in "Verde: Verification via Refereed
+ * Delegation for Machine Learning Programs" (arXiv 2502.19405), Section 3:
+ * every output is produced by one fixed sequence of IEEE-754 binary32
+ * operations that depends only on the problem sizes and on the canonical-order
+ * descriptor below -- never on the launch configuration, tile sizes, strides,
+ * transposition, the GPU model or the run.  Two calls with the same order
+ * descriptor and the same logical inputs return the same bits.
+ *
+ * General conventions
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *     allocates no device memory and keeps no mutable global state.
+ *   - Storage is row-major; leading dimensions and batch strides count
+ *     elements (float), not bytes.
+ *   - Calls are asynchronous on `hip_stream` (a hipStream_t; NULL means the
+ *     null stream).  Device faults surface at the caller's next
+ *     synchronisation.  Calls are thread-safe.
+ *   - On any error nothing is enqueued and a nonzero repops_status_t is
+ *     returned.  Zero-sized problems (m, n, rows, batch or element count 0)
+ *     succeed without launching anything.
+ *   - `launch` selects speed only and may be NULL (automatic choice).  A
+ *     launch configuration never changes an output bit.
+ *   - Inputs are expected finite; infinities and NaNs propagate
+ *     deterministically, but only "NaN in, NaN out" is promised for them.
+ */
+#ifndef REPOPS_H
+#define REPOPS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REPOPS_ABI_VERSION 1u
+
+typedef int32_t repops_status_t;
+enum {
+    REPOPS_OK = 0,
+    REPOPS_ERR_NULL = 1,   /* a required pointer is NULL */
+    REPOPS_ERR_SHAPE = 2,  /* negative size, or a size the operator cannot take */
+    REPOPS_ERR_STRIDE = 3, /* leading dimension smaller than the row it holds */
+    REPOPS_ERR_ALIAS = 4,  /* output overlaps an input where that is not allowed */
+    REPOPS_ERR_ORDER = 5,  /* unknown or unsupported order descriptor; never silently replaced */
+    REPOPS_ERR_LAUNCH = 6, /* launch configuration invalid for this call */
+    REPOPS_ERR_HIP = 7     /* the HIP runtime rejected the kernel launch */
+};
+
+/*
+ * Canonical-order descriptor: selects the BITS.
+ *
+ * Contraction (matmul, bmm) -- Section 3.2, matrix-multiplication listing: the
+ * output indices run in any order, the contraction index k in one fixed order.
+ * For an output with terms (a_k, b_k), k = 0..K-1:
+ *     for each block beta = 0, 1, ... of k_block consecutive k (last one short):
+ *         P = +0;  for k in the block, ascending:  P = fma(a_k, b_k, P)
+ *                                         (k_inner MUL_ADD: P = P + RN(a_k*b_k))
+ *     acc = +0;  for beta ascending:  acc = acc + P_beta
+ * k_block = 0 is a single block: the listing itself.
+ *
+ * Row reductions (softmax, LayerNorm) -- not fixed by the paper; the order is a
+ * function of the row length n and row_width W only:
+ *     STRIDED_TREE: q[l] = +0 for l < W; x_j is added to q[j mod W] in
+ *         ascending j; then for s = W/2, ..., 1: q[l] = q[l] + q[l+s] (l < s);
+ *         the sum is q[0].
+ *     BLOCKED_LTR: the contraction rule with additions, blocks of W elements.
+ *     For LayerNorm's sum of squares the term update is q = fma(d, d, q).
+ *
+ * version 1 also freezes the operation sequences of exp, GELU, softmax and
+ * LayerNorm documented at each function below.
+ */
+typedef struct repops_order {
+    uint32_t version;     /* must be 1 */
+    uint32_t k_block;     /* contraction block length; 0 = unblocked; default 64 */
+    uint32_t k_inner;     /* REPOPS_K_FMA (default) or REPOPS_K_MUL_ADD */
+    uint32_t k_combine;   /* REPOPS_COMBINE_LTR (only value in version 1) */
+    uint32_t row_width;   /* W: power of two in [1, 1024]; default 64 */
+    uint32_t row_combine; /* REPOPS_ROW_STRIDED_TREE (default) or REPOPS_ROW_BLOCKED_LTR */
+    uint32_t reserved[2]; /* must be 0 */
+} repops_order_t;
+
+enum { REPOPS_K_FMA = 0, REPOPS_K_MUL_ADD = 1 };
+enum { REPOPS_COMBINE_LTR = 0 };
+enum { REPOPS_ROW_STRIDED_TREE = 0, REPOPS_ROW_BLOCKED_LTR = 1 };
+
+/*
+ * Launch descriptor: selects the SPEED only.
+ *   kind AUTO (0): the library chooses.
+ *   matmul / bmm:
+ *     GEMM_SIMPLE (1): one output per thread, operands read from global memory.
+ *     GEMM_TILED  (2): LDS-staged tiles, per-lane FMA chains; p[0] = index into
+ *         the table reported by repops_gemm_config_name().  Needs k_block = 0
+ *         or k_block a multiple of the configuration's k tile.
+ *     GEMM_MFMA   (3): matrix-core tiles whose single-term updates equal the
+ *         FMA chain; p[0] = index into the same table.  Needs k_inner FMA.
+ *   softmax_rows / layernorm_rows:
+ *     ROWS_GENERIC (1): any supported order descriptor.
+ *     ROWS_WAVE    (2): one 64-lane wave per row, STRIDED_TREE with W = 64;
+ *         p[0] = rows (waves) per block, one of 1, 2, 4, 8.
+ *   gelu / exp:
+ *     ELEMENTWISE (1): p[0] = threads per block (multiple of 64, <= 1024),
+ *         p[1] = maximum number of blocks (0 = as many as needed).
+ * Unused p[] entries must be 0.
+ */
+typedef struct repops_launch {
+    uint32_t kind;
+    uint32_t p[7];
+} repops_launch_t;
+
+enum {
+    REPOPS_LAUNCH_AUTO = 0,
+    REPOPS_LAUNCH_GEMM_SIMPLE = 1,
+    REPOPS_LAUNCH_GEMM_TILED = 2,
+    REPOPS_LAUNCH_GEMM_MFMA = 3,
+    REPOPS_LAUNCH_ROWS_GENERIC = 1,
+    REPOPS_LAUNCH_ROWS_WAVE = 2,
+    REPOPS_LAUNCH_ELEMENTWISE = 1
+};
+
+/* Fills *order with version 1, k_block 64, FMA, left-to-right, W 64, strided tree. */
+void repops_order_default(repops_order_t *order);
+const char *repops_status_str(repops_status_t status);
+uint32_t repops_abi_version(void);
+
+/* Number of entries in the tiled / matrix-core configuration tables, and a
+ * static description of entry `index` ("BMxBNxBK/TMxTN", NULL if out of range). */
+int32_t repops_gemm_config_count(uint32_t kind);
+const char *repops_gemm_config_name(uint32_t kind, uint32_t index);
+
+/*
+ * repops_matmul -- C = A.B (+ bias), Section 3.2 (matrix multiplication).
+ *   m, n, k   logical sizes: A is m x k, B is k x n, C is m x n; k = 0 gives
+ *             C = +0 (or bias).
+ *   A, lda    trans_a = 0: A[i][kk] at A[i*lda + kk] (lda >= k);
+ *             trans_a = 1: A stored k x m, A[i][kk] at A[kk*lda + i] (lda >= m).
+ *   B, ldb    trans_b = 0: B[kk][j] at B[kk*ldb + j] (ldb >= n);
+ *             trans_b = 1: B stored n x k, B[kk][j] at B[j*ldb + kk] (ldb >= k).
+ *   bias      NULL or [n]: C[i][j] = acc + bias[j], one rounded addition after
+ *             the contraction.
+ *   C, ldc    output, ldc >= n; must not overlap A, B or bias (REPOPS_ERR_ALIAS).
+ */
+repops_status_t repops_matmul(const repops_order_t *order, int64_t m, int64_t n, int64_t k,
+                              const float *A, int64_t lda, int32_t trans_a,
+                              const float *B, int64_t ldb, int32_t trans_b,
+                              const float *bias, float *C, int64_t ldc,
+                              const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_bmm -- batched product over (i0, i1) in [0,batch0) x [0,batch1), the
+ * batched key-query and probability-value products of attention that Section
+ * 2.2 decomposes into independent matrix products.  Batch element (i0, i1)
+ * reads A + i0*sa0 + i1*sa1 and B + i0*sb0 + i1*sb1 with the matmul layout
+ * rules, and writes C + i0*sc0 + i1*sc1:  C[i][j] = acc * alpha (one rounded
+ * multiplication).  Strides may be 0 for A and B; the C regions of different
+ * batch elements must not overlap each other (not checked) nor A or B.
+ */
+repops_status_t repops_bmm(const repops_order_t *order, int64_t batch0, int64_t batch1,
+                           int64_t m, int64_t n, int64_t k,
+                           const float *A, int64_t sa0, int64_t sa1, int64_t lda, int32_t trans_a,
+                           const float *B, int64_t sb0, int64_t sb1, int64_t ldb, int32_t trans_b,
+                           float alpha, float *C, int64_t sc0, int64_t sc1, int64_t ldc,
+                           const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_softmax_rows -- row softmax (an operator of the DistilBERT and Llama
+ * programs of Section 4.2; order fixed by the descriptor):
+ *     m = max over unmasked x_j;  e_j = exp_rep(x_j - m) (masked: +0);
+ *     s = row sum of e in the descriptor's row order;  r = 1 / s;  y_j = e_j * r.
+ *   X, ldx / Y, ldy   rows x cols, ldx >= cols, ldy >= cols.  Y == X with
+ *                     ldy == ldx (in place) is allowed; other overlap is not.
+ *   causal_period     0: no mask; p > 0: row i masks columns j > i mod p.
+ */
+repops_status_t repops_softmax_rows(const repops_order_t *order, int64_t rows, int64_t cols,
+                                    const float *X, int64_t ldx, float *Y, int64_t ldy,
+                                    int64_t causal_period, const repops_launch_t *launch,
+                                    void *hip_stream);
+
+/*
+ * repops_layernorm_rows -- row LayerNorm (named among DistilBERT's operators in
+ * Section 4.2), biased variance:
+ *     mean = rowsum(x) / n;  d_j = x_j - mean;  var = rowsum(fma(d,d,.)) / n;
+ *     rstd = 1 / sqrt(var + eps);  t_j = d_j * rstd;  y_j = fma(t_j, gamma_j, beta_j).
+ *   sqrt and the division are correctly rounded.  gamma / beta may be NULL:
+ *   the operation is skipped (y = t, t + beta or t * gamma), which differs from
+ *   passing ones / zeros in the sign of zero.  mean_out / rstd_out: NULL or
+ *   [rows].  cols must be >= 1.  In-place as for softmax.
+ */
+repops_status_t repops_layernorm_rows(const repops_order_t *order, int64_t rows, int64_t cols,
+                                      const float *X, int64_t ldx, const float *gamma,
+                                      const float *beta, float eps, float *Y, int64_t ldy,
+                                      float *mean_out, float *rstd_out,
+                                      const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_gelu -- tanh-form GELU over n contiguous elements (Section 4.2 names
+ * GeLU among DistilBERT's operators), using 0.5(1 + tanh z) = 1/(1 + exp(-2z)):
+ *     u = (x*x)*x;  z = fma(0.044715f, u, x) * 0.7978846f;  w = -2*z;
+ *     y = x / (1 + exp_rep(w)).
+ *   Constants are the binary32 values nearest 0.044715 and sqrt(2/pi).
+ *   Y == X (in place) is allowed.
+ */
+repops_status_t repops_gelu(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                            const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_exp -- the reproducible exp used inside softmax and GELU (Section 3.1
+ * lists exp among the functions RepOps rebuilds with a controlled order),
+ * exported for testing.  Cody-Waite reduction and a degree-7 Taylor polynomial:
+ *     n = rint(x * log2e) (ties to even); n > 128: +inf; n < -151: +0;
+ *     r = fma(n, -ln2_hi, x); r = fma(n, -ln2_lo, r);
+ *     p = Horner over 1/i!, i = 7..0, with fma;
+ *     y = (p * 2^floor(n/2)) * 2^(n - floor(n/2)).
+ *   Y == X (in place) is allowed.
+ */
+repops_status_t repops_exp(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                           const repops_launch_t *launch, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

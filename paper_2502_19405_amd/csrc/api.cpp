@@ -1,0 +1,371 @@
+// C ABI of librepops: argument validation, order-descriptor checks and launch
+// selection.  Every error is detected before anything is enqueued.
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/repops.h"
+#include "repops_internal.h"
+
+using repops::GemmArgs;
+using repops::RowArgs;
+
+namespace {
+
+constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
+
+bool order_valid(const repops_order_t* o) {
+  if (!o) return false;
+  if (o->version != 1) return false;
+  if (o->k_inner != REPOPS_K_FMA && o->k_inner != REPOPS_K_MUL_ADD) return false;
+  if (o->k_combine != REPOPS_COMBINE_LTR) return false;
+  const uint32_t w = o->row_width;
+  if (w < 1 || w > 1024 || (w & (w - 1)) != 0) return false;
+  if (o->row_combine != REPOPS_ROW_STRIDED_TREE && o->row_combine != REPOPS_ROW_BLOCKED_LTR)
+    return false;
+  if (o->reserved[0] != 0 || o->reserved[1] != 0) return false;
+  return true;
+}
+
+bool launch_params_zero_from(const repops_launch_t* l, int first) {
+  for (int i = first; i < 7; ++i)
+    if (l->p[i] != 0) return false;
+  return true;
+}
+
+// Byte range [lo, hi) touched by a strided operand: `rows` rows of `cols`
+// elements, leading dimension ld, replicated over two batch strides.
+struct Extent {
+  uintptr_t lo, hi;
+};
+
+Extent extent_of(const float* p, int64_t b0, int64_t s0, int64_t b1, int64_t s1, int64_t rows,
+                 int64_t cols, int64_t ld) {
+  int64_t lo = 0, hi = 0;  // element offsets, hi inclusive
+  auto span = [&](int64_t count, int64_t stride) {
+    if (count <= 1) return;
+    const int64_t d = (count - 1) * stride;
+    if (d < 0) lo += d; else hi += d;
+  };
+  span(b0, s0);
+  span(b1, s1);
+  span(rows, ld);
+  hi += cols - 1;
+  const uintptr_t base = reinterpret_cast<uintptr_t>(p);
+  return {base + static_cast<uintptr_t>(lo * 4), base + static_cast<uintptr_t>((hi + 1) * 4)};
+}
+
+bool overlaps(Extent a, Extent b) { return a.lo < b.hi && b.lo < a.hi; }
+
+repops_status_t hip_status(hipError_t e) { return e == hipSuccess ? REPOPS_OK : REPOPS_ERR_HIP; }
+
+repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_launch_t* launch,
+                         hipStream_t stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  g.k_block = order->k_block;
+  g.fused = order->k_inner == REPOPS_K_FMA ? 1 : 0;
+
+  uint32_t kind = launch ? launch->kind : REPOPS_LAUNCH_AUTO;
+  uint32_t index = 0;
+  if (launch) {
+    if (kind == REPOPS_LAUNCH_AUTO || kind == REPOPS_LAUNCH_GEMM_SIMPLE) {
+      if (!launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
+    } else if (kind == REPOPS_LAUNCH_GEMM_TILED || kind == REPOPS_LAUNCH_GEMM_MFMA) {
+      if (!launch_params_zero_from(launch, 1)) return REPOPS_ERR_LAUNCH;
+      index = launch->p[0];
+    } else {
+      return REPOPS_ERR_LAUNCH;
+    }
+  }
+  auto tiled_ok = [&](const repops::GemmConfig* c) {
+    return c && (g.k_block == 0 || g.k_block % c->bk == 0);
+  };
+  if (kind == REPOPS_LAUNCH_AUTO) {
+    // Largest tile for big outputs, the small tile otherwise; the simple path
+    // for block lengths no tile divides.
+    const int64_t outputs = g.m * g.n * g.batch0 * g.batch1;
+    const int preferred = outputs >= int64_t(1) << 22 ? 1 : 0;
+    if (tiled_ok(repops::gemm_tiled_config(preferred))) {
+      kind = REPOPS_LAUNCH_GEMM_TILED;
+      index = preferred;
+    } else if (tiled_ok(repops::gemm_tiled_config(0))) {
+      kind = REPOPS_LAUNCH_GEMM_TILED;
+      index = 0;
+    } else {
+      kind = REPOPS_LAUNCH_GEMM_SIMPLE;
+    }
+  }
+  if (kind == REPOPS_LAUNCH_GEMM_SIMPLE) return hip_status(repops::launch_gemm_simple(g, stream));
+  if (kind == REPOPS_LAUNCH_GEMM_TILED) {
+    if (!tiled_ok(repops::gemm_tiled_config(static_cast<int>(index)))) return REPOPS_ERR_LAUNCH;
+    return hip_status(repops::launch_gemm_tiled(g, static_cast<int>(index), stream));
+  }
+  // matrix-core path
+  const repops::GemmConfig* c = repops::gemm_mfma_config(static_cast<int>(index));
+  if (!c || !g.fused || (g.k_block != 0 && g.k_block % c->bk != 0)) return REPOPS_ERR_LAUNCH;
+  return hip_status(repops::launch_gemm_mfma(g, static_cast<int>(index), stream));
+}
+
+repops_status_t check_operands(const GemmArgs& g) {
+  if (g.batch0 < 0 || g.batch1 < 0 || g.m < 0 || g.n < 0 || g.k < 0) return REPOPS_ERR_SHAPE;
+  if (g.batch0 > kMaxDim || g.batch1 > kMaxDim || g.m > kMaxDim || g.n > kMaxDim ||
+      g.k > kMaxDim)
+    return REPOPS_ERR_SHAPE;
+  if (g.k_block < 0) return REPOPS_ERR_ORDER;
+  if (g.ta != 0 && g.ta != 1) return REPOPS_ERR_SHAPE;
+  if (g.tb != 0 && g.tb != 1) return REPOPS_ERR_SHAPE;
+  const bool empty = g.batch0 == 0 || g.batch1 == 0 || g.m == 0 || g.n == 0;
+  if (empty) return REPOPS_OK;
+  if (!g.C) return REPOPS_ERR_NULL;
+  if (g.k > 0 && (!g.A || !g.B)) return REPOPS_ERR_NULL;
+  if (g.ldc < g.n || g.ldc < 1) return REPOPS_ERR_STRIDE;
+  if (g.k > 0) {
+    if (g.lda < (g.ta ? g.m : g.k)) return REPOPS_ERR_STRIDE;
+    if (g.ldb < (g.tb ? g.k : g.n)) return REPOPS_ERR_STRIDE;
+  }
+  const Extent ce = extent_of(g.C, g.batch0, g.sc0, g.batch1, g.sc1, g.m, g.n, g.ldc);
+  if (g.k > 0) {
+    const Extent ae = g.ta ? extent_of(g.A, g.batch0, g.sa0, g.batch1, g.sa1, g.k, g.m, g.lda)
+                           : extent_of(g.A, g.batch0, g.sa0, g.batch1, g.sa1, g.m, g.k, g.lda);
+    const Extent be = g.tb ? extent_of(g.B, g.batch0, g.sb0, g.batch1, g.sb1, g.n, g.k, g.ldb)
+                           : extent_of(g.B, g.batch0, g.sb0, g.batch1, g.sb1, g.k, g.n, g.ldb);
+    if (overlaps(ce, ae) || overlaps(ce, be)) return REPOPS_ERR_ALIAS;
+  }
+  if (g.bias) {
+    const Extent bi = extent_of(g.bias, 1, 0, 1, 0, 1, g.n, g.n);
+    if (overlaps(ce, bi)) return REPOPS_ERR_ALIAS;
+  }
+  return REPOPS_OK;
+}
+
+// Rows: Y may equal X exactly (same base, same leading dimension); any other
+// overlap is rejected.
+repops_status_t check_rows(int64_t rows, int64_t cols, const float* X, int64_t ldx, const float* Y,
+                           int64_t ldy, bool* empty) {
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return REPOPS_ERR_SHAPE;
+  *empty = rows == 0 || cols == 0;
+  if (*empty) return REPOPS_OK;
+  if (!X || !Y) return REPOPS_ERR_NULL;
+  if (ldx < cols || ldy < cols) return REPOPS_ERR_STRIDE;
+  const Extent xe = extent_of(X, 1, 0, 1, 0, rows, cols, ldx);
+  const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
+  if (X == Y && ldx == ldy) return REPOPS_OK;
+  if (overlaps(xe, ye)) return REPOPS_ERR_ALIAS;
+  return REPOPS_OK;
+}
+
+repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch_t* launch,
+                                int64_t cols, uint32_t* kind, int* wpb) {
+  const bool wave_order =
+      order->row_width == 64 && order->row_combine == REPOPS_ROW_STRIDED_TREE;
+  const bool wave_fits = cols <= repops::rows_wave_max_cols();
+  *wpb = 4;
+  if (!launch || launch->kind == REPOPS_LAUNCH_AUTO) {
+    if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
+    *kind = (wave_order && wave_fits) ? REPOPS_LAUNCH_ROWS_WAVE : REPOPS_LAUNCH_ROWS_GENERIC;
+    return REPOPS_OK;
+  }
+  if (launch->kind == REPOPS_LAUNCH_ROWS_GENERIC) {
+    if (!launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
+    *kind = REPOPS_LAUNCH_ROWS_GENERIC;
+    return REPOPS_OK;
+  }
+  if (launch->kind == REPOPS_LAUNCH_ROWS_WAVE) {
+    const uint32_t w = launch->p[0];
+    if (!(w == 1 || w == 2 || w == 4 || w == 8) || !launch_params_zero_from(launch, 1))
+      return REPOPS_ERR_LAUNCH;
+    if (!wave_order || !wave_fits) return REPOPS_ERR_LAUNCH;
+    *kind = REPOPS_LAUNCH_ROWS_WAVE;
+    *wpb = static_cast<int>(w);
+    return REPOPS_OK;
+  }
+  return REPOPS_ERR_LAUNCH;
+}
+
+repops_status_t ew_launch(const repops_launch_t* launch, int* threads, int* max_blocks) {
+  *threads = 256;
+  *max_blocks = 0;
+  if (!launch || launch->kind == REPOPS_LAUNCH_AUTO) {
+    if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
+    return REPOPS_OK;
+  }
+  if (launch->kind != REPOPS_LAUNCH_ELEMENTWISE) return REPOPS_ERR_LAUNCH;
+  const uint32_t t = launch->p[0];
+  if (t == 0 || t > 1024 || t % 64 != 0 || !launch_params_zero_from(launch, 2))
+    return REPOPS_ERR_LAUNCH;
+  if (launch->p[1] > (1u << 30)) return REPOPS_ERR_LAUNCH;
+  *threads = static_cast<int>(t);
+  *max_blocks = static_cast<int>(launch->p[1]);
+  return REPOPS_OK;
+}
+
+repops_status_t check_elementwise(const repops_order_t* order, int64_t n, const float* X,
+                                  const float* Y) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (n < 0 || n > kMaxDim) return REPOPS_ERR_SHAPE;
+  if (n == 0) return REPOPS_OK;
+  if (!X || !Y) return REPOPS_ERR_NULL;
+  if (X != Y) {
+    const Extent xe = extent_of(X, 1, 0, 1, 0, 1, n, n), ye = extent_of(Y, 1, 0, 1, 0, 1, n, n);
+    if (overlaps(xe, ye)) return REPOPS_ERR_ALIAS;
+  }
+  return REPOPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void repops_order_default(repops_order_t* order) {
+  if (!order) return;
+  memset(order, 0, sizeof(*order));
+  order->version = 1;
+  order->k_block = 64;
+  order->k_inner = REPOPS_K_FMA;
+  order->k_combine = REPOPS_COMBINE_LTR;
+  order->row_width = 64;
+  order->row_combine = REPOPS_ROW_STRIDED_TREE;
+}
+
+const char* repops_status_str(repops_status_t s) {
+  switch (s) {
+    case REPOPS_OK: return "ok";
+    case REPOPS_ERR_NULL: return "null pointer";
+    case REPOPS_ERR_SHAPE: return "invalid shape";
+    case REPOPS_ERR_STRIDE: return "invalid stride";
+    case REPOPS_ERR_ALIAS: return "output overlaps an input";
+    case REPOPS_ERR_ORDER: return "unsupported order descriptor";
+    case REPOPS_ERR_LAUNCH: return "invalid launch configuration";
+    case REPOPS_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+uint32_t repops_abi_version(void) { return REPOPS_ABI_VERSION; }
+
+int32_t repops_gemm_config_count(uint32_t kind) {
+  if (kind == REPOPS_LAUNCH_GEMM_TILED) return repops::gemm_tiled_count();
+  if (kind == REPOPS_LAUNCH_GEMM_MFMA) return repops::gemm_mfma_count();
+  return 0;
+}
+
+const char* repops_gemm_config_name(uint32_t kind, uint32_t index) {
+  const repops::GemmConfig* c = nullptr;
+  if (kind == REPOPS_LAUNCH_GEMM_TILED) c = repops::gemm_tiled_config(static_cast<int>(index));
+  if (kind == REPOPS_LAUNCH_GEMM_MFMA) c = repops::gemm_mfma_config(static_cast<int>(index));
+  return c ? c->name : nullptr;
+}
+
+repops_status_t repops_matmul(const repops_order_t* order, int64_t m, int64_t n, int64_t k,
+                              const float* A, int64_t lda, int32_t trans_a, const float* B,
+                              int64_t ldb, int32_t trans_b, const float* bias, float* C,
+                              int64_t ldc, const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  GemmArgs g{};
+  g.batch0 = 1; g.batch1 = 1; g.m = m; g.n = n; g.k = k;
+  g.A = A; g.lda = lda; g.ta = trans_a;
+  g.B = B; g.ldb = ldb; g.tb = trans_b;
+  g.C = C; g.ldc = ldc;
+  g.bias = bias; g.alpha = 1.0f; g.has_alpha = 0;
+  g.k_block = order->k_block;
+  const repops_status_t st = check_operands(g);
+  if (st != REPOPS_OK) return st;
+  if (m == 0 || n == 0) return REPOPS_OK;
+  return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
+}
+
+repops_status_t repops_bmm(const repops_order_t* order, int64_t batch0, int64_t batch1, int64_t m,
+                           int64_t n, int64_t k, const float* A, int64_t sa0, int64_t sa1,
+                           int64_t lda, int32_t trans_a, const float* B, int64_t sb0, int64_t sb1,
+                           int64_t ldb, int32_t trans_b, float alpha, float* C, int64_t sc0,
+                           int64_t sc1, int64_t ldc, const repops_launch_t* launch,
+                           void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  GemmArgs g{};
+  g.batch0 = batch0; g.batch1 = batch1; g.m = m; g.n = n; g.k = k;
+  g.A = A; g.sa0 = sa0; g.sa1 = sa1; g.lda = lda; g.ta = trans_a;
+  g.B = B; g.sb0 = sb0; g.sb1 = sb1; g.ldb = ldb; g.tb = trans_b;
+  g.C = C; g.sc0 = sc0; g.sc1 = sc1; g.ldc = ldc;
+  g.bias = nullptr; g.alpha = alpha; g.has_alpha = 1;
+  g.k_block = order->k_block;
+  const repops_status_t st = check_operands(g);
+  if (st != REPOPS_OK) return st;
+  if (batch0 == 0 || batch1 == 0 || m == 0 || n == 0) return REPOPS_OK;
+  return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
+}
+
+repops_status_t repops_softmax_rows(const repops_order_t* order, int64_t rows, int64_t cols,
+                                    const float* X, int64_t ldx, float* Y, int64_t ldy,
+                                    int64_t causal_period, const repops_launch_t* launch,
+                                    void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (causal_period < 0) return REPOPS_ERR_SHAPE;
+  bool empty = false;
+  repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
+  if (st != REPOPS_OK) return st;
+  uint32_t kind;
+  int wpb;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  if (st != REPOPS_OK || empty) return st;
+  RowArgs a{};
+  a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
+  a.W = static_cast<int>(order->row_width);
+  a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
+  a.period = causal_period;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_softmax_wave(a, wpb, s));
+  return hip_status(repops::launch_softmax_generic(a, s));
+}
+
+repops_status_t repops_layernorm_rows(const repops_order_t* order, int64_t rows, int64_t cols,
+                                      const float* X, int64_t ldx, const float* gamma,
+                                      const float* beta, float eps, float* Y, int64_t ldy,
+                                      float* mean_out, float* rstd_out,
+                                      const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (rows > 0 && cols == 0) return REPOPS_ERR_SHAPE;
+  if (cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;  // n must convert to float exactly
+  bool empty = false;
+  repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
+  if (st != REPOPS_OK) return st;
+  uint32_t kind;
+  int wpb;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  if (st != REPOPS_OK || empty) return st;
+  const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
+  if (gamma && overlaps(ye, extent_of(gamma, 1, 0, 1, 0, 1, cols, cols))) return REPOPS_ERR_ALIAS;
+  if (beta && overlaps(ye, extent_of(beta, 1, 0, 1, 0, 1, cols, cols))) return REPOPS_ERR_ALIAS;
+  RowArgs a{};
+  a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
+  a.W = static_cast<int>(order->row_width);
+  a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
+  a.gamma = gamma; a.beta = beta; a.eps = eps;
+  a.mean_out = mean_out; a.rstd_out = rstd_out;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_wave(a, wpb, s));
+  return hip_status(repops::launch_layernorm_generic(a, s));
+}
+
+repops_status_t repops_gelu(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                            const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(
+      repops::launch_gelu(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_exp(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                           const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(
+      repops::launch_exp(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+// Reproducible elementary functions for gfx950, built only from IEEE-754
+// binary32 basic operations (add, multiply, fused multiply-add, correctly
+// rounded divide, round-to-integral) whose results every conforming unit
+// returns bit for bit.  No hardware approximation (v_exp_f32, v_rcp_f32,
+// v_rsq_f32) is used.
+//
+// exp:  Cody and Waite's additive reduction x = n ln2 + r with ln2 split in a
+//       high and a low binary32 part, then the degree-7 Taylor polynomial of
+//       exp(r) by Horner's rule, then scaling by 2^n in two exact-exponent
+//       steps (RepOps rebuilds exp with a controlled order, Section 3.1 of the
+//       Verde paper; the method is Cody-Waite + Taylor).
+// gelu: tanh form through 0.5 (1 + tanh z) = 1 / (1 + exp(-2z)).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#pragma clang fp contract(off)
+
+namespace repops {
+
+// Nearest binary32 values to log2(e), ln2 (high part) and ln2 - ln2_hi.
+constexpr float kLog2e = 0x1.715476p+0f;
+constexpr float kLn2Hi = 0x1.62e43p-1f;
+constexpr float kLn2Lo = -0x1.05c61p-29f;
+// 1/k! rounded to binary32, k = 2..7 (the k = 0, 1 coefficients are 1).
+constexpr float kInvFact2 = 0x1p-1f;
+constexpr float kInvFact3 = 0x1.555556p-3f;
+constexpr float kInvFact4 = 0x1.555556p-5f;
+constexpr float kInvFact5 = 0x1.111112p-7f;
+constexpr float kInvFact6 = 0x1.6c16c2p-10f;
+constexpr float kInvFact7 = 0x1.a01a02p-13f;
+// Nearest binary32 values to 0.044715 and sqrt(2/pi).
+constexpr float kGeluCubic = 0x1.6e4e26p-5f;
+constexpr float kGeluScale = 0x1.988454p-1f;
+
+__device__ __forceinline__ float pow2_exact(int e) {
+  // 2^e for e in [-126, 127] from the exponent field alone.
+  return __int_as_float((e + 127) << 23);
+}
+
+__device__ __forceinline__ float rep_exp(float x) {
+  const float t = x * kLog2e;
+  const float nf = __builtin_rintf(t);  // v_rndne_f32: nearest, ties to even
+  // Clamp before the integer conversion so that every lane takes the same
+  // straight-line path; out-of-range lanes are replaced below.
+  const float nc = __builtin_fminf(__builtin_fmaxf(nf, -151.0f), 128.0f);
+  float r = __builtin_fmaf(nc, -kLn2Hi, x);
+  r = __builtin_fmaf(nc, -kLn2Lo, r);
+  float p = __builtin_fmaf(kInvFact7, r, kInvFact6);
+  p = __builtin_fmaf(p, r, kInvFact5);
+  p = __builtin_fmaf(p, r, kInvFact4);
+  p = __builtin_fmaf(p, r, kInvFact3);
+  p = __builtin_fmaf(p, r, kInvFact2);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  const int n = static_cast<int>(nc);
+  const int lo = n >> 1;  // floor(n / 2): arithmetic shift
+  const int hi = n - lo;
+  float y = (p * pow2_exact(lo)) * pow2_exact(hi);
+  y = (nf > 128.0f) ? __builtin_huge_valf() : y;
+  y = (nf < -151.0f) ? 0.0f : y;
+  y = (x != x) ? x : y;  // NaN in, NaN out
+  return y;
+}
+
+__device__ __forceinline__ float rep_gelu(float x) {
+  float u = x * x;
+  u = u * x;
+  float z = __builtin_fmaf(kGeluCubic, u, x);
+  z = z * kGeluScale;
+  const float w = z * -2.0f;
+  const float d = 1.0f + rep_exp(w);
+  return x / d;  // correctly rounded division
+}
+
+}  // namespace repops

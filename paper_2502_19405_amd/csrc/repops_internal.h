@@ -1,0 +1,61 @@
+// Internal interfaces between the C ABI layer (api.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace repops {
+
+struct GemmArgs {
+  int64_t batch0, batch1, m, n, k;
+  const float* A; int64_t sa0, sa1, lda; int ta;
+  const float* B; int64_t sb0, sb1, ldb; int tb;
+  float* C; int64_t sc0, sc1, ldc;
+  const float* bias;  // nullable, [n]
+  float alpha;
+  int has_alpha;      // 1: C = acc * alpha
+  int64_t k_block;    // 0 = one block
+  int fused;          // 1: fma chain, 0: rounded product then add
+};
+
+struct GemmConfig {
+  const char* name;
+  int bm, bn, bk;
+};
+
+// Tables of compiled tile configurations.
+int gemm_tiled_count();
+const GemmConfig* gemm_tiled_config(int index);
+int gemm_mfma_count();
+const GemmConfig* gemm_mfma_config(int index);
+
+hipError_t launch_gemm_simple(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_tiled(const GemmArgs& a, int index, hipStream_t s);
+hipError_t launch_gemm_mfma(const GemmArgs& a, int index, hipStream_t s);
+
+struct RowArgs {
+  int64_t rows, cols;
+  const float* X; int64_t ldx;
+  float* Y; int64_t ldy;
+  int W;              // row width
+  int blocked;        // 0 = strided tree, 1 = blocked left-to-right
+  // softmax
+  int64_t period;     // causal period, 0 = none
+  // layernorm
+  const float* gamma; const float* beta; float eps;
+  float* mean_out; float* rstd_out;
+};
+
+hipError_t launch_softmax_wave(const RowArgs& a, int waves_per_block, hipStream_t s);
+hipError_t launch_softmax_generic(const RowArgs& a, hipStream_t s);
+hipError_t launch_layernorm_wave(const RowArgs& a, int waves_per_block, hipStream_t s);
+hipError_t launch_layernorm_generic(const RowArgs& a, hipStream_t s);
+// Largest row length the register-resident wave kernels hold.
+int64_t rows_wave_max_cols();
+
+hipError_t launch_gelu(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                       hipStream_t s);
+hipError_t launch_exp(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                      hipStream_t s);
+
+}  // namespace repops

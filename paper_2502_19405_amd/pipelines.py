@@ -1,0 +1,79 @@
+"""Model-shaped compositions of the reproducible operators.
+
+Each function only chains C-ABI calls through the binding (no arithmetic of
+its own), in the shapes of the programs Verde's evaluation runs (Section 4.2):
+a DistilBERT feed-forward block, a Llama attention block and the backward
+products of a Llama linear layer.  Elementwise work is not fused into the
+GEMMs, so every intermediate keeps the bits of the operator that made it.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import repops
+
+
+def mlp_forward(X, W1, b1, W2, b2, gamma, beta, eps=1e-5, order=None, gemm_launch=None,
+                keep=False):
+    """LayerNorm(gelu(X W1 + b1) W2 + b2): X [t, h], W1 [h, f], W2 [f, h]."""
+    H1 = repops.matmul(X, W1, b1, order=order, launch=gemm_launch)
+    G = repops.gelu(H1, order=order)
+    H2 = repops.matmul(G, W2, b2, order=order, launch=gemm_launch)
+    Y = repops.layernorm_rows(H2, gamma, beta, eps=eps, order=order)
+    if keep:
+        return {"H1": H1, "G": G, "H2": H2, "Y": Y}
+    return Y
+
+
+def attention_scale(head_dim: int) -> float:
+    """The binary32 value nearest 1/sqrt(head_dim) (exact for powers of 4)."""
+    return float(torch.tensor(1.0 / math.sqrt(head_dim), dtype=torch.float32).item())
+
+
+def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_launch=None,
+                      keep=False, buffers=None):
+    """Causal multi-head self-attention, fp32:
+        Q, K, V = X Wq, X Wk, X Wv            [batch*seq, d]
+        S[b,h]  = alpha * Q_h K_h^T            (bmm reading Q, K in place)
+        P       = causal row softmax of S
+        O_h     = P[b,h] V_h                   (written in place into [batch*seq, d])
+        out     = O Wo
+    Heads are column blocks of width d/heads of the projections."""
+    d = X.shape[1]
+    hd = d // heads
+    alpha = attention_scale(hd)
+    bufs = buffers or {}
+    Q = repops.matmul(X, Wq, order=order, launch=gemm_launch, out=bufs.get("Q"))
+    K = repops.matmul(X, Wk, order=order, launch=gemm_launch, out=bufs.get("K"))
+    V = repops.matmul(X, Wv, order=order, launch=gemm_launch, out=bufs.get("V"))
+    S = bufs.get("S")
+    if S is None:
+        S = torch.empty((batch, heads, seq, seq), dtype=torch.float32, device=X.device)
+    # S[b,h] = Q[b*seq:(b+1)*seq, h*hd:(h+1)*hd] . K[...]^T
+    repops.bmm_raw(batch, heads, seq, seq, hd,
+                   Q, seq * d, hd, d, 0,
+                   K, seq * d, hd, d, 1, alpha,
+                   S, heads * seq * seq, seq * seq, seq, order=order, launch=gemm_launch)
+    P = repops.softmax_rows(S.view(batch * heads * seq, seq), causal_period=seq, order=order,
+                            out=bufs.get("P"))
+    O = bufs.get("O")
+    if O is None:
+        O = torch.empty((batch * seq, d), dtype=torch.float32, device=X.device)
+    repops.bmm_raw(batch, heads, seq, hd, seq,
+                   P, heads * seq * seq, seq * seq, seq, 0,
+                   V, seq * d, hd, d, 0, 1.0,
+                   O, seq * d, hd, d, order=order, launch=gemm_launch)
+    out = repops.matmul(O, Wo, order=order, launch=gemm_launch, out=bufs.get("out"))
+    if keep:
+        return {"Q": Q, "K": K, "V": V, "S": S, "P": P, "O": O, "out": out}
+    return out
+
+
+def linear_backward(X, dY, W, order=None, gemm_launch=None, out_dx=None, out_dw=None):
+    """Gradients of Y = X W: dX = dY W^T (contraction over the output
+    features) and dW = X^T dY (contraction over the tokens)."""
+    dX = repops.matmul(dY, W.t(), order=order, launch=gemm_launch, out=out_dx)
+    dW = repops.matmul(X.t(), dY, order=order, launch=gemm_launch, out=out_dw)
+    return dX, dW

@@ -1,0 +1,304 @@
+"""Python binding of librepops (ctypes over the C ABI in include/repops.h).
+
+Argument marshalling only: every step of every operator runs in the HIP
+kernels of librepops.so.  torch supplies device memory (``data_ptr``) and the
+current HIP stream; nothing here computes on tensor values.  If the library is
+missing, every call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librepops.so")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_STRIDE, ERR_ALIAS, ERR_ORDER, ERR_LAUNCH, ERR_HIP = range(8)
+K_FMA, K_MUL_ADD = 0, 1
+ROW_STRIDED_TREE, ROW_BLOCKED_LTR = 0, 1
+LAUNCH_AUTO = 0
+LAUNCH_GEMM_SIMPLE, LAUNCH_GEMM_TILED, LAUNCH_GEMM_MFMA = 1, 2, 3
+LAUNCH_ROWS_GENERIC, LAUNCH_ROWS_WAVE = 1, 2
+LAUNCH_ELEMENTWISE = 1
+
+
+class OrderT(ctypes.Structure):
+    _fields_ = [("version", ctypes.c_uint32), ("k_block", ctypes.c_uint32),
+                ("k_inner", ctypes.c_uint32), ("k_combine", ctypes.c_uint32),
+                ("row_width", ctypes.c_uint32), ("row_combine", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32 * 2)]
+
+
+class LaunchT(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_uint32), ("p", ctypes.c_uint32 * 7)]
+
+
+@dataclass(frozen=True)
+class Order:
+    """Canonical-order descriptor (selects the bits)."""
+    k_block: int = 64
+    k_inner: int = K_FMA
+    row_width: int = 64
+    row_combine: int = ROW_STRIDED_TREE
+    version: int = 1
+    k_combine: int = 0
+
+    def c(self) -> OrderT:
+        o = OrderT()
+        o.version, o.k_block, o.k_inner = self.version, self.k_block, self.k_inner
+        o.k_combine, o.row_width, o.row_combine = self.k_combine, self.row_width, self.row_combine
+        return o
+
+
+@dataclass(frozen=True)
+class Launch:
+    """Launch descriptor (selects the speed only)."""
+    kind: int = LAUNCH_AUTO
+    p: tuple = field(default_factory=tuple)
+
+    def c(self) -> LaunchT:
+        l = LaunchT()
+        l.kind = self.kind
+        for i, v in enumerate(self.p):
+            l.p[i] = v
+        return l
+
+
+class RepopsError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {status_str(code)} (code {code})")
+
+
+_lib = None
+_i64, _i32, _u32, _f32, _vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_void_p
+_op, _lp = ctypes.POINTER(OrderT), ctypes.POINTER(LaunchT)
+
+_SIGNATURES = {
+    "repops_order_default": (None, [_op]),
+    "repops_status_str": (ctypes.c_char_p, [_i32]),
+    "repops_abi_version": (_u32, []),
+    "repops_gemm_config_count": (_i32, [_u32]),
+    "repops_gemm_config_name": (ctypes.c_char_p, [_u32, _u32]),
+    "repops_matmul": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp, _vp,
+                             _i64, _lp, _vp]),
+    "repops_bmm": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
+                          _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _lp, _vp]),
+    "repops_softmax_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _lp, _vp]),
+    "repops_layernorm_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _vp, _f32, _vp, _i64, _vp,
+                                     _vp, _lp, _vp]),
+    "repops_gelu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_exp": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+}
+EXPORTS = tuple(_SIGNATURES)
+
+
+def load(path: str | None = None):
+    """Load librepops.so (built in-tree by ``paper_2502_19405_amd.build``)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"librepops.so not found at {p}: build it with "
+                           "`python -m paper_2502_19405_amd.build` (no fallback exists)")
+    lib = ctypes.CDLL(p)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_str(code: int) -> str:
+    return load().repops_status_str(code).decode()
+
+
+def abi_version() -> int:
+    return load().repops_abi_version()
+
+
+def gemm_configs(kind: int = LAUNCH_GEMM_TILED) -> list[str]:
+    lib = load()
+    return [lib.repops_gemm_config_name(kind, i).decode()
+            for i in range(lib.repops_gemm_config_count(kind))]
+
+
+_DEFAULT_ORDER = Order()
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise RepopsError(rc, what)
+
+
+def _dev(t: torch.Tensor, name: str):
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+    if not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    return t.data_ptr()
+
+
+def _stream(t: torch.Tensor):
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _mat(t: torch.Tensor, name: str):
+    """(pointer, rows, cols, ld, transposed) of a 2-D tensor with unit stride in
+    one dimension: a row-major view, or the transpose of one."""
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    r, c = t.shape
+    s0, s1 = t.stride()
+    if t.numel() == 0:
+        return t.data_ptr(), r, c, max(c, 1), 0
+    if s1 == 1 and (s0 >= max(c, 1) or r <= 1):
+        return _dev(t, name), r, c, max(s0, c, 1), 0
+    if s0 == 1 and (s1 >= max(r, 1) or c <= 1):
+        return _dev(t, name), r, c, max(s1, r, 1), 1
+    raise ValueError(f"{name}: needs unit stride along one dimension (got strides {t.stride()})")
+
+
+def _launch(launch):
+    return None if launch is None else ctypes.byref(launch.c())
+
+
+def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
+           order: Order | None = None, launch: Launch | None = None,
+           out: torch.Tensor | None = None) -> torch.Tensor:
+    """C = A @ B (+ bias).  A [m,k] and B [k,n] may be row-major or transposed
+    views (``x.t()`` of a row-major tensor); out must be row-major."""
+    pa, m, k, lda, ta = _mat(A, "A")
+    pb, k2, n, ldb, tb = _mat(B, "B")
+    if k != k2:
+        raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    if out.shape != (m, n) or out.stride(1) != 1:
+        raise ValueError("out must be a row-major [m, n] tensor")
+    pbias = None
+    if bias is not None:
+        if bias.shape != (n,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous [n] tensor")
+        pbias = _dev(bias, "bias")
+    rc = load().repops_matmul(ctypes.byref((order or _DEFAULT_ORDER).c()), m, n, k, pa, lda, ta,
+                              pb, ldb, tb, pbias, _dev(out, "out"), max(out.stride(0), n, 1),
+                              _launch(launch), _stream(out))
+    _check(rc, "repops_matmul")
+    return out
+
+
+def bmm_raw(batch0: int, batch1: int, m: int, n: int, k: int,
+            A: torch.Tensor, sa0: int, sa1: int, lda: int, trans_a: int,
+            B: torch.Tensor, sb0: int, sb1: int, ldb: int, trans_b: int, alpha: float,
+            C: torch.Tensor, sc0: int, sc1: int, ldc: int,
+            a_offset: int = 0, b_offset: int = 0, c_offset: int = 0,
+            order: Order | None = None, launch: Launch | None = None):
+    """The C-ABI bmm on raw element strides over the storage of A, B, C
+    (offsets in elements from each tensor's data pointer)."""
+    rc = load().repops_bmm(ctypes.byref((order or _DEFAULT_ORDER).c()), batch0, batch1, m, n, k,
+                           _dev(A, "A") + 4 * a_offset, sa0, sa1, lda, trans_a,
+                           _dev(B, "B") + 4 * b_offset, sb0, sb1, ldb, trans_b, alpha,
+                           _dev(C, "C") + 4 * c_offset, sc0, sc1, ldc, _launch(launch), _stream(C))
+    _check(rc, "repops_bmm")
+    return C
+
+
+def bmm(A: torch.Tensor, B: torch.Tensor, alpha: float = 1.0, order: Order | None = None,
+        launch: Launch | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """C[b0,b1] = alpha * A[b0,b1] @ B[b0,b1] for 4-D tensors [b0, b1, r, c]
+    whose last two dimensions are row-major or transposed views."""
+    if A.dim() != 4 or B.dim() != 4:
+        raise ValueError("bmm takes 4-D tensors [batch0, batch1, rows, cols]")
+    b0, b1 = A.shape[:2]
+    if tuple(B.shape[:2]) != (b0, b1):
+        raise ValueError("batch dimensions differ")
+    _, m, k, lda, ta = _mat(A[0, 0], "A")
+    _, k2, n, ldb, tb = _mat(B[0, 0], "B")
+    if k != k2:
+        raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+    if out is None:
+        out = torch.empty((b0, b1, m, n), dtype=torch.float32, device=A.device)
+    if out.stride(3) != 1:
+        raise ValueError("out must be row-major in its last two dimensions")
+    rc = load().repops_bmm(ctypes.byref((order or _DEFAULT_ORDER).c()), b0, b1, m, n, k,
+                           _dev(A, "A"), A.stride(0), A.stride(1), lda, ta,
+                           _dev(B, "B"), B.stride(0), B.stride(1), ldb, tb, float(alpha),
+                           _dev(out, "out"), out.stride(0), out.stride(1),
+                           max(out.stride(2), n, 1), _launch(launch), _stream(out))
+    _check(rc, "repops_bmm")
+    return out
+
+
+def _rows(X: torch.Tensor, name: str):
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D tensor with unit column stride")
+    return X.shape[0], X.shape[1], max(X.stride(0), X.shape[1], 1)
+
+
+def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = None,
+                 launch: Launch | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    rows, cols, ldx = _rows(X, "X")
+    if out is None:
+        out = torch.empty_like(X, memory_format=torch.contiguous_format)
+    _, _, ldy = _rows(out, "out")
+    rc = load().repops_softmax_rows(ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols,
+                                    _dev(X, "X"), ldx, _dev(out, "out"), ldy, causal_period,
+                                    _launch(launch), _stream(out))
+    _check(rc, "repops_softmax_rows")
+    return out
+
+
+def layernorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None,
+                   beta: torch.Tensor | None = None, eps: float = 1e-5,
+                   order: Order | None = None, launch: Launch | None = None,
+                   out: torch.Tensor | None = None, mean_out: torch.Tensor | None = None,
+                   rstd_out: torch.Tensor | None = None) -> torch.Tensor:
+    rows, cols, ldx = _rows(X, "X")
+    if out is None:
+        out = torch.empty_like(X, memory_format=torch.contiguous_format)
+    _, _, ldy = _rows(out, "out")
+    ptrs = []
+    for t, name, size in ((gamma, "gamma", cols), (beta, "beta", cols), (mean_out, "mean_out", rows),
+                          (rstd_out, "rstd_out", rows)):
+        if t is None:
+            ptrs.append(None)
+            continue
+        if t.numel() != size or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [{size}] tensor")
+        ptrs.append(_dev(t, name))
+    rc = load().repops_layernorm_rows(ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols,
+                                      _dev(X, "X"), ldx, ptrs[0], ptrs[1], float(eps),
+                                      _dev(out, "out"), ldy, ptrs[2], ptrs[3], _launch(launch),
+                                      _stream(out))
+    _check(rc, "repops_layernorm_rows")
+    return out
+
+
+def _elementwise(fn_name: str, X: torch.Tensor, order, launch, out):
+    if not X.is_contiguous():
+        raise ValueError("X must be contiguous")
+    if out is None:
+        out = torch.empty_like(X)
+    if not out.is_contiguous() or out.numel() != X.numel():
+        raise ValueError("out must be contiguous with X's element count")
+    rc = getattr(load(), fn_name)(ctypes.byref((order or _DEFAULT_ORDER).c()), X.numel(),
+                                  _dev(X, "X"), _dev(out, "out"), _launch(launch), _stream(out))
+    _check(rc, fn_name)
+    return out
+
+
+def gelu(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    return _elementwise("repops_gelu", X, order, launch, out)
+
+
+def exp(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+        out: torch.Tensor | None = None) -> torch.Tensor:
+    return _elementwise("repops_exp", X, order, launch, out)

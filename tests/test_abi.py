@@ -1,0 +1,166 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/repops.h declares, and rejects bad arguments before anything is
+launched (every call here fails validation, so no kernel is ever enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "repops.h")
+LIB = os.path.join(ROOT, "paper_2502_19405_amd", "librepops.so")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(repops_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def rp():
+    if not os.path.exists(LIB):
+        pytest.fail("librepops.so is not built (run __graft_entry__.build())")
+    from paper_2502_19405_amd import repops
+    return repops
+
+
+def test_header_declares_the_operator_calls():
+    names = declared_functions()
+    for fn in ("repops_matmul", "repops_bmm", "repops_softmax_rows", "repops_layernorm_rows",
+               "repops_gelu", "repops_exp", "repops_order_default"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_function(rp):
+    lib = ctypes.CDLL(LIB)
+    missing = [fn for fn in declared_functions() if not hasattr(lib, fn)]
+    assert not missing, missing
+    assert set(declared_functions()) == set(rp.EXPORTS)
+
+
+def test_version_default_order_and_status_strings(rp):
+    lib = rp.load()
+    assert lib.repops_abi_version() == 1
+    o = rp.OrderT()
+    lib.repops_order_default(ctypes.byref(o))
+    assert (o.version, o.k_block, o.k_inner, o.k_combine, o.row_width, o.row_combine) == (
+        1, 64, 0, 0, 64, 0)
+    assert list(o.reserved) == [0, 0]
+    assert rp.status_str(rp.OK) == "ok"
+    assert "order" in rp.status_str(rp.ERR_ORDER)
+    assert rp.status_str(99) == "unknown status"
+
+
+def test_gemm_config_tables(rp):
+    tiled = rp.gemm_configs(rp.LAUNCH_GEMM_TILED)
+    assert len(tiled) >= 3
+    assert all(re.match(r"\d+x\d+x\d+/", n) for n in tiled)
+    lib = rp.load()
+    assert lib.repops_gemm_config_name(rp.LAUNCH_GEMM_TILED, len(tiled)) is None
+    assert lib.repops_gemm_config_count(99) == 0
+
+
+FAKE_A, FAKE_B, FAKE_C = 0x100000, 0x200000, 0x300000  # never dereferenced
+
+# The calls below pass fake device addresses and must all fail validation.  A
+# validation bug would let one reach a kernel launch, so they only run where no
+# GPU is present (on a GPU host the launch would read unmapped memory).
+no_gpu_only = pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                                 reason="fake-pointer validation tests run only without a GPU")
+
+
+def _order(**kw):
+    from paper_2502_19405_amd.repops import Order
+    return ctypes.byref(Order(**kw).c())
+
+
+def _matmul(rp, order=None, m=4, n=4, k=4, A=FAKE_A, lda=4, ta=0, B=FAKE_B, ldb=4, tb=0,
+            bias=None, C=FAKE_C, ldc=4, launch=None):
+    return rp.load().repops_matmul(order or _order(), m, n, k, A, lda, ta, B, ldb, tb, bias, C,
+                                   ldc, launch, None)
+
+
+@no_gpu_only
+def test_matmul_rejections(rp):
+    assert _matmul(rp, m=-1) == rp.ERR_SHAPE
+    assert _matmul(rp, C=None) == rp.ERR_NULL
+    assert _matmul(rp, A=None) == rp.ERR_NULL
+    assert _matmul(rp, lda=3) == rp.ERR_STRIDE
+    assert _matmul(rp, ldc=3) == rp.ERR_STRIDE
+    assert _matmul(rp, ta=2) == rp.ERR_SHAPE
+    assert _matmul(rp, C=FAKE_A + 8) == rp.ERR_ALIAS
+    assert _matmul(rp, bias=FAKE_C + 4) == rp.ERR_ALIAS
+    assert _matmul(rp, order=_order(version=2)) == rp.ERR_ORDER
+    assert _matmul(rp, order=_order(k_inner=2)) == rp.ERR_ORDER
+    assert _matmul(rp, order=_order(k_combine=1)) == rp.ERR_ORDER
+    assert _matmul(rp, order=_order(row_width=48)) == rp.ERR_ORDER
+    bad = rp.OrderT()
+    rp.load().repops_order_default(ctypes.byref(bad))
+    bad.reserved[1] = 1
+    assert _matmul(rp, order=ctypes.byref(bad)) == rp.ERR_ORDER
+    assert rp.load().repops_matmul(None, 4, 4, 4, FAKE_A, 4, 0, FAKE_B, 4, 0, None, FAKE_C, 4,
+                                   None, None) == rp.ERR_ORDER
+    # launch descriptors: unknown kind, out-of-table index, block length the tile cannot take
+    L = rp.Launch
+    assert _matmul(rp, launch=ctypes.byref(L(7).c())) == rp.ERR_LAUNCH
+    assert _matmul(rp, launch=ctypes.byref(L(rp.LAUNCH_GEMM_TILED, (99,)).c())) == rp.ERR_LAUNCH
+    assert _matmul(rp, launch=ctypes.byref(L(rp.LAUNCH_GEMM_SIMPLE, (1,)).c())) == rp.ERR_LAUNCH
+    assert _matmul(rp, order=_order(k_block=24),
+                   launch=ctypes.byref(L(rp.LAUNCH_GEMM_TILED, (0,)).c())) == rp.ERR_LAUNCH
+
+
+@no_gpu_only
+def test_matmul_zero_sized_is_a_noop(rp):
+    # nothing to write: succeeds without touching any pointer or the device
+    assert _matmul(rp, m=0, A=None, B=None, C=None) == rp.OK
+    assert _matmul(rp, n=0, A=None, B=None, C=None) == rp.OK
+
+
+@no_gpu_only
+def test_bmm_rejections(rp):
+    lib = rp.load()
+
+    def call(**kw):
+        args = dict(b0=2, b1=3, m=4, n=4, k=4, A=FAKE_A, sa0=48, sa1=16, lda=4, ta=0, B=FAKE_B,
+                    sb0=48, sb1=16, ldb=4, tb=0, alpha=1.0, C=FAKE_C, sc0=48, sc1=16, ldc=4)
+        args.update(kw)
+        return lib.repops_bmm(_order(), *args.values(), None, None)
+
+    assert call(b0=-1) == rp.ERR_SHAPE
+    # A spans elements [0, 48 + 2*16 + 3*4 + 4) = [0, 96): C starting at 90 overlaps it
+    assert call(C=FAKE_A + 4 * 90) == rp.ERR_ALIAS
+    assert call(ldb=3) == rp.ERR_STRIDE
+    assert call(b1=0, A=None, B=None, C=None) == rp.OK
+
+
+@no_gpu_only
+def test_rows_and_elementwise_rejections(rp):
+    lib = rp.load()
+    o = _order()
+    assert lib.repops_softmax_rows(o, 4, 8, FAKE_A, 7, FAKE_C, 8, 0, None, None) == rp.ERR_STRIDE
+    assert lib.repops_softmax_rows(o, 4, 8, FAKE_A, 8, FAKE_A + 4, 8, 0, None, None) == rp.ERR_ALIAS
+    assert lib.repops_softmax_rows(o, 4, 8, FAKE_A, 8, FAKE_C, 8, -1, None, None) == rp.ERR_SHAPE
+    assert lib.repops_softmax_rows(o, 0, 8, None, 8, None, 8, 0, None, None) == rp.OK
+    wave = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (3,)).c())
+    assert lib.repops_softmax_rows(o, 4, 8, FAKE_A, 8, FAKE_C, 8, 0, wave, None) == rp.ERR_LAUNCH
+    wave4 = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (4,)).c())
+    assert lib.repops_softmax_rows(_order(row_width=32), 4, 8, FAKE_A, 8, FAKE_C, 8, 0, wave4,
+                                   None) == rp.ERR_LAUNCH
+    assert lib.repops_layernorm_rows(o, 4, 0, FAKE_A, 8, None, None, 1e-5, FAKE_C, 8, None, None,
+                                     None, None) == rp.ERR_SHAPE
+    assert lib.repops_layernorm_rows(o, 4, 8, FAKE_A, 8, FAKE_C + 4, None, 1e-5, FAKE_C, 8, None,
+                                     None, None, None) == rp.ERR_ALIAS
+    assert lib.repops_gelu(o, -1, FAKE_A, FAKE_C, None, None) == rp.ERR_SHAPE
+    assert lib.repops_gelu(o, 8, FAKE_A, FAKE_A + 4, None, None) == rp.ERR_ALIAS
+    assert lib.repops_exp(o, 8, None, FAKE_C, None, None) == rp.ERR_NULL
+    ew = ctypes.byref(rp.Launch(rp.LAUNCH_ELEMENTWISE, (100,)).c())
+    assert lib.repops_exp(o, 8, FAKE_A, FAKE_C, ew, None) == rp.ERR_LAUNCH
+    assert lib.repops_exp(o, 0, None, None, None, None) == rp.OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    from paper_2502_19405_amd import repops
+    with pytest.raises(RuntimeError, match="not found"):
+        repops.load(str(tmp_path / "missing.so"))

@@ -1,0 +1,191 @@
+"""GPU parity of repops_matmul / repops_bmm against the CPU oracle (0 ULP).
+
+Small and ragged shapes are compared on every output; every launch
+configuration (simple, each tiled table entry) must give the same bits, under
+every transposition and order descriptor the configuration accepts.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from bitcmp import assert_bits_equal
+from gpu_util import announce, dev, host, same_bits
+from paper_2502_19405_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "order_witnesses.json")
+
+
+@pytest.fixture(scope="module")
+def rp():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    from paper_2502_19405_amd import repops
+    repops.load()
+    return repops
+
+
+def launches(rp, k_block=64, fused=True):
+    """Every launch configuration that accepts this order descriptor."""
+    out = [("simple", rp.Launch(rp.LAUNCH_GEMM_SIMPLE))]
+    for idx, name in enumerate(rp.gemm_configs(rp.LAUNCH_GEMM_TILED)):
+        bk = int(name.split("/")[0].split("x")[2])
+        if k_block == 0 or k_block % bk == 0:
+            out.append((f"tiled{idx}:{name}", rp.Launch(rp.LAUNCH_GEMM_TILED, (idx,))))
+    if fused:
+        for idx, name in enumerate(rp.gemm_configs(rp.LAUNCH_GEMM_MFMA)):
+            bk = int(name.split("/")[0].split("x")[2])
+            if k_block == 0 or k_block % bk == 0:
+                out.append((f"mfma{idx}:{name}", rp.Launch(rp.LAUNCH_GEMM_MFMA, (idx,))))
+    return out
+
+
+SHAPES = [(1, 1, 1), (7, 5, 3), (33, 17, 64), (65, 70, 130), (129, 257, 100), (200, 131, 333),
+          (64, 64, 0)]
+ORDERS = [(64, 0), (0, 0), (128, 0), (64, 1), (32, 1)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("k_block,k_inner", ORDERS)
+def test_matmul_small_all_launches(rp, shape, k_block, k_inner):
+    m, n, k = shape
+    g = inputs.rng(m + 3 * n + 7 * k + k_block + k_inner)
+    A = inputs.normal(g, (m, k))
+    B = inputs.normal(g, (k, n))
+    bias = inputs.uniform(g, (n,), -0.1, 0.1)
+    want = oracle.matmul(A, B, bias, k_block=k_block, k_inner=k_inner)
+    want_t = oracle.matmul(np.ascontiguousarray(A.T), np.ascontiguousarray(B.T), bias,
+                           trans_a=True, trans_b=True, k_block=k_block, k_inner=k_inner)
+    assert_bits_equal(want_t, want, "oracle layout invariance")
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    dA, dB, dbias = dev(A), dev(B), dev(bias)
+    dAt, dBt = dev(np.ascontiguousarray(A.T)), dev(np.ascontiguousarray(B.T))
+    for name, launch in launches(rp, k_block, k_inner == 0):
+        announce("matmul", shape, k_block, k_inner, name)
+        got = rp.matmul(dA, dB, dbias, order=order, launch=launch)
+        assert_bits_equal(host(got), want, f"{name} {shape}")
+        for ta, tb in ((1, 0), (0, 1), (1, 1)):
+            a = dAt.t() if ta else dA
+            b = dBt.t() if tb else dB
+            got_t = rp.matmul(a, b, dbias, order=order, launch=launch)
+            assert_bits_equal(host(got_t), want, f"{name} trans {ta}{tb}")
+
+
+def test_matmul_witnesses_on_gpu(rp):
+    """The hand-derived order witnesses, through every launch configuration."""
+    ws = {w["name"]: w for w in json.load(open(GOLDEN))["witnesses"]}
+
+    def vec(spec, n):
+        v = np.zeros(n, np.float32)
+        for key, val in spec.items():
+            lo, hi = (map(int, key.split(":")) if ":" in key else (int(key), int(key) + 1))
+            v[lo:hi] = np.float32(float.fromhex(val))
+        return v
+
+    w1, w2, w3 = ws["W1_blocked_vs_sequential"], ws["W2_left_to_right_vs_pairwise"], ws["W3_fused_vs_unfused"]
+    cases = [
+        (vec(w1["a_nonzero"], 128), np.ones(128, np.float32), 64, 0, w1["expect"]),
+        (vec(w1["a_nonzero"], 128), np.ones(128, np.float32), 0, 0, w1["wrong_order"]["expect"]),
+        (vec(w2["a_nonzero"], 256), np.ones(256, np.float32), 64, 0, w2["expect"]),
+        (np.array([float.fromhex(s) for s in w3["a"]], np.float32),
+         np.array([float.fromhex(s) for s in w3["b"]], np.float32), 64, 0, w3["expect_fma"]),
+        (np.array([float.fromhex(s) for s in w3["a"]], np.float32),
+         np.array([float.fromhex(s) for s in w3["b"]], np.float32), 64, 1, w3["expect_mul_add"]),
+    ]
+    for a, b, kb, ki, expect in cases:
+        # replicate the witness over a 70 x 70 output so every tile position sees it
+        A = np.tile(a, (70, 1)).astype(np.float32)
+        B = np.tile(b[:, None], (1, 70)).astype(np.float32)
+        want = np.float32(float.fromhex(expect))
+        for name, launch in launches(rp, kb, ki == 0):
+            announce("witness", kb, ki, name)
+            got = host(rp.matmul(dev(A), dev(B), order=rp.Order(k_block=kb, k_inner=ki),
+                                 launch=launch))
+            assert (got.view(np.uint32) == want.view(np.uint32)).all(), (name, expect)
+
+
+def test_matmul_integer_exact_and_bias_null(rp):
+    d = inputs.gemm2048_int(n=512)
+    exact = d["A"].astype(np.float64) @ d["B"].astype(np.float64)
+    for name, launch in launches(rp):
+        announce("int512", name)
+        got = host(rp.matmul(dev(d["A"]), dev(d["B"]), dev(d["bias"]), launch=launch))
+        assert np.array_equal(got, (exact + d["bias"]).astype(np.float32)), name
+        got0 = host(rp.matmul(dev(d["A"]), dev(d["B"]), None, launch=launch))
+        assert np.array_equal(got0, exact.astype(np.float32)), name
+
+
+def test_matmul_k_zero_gives_bias_or_plus_zero(rp):
+    import torch
+    A = torch.empty((5, 0), device="cuda:0")
+    B = torch.empty((0, 6), device="cuda:0")
+    bias = dev(np.arange(6, dtype=np.float32) - 2.5)
+    announce("k=0")
+    got = host(rp.matmul(A, B))
+    assert (got.view(np.uint32) == 0).all()
+    got_b = host(rp.matmul(A, B, bias))
+    assert_bits_equal(got_b, np.broadcast_to(host(bias), (5, 6)), "k=0 bias")
+
+
+def test_matmul_padded_leading_dimensions(rp):
+    import torch
+    g = inputs.rng(77)
+    m, n, k = 45, 37, 150
+    A = inputs.normal(g, (m, k)); B = inputs.normal(g, (k, n))
+    want = oracle.matmul(A, B)
+    Ap = torch.zeros((m, k + 9), device="cuda:0"); Ap[:, :k] = dev(A)
+    Bp = torch.zeros((k, n + 5), device="cuda:0"); Bp[:, :n] = dev(B)
+    Cp = torch.full((m, n + 3), float("nan"), device="cuda:0")
+    for name, launch in launches(rp):
+        announce("padded", name)
+        rp.matmul(Ap[:, :k], Bp[:, :n], launch=launch, out=Cp[:, :n])
+        got = host(Cp)
+        assert_bits_equal(got[:, :n], want, name)
+        assert np.isnan(got[:, n:]).all()
+
+
+def test_bmm_batches_and_alpha(rp):
+    g = inputs.rng(78)
+    A = inputs.normal(g, (2, 3, 70, 130))
+    B = inputs.normal(g, (2, 3, 130, 45))
+    alpha = np.float32(1 / math.sqrt(128))
+    want = oracle.bmm(A, B, alpha=alpha)
+    for name, launch in launches(rp):
+        announce("bmm", name)
+        got = host(rp.bmm(dev(A), dev(B), alpha=float(alpha), launch=launch))
+        assert_bits_equal(got, want, name)
+        # transposed operands (views) give the same bits
+        At = dev(np.ascontiguousarray(A.transpose(0, 1, 3, 2))).transpose(2, 3)
+        Bt = dev(np.ascontiguousarray(B.transpose(0, 1, 3, 2))).transpose(2, 3)
+        got_t = host(rp.bmm(At, Bt, alpha=float(alpha), launch=launch))
+        assert_bits_equal(got_t, want, name + " transposed")
+
+
+def test_bmm_batch_one_equals_matmul_and_loop(rp):
+    g = inputs.rng(79)
+    A = inputs.normal(g, (1, 1, 90, 200))
+    B = inputs.normal(g, (1, 1, 200, 66))
+    dA, dB = dev(A), dev(B)
+    announce("bmm batch 1 vs matmul")
+    assert same_bits(rp.bmm(dA, dB)[0, 0], rp.matmul(dA[0, 0], dB[0, 0]))
+
+
+def test_determinism_run_to_run_and_streams(rp):
+    import torch
+    g = inputs.rng(80)
+    A = dev(inputs.normal(g, (300, 500)))
+    B = dev(inputs.normal(g, (500, 400)))
+    announce("determinism")
+    first = rp.matmul(A, B)
+    for _ in range(3):
+        assert same_bits(rp.matmul(A, B), first)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        other = rp.matmul(A, B)
+    s.synchronize()
+    assert same_bits(other, first)
