@@ -80,14 +80,22 @@ repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_
   auto tiled_ok = [&](const repops::GemmConfig* c) {
     return c && (g.k_block == 0 || g.k_block % c->bk == 0);
   };
+  auto mfma_ok = [&](const repops::GemmConfig* c) {
+    return c && g.fused && (g.k_block == 0 || g.k_block % c->bk == 0);
+  };
   if (kind == REPOPS_LAUNCH_AUTO) {
-    // Largest tile for big outputs, the small tile otherwise; the simple path
-    // for block lengths no tile divides.
+    // Matrix cores for the fused order (their single-term updates are the fma
+    // chain), the large tile for big outputs; vector tiles for the unfused
+    // order; the simple path for block lengths no tile divides.
     const int64_t outputs = g.m * g.n * g.batch0 * g.batch1;
-    const int preferred = outputs >= int64_t(1) << 22 ? 1 : 0;
-    if (tiled_ok(repops::gemm_tiled_config(preferred))) {
+    const int mfma_pref = outputs >= (int64_t(1) << 20) ? 0 : 3;
+    const int tiled_pref = outputs >= (int64_t(1) << 22) ? 1 : 0;
+    if (mfma_ok(repops::gemm_mfma_config(mfma_pref))) {
+      kind = REPOPS_LAUNCH_GEMM_MFMA;
+      index = mfma_pref;
+    } else if (tiled_ok(repops::gemm_tiled_config(tiled_pref))) {
       kind = REPOPS_LAUNCH_GEMM_TILED;
-      index = preferred;
+      index = tiled_pref;
     } else if (tiled_ok(repops::gemm_tiled_config(0))) {
       kind = REPOPS_LAUNCH_GEMM_TILED;
       index = 0;
@@ -101,8 +109,7 @@ repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_
     return hip_status(repops::launch_gemm_tiled(g, static_cast<int>(index), stream));
   }
   // matrix-core path
-  const repops::GemmConfig* c = repops::gemm_mfma_config(static_cast<int>(index));
-  if (!c || !g.fused || (g.k_block != 0 && g.k_block % c->bk != 0)) return REPOPS_ERR_LAUNCH;
+  if (!mfma_ok(repops::gemm_mfma_config(static_cast<int>(index)))) return REPOPS_ERR_LAUNCH;
   return hip_status(repops::launch_gemm_mfma(g, static_cast<int>(index), stream));
 }
 

@@ -253,10 +253,3 @@ hipError_t launch_gemm_tiled(const GemmArgs& g, int index, hipStream_t s) {
 
 }  // namespace repops
 
-namespace repops {
-// No matrix-core configuration is compiled in yet: the table is empty and the
-// MFMA launch kind is rejected by the ABI layer.
-int gemm_mfma_count() { return 0; }
-const GemmConfig* gemm_mfma_config(int) { return nullptr; }
-hipError_t launch_gemm_mfma(const GemmArgs&, int, hipStream_t) { return hipErrorInvalidValue; }
-}  // namespace repops

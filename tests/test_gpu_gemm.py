@@ -1,8 +1,9 @@
 """GPU parity of repops_matmul / repops_bmm against the CPU oracle (0 ULP).
 
 Small and ragged shapes are compared on every output; every launch
-configuration (simple, each tiled table entry) must give the same bits, under
-every transposition and order descriptor the configuration accepts.
+configuration (simple, each vector-tiled and each matrix-core table entry)
+must give the same bits, under every transposition and order descriptor the
+configuration accepts.
 """
 import json
 import math
@@ -189,3 +190,49 @@ def test_determinism_run_to_run_and_streams(rp):
         other = rp.matmul(A, B)
     s.synchronize()
     assert same_bits(other, first)
+
+
+def _adversarial(mode, g, m, n, k):
+    """Operands whose fma chains expose any difference from IEEE fused
+    multiply-add with one rounding and gradual underflow."""
+    A = inputs.normal(g, (m, k))
+    B = inputs.normal(g, (k, n))
+    if mode == "subnormal_products":
+        A = np.ldexp(A, -70).astype(np.float32); B = np.ldexp(B, -70).astype(np.float32)
+    elif mode == "near_min_normal":
+        A = np.ldexp(A, -63).astype(np.float32); B = np.ldexp(B, -62).astype(np.float32)
+    elif mode == "overflow":
+        A = np.ldexp(A, 60).astype(np.float32)
+        B = np.ldexp(B, 60 + g.integers(0, 8, B.shape)).astype(np.float32)
+    elif mode == "fused_witness":
+        a0, a1 = -(1 + 2.0 ** -11), 1 + 2.0 ** -12
+        A = np.where(np.arange(k) % 2 == 0, a0, a1)[None, :].repeat(m, 0).astype(np.float32)
+        A[1::2] *= -1
+        B = np.where(np.arange(k) % 2 == 0, 1.0, a1)[:, None].repeat(n, 1).astype(np.float32)
+    elif mode == "subnormal_inputs":
+        A = (A.view(np.uint32) & np.uint32(0x807FFFFF)).view(np.float32)
+    elif mode == "signed_zeros":
+        A = inputs.integers(g, (m, k), -4, 4); B = inputs.integers(g, (k, n), -4, 4)
+        A[g.random((m, k)) < 0.2] = -0.0
+    elif mode == "ties":
+        A = np.ldexp(A, 20).astype(np.float32); B = np.ldexp(B, -20).astype(np.float32)
+        A[:, ::3] *= -1
+    return np.ascontiguousarray(A, np.float32), np.ascontiguousarray(B, np.float32)
+
+
+@pytest.mark.parametrize("mode", ["normal", "subnormal_products", "near_min_normal", "overflow",
+                                  "fused_witness", "subnormal_inputs", "signed_zeros", "ties"])
+@pytest.mark.parametrize("k_block", [64, 0])
+def test_matrix_core_chain_equals_fma_chain(rp, mode, k_block):
+    """The matrix-core path is allowed only because its single-term updates
+    equal the IEEE fma chain: checked here on operands built to expose any
+    flush of subnormals, double rounding, wrong zero signs or overflow
+    handling, through every launch configuration (matrix-core and vector)."""
+    g = inputs.rng(sum(map(ord, mode)) + k_block)
+    m, n, k = 96, 80, 256
+    A, B = _adversarial(mode, g, m, n, k)
+    want = oracle.matmul(A, B, k_block=k_block)
+    for name, launch in launches(rp, k_block, True):
+        announce("adversarial", mode, k_block, name)
+        got = host(rp.matmul(dev(A), dev(B), order=rp.Order(k_block=k_block), launch=launch))
+        assert_bits_equal(got, want, f"{mode} {name}")
