@@ -56,133 +56,139 @@ __device__ __forceinline__ void tile_coords(int64_t t, int64_t ntiles, int64_t t
   *tn = in_group / gsize;
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmArgs g, int64_t tiles_m,
-                                                                 int64_t tiles_n, int64_t ntiles,
-                                                                 int a_vec, int b_vec) {
-  constexpr int NT = 64 * WM * WN;
-  constexpr int TWM = BM / WM, TWN = BN / WN;  // wave tile
-  constexpr int IM = TWM / 64, IN = TWN / 32;  // instruction tiles per wave
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
+struct MfmaTile {
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int TWM = BM / WM, TWN = BN / WN;  // wave tile
+  static constexpr int IM = TWM / 64, IN = TWN / 32;  // instruction tiles per wave
   static_assert(TWM % 64 == 0 && TWN % 32 == 0, "wave tile must hold whole instruction tiles");
   static_assert(BK % 4 == 0, "k slice must hold whole float4 groups");
-  constexpr int PAD = 4;
-  constexpr int AV = BM * BK / 4 / NT;  // float4 groups per thread and slice
-  constexpr int BV = BK * BN / 4 / NT;
+  static constexpr int PAD = 4;
+  static constexpr int AV = BM * BK / 4 / NT;  // float4 groups per thread and slice
+  static constexpr int BV = BK * BN / 4 / NT;
   static_assert(AV * NT * 4 == BM * BK && BV * NT * 4 == BK * BN, "slice not divisible");
-  __shared__ float As[2][BK][BM + PAD];
-  __shared__ float Bs[2][BK][BN + PAD];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm0 = (wave / WN) * TWM;
-  const int wn0 = (wave % WN) * TWN;
-  const int64_t K = g.k;
-  const int64_t nslices = (K + BK - 1) / BK;
-  const int64_t slices_per_block = g.k_block > 0 ? g.k_block / BK : (nslices > 0 ? nslices : 1);
+  struct Smem {
+    float a[2][BK][BM + PAD];
+    float b[2][BK][BN + PAD];
+  };
 
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    int64_t bz, tm, tn;
-    tile_coords(t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
-    const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
-    const int64_t m0 = tm * BM, n0 = tn * BN;
+  // Coordinates of float4 group q of this thread inside the A / B slice.
+  // Groups run along the stored contiguous dimension: k for row-major A and
+  // for transposed B, m for transposed A, n for row-major B.
+  __device__ static void a_group(int e, int* row, int* kk) {
+    if constexpr (!TA) { *row = e / (BK / 4); *kk = (e % (BK / 4)) * 4; }
+    else { *kk = e / (BM / 4); *row = (e % (BM / 4)) * 4; }
+  }
+  __device__ static void b_group(int e, int* col, int* kk) {
+    if constexpr (!TB) { *kk = e / (BN / 4); *col = (e % (BN / 4)) * 4; }
+    else { *col = e / (BK / 4); *kk = (e % (BK / 4)) * 4; }
+  }
+
+  template <bool EDGE>
+  __device__ static float4 fetch4(const float* p, bool in0, int valid) {
+    // valid: how many of the 4 consecutive elements exist (EDGE only)
+    if constexpr (!EDGE) {
+      return *reinterpret_cast<const float4*>(p);
+    } else {
+      float v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[c] = (in0 && c < valid) ? p[c] : 0.0f;
+      return make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
+
+  template <bool EDGE>
+  __device__ static void load(const GemmArgs& g, const float* A, const float* B, int64_t m0,
+                              int64_t n0, int64_t k0, int tid, float4* ra, float4* rb) {
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      int row, kk;
+      a_group(tid + q * NT, &row, &kk);
+      const int64_t gi = m0 + row, gk = k0 + kk;
+      if constexpr (!TA) {
+        ra[q] = fetch4<EDGE>(A + gi * g.lda + gk, gi < g.m, static_cast<int>(g.k - gk));
+      } else {
+        ra[q] = fetch4<EDGE>(A + gk * g.lda + gi, gk < g.k, static_cast<int>(g.m - gi));
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < BV; ++q) {
+      int col, kk;
+      b_group(tid + q * NT, &col, &kk);
+      const int64_t gj = n0 + col, gk = k0 + kk;
+      if constexpr (!TB) {
+        rb[q] = fetch4<EDGE>(B + gk * g.ldb + gj, gk < g.k, static_cast<int>(g.n - gj));
+      } else {
+        rb[q] = fetch4<EDGE>(B + gj * g.ldb + gk, gj < g.n, static_cast<int>(g.k - gk));
+      }
+    }
+  }
+
+  __device__ static void store(Smem& sm, int buf, int tid, const float4* ra, const float4* rb) {
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      int row, kk;
+      a_group(tid + q * NT, &row, &kk);
+      if constexpr (!TA) {
+        sm.a[buf][kk + 0][row] = ra[q].x;
+        sm.a[buf][kk + 1][row] = ra[q].y;
+        sm.a[buf][kk + 2][row] = ra[q].z;
+        sm.a[buf][kk + 3][row] = ra[q].w;
+      } else {
+        *reinterpret_cast<float4*>(&sm.a[buf][kk][row]) = ra[q];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < BV; ++q) {
+      int col, kk;
+      b_group(tid + q * NT, &col, &kk);
+      if constexpr (!TB) {
+        *reinterpret_cast<float4*>(&sm.b[buf][kk][col]) = rb[q];
+      } else {
+        sm.b[buf][kk + 0][col] = rb[q].x;
+        sm.b[buf][kk + 1][col] = rb[q].y;
+        sm.b[buf][kk + 2][col] = rb[q].z;
+        sm.b[buf][kk + 3][col] = rb[q].w;
+      }
+    }
+  }
+
+  // One BK-deep slice of single-term updates.  FIRST: the slice opens a new
+  // k block, so its first update starts the block partial from +0.
+  template <bool FIRST>
+  __device__ static void slice(const Smem& sm, int buf, int lane, int wm0, int wn0,
+                               v32f (&P)[IM][IN]) {
+    const v32f zero = {};
+#pragma unroll
+    for (int kk = 0; kk < BK; ++kk) {
+      float av[IM], bv[IN];
+#pragma unroll
+      for (int a = 0; a < IM; ++a) av[a] = sm.a[buf][kk][wm0 + a * 64 + lane];
+#pragma unroll
+      for (int b = 0; b < IN; ++b) bv[b] = sm.b[buf][kk][wn0 + b * 32 + (lane & 31)];
+#pragma unroll
+      for (int a = 0; a < IM; ++a)
+#pragma unroll
+        for (int b = 0; b < IN; ++b)
+          P[a][b] = __builtin_amdgcn_mfma_f32_32x32x1f32(
+              av[a], bv[b], (FIRST && kk == 0) ? zero : P[a][b], 0, 0, 0);
+    }
+  }
+
+  template <bool EDGE>
+  __device__ static void run(const GemmArgs& g, Smem& sm, int64_t b0, int64_t b1, int64_t m0,
+                             int64_t n0) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm0 = (wave / WN) * TWM;
+    const int wn0 = (wave % WN) * TWN;
+    const int64_t K = g.k;
+    const int64_t nslices = (K + BK - 1) / BK;
+    const int64_t spb = g.k_block > 0 ? g.k_block / BK : (nslices > 0 ? nslices : 1);
     const float* A = g.A + b0 * g.sa0 + b1 * g.sa1;
     const float* B = g.B + b0 * g.sb0 + b1 * g.sb1;
-
-    float4 ra[AV], rb[BV];
-    // Global -> registers for slice k0.  Element (row, k) of the logical A
-    // lands in As[k][row]; element (k, col) of B in Bs[k][col].  Groups of 4
-    // run along the stored contiguous dimension.
-    auto load = [&](int64_t k0) {
-#pragma unroll
-      for (int q = 0; q < AV; ++q) {
-        const int e = tid + q * NT;
-        float v[4];
-        if (!g.ta) {  // A row-major: groups along k
-          const int i = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-          const int64_t gi = m0 + i, gk = k0 + kq;
-          const float* p = A + gi * g.lda + gk;
-          if (a_vec && gi < g.m && gk + 4 <= K) {
-            const float4 f = *reinterpret_cast<const float4*>(p);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] = (gi < g.m && gk + c < K) ? p[c] : 0.0f;
-          }
-        } else {  // A stored k x m: groups along m
-          const int kk = e / (BM / 4), i = (e % (BM / 4)) * 4;
-          const int64_t gi = m0 + i, gk = k0 + kk;
-          const float* p = A + gk * g.lda + gi;
-          if (a_vec && gk < K && gi + 4 <= g.m) {
-            const float4 f = *reinterpret_cast<const float4*>(p);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] = (gk < K && gi + c < g.m) ? p[c] : 0.0f;
-          }
-        }
-        ra[q] = make_float4(v[0], v[1], v[2], v[3]);
-      }
-#pragma unroll
-      for (int q = 0; q < BV; ++q) {
-        const int e = tid + q * NT;
-        float v[4];
-        if (!g.tb) {  // B row-major: groups along n
-          const int kk = e / (BN / 4), j = (e % (BN / 4)) * 4;
-          const int64_t gj = n0 + j, gk = k0 + kk;
-          const float* p = B + gk * g.ldb + gj;
-          if (b_vec && gk < K && gj + 4 <= g.n) {
-            const float4 f = *reinterpret_cast<const float4*>(p);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] = (gk < K && gj + c < g.n) ? p[c] : 0.0f;
-          }
-        } else {  // B stored n x k: groups along k
-          const int j = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-          const int64_t gj = n0 + j, gk = k0 + kq;
-          const float* p = B + gj * g.ldb + gk;
-          if (b_vec && gj < g.n && gk + 4 <= K) {
-            const float4 f = *reinterpret_cast<const float4*>(p);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] = (gj < g.n && gk + c < K) ? p[c] : 0.0f;
-          }
-        }
-        rb[q] = make_float4(v[0], v[1], v[2], v[3]);
-      }
-    };
-    auto store = [&](int buf) {
-#pragma unroll
-      for (int q = 0; q < AV; ++q) {
-        const int e = tid + q * NT;
-        if (!g.ta) {
-          const int i = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-          As[buf][kq + 0][i] = ra[q].x;
-          As[buf][kq + 1][i] = ra[q].y;
-          As[buf][kq + 2][i] = ra[q].z;
-          As[buf][kq + 3][i] = ra[q].w;
-        } else {
-          const int kk = e / (BM / 4), i = (e % (BM / 4)) * 4;
-          *reinterpret_cast<float4*>(&As[buf][kk][i]) = ra[q];
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < BV; ++q) {
-        const int e = tid + q * NT;
-        if (!g.tb) {
-          const int kk = e / (BN / 4), j = (e % (BN / 4)) * 4;
-          *reinterpret_cast<float4*>(&Bs[buf][kk][j]) = rb[q];
-        } else {
-          const int j = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-          Bs[buf][kq + 0][j] = rb[q].x;
-          Bs[buf][kq + 1][j] = rb[q].y;
-          Bs[buf][kq + 2][j] = rb[q].z;
-          Bs[buf][kq + 3][j] = rb[q].w;
-        }
-      }
-    };
 
     v32f P[IM][IN], acc[IM][IN];
 #pragma unroll
@@ -192,39 +198,25 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmArgs g, int
         P[a][b] = v32f{};
         acc[a][b] = v32f{};
       }
-
+    float4 ra[AV], rb[BV];
     if (nslices > 0) {
-      load(0);
-      store(0);
+      load<EDGE>(g, A, B, m0, n0, 0, tid, ra, rb);
+      store(sm, 0, tid, ra, rb);
     }
     __syncthreads();
     for (int64_t s = 0; s < nslices; ++s) {
       const int cur = static_cast<int>(s & 1);
-      if (s + 1 < nslices) load((s + 1) * BK);
-#pragma unroll
-      for (int kk = 0; kk < BK; ++kk) {
-        float av[IM], bv[IN];
-#pragma unroll
-        for (int a = 0; a < IM; ++a) av[a] = As[cur][kk][wm0 + a * 64 + lane];
-#pragma unroll
-        for (int b = 0; b < IN; ++b) bv[b] = Bs[cur][kk][wn0 + b * 32 + (lane & 31)];
+      if (s + 1 < nslices) load<EDGE>(g, A, B, m0, n0, (s + 1) * BK, tid, ra, rb);
+      if (s % spb == 0) slice<true>(sm, cur, lane, wm0, wn0, P);
+      else slice<false>(sm, cur, lane, wm0, wn0, P);
+      if (s + 1 < nslices) store(sm, cur ^ 1, tid, ra, rb);
+      if ((s + 1) % spb == 0 || s + 1 == nslices) {
 #pragma unroll
         for (int a = 0; a < IM; ++a)
 #pragma unroll
-          for (int b = 0; b < IN; ++b)
-            P[a][b] = __builtin_amdgcn_mfma_f32_32x32x1f32(av[a], bv[b], P[a][b], 0, 0, 0);
+          for (int b = 0; b < IN; ++b) acc[a][b] = acc[a][b] + P[a][b];
       }
-      if (s + 1 < nslices) store(cur ^ 1);
       __syncthreads();
-      if ((s + 1) % slices_per_block == 0 || s + 1 == nslices) {
-#pragma unroll
-        for (int a = 0; a < IM; ++a)
-#pragma unroll
-          for (int b = 0; b < IN; ++b) {
-            acc[a][b] = acc[a][b] + P[a][b];
-            P[a][b] = v32f{};
-          }
-      }
     }
 
     // Accumulator layout of the instruction (lane l, register r): block
@@ -240,27 +232,51 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmArgs g, int
         for (int r = 0; r < 32; ++r) {
           const int row = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t i = m0 + wm0 + a * 64 + row;
-          if (i < g.m && j < g.n) C[i * g.ldc + j] = epilogue(g, acc[a][b][r], j);
+          if (!EDGE || (i < g.m && j < g.n)) C[i * g.ldc + j] = epilogue(g, acc[a][b][r], j);
         }
       }
+  }
+};
+
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmArgs g, int64_t tiles_m,
+                                                                 int64_t tiles_n, int64_t ntiles,
+                                                                 int vec_ok) {
+  using T = MfmaTile<BM, BN, BK, WM, WN, TA, TB>;
+  __shared__ typename T::Smem sm;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int64_t bz, tm, tn;
+    tile_coords(t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
+    const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
+    const int64_t m0 = tm * BM, n0 = tn * BN;
+    // Interior tiles (whole tile inside C, whole k slices, aligned rows) take
+    // the path without per-element checks; the choice is uniform per tile.
+    const bool interior = vec_ok && m0 + BM <= g.m && n0 + BN <= g.n && g.k % BK == 0;
+    if (interior) T::template run<false>(g, sm, b0, b1, m0, n0);
+    else T::template run<true>(g, sm, b0, b1, m0, n0);
+    __syncthreads();
   }
 }
 
 struct MfmaEntry {
   GemmConfig cfg;
   int threads;
-  void (*kernel)(GemmArgs, int64_t, int64_t, int64_t, int, int);
+  void (*kernel[4])(GemmArgs, int64_t, int64_t, int64_t, int);  // [ta * 2 + tb]
 };
 
 #define REPOPS_MFMA(BM, BN, BK, WM, WN)                                                       \
-  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN, BM, BN, BK}, 64 * WM * WN,                          \
-   gemm_mfma_kernel<BM, BN, BK, WM, WN>}
+  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN, BM, BN, BK},                                        \
+   64 * WM * WN,                                                                              \
+   {gemm_mfma_kernel<BM, BN, BK, WM, WN, false, false>,                                       \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, false, true>,                                        \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, true, false>,                                        \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, true, true>}}
 
 const MfmaEntry kMfma[] = {
-    REPOPS_MFMA(128, 128, 16, 2, 2),
-    REPOPS_MFMA(128, 64, 16, 2, 2),
+    REPOPS_MFMA(128, 128, 32, 2, 2),
+    REPOPS_MFMA(128, 64, 32, 2, 2),
     REPOPS_MFMA(256, 128, 16, 4, 2),
-    REPOPS_MFMA(64, 64, 16, 1, 2),
+    REPOPS_MFMA(64, 64, 32, 1, 2),
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
@@ -281,10 +297,10 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
   const int64_t cap = int64_t(1) << 30;
   const unsigned grid = static_cast<unsigned>(ntiles < cap ? ntiles : cap);
   // float4 loads need 16-byte aligned rows and batch origins
-  const int a_vec = aligned16(g.A) && g.lda % 4 == 0 && g.sa0 % 4 == 0 && g.sa1 % 4 == 0;
-  const int b_vec = aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
-  hipLaunchKernelGGL(e.kernel, dim3(grid), dim3(e.threads), 0, s, g, tiles_m, tiles_n, ntiles,
-                     a_vec, b_vec);
+  const int vec_ok = aligned16(g.A) && g.lda % 4 == 0 && g.sa0 % 4 == 0 && g.sa1 % 4 == 0 &&
+                     aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
+  hipLaunchKernelGGL(e.kernel[g.ta * 2 + g.tb], dim3(grid), dim3(e.threads), 0, s, g, tiles_m,
+                     tiles_n, ntiles, vec_ok);
   return hipGetLastError();
 }
 
