@@ -88,7 +88,7 @@ repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_
     // chain), the large tile for big outputs; vector tiles for the unfused
     // order; the simple path for block lengths no tile divides.
     const int64_t outputs = g.m * g.n * g.batch0 * g.batch1;
-    const int mfma_pref = outputs >= (int64_t(1) << 20) ? 0 : 3;
+    const int mfma_pref = outputs >= (int64_t(1) << 18) ? 0 : 3;
     const int tiled_pref = outputs >= (int64_t(1) << 22) ? 1 : 0;
     if (mfma_ok(repops::gemm_mfma_config(mfma_pref))) {
       kind = REPOPS_LAUNCH_GEMM_MFMA;

@@ -238,8 +238,8 @@ struct MfmaTile {
   }
 };
 
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmArgs g, int64_t tiles_m,
+template <int BM, int BN, int BK, int WM, int WN, int MINW, bool TA, bool TB>
+__global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_kernel(GemmArgs g, int64_t tiles_m,
                                                                  int64_t tiles_n, int64_t ntiles,
                                                                  int vec_ok) {
   using T = MfmaTile<BM, BN, BK, WM, WN, TA, TB>;
@@ -264,19 +264,21 @@ struct MfmaEntry {
   void (*kernel[4])(GemmArgs, int64_t, int64_t, int64_t, int);  // [ta * 2 + tb]
 };
 
-#define REPOPS_MFMA(BM, BN, BK, WM, WN)                                                       \
-  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN, BM, BN, BK},                                        \
+// MINW: waves per SIMD the register allocation must leave room for.
+#define REPOPS_MFMA(BM, BN, BK, WM, WN, MINW)                                                 \
+  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW, BM, BN, BK},                             \
    64 * WM * WN,                                                                              \
-   {gemm_mfma_kernel<BM, BN, BK, WM, WN, false, false>,                                       \
-    gemm_mfma_kernel<BM, BN, BK, WM, WN, false, true>,                                        \
-    gemm_mfma_kernel<BM, BN, BK, WM, WN, true, false>,                                        \
-    gemm_mfma_kernel<BM, BN, BK, WM, WN, true, true>}}
+   {gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, false>,                                 \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, true>,                                  \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, false>,                                  \
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>}}
 
 const MfmaEntry kMfma[] = {
-    REPOPS_MFMA(128, 128, 32, 2, 2),
-    REPOPS_MFMA(128, 64, 32, 2, 2),
-    REPOPS_MFMA(256, 128, 16, 4, 2),
-    REPOPS_MFMA(64, 64, 32, 1, 2),
+    REPOPS_MFMA(128, 128, 16, 2, 2, 2),  // default: two waves per SIMD
+    REPOPS_MFMA(256, 128, 32, 4, 2, 1),  // large outputs
+    REPOPS_MFMA(128, 128, 32, 2, 2, 1),
+    REPOPS_MFMA(64, 64, 32, 1, 2, 2),    // small outputs
+    REPOPS_MFMA(128, 64, 32, 2, 2, 2),
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
