@@ -258,10 +258,222 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_kernel(GemmArgs 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Staged variant: operands go from global memory straight into LDS
+// (global_load_lds_dwordx4: each lane's 16 bytes land at base + lane * 16),
+// through an NS-deep ring of 16-deep k slices, so several slices are in
+// flight without holding them in registers.  Instruction tiles are 32 rows x
+// 64 columns here (the instruction's two 32 x 32 blocks side by side along
+// columns, both reading the same 32 A rows).
+//
+// LDS forms of one slice (16 k values):
+//   k-packed: [4 groups of 4 k][rows][4]: a lane reads its row's 4 k values
+//     with one 16-byte LDS read (row-major A; transposed B);
+//   k-major:  [16 k][rows]: a lane reads one value per k (transposed A;
+//     row-major B), two k at once with a paired read.
+// Rows past M (columns past N) are loaded from the last valid row (column):
+// they only feed outputs that are never stored.  K must be a multiple of BK,
+// rows 16-byte aligned and the k-major operand's row count (N of row-major B,
+// M of transposed A) a multiple of 4; otherwise the register-staged kernel of
+// the same tile shape runs.
+// ---------------------------------------------------------------------------
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// s_waitcnt with only the vector-memory counter bounded (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* global_void_ptr;
+
+// Workgroup barrier that waits for this wave's LDS reads and writes only.
+// Unlike __syncthreads() it does not wait for outstanding global-to-LDS
+// loads (later slices stay in flight); the slice about to be read is waited
+// for explicitly with wait_vmcnt before it.  The memory clobber keeps the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB>
+struct StagedTile {
+  static_assert(BK % 16 == 0, "k slices hold whole 16-step groups");
+  static constexpr int NW = WM * WN;
+  static constexpr int TWM = BM / WM, TWN = BN / WN;
+  static constexpr int IM = TWM / 32, IN = TWN / 64;
+  static_assert(TWM % 32 == 0 && TWN % 64 == 0, "wave tile must hold whole instruction tiles");
+  static constexpr int A_FLOATS = BM * BK, B_FLOATS = BN * BK;
+  static constexpr int A_LOADS = A_FLOATS / 256, B_LOADS = B_FLOATS / 256;  // wave loads per slice
+  static_assert(A_LOADS % NW == 0 && B_LOADS % NW == 0, "slice loads must split evenly over waves");
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "tile edges must hold whole wave loads");
+
+  struct Smem {
+    float a[NS][A_FLOATS];
+    float b[NS][B_FLOATS];
+  };
+
+  // Issue this wave's share of the direct loads of slice k0 into ring slot.
+  // k-packed chunk q of an operand with R rows: [q][R][4]; wave load t covers
+  // rows 64t' .. 64t'+63 of chunk t / (R/64).  k-major with R rows: wave load
+  // t covers floats [256t, 256t+256) = k rows 256t/R ...
+  template <bool KPACKED, int R>
+  __device__ static void issue(const float* base, int64_t ld, int64_t r0, int64_t rmax,
+                               int64_t k0, float* slot, int wave, int lane) {
+    constexpr int LOADS = R * BK / 256;
+#pragma unroll
+    for (int u = 0; u < LOADS / NW; ++u) {
+      const int t = wave + u * NW;
+      const float* src;
+      if constexpr (KPACKED) {
+        const int q = t / (R / 64);                 // k group of 4
+        const int row = (t % (R / 64)) * 64 + lane;
+        int64_t gr = r0 + row;
+        gr = gr < rmax ? gr : rmax - 1;
+        src = base + gr * ld + k0 + 4 * q;
+      } else {
+        const int flat = t * 256 + lane * 4;        // = k * R + row
+        const int kk = flat / R, row = flat % R;
+        // rmax is a multiple of 4 here, so a group is either wholly inside
+        // or wholly past the edge (then it re-reads the last group)
+        int64_t gr = r0 + row;
+        gr = gr < rmax ? gr : rmax - 4;
+        src = base + (k0 + kk) * ld + gr;
+      }
+      __builtin_amdgcn_global_load_lds((global_void_ptr)src, (lds_void_ptr)(slot + t * 256), 16,
+                                       0, 0);
+    }
+  }
+
+  template <bool FIRST>
+  __device__ static void compute(const float* sa, const float* sb, int lane, int wm0, int wn0,
+                                 v32f (&P)[IM][IN]) {
+    const v32f zero = {};
+#pragma unroll
+    for (int q = 0; q < BK / 4; ++q) {
+      v4f av[IM], bv[IN];
+#pragma unroll
+      for (int i = 0; i < IM; ++i) {
+        const int row = wm0 + i * 32 + (lane & 31);
+        if constexpr (!TA) {
+          av[i] = *reinterpret_cast<const v4f*>(sa + (q * BM + row) * 4);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) av[i][c] = sa[(4 * q + c) * BM + row];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < IN; ++j) {
+        const int col = wn0 + j * 64 + lane;
+        if constexpr (TB) {
+          bv[j] = *reinterpret_cast<const v4f*>(sb + (q * BN + col) * 4);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) bv[j][c] = sb[(4 * q + c) * BN + col];
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+#pragma unroll
+          for (int j = 0; j < IN; ++j)
+            P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(
+                av[i][c], bv[j][c], (FIRST && q == 0 && c == 0) ? zero : P[i][j], 0, 0, 0);
+    }
+  }
+
+  __device__ static void run(const GemmArgs& g, Smem& sm, int64_t b0, int64_t b1, int64_t m0,
+                             int64_t n0) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm0 = (wave / WN) * TWM;
+    const int wn0 = (wave % WN) * TWN;
+    const int64_t nslices = g.k / BK;
+    const int64_t spb = g.k_block > 0 ? g.k_block / BK : (nslices > 0 ? nslices : 1);
+    const float* A = g.A + b0 * g.sa0 + b1 * g.sa1;
+    const float* B = g.B + b0 * g.sb0 + b1 * g.sb1;
+
+    auto issue_slice = [&](int64_t s) {
+      const int slot = static_cast<int>(s % NS);
+      issue<!TA, BM>(A, g.lda, m0, g.m, s * BK, sm.a[slot], wave, lane);
+      issue<TB, BN>(B, g.ldb, n0, g.n, s * BK, sm.b[slot], wave, lane);
+    };
+
+    v32f P[IM][IN], acc[IM][IN];
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < IN; ++j) {
+        P[i][j] = v32f{};
+        acc[i][j] = v32f{};
+      }
+    // Prologue: NS - 1 slices in flight.
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < nslices) issue_slice(s);
+    for (int64_t s = 0; s < nslices; ++s) {
+      // Slice s has landed once at most (NS - 2) later slices' loads of this
+      // wave are outstanding; the barrier then publishes every wave's part
+      // and guarantees that slot (s - 1) % NS is no longer read.
+      const int64_t later = (nslices - 1 - s) < (NS - 2) ? (nslices - 1 - s) : (NS - 2);
+      constexpr int PER = (A_LOADS + B_LOADS) / NW;
+      if (later >= 2) wait_vmcnt<2 * PER>();
+      else if (later == 1) wait_vmcnt<PER>();
+      else wait_vmcnt<0>();
+      lds_barrier();
+      if (s + NS - 1 < nslices) issue_slice(s + NS - 1);
+      const int slot = static_cast<int>(s % NS);
+      if (s % spb == 0) compute<true>(sm.a[slot], sm.b[slot], lane, wm0, wn0, P);
+      else compute<false>(sm.a[slot], sm.b[slot], lane, wm0, wn0, P);
+      if ((s + 1) % spb == 0 || s + 1 == nslices) {
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+#pragma unroll
+          for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+      }
+    }
+    __syncthreads();
+
+    // Accumulator layout (lane l, register r): block r / 16 holds columns
+    // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
+    float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < IN; ++j)
+#pragma unroll
+        for (int r = 0; r < 32; ++r) {
+          const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
+          const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
+          if (row < g.m && col < g.n) C[row * g.ldc + col] = epilogue(g, acc[i][j][r], col);
+        }
+  }
+};
+
+template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool TA, bool TB>
+__global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
+    GemmArgs g, int64_t tiles_m, int64_t tiles_n, int64_t ntiles, int) {
+  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB>;
+  __shared__ typename T::Smem sm;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int64_t bz, tm, tn;
+    tile_coords(t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
+    const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
+    T::run(g, sm, b0, b1, tm * BM, tn * BN);
+  }
+}
+
 struct MfmaEntry {
   GemmConfig cfg;
   int threads;
   void (*kernel[4])(GemmArgs, int64_t, int64_t, int64_t, int);  // [ta * 2 + tb]
+  // staged variant of the same tile shape (nullptr: none); needs K % 16 == 0
+  // and 16-byte aligned rows
+  void (*staged[4])(GemmArgs, int64_t, int64_t, int64_t, int);
 };
 
 // MINW: waves per SIMD the register allocation must leave room for.
@@ -271,14 +483,30 @@ struct MfmaEntry {
    {gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, false>,                                 \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, true>,                                  \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, false>,                                  \
-    gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>}}
+    gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>},                                  \
+   {nullptr, nullptr, nullptr, nullptr}}
 
+#define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN)                                \
+  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW "/s" #NS, BM, BN, BK},                    \
+   64 * WM * WN,                                                                              \
+   {gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, false>,                               \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, true>,                                \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, false>,                                \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, true>},                                \
+   {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                      \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                       \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
+
+// Staged entries fall back to the register-staged kernel of the same
+// workgroup tile (FWM x FWN waves) for shapes the staged kernel declines.
 const MfmaEntry kMfma[] = {
-    REPOPS_MFMA(128, 128, 16, 2, 2, 2),  // default: two waves per SIMD
-    REPOPS_MFMA(256, 128, 32, 4, 2, 1),  // large outputs
-    REPOPS_MFMA(128, 128, 32, 2, 2, 1),
-    REPOPS_MFMA(64, 64, 32, 1, 2, 2),    // small outputs
-    REPOPS_MFMA(128, 64, 32, 2, 2, 2),
+    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 0: large outputs
+    REPOPS_STAGED(128, 128, 64, 2, 2, 2, 1, 2, 2),  // 1: at most one tile per CU, long k
+    REPOPS_MFMA(128, 128, 16, 2, 2, 2),             // 2: short k (attention scores)
+    REPOPS_STAGED(128, 128, 32, 2, 2, 4, 1, 2, 2),  // 3
+    REPOPS_STAGED(256, 128, 16, 4, 2, 3, 1, 4, 2),  // 4
+    REPOPS_MFMA(64, 64, 32, 1, 2, 2),               // 5: small outputs
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
@@ -301,8 +529,13 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
   // float4 loads need 16-byte aligned rows and batch origins
   const int vec_ok = aligned16(g.A) && g.lda % 4 == 0 && g.sa0 % 4 == 0 && g.sa1 % 4 == 0 &&
                      aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
-  hipLaunchKernelGGL(e.kernel[g.ta * 2 + g.tb], dim3(grid), dim3(e.threads), 0, s, g, tiles_m,
-                     tiles_n, ntiles, vec_ok);
+  auto kernel = e.kernel[g.ta * 2 + g.tb];
+  // the staged kernel takes whole slices only: K a multiple of its depth
+  const bool staged_ok = vec_ok && g.k % e.cfg.bk == 0 && (!g.ta || g.m % 4 == 0) &&
+                         (g.tb || g.n % 4 == 0);
+  if (e.staged[0] && staged_ok) kernel = e.staged[g.ta * 2 + g.tb];
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(e.threads), 0, s, g, tiles_m, tiles_n, ntiles,
+                     vec_ok);
   return hipGetLastError();
 }
 

@@ -46,8 +46,11 @@ def launches(rp, k_block=64, fused=True):
     return out
 
 
+# Includes shapes the global-to-LDS staged kernels take (K % 16 == 0, N % 4 == 0)
+# with ragged row / column edges, and shapes they decline (fallback kernels).
 SHAPES = [(1, 1, 1), (7, 5, 3), (33, 17, 64), (65, 70, 130), (129, 257, 100), (200, 131, 333),
-          (64, 64, 0)]
+          (64, 64, 0), (96, 80, 64), (200, 132, 48), (65, 68, 256), (130, 260, 160),
+          (300, 36, 1024)]
 ORDERS = [(64, 0), (0, 0), (128, 0), (64, 1), (32, 1)]
 
 
@@ -165,6 +168,21 @@ def test_bmm_batches_and_alpha(rp):
         Bt = dev(np.ascontiguousarray(B.transpose(0, 1, 3, 2))).transpose(2, 3)
         got_t = host(rp.bmm(At, Bt, alpha=float(alpha), launch=launch))
         assert_bits_equal(got_t, want, name + " transposed")
+
+
+def test_bmm_staged_shapes(rp):
+    """Batched products whose shapes the staged kernels take (k = 128, the
+    attention head size), ragged rows and columns."""
+    g = inputs.rng(81)
+    A = inputs.normal(g, (2, 3, 70, 128))
+    B = inputs.normal(g, (2, 3, 128, 44))
+    want = oracle.bmm(A, B, alpha=0.125)
+    Bt = np.ascontiguousarray(B.transpose(0, 1, 3, 2))
+    for name, launch in launches(rp):
+        announce("bmm staged", name)
+        assert_bits_equal(host(rp.bmm(dev(A), dev(B), alpha=0.125, launch=launch)), want, name)
+        got_t = rp.bmm(dev(A), dev(Bt).transpose(2, 3), alpha=0.125, launch=launch)
+        assert_bits_equal(host(got_t), want, name + " trans_b")
 
 
 def test_bmm_batch_one_equals_matmul_and_loop(rp):
