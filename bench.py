@@ -44,7 +44,7 @@ def measured_traffic(launch_spec):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when the summary does not cover this kernel as it now stands."""
     import hashlib
-    if launch_spec != "mfma:1" or not os.path.exists(COUNTERS_MD):
+    if launch_spec != "mfma:0" or not os.path.exists(COUNTERS_MD):
         return None
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
@@ -150,8 +150,8 @@ def main():
     # 500 warmup steps (about 0.1 s) keep the ramp out of the timed region.
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=500)
-    ap.add_argument("--launch", default="mfma:1",
-                    help="auto | simple | tiled:I | mfma:I (mfma:1 is what auto picks here)")
+    ap.add_argument("--launch", default="mfma:0",
+                    help="auto | simple | tiled:I | mfma:I (mfma:0 is what auto picks here)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",

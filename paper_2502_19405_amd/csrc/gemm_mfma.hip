@@ -347,41 +347,61 @@ struct StagedTile {
     }
   }
 
+  struct Pack {
+    v4f a[IM];
+    v4f b[IN];
+  };
+
+  // LDS reads of one group of 4 k (a lane's operands for 4 matrix steps).
+  __device__ static void read_pack(const float* sa, const float* sb, int lane, int wm0, int wn0,
+                                   int q, Pack& pk) {
+#pragma unroll
+    for (int i = 0; i < IM; ++i) {
+      const int row = wm0 + i * 32 + (lane & 31);
+      if constexpr (!TA) {
+        pk.a[i] = *reinterpret_cast<const v4f*>(sa + (q * BM + row) * 4);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pk.a[i][c] = sa[(4 * q + c) * BM + row];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < IN; ++j) {
+      const int col = wn0 + j * 64 + lane;
+      if constexpr (TB) {
+        pk.b[j] = *reinterpret_cast<const v4f*>(sb + (q * BN + col) * 4);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pk.b[j][c] = sb[(4 * q + c) * BN + col];
+      }
+    }
+  }
+
+  template <bool OPEN>
+  __device__ static void mfma_pack(const Pack& pk, v32f (&P)[IM][IN]) {
+    const v32f zero = {};
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int j = 0; j < IN; ++j)
+          P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(pk.a[i][c], pk.b[j][c],
+                                                         (OPEN && c == 0) ? zero : P[i][j], 0,
+                                                         0, 0);
+  }
+
+  // One BK-deep slice.  FIRST: the slice opens a k block (its first update
+  // starts the block partial from +0).
   template <bool FIRST>
   __device__ static void compute(const float* sa, const float* sb, int lane, int wm0, int wn0,
                                  v32f (&P)[IM][IN]) {
-    const v32f zero = {};
 #pragma unroll
     for (int q = 0; q < BK / 4; ++q) {
-      v4f av[IM], bv[IN];
-#pragma unroll
-      for (int i = 0; i < IM; ++i) {
-        const int row = wm0 + i * 32 + (lane & 31);
-        if constexpr (!TA) {
-          av[i] = *reinterpret_cast<const v4f*>(sa + (q * BM + row) * 4);
-        } else {
-#pragma unroll
-          for (int c = 0; c < 4; ++c) av[i][c] = sa[(4 * q + c) * BM + row];
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < IN; ++j) {
-        const int col = wn0 + j * 64 + lane;
-        if constexpr (TB) {
-          bv[j] = *reinterpret_cast<const v4f*>(sb + (q * BN + col) * 4);
-        } else {
-#pragma unroll
-          for (int c = 0; c < 4; ++c) bv[j][c] = sb[(4 * q + c) * BN + col];
-        }
-      }
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int i = 0; i < IM; ++i)
-#pragma unroll
-          for (int j = 0; j < IN; ++j)
-            P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(
-                av[i][c], bv[j][c], (FIRST && q == 0 && c == 0) ? zero : P[i][j], 0, 0, 0);
+      Pack pk;
+      read_pack(sa, sb, lane, wm0, wn0, q, pk);
+      if (FIRST && q == 0) mfma_pack<true>(pk, P);
+      else mfma_pack<false>(pk, P);
     }
   }
 
@@ -498,11 +518,9 @@ struct MfmaEntry {
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
 
-// Staged entries fall back to the register-staged kernel of the same
-// workgroup tile (FWM x FWN waves) for shapes the staged kernel declines.
 const MfmaEntry kMfma[] = {
-    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 0: large outputs
-    REPOPS_STAGED(128, 128, 64, 2, 2, 2, 1, 2, 2),  // 1: at most one tile per CU, long k
+    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 0: default for large outputs
+    REPOPS_STAGED(128, 128, 64, 2, 2, 2, 1, 2, 2),  // 1
     REPOPS_MFMA(128, 128, 16, 2, 2, 2),             // 2: short k (attention scores)
     REPOPS_STAGED(128, 128, 32, 2, 2, 4, 1, 2, 2),  // 3
     REPOPS_STAGED(256, 128, 16, 4, 2, 3, 1, 4, 2),  // 4
