@@ -1,6 +1,6 @@
 """GPU parity of repops_exp / repops_gelu against the CPU oracle (0 ULP) over
-binary32 bit patterns: a dense strided sweep of the whole 2^32 space, special
-values, and every elementwise launch shape."""
+binary32 bit patterns: all 2^32 inputs, a strided sweep, the dense core
+range, special values, and every elementwise launch shape."""
 import numpy as np
 import pytest
 
@@ -73,3 +73,23 @@ def test_launch_shapes_and_alignment(rp, fn):
         getattr(rp, fn)(d, launch=launch, out=d)
         assert_bits_equal(host(d), want, "in place")
     assert getattr(rp, fn)(torch.empty(0, device="cuda:0")).numel() == 0
+
+
+@pytest.mark.parametrize("fn", ["exp", "gelu"])
+def test_exhaustive_all_bit_patterns(rp, fn):
+    """Every one of the 2^32 binary32 inputs, in 16 chunks of 2^28: the GPU
+    equals the oracle bit for bit (NaN inputs: NaN outputs)."""
+    import torch
+    chunk = 1 << 28
+    ref = getattr(oracle, fn)
+    for c in range(16):
+        announce(fn, "exhaustive chunk", c)
+        base = c * chunk
+        # bit patterns base .. base + chunk - 1 as float32 (int64 -> int32 wraps)
+        x = (torch.arange(base, base + chunk, dtype=torch.int64, device="cuda:0")
+             .to(torch.int32).view(torch.float32))
+        got = host(getattr(rp, fn)(x))
+        xs = (np.arange(base, base + chunk, dtype=np.uint64).astype(np.uint32)).view(np.float32)
+        want = ref(xs)
+        assert_bits_equal(got, want, f"{fn} chunk {c}")
+        del x, got, xs, want
