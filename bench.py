@@ -102,44 +102,96 @@ def cpu_baseline(d, flops_per_row_unit, target_s=12.0):
                       f"{dt:.2f} s wall on {threads} threads"}
 
 
+def _rate(ms, nbytes=None, flops=None):
+    out = {"ms": round(ms, 4)}
+    if nbytes is not None:
+        gbps = nbytes / ms / 1e6
+        out.update({"GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
+    if flops is not None:
+        tf = flops / ms / 1e9
+        out.update({"TFLOP/s": round(tf, 2), "frac_peak": round(tf / FP32_VECTOR_PEAK_TFLOPS, 4)})
+    return out
+
+
 def secondary(repops, steps):
-    """Row reductions and GELU at their model shapes: GB/s of algorithmic
-    bytes (each element read once and written once; causal softmax reads only
-    the unmasked part)."""
-    import numpy as np
+    """The other workloads, each timed with HIP events after warmup:
+    row reductions and elementwise ops in GB/s of algorithmic bytes (each
+    element read once and written once; causal softmax reads only the
+    unmasked part), GEMM-shaped steps and the model-shaped pipelines in
+    TFLOP/s of 2*M*N*K."""
     import torch
-    from paper_2502_19405_amd import inputs
+    from paper_2502_19405_amd import inputs, pipelines
 
     out = {}
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(a).to(dev)  # noqa: E731
     g = inputs.rng(4)
+
+    # 256^3 GEMM and 256 x 256 softmax (launch-bound sizes)
+    d = inputs.gemm256_softmax256()
+    A, B, S = t(d["A"]), t(d["B"]), t(d["S"])
+    C, P = torch.empty_like(A), torch.empty_like(S)
+    out["gemm_256"] = _rate(event_time_ms(lambda: repops.matmul(A, B, out=C), steps * 5),
+                            flops=2 * 256 ** 3)
+    out["softmax_256x256"] = _rate(event_time_ms(lambda: repops.softmax_rows(S, out=P), steps * 5),
+                                   nbytes=8 * 256 * 256)
+
     # causal softmax, Llama attention scores: 4 x 32 heads x 1024 rows of 1024
     T, rows = 1024, 4 * 32 * 1024
-    S = torch.from_numpy(inputs.normal(g, (rows, T), var=4.0)).cuda()
+    S = t(inputs.normal(g, (rows, T), var=4.0))
     P = torch.empty_like(S)
     ms = event_time_ms(lambda: repops.softmax_rows(S, causal_period=T, out=P), steps)
-    nbytes = 4 * (rows // T) * (T * (T + 1) // 2 + T * T)
-    out["softmax_causal_131072x1024"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
-                                         "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    out["softmax_causal_131072x1024"] = _rate(ms, nbytes=4 * (rows // T) * (T * (T + 1) // 2 + T * T))
     ms = event_time_ms(lambda: repops.softmax_rows(S, out=P), steps)
-    nbytes = 4 * rows * T * 2
-    out["softmax_dense_131072x1024"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
-                                        "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    out["softmax_dense_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
+    ms = event_time_ms(lambda: repops.exp(S, out=P), steps)
+    out["exp_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
     del S, P
+
     d = inputs.distilbert_mlp()
+    gam, bet = t(d["gamma"]), t(d["beta"])
     for name, shape in (("layernorm_4096x768", (4096, 768)), ("layernorm_65536x768", (65536, 768))):
-        Z = torch.from_numpy(inputs.normal(g, shape, var=0.5)).cuda()
+        Z = t(inputs.normal(g, shape, var=0.5))
         Y = torch.empty_like(Z)
-        gam, bet = torch.from_numpy(d["gamma"]).cuda(), torch.from_numpy(d["beta"]).cuda()
         ms = event_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y), steps)
-        nbytes = 4 * Z.numel() * 2
-        out[name] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
-                     "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
-    H = torch.from_numpy(inputs.normal(g, (4096, 3072), var=0.31)).cuda()
+        out[name] = _rate(ms, nbytes=4 * Z.numel() * 2)
+    H = t(inputs.normal(g, (4096, 3072), var=0.31))
     G = torch.empty_like(H)
-    ms = event_time_ms(lambda: repops.gelu(H, out=G), steps)
-    nbytes = 4 * H.numel() * 2
-    out["gelu_4096x3072"] = {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
-                             "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    out["gelu_4096x3072"] = _rate(event_time_ms(lambda: repops.gelu(H, out=G), steps),
+                                  nbytes=4 * H.numel() * 2)
+    del H, G
+
+    # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
+    X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
+    ms = event_time_ms(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet), steps)
+    out["distilbert_mlp_block"] = _rate(ms, flops=2 * 2 * 4096 * 768 * 3072)
+    del X, W1, W2, b1, b2
+
+    # Llama attention block: 4 x 1024 tokens, d 4096, 32 heads
+    d = inputs.llama_attention()
+    X, Wq, Wk, Wv, Wo = (t(d[k]) for k in ("X", "Wq", "Wk", "Wv", "Wo"))
+    bufs = {k: torch.empty((4096, 4096), device=dev) for k in ("Q", "K", "V", "O", "out")}
+    bufs["S"] = torch.empty((4, 32, 1024, 1024), device=dev)
+    bufs["P"] = torch.empty((4 * 32 * 1024, 1024), device=dev)
+    fl = 4 * 2 * 4096 ** 3 + 2 * 2 * 4 * 32 * 1024 * 1024 * 128
+    ms = event_time_ms(lambda: pipelines.attention_forward(X, Wq, Wk, Wv, Wo, 4, 1024, 32,
+                                                           buffers=bufs), max(steps // 4, 3))
+    out["llama_attention_block"] = _rate(ms, flops=fl)
+    Q, K, S = bufs["Q"], bufs["K"], bufs["S"]
+    ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 1024, 128, Q, 1024 * 4096, 128, 4096, 0,
+                                              K, 1024 * 4096, 128, 4096, 1, 0.08838835, S,
+                                              32 * 1024 * 1024, 1024 * 1024, 1024), steps)
+    out["bmm_qkT_4x32x1024x1024x128"] = _rate(ms, flops=2 * 4 * 32 * 1024 * 1024 * 128)
+    del X, Wq, Wk, Wv, Wo, bufs, Q, K, S
+
+    # Llama linear backward: dX = dY W^T, dW = X^T dY (8192 tokens, 4096 -> 14336)
+    d = inputs.llama_linear_backward()
+    X, dY, W = t(d["X"]), t(d["dY"]), t(d["W"])
+    gx = torch.empty((8192, 4096), device=dev)
+    gw = torch.empty((4096, 14336), device=dev)
+    ms = event_time_ms(lambda: pipelines.linear_backward(X, dY, W, out_dx=gx, out_dw=gw),
+                       max(steps // 4, 3))
+    out["llama_linear_backward"] = _rate(ms, flops=2 * 2 * 8192 * 4096 * 14336)
     return out
 
 
