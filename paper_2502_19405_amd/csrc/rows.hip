@@ -63,12 +63,16 @@ __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
     valid = v < valid ? v : valid;
   }
   const float ninf = -__builtin_huge_valf();
+  // Segments of 64 columns wholly past the mask are neither read nor
+  // exponentiated (a uniform test); their outputs are +0.
+  const int64_t live = (valid + kWave - 1) / kWave;
   float v[T];
   float m = ninf;
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int64_t j = lane + kWave * t;
-    v[t] = (j < valid) ? x[j] : ninf;  // masked entries are never read
+    v[t] = ninf;
+    if (t < live) v[t] = (j < valid) ? x[j] : ninf;  // masked entries are never read
     m = v[t] > m ? v[t] : m;
   }
   m = wave_max(m);
@@ -76,15 +80,22 @@ __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int64_t j = lane + kWave * t;
-    v[t] = (j < valid) ? rep_exp(v[t] - m) : 0.0f;
-    q = q + v[t];
+    float e = 0.0f;
+    if (t < live) e = (j < valid) ? rep_exp(v[t] - m) : 0.0f;
+    v[t] = e;
+    q = q + e;  // masked terms are +0 and leave q unchanged
   }
   const float s = wave_tree_sum(q);
   const float r = 1.0f / s;
+  if (a.cols == kWave * T) {  // full-width row: unconditional stores
 #pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const int64_t j = lane + kWave * t;
-    if (j < a.cols) y[j] = v[t] * r;
+    for (int t = 0; t < T; ++t) y[lane + kWave * t] = v[t] * r;
+  } else {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      if (j < a.cols) y[j] = v[t] * r;
+    }
   }
 }
 
@@ -114,17 +125,23 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
   }
   const float var = wave_tree_sum(q2) / n;
   const float rstd = 1.0f / __builtin_sqrtf(var + a.eps);
+  auto out = [&](int t, int64_t j) {
+    const float tv = v[t] * rstd;
+    float o;
+    if (a.gamma && a.beta) o = __builtin_fmaf(tv, a.gamma[j], a.beta[j]);
+    else if (a.gamma) o = tv * a.gamma[j];
+    else if (a.beta) o = tv + a.beta[j];
+    else o = tv;
+    y[j] = o;
+  };
+  if (a.cols == kWave * T) {  // full-width row: unconditional stores
 #pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const int64_t j = lane + kWave * t;
-    if (j < a.cols) {
-      const float tv = v[t] * rstd;
-      float o;
-      if (a.gamma && a.beta) o = __builtin_fmaf(tv, a.gamma[j], a.beta[j]);
-      else if (a.gamma) o = tv * a.gamma[j];
-      else if (a.beta) o = tv + a.beta[j];
-      else o = tv;
-      y[j] = o;
+    for (int t = 0; t < T; ++t) out(t, lane + kWave * t);
+  } else {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      if (j < a.cols) out(t, j);
     }
   }
   if (lane == 0) {
