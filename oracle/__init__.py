@@ -83,6 +83,18 @@ def _declare(lib):
         "repops_ref_layernorm_rows": (_int, [_int, _int, _i64, _i64, _f32p, _i64, _f32p, _f32p,
                                              _flt, _f32p, _i64, _f32p, _f32p, _int]),
     }
+    sig.update({
+        "repops_ref_softmax_backward_rows": (_int, [_int, _int, _i64, _i64, _f32p, _i64, _f32p,
+                                                    _i64, _f32p, _i64, _i64, _int]),
+        "repops_ref_layernorm_backward_rows": (_int, [_int, _int, _i64, _i64, _i64, _f32p, _i64,
+                                                      _f32p, _i64, _f32p, _f32p, _f32p, _f32p,
+                                                      _i64, _f32p, _f32p, _int]),
+        "repops_ref_gelu_grad1": (_flt, [_flt]),
+        "repops_ref_gelu_backward": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
+        "repops_ref_adam_step": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _flt, _flt, _flt, _flt,
+                                        _flt, _i64, _int, _int]),
+        "repops_ref_adam_scalars": (_int, [_flt, _flt, _flt, _flt, _i64, _f32p]),
+    })
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
         fn.restype = res
@@ -255,3 +267,74 @@ def layernorm_rows(X, gamma=None, beta=None, eps=1e-5, row_width=64, row_combine
                                                    _p(Y), cols, _p(mean), _p(rstd), nthreads)
     _check(rc, "layernorm_rows")
     return (Y, mean, rstd) if with_stats else Y
+
+
+# --------------------------------------------------------------------------
+# training-step operators
+# --------------------------------------------------------------------------
+
+def softmax_backward_rows(Y, dY, causal_period=0, row_width=64, row_combine=ROW_TREE,
+                          nthreads=0, lib=None):
+    Y = np.ascontiguousarray(Y, np.float32)
+    dY = np.ascontiguousarray(dY, np.float32)
+    rows, cols = Y.shape
+    dX = np.empty_like(Y)
+    rc = (lib or load()).repops_ref_softmax_backward_rows(row_width, row_combine, rows, cols,
+                                                          _p(Y), cols, _p(dY), cols, _p(dX), cols,
+                                                          causal_period, nthreads)
+    _check(rc, "softmax_backward_rows")
+    return dX
+
+
+def layernorm_backward_rows(X, dY, mean, rstd, gamma=None, row_width=64, row_combine=ROW_TREE,
+                            k_block=64, want_dx=True, want_params=True, nthreads=0, lib=None):
+    """Returns (dX, dgamma, dbeta); entries not requested are None."""
+    X = np.ascontiguousarray(X, np.float32)
+    dY = np.ascontiguousarray(dY, np.float32)
+    rows, cols = X.shape
+    dX = np.empty_like(X) if want_dx else None
+    dg = np.empty(cols, np.float32) if want_params else None
+    db = np.empty(cols, np.float32) if want_params else None
+    rc = (lib or load()).repops_ref_layernorm_backward_rows(
+        row_width, row_combine, k_block, rows, cols, _p(X), cols, _p(dY), cols,
+        _p(np.ascontiguousarray(mean, np.float32)), _p(np.ascontiguousarray(rstd, np.float32)),
+        _p(gamma), _p(dX), cols, _p(dg), _p(db), nthreads)
+    _check(rc, "layernorm_backward_rows")
+    return dX, dg, db
+
+
+def gelu_grad1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_gelu_grad1(float(np.float32(x))))
+
+
+def gelu_backward(x, dy, nthreads=0, lib=None):
+    x = np.ascontiguousarray(x, np.float32)
+    dy = np.ascontiguousarray(dy, np.float32)
+    dx = np.empty_like(x)
+    _check((lib or load()).repops_ref_gelu_backward(x.size, _p(x), _p(dy), _p(dx), nthreads),
+           "gelu_backward")
+    return dx
+
+
+def adam_step(param, grad, exp_avg, exp_avg_sq, lr, beta1=0.9, beta2=0.999, eps=1e-8,
+              weight_decay=0.0, step=1, decoupled=False, nthreads=0, lib=None):
+    """In place on copies: returns (param, exp_avg, exp_avg_sq) after one step."""
+    p = np.array(param, np.float32, copy=True)
+    m = np.array(exp_avg, np.float32, copy=True)
+    v = np.array(exp_avg_sq, np.float32, copy=True)
+    g = np.ascontiguousarray(grad, np.float32)
+    rc = (lib or load()).repops_ref_adam_step(p.size, _p(p), _p(g), _p(m), _p(v),
+                                              *(float(np.float32(a)) for a in
+                                                (lr, beta1, beta2, eps, weight_decay)),
+                                              int(step), int(decoupled), nthreads)
+    _check(rc, "adam_step")
+    return p, m, v
+
+
+def adam_scalars(lr, beta1, beta2, weight_decay, step, lib=None):
+    out = np.empty(6, np.float32)
+    rc = (lib or load()).repops_ref_adam_scalars(*(float(np.float32(a)) for a in
+                                                   (lr, beta1, beta2, weight_decay)),
+                                                 int(step), _p(out))
+    _check(rc, "adam_scalars")
+    return out

@@ -351,31 +351,43 @@ int repops_ref_bmm_at(int64_t k_block, int k_inner, int64_t batch0, int64_t batc
  *   blocked left-to-right (row_combine 1): the c1 rule with addition, blocks of
  *   W consecutive elements, block partials added left to right.
  *
- * For a sum of squares the term update is q = fma(x, x, q) instead of q + x.
+ * Terms: kind 0 adds a_j (q + a_j); kind 1 is a sum of squares, fma(a_j, a_j, q);
+ * kind 2 an inner product, fma(a_j, b_j, q).  Positions j >= valid contribute
+ * no operation (masked columns), but keep their place in the order.
  */
-static float term_update(float q, float x, int squares)
+static float term2(float q, const float *a, const float *b, int64_t j, int kind)
 {
-    return squares ? fmaf(x, x, q) : q + x;
+    if (kind == 0) return q + a[j];
+    if (kind == 1) return fmaf(a[j], a[j], q);
+    return fmaf(a[j], b[j], q);
 }
 
-float repops_ref_rowsum(int row_width, int row_combine, int64_t n, const float *x, int squares)
+static float rowsum_terms(int row_width, int row_combine, int64_t n, int64_t valid,
+                          const float *a, const float *b, int kind)
 {
     const int64_t W = row_width;
     if (row_combine == REF_ROW_BLOCKED) {
         float acc = 0.0f;
         for (int64_t j0 = 0; j0 < n; j0 += W) {
             float p = 0.0f;
-            for (int64_t j = j0; j < j0 + W && j < n; ++j) p = term_update(p, x[j], squares);
+            for (int64_t j = j0; j < j0 + W && j < n; ++j)
+                if (j < valid) p = term2(p, a, b, j, kind);
             acc = acc + p;
         }
         return acc;
     }
     float q[1024];
     for (int64_t l = 0; l < W; ++l) q[l] = 0.0f;
-    for (int64_t j = 0; j < n; ++j) q[j % W] = term_update(q[j % W], x[j], squares);
+    for (int64_t j = 0; j < n; ++j)
+        if (j < valid) q[j % W] = term2(q[j % W], a, b, j, kind);
     for (int64_t s = W / 2; s >= 1; s /= 2)
         for (int64_t l = 0; l < s; ++l) q[l] = q[l] + q[l + s];
     return q[0];
+}
+
+float repops_ref_rowsum(int row_width, int row_combine, int64_t n, const float *x, int squares)
+{
+    return rowsum_terms(row_width, row_combine, n, n, x, NULL, squares ? 1 : 0);
 }
 
 static int check_order_rows(int row_width, int row_combine)
@@ -633,5 +645,340 @@ int repops_ref_layernorm_rows(int row_width, int row_combine, int64_t rows, int6
     if (rows > 0 && cols == 0) return -1; /* mean of an empty row is undefined */
     ln_ctx c = {row_width, row_combine, cols, X, ldx, gamma, beta, eps, Y, ldy, mean_out, rstd_out};
     parallel_for(nthreads, rows, ln_range, &c);
+    return 0;
+}
+
+/* ========================================================================= */
+/* Training-step operators                                                   */
+/* ========================================================================= */
+
+/*
+ * The training runs of Section 4.2 (with the Adam optimizer) execute the
+ * extended graph of Section 2.2: forward nodes, their backward nodes and the
+ * optimizer update.  The backward operators below are the usual derivatives
+ * of the forward operators above; the paper fixes no operation order for
+ * them, so each reading is stated with its definition.
+ */
+
+/*
+ * Softmax backward: dx = y * (dy - <y, dy>) row by row.  Reading: the inner
+ * product is the fixed-order row sum of fma(y_j, dy_j, .) over the unmasked
+ * columns; dx_j = y_j * (dy_j - s); masked columns get +0.
+ */
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *Y; int64_t ldy;
+    const float *dY; int64_t lddy;
+    float *dX; int64_t lddx;
+    int64_t period;
+} smb_ctx;
+
+static void softmax_bwd_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const smb_ctx *c = (const smb_ctx *)vctx;
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *y = c->Y + r * c->ldy;
+        const float *dy = c->dY + r * c->lddy;
+        float *dx = c->dX + r * c->lddx;
+        const int64_t valid = (c->period > 0) ? (r % c->period) + 1 : c->cols;
+        const int64_t nv = valid < c->cols ? valid : c->cols;
+        const float s = rowsum_terms(c->W, c->combine, c->cols, nv, y, dy, 2);
+        for (int64_t j = 0; j < c->cols; ++j) {
+            if (j < nv) {
+                const float diff = dy[j] - s;
+                dx[j] = y[j] * diff;
+            } else {
+                dx[j] = 0.0f;
+            }
+        }
+    }
+}
+
+int repops_ref_softmax_backward_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                                     const float *Y, int64_t ldy, const float *dY, int64_t lddy,
+                                     float *dX, int64_t lddx, int64_t causal_period, int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || rows < 0 || cols < 0 || causal_period < 0)
+        return -1;
+    smb_ctx c = {row_width, row_combine, cols, Y, ldy, dY, lddy, dX, lddx, causal_period};
+    parallel_for(nthreads, rows, softmax_bwd_range, &c);
+    return 0;
+}
+
+/*
+ * LayerNorm backward (input gradient), with the forward's saved mean and
+ * rstd: t_j = (x_j - mean) * rstd exactly as in the forward; g_j = dy_j *
+ * gamma_j (dy_j when gamma is absent); a = rowsum(g) / n; b = rowsum of
+ * fma(g, t, .) / n; dx_j = rstd * ((g_j - a) - t_j * b).
+ */
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *X; int64_t ldx;
+    const float *dY; int64_t lddy;
+    const float *mean, *rstd, *gamma;
+    float *dX; int64_t lddx;
+} lnb_ctx;
+
+static void ln_bwd_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const lnb_ctx *c = (const lnb_ctx *)vctx;
+    const size_t n = (size_t)(c->cols > 0 ? c->cols : 1);
+    float *t = (float *)malloc(sizeof(float) * n);
+    float *g = (float *)malloc(sizeof(float) * n);
+    if (!t || !g) abort();
+    const float nf = (float)c->cols;
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *x = c->X + r * c->ldx;
+        const float *dy = c->dY + r * c->lddy;
+        float *dx = c->dX + r * c->lddx;
+        const float mean = c->mean[r], rstd = c->rstd[r];
+        for (int64_t j = 0; j < c->cols; ++j) {
+            const float d = x[j] - mean;
+            t[j] = d * rstd;
+            g[j] = c->gamma ? dy[j] * c->gamma[j] : dy[j];
+        }
+        const float a = rowsum_terms(c->W, c->combine, c->cols, c->cols, g, NULL, 0) / nf;
+        const float b = rowsum_terms(c->W, c->combine, c->cols, c->cols, g, t, 2) / nf;
+        for (int64_t j = 0; j < c->cols; ++j) {
+            const float u = g[j] - a;
+            const float tb = t[j] * b;
+            const float w = u - tb;
+            dx[j] = rstd * w;
+        }
+    }
+    free(t);
+    free(g);
+}
+
+/*
+ * LayerNorm parameter gradients: dgamma_j = sum over rows i of dy_ij * t_ij,
+ * dbeta_j = sum over rows of dy_ij.  Reading: the row index is a contraction
+ * index, so the canonical blocked left-to-right rule of the matrix product
+ * applies with the same block length (k_block): fused terms fma(dy, t, P) for
+ * dgamma, plain additions for dbeta.
+ */
+typedef struct {
+    int64_t k_block;
+    int64_t rows, cols;
+    const float *X; int64_t ldx;
+    const float *dY; int64_t lddy;
+    const float *mean, *rstd;
+    float *dgamma, *dbeta;
+} lnp_ctx;
+
+static void ln_param_range(void *vctx, int64_t j0, int64_t j1)
+{
+    const lnp_ctx *c = (const lnp_ctx *)vctx;
+    const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;
+    for (int64_t j = j0; j < j1; ++j) {
+        float accg = 0.0f, accb = 0.0f;
+        for (int64_t i0 = 0; i0 < c->rows; i0 += blk) {
+            const int64_t i1 = (i0 + blk < c->rows) ? i0 + blk : c->rows;
+            float pg = 0.0f, pb = 0.0f;
+            for (int64_t i = i0; i < i1; ++i) {
+                const float dy = c->dY[i * c->lddy + j];
+                const float d = c->X[i * c->ldx + j] - c->mean[i];
+                const float t = d * c->rstd[i];
+                pg = fmaf(dy, t, pg);
+                pb = pb + dy;
+            }
+            accg = accg + pg;
+            accb = accb + pb;
+        }
+        if (c->dgamma) c->dgamma[j] = accg;
+        if (c->dbeta) c->dbeta[j] = accb;
+    }
+}
+
+int repops_ref_layernorm_backward_rows(int row_width, int row_combine, int64_t k_block,
+                                       int64_t rows, int64_t cols,
+                                       const float *X, int64_t ldx, const float *dY, int64_t lddy,
+                                       const float *mean, const float *rstd, const float *gamma,
+                                       float *dX, int64_t lddx, float *dgamma, float *dbeta,
+                                       int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || k_block < 0 || rows < 0 || cols < 0)
+        return -1;
+    if (rows > 0 && cols == 0) return -1;
+    if (dX) {
+        lnb_ctx c = {row_width, row_combine, cols, X, ldx, dY, lddy, mean, rstd, gamma, dX, lddx};
+        parallel_for(nthreads, rows, ln_bwd_range, &c);
+    }
+    if (dgamma || dbeta) {
+        lnp_ctx p = {k_block, rows, cols, X, ldx, dY, lddy, mean, rstd, dgamma, dbeta};
+        parallel_for(nthreads, cols, ln_param_range, &p);
+    }
+    return 0;
+}
+
+/*
+ * GELU backward (tanh form): with s = 1 / (1 + exp_rep(-2z)) the forward is
+ * x * s, so d/dx = s + x s (1 - s) * 2 sqrt(2/pi) (1 + 3 * 0.044715 x^2).
+ * Reading (op sequence): u = x*x; z = fma(c, u*x, x) * sq; e = exp_rep(-2z);
+ * s = 1 / (1 + e); om = 1 - s; v = fma(c3, u, 1); t2 = (x*s)*om;
+ * t3 = sq2 * v; dx = dy * fma(t2, t3, s).  Constants: c = RN(0.044715),
+ * c3 = RN(0.134145) (= 3 * 0.044715), sq = RN(sqrt(2/pi)), sq2 = 2 * sq.
+ */
+static const float GELU_C3 = 0x1.12ba9ep-3f;
+static const float GELU_SQ2 = 0x1.988454p+0f;
+
+float repops_ref_gelu_grad1(float x)
+{
+    const float u = x * x;
+    const float u3 = u * x;
+    float z = fmaf(GELU_C, u3, x);
+    z = z * GELU_SQ;
+    const float w = z * -2.0f;
+    const float e = repops_ref_exp1(w);
+    const float d = 1.0f + e;
+    const float s = 1.0f / d;
+    const float om = 1.0f - s;
+    const float v = fmaf(GELU_C3, u, 1.0f);
+    const float t1 = x * s;
+    const float t2 = t1 * om;
+    const float t3 = GELU_SQ2 * v;
+    return fmaf(t2, t3, s);
+}
+
+typedef struct {
+    const float *x, *dy;
+    float *dx;
+} gb_ctx;
+
+static void gelu_bwd_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const gb_ctx *c = (const gb_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) c->dx[i] = c->dy[i] * repops_ref_gelu_grad1(c->x[i]);
+}
+
+int repops_ref_gelu_backward(int64_t n, const float *x, const float *dy, float *dx, int nthreads)
+{
+    if (n < 0) return -1;
+    gb_ctx c = {x, dy, dx};
+    parallel_for(nthreads, n, gelu_bwd_range, &c);
+    return 0;
+}
+
+/*
+ * Adam / AdamW step (Kingma and Ba; decoupled weight decay of Loshchilov and
+ * Hutter), the optimizer of the training runs in Section 4.2.  Reading (op
+ * sequence):
+ *   scalars, in binary64 from the binary32 arguments, each rounded once to
+ *   binary32 at the end (1 - b^t loses most of its bits to cancellation in
+ *   binary32 when b is close to 1 and t is small):
+ *     pw = b^t by binary exponentiation (result *= base for each set bit of t
+ *     from the lowest, base *= base after each bit); c1 = 1 - b1; c2 = 1 - b2;
+ *     step = lr / (1 - b1^t); sbc2 = sqrt(1 - b2^t); dec = 1 - lr * wd.
+ *   per element, binary32: decoupled: p = p * dec (when wd != 0); coupled:
+ *     g = fma(wd, p, g); m = fma(b1, m, c1 * g); v = fma(b2, v, c2 * (g * g));
+ *     den = sqrt(v) / sbc2 + eps; p = p - step * (m / den).
+ */
+typedef struct {
+    float c1, c2, step, sbc2, dec, eps, wd;
+    float b1, b2;
+    int decoupled;
+} adam_scalars;
+
+static double pow_binary(double base, int64_t t)
+{
+    double result = 1.0;
+    while (t > 0) {
+        if (t & 1) result = result * base;
+        base = base * base;
+        t >>= 1;
+    }
+    return result;
+}
+
+static adam_scalars adam_prepare(float lr, float b1, float b2, float eps, float wd, int64_t t,
+                                 int decoupled)
+{
+    adam_scalars s;
+    const double dlr = lr, db1 = b1, db2 = b2, dwd = wd;
+    s.b1 = b1;
+    s.b2 = b2;
+    s.c1 = (float)(1.0 - db1);
+    s.c2 = (float)(1.0 - db2);
+    const double bc1 = 1.0 - pow_binary(db1, t);
+    const double bc2 = 1.0 - pow_binary(db2, t);
+    s.step = (float)(dlr / bc1);
+    s.sbc2 = (float)sqrt(bc2);
+    const double lw = dlr * dwd;
+    s.dec = (float)(1.0 - lw);
+    s.eps = eps;
+    s.wd = wd;
+    s.decoupled = decoupled;
+    return s;
+}
+
+typedef struct {
+    adam_scalars s;
+    float *p, *m, *v;
+    const float *g;
+} adam_ctx;
+
+static void adam_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const adam_ctx *c = (const adam_ctx *)vctx;
+    const adam_scalars s = c->s;
+    for (int64_t i = i0; i < i1; ++i) {
+        float p = c->p[i], g = c->g[i];
+        if (s.wd != 0.0f) {
+            if (s.decoupled) p = p * s.dec;
+            else g = fmaf(s.wd, p, g);
+        }
+        const float cg = s.c1 * g;
+        const float m = fmaf(s.b1, c->m[i], cg);
+        const float gg = g * g;
+        const float cgg = s.c2 * gg;
+        const float v = fmaf(s.b2, c->v[i], cgg);
+        const float rv = sqrtf(v);
+        const float q = rv / s.sbc2;
+        const float den = q + s.eps;
+        const float upd = m / den;
+        const float su = s.step * upd;
+        c->p[i] = p - su;
+        c->m[i] = m;
+        c->v[i] = v;
+    }
+}
+
+int repops_ref_adam_step(int64_t n, float *param, const float *grad, float *exp_avg,
+                         float *exp_avg_sq, float lr, float beta1, float beta2, float eps,
+                         float weight_decay, int64_t step, int decoupled, int nthreads)
+{
+    if (n < 0 || step < 1) return -1;
+    adam_ctx c;
+    fenv_t saved;
+    fegetenv(&saved);
+    install_ieee_env();
+    c.s = adam_prepare(lr, beta1, beta2, eps, weight_decay, step, decoupled);
+    fesetenv(&saved);
+    c.p = param;
+    c.m = exp_avg;
+    c.v = exp_avg_sq;
+    c.g = grad;
+    parallel_for(nthreads, n, adam_range, &c);
+    return 0;
+}
+
+/* The step-dependent scalars, exported for the pins. */
+int repops_ref_adam_scalars(float lr, float beta1, float beta2, float weight_decay, int64_t step,
+                            float *out6)
+{
+    if (step < 1) return -1;
+    fenv_t saved;
+    fegetenv(&saved);
+    install_ieee_env();
+    const adam_scalars s = adam_prepare(lr, beta1, beta2, 0.0f, weight_decay, step, 1);
+    fesetenv(&saved);
+    out6[0] = s.c1;
+    out6[1] = s.c2;
+    out6[2] = s.step;
+    out6[3] = s.sbc2;
+    out6[4] = s.dec;
+    out6[5] = (float)pow_binary(beta1, step);
     return 0;
 }

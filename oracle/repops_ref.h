@@ -104,6 +104,37 @@ int repops_ref_layernorm_rows(int row_width, int row_combine, int64_t rows, int6
                               const float *beta, float eps, float *Y, int64_t ldy,
                               float *mean_out, float *rstd_out, int nthreads);
 
+/* ---- training-step operators ---- */
+
+/* dX = Y * (dY - rowsum(Y * dY)) per row; masked columns (causal_period > 0:
+ * j > r % period) are skipped in the sum and get dX = +0. */
+int repops_ref_softmax_backward_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                                     const float *Y, int64_t ldy, const float *dY, int64_t lddy,
+                                     float *dX, int64_t lddx, int64_t causal_period, int nthreads);
+
+/* LayerNorm backward from the forward's mean / rstd; gamma may be NULL.  dX,
+ * dgamma, dbeta may each be NULL (not computed).  dgamma/dbeta reduce over rows
+ * with the contraction rule and block length k_block. */
+int repops_ref_layernorm_backward_rows(int row_width, int row_combine, int64_t k_block,
+                                       int64_t rows, int64_t cols,
+                                       const float *X, int64_t ldx, const float *dY, int64_t lddy,
+                                       const float *mean, const float *rstd, const float *gamma,
+                                       float *dX, int64_t lddx, float *dgamma, float *dbeta,
+                                       int nthreads);
+
+/* d gelu(x) / dx and dX = dY * gelu'(X). */
+float repops_ref_gelu_grad1(float x);
+int repops_ref_gelu_backward(int64_t n, const float *x, const float *dy, float *dx, int nthreads);
+
+/* One Adam (decoupled = 0) or AdamW (decoupled = 1) step, in place; step >= 1. */
+int repops_ref_adam_step(int64_t n, float *param, const float *grad, float *exp_avg,
+                         float *exp_avg_sq, float lr, float beta1, float beta2, float eps,
+                         float weight_decay, int64_t step, int decoupled, int nthreads);
+/* out6 = {1 - b1, 1 - b2, lr / (1 - b1^t), sqrt(1 - b2^t), 1 - lr*wd, b1^t}, each
+ * computed in binary64 and rounded once to binary32. */
+int repops_ref_adam_scalars(float lr, float beta1, float beta2, float weight_decay, int64_t step,
+                            float *out6);
+
 #ifdef __cplusplus
 }
 #endif

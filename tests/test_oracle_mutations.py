@@ -12,6 +12,7 @@ import pytest
 
 import oracle
 import test_oracle as pins
+import test_oracle_training as tpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")
 
@@ -48,6 +49,32 @@ MUTATIONS = {
     "ln_unbiased": ("const float var = q / nf;", "const float var = q / (nf - 1.0f);", ["ln"]),
     # c7: eps outside the square root
     "ln_eps_outside": ("const float sd = sqrtf(ve);", "const float sd = sqrtf(var) + c->eps;", ["ln"]),
+    # softmax backward: sign of the inner product flipped
+    "smb_sign": ("const float diff = dy[j] - s;", "const float diff = dy[j] + s;", ["smb", "smb_onehot"]),
+    # softmax backward: masked columns get the unmasked formula
+    "smb_mask": ("                dx[j] = 0.0f;", "                dx[j] = y[j] * dy[j];", ["smb_causal"]),
+    # LayerNorm backward: the t * b projection dropped
+    "lnb_no_proj": ("const float w = u - tb;", "const float w = u;", ["lnb"]),
+    # LayerNorm backward: gamma not applied to dy
+    "lnb_no_gamma": ("g[j] = c->gamma ? dy[j] * c->gamma[j] : dy[j];", "g[j] = dy[j];", ["lnb"]),
+    # LayerNorm parameter gradients: rows summed in one block
+    "lnp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;",
+                      "const int64_t blk = c->rows;", ["lnp_order"]),
+    # LayerNorm parameter gradients: dbeta weighted by t
+    "lnp_dbeta_t": ("pb = pb + dy;", "pb = fmaf(dy, t, pb);", ["lnp_int"]),
+    # GELU backward: (1 - s) factor replaced by s
+    "gelu_grad_om": ("const float t2 = t1 * om;", "const float t2 = t1 * s;", ["gelu_grad"]),
+    # GELU backward: 3 * 0.044715 coefficient one ulp off
+    "gelu_c3_ulp": ("GELU_C3 = 0x1.12ba9ep-3f;", "GELU_C3 = 0x1.12baa0p-3f;", ["tconst"]),
+    # Adam: first-moment bias correction missing
+    "adam_no_bc1": ("s.step = (float)(dlr / bc1);", "s.step = (float)dlr;", ["adam_sc", "adam"]),
+    # Adam: second-moment bias correction multiplied instead of divided
+    "adam_bc2_mul": ("const float q = rv / s.sbc2;", "const float q = rv * s.sbc2;", ["adam"]),
+    # Adam: coupled weight decay with the wrong sign
+    "adam_wd_sign": ("else g = fmaf(s.wd, p, g);", "else g = fmaf(-s.wd, p, g);", ["adam_coupled"]),
+    # Adam: binary exponentiation tests the wrong bit
+    "adam_pow_bit": ("if (t & 1) result = result * base;", "if (t & 2) result = result * base;",
+                     ["adam_sc"]),
 }
 
 CHECKS = {
@@ -62,6 +89,18 @@ CHECKS = {
     "gelu": lambda lib: pins.test_gelu_accuracy_bound(lib),
     "softmax_const": lambda lib: pins.test_softmax_constant_row_is_reciprocal(lib),
     "ln": lambda lib: pins.test_layernorm_bound(lib, 3e-3),
+    "smb": lambda lib: tpins.test_softmax_backward_bound(lib, 64, 0),
+    "smb_onehot": lambda lib: tpins.test_softmax_backward_one_hot_closed_form(lib),
+    "smb_causal": lambda lib: tpins.test_softmax_backward_causal_masked_zero(lib),
+    "lnb": lambda lib: tpins.test_layernorm_backward_bound(lib),
+    "lnp_order": lambda lib: tpins.test_layernorm_param_grads_order_witness(lib),
+    "lnp_int": lambda lib: tpins.test_layernorm_param_grads_integer_exact(lib),
+    "gelu_grad": lambda lib: tpins.test_gelu_grad_bound(lib),
+    "tconst": lambda lib: tpins.check_training_constants(
+        open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
+    "adam_sc": lambda lib: tpins.test_adam_scalars(lib),
+    "adam": lambda lib: tpins.test_adam_against_float64(lib, 0.0, False),
+    "adam_coupled": lambda lib: tpins.test_adam_against_float64(lib, 0.01, False),
 }
 
 
