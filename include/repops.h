@@ -46,7 +46,9 @@ enum {
     REPOPS_ERR_ALIAS = 4,  /* output overlaps an input where that is not allowed */
     REPOPS_ERR_ORDER = 5,  /* unknown or unsupported order descriptor; never silently replaced */
     REPOPS_ERR_LAUNCH = 6, /* launch configuration invalid for this call */
-    REPOPS_ERR_HIP = 7     /* the HIP runtime rejected the kernel launch */
+    REPOPS_ERR_HIP = 7,    /* the HIP runtime rejected the kernel launch */
+    REPOPS_ERR_VALUE = 8,  /* a scalar argument outside its domain */
+    REPOPS_ERR_WORKSPACE = 9 /* workspace NULL or smaller than the size the query returns */
 };
 
 /*
@@ -217,6 +219,106 @@ repops_status_t repops_gelu(const repops_order_t *order, int64_t n, const float 
  */
 repops_status_t repops_exp(const repops_order_t *order, int64_t n, const float *X, float *Y,
                            const repops_launch_t *launch, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Training-step operators.  The training runs of Section 4.2 (Adam optimizer)
+ * execute the extended graph of Section 2.2: every forward node, its backward
+ * node and the optimizer update.  The paper fixes no order for these
+ * operators; version 1 fixes the operation sequences documented below.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * repops_softmax_backward_rows -- gradient of repops_softmax_rows:
+ *     s = row sum of fma(y_j, dy_j, .) over the unmasked columns, in the
+ *         descriptor's row order (masked columns contribute no operation);
+ *     dx_j = y_j * (dy_j - s);  masked columns: dx_j = +0.
+ *   Y, ldy    the forward output (rows x cols); dY, lddy the incoming gradient.
+ *   dX, lddx  output; may coincide exactly (same base and leading dimension)
+ *             with Y or with dY; other overlap is REPOPS_ERR_ALIAS.
+ *   causal_period  as for the forward.  Launch kinds as for softmax_rows.
+ */
+repops_status_t repops_softmax_backward_rows(const repops_order_t *order, int64_t rows,
+                                             int64_t cols, const float *Y, int64_t ldy,
+                                             const float *dY, int64_t lddy, float *dX,
+                                             int64_t lddx, int64_t causal_period,
+                                             const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_layernorm_backward_workspace -- bytes of device workspace that
+ * repops_layernorm_backward_rows needs for the parameter gradients at this
+ * size and order: 2 * ceil(rows / k_block) * cols floats when that is more
+ * than one block of rows, else 0.
+ */
+repops_status_t repops_layernorm_backward_workspace(const repops_order_t *order, int64_t rows,
+                                                    int64_t cols, uint64_t *bytes);
+
+/*
+ * repops_layernorm_backward_rows -- gradients of repops_layernorm_rows, from
+ * the forward's mean and rstd (its mean_out / rstd_out):
+ *   input gradient, per row, with the descriptor's row order:
+ *     t_j = (x_j - mean) * rstd;  g_j = dy_j * gamma_j (dy_j if gamma is NULL);
+ *     a = rowsum(g) / n;  b = rowsum of fma(g_j, t_j, .) / n;
+ *     dx_j = rstd * ((g_j - a) - t_j * b).
+ *   parameter gradients, per column j: the row index is a contraction index
+ *   and takes the matmul rule with block length k_block:
+ *     dgamma_j: P = fma(dy_ij, t_ij, P) over the rows of a block;
+ *     dbeta_j:  P = P + dy_ij;  block partials added left to right.
+ *     rows = 0 gives +0.
+ *   X, ldx / dY, lddy   forward input and incoming gradient, rows x cols.
+ *   mean, rstd          [rows]; gamma NULL or [cols].
+ *   dX, lddx            NULL or output; may coincide exactly with X or dY.
+ *   dgamma, dbeta       NULL or [cols] outputs.
+ *   workspace           device memory of at least the size that
+ *                       repops_layernorm_backward_workspace returns (may be NULL
+ *                       when that is 0 or when dgamma and dbeta are NULL);
+ *                       owned by the caller, contents on return unspecified.
+ *                       REPOPS_ERR_WORKSPACE if missing or too small.
+ *   No output may overlap another output, the workspace or an input (other
+ *   than dX as stated).  cols must be >= 1 when rows > 0, and <= 2^24.
+ *   Launch kinds (for the input gradient) as for layernorm_rows.
+ */
+repops_status_t repops_layernorm_backward_rows(
+    const repops_order_t *order, int64_t rows, int64_t cols, const float *X, int64_t ldx,
+    const float *dY, int64_t lddy, const float *mean, const float *rstd, const float *gamma,
+    float *dX, int64_t lddx, float *dgamma, float *dbeta, void *workspace,
+    uint64_t workspace_bytes, const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_gelu_backward -- dx = dy * gelu'(x) over n contiguous elements, the
+ * derivative of repops_gelu.  With s = 1 / (1 + exp_rep(w)) from the forward's
+ * sequence (y = x * s), one fixed sequence:
+ *     u = x*x;  z = fma(0.044715f, u*x, x) * 0.7978846f;  s = 1 / (1 + exp_rep(-2z));
+ *     om = 1 - s;  v = fma(0.134145f, u, 1);  t2 = (x*s) * om;  t3 = 1.5957692f * v;
+ *     dx = dy * fma(t2, t3, s).
+ *   Constants are the binary32 values nearest 0.044715, sqrt(2/pi), 0.134145
+ *   and 2 sqrt(2/pi).  dX may coincide exactly with X or dY.
+ */
+repops_status_t repops_gelu_backward(const repops_order_t *order, int64_t n, const float *X,
+                                     const float *dY, float *dX, const repops_launch_t *launch,
+                                     void *hip_stream);
+
+/*
+ * repops_adam_step -- one Adam (decoupled = 0) or AdamW (decoupled = 1) update
+ * of n contiguous parameters in place (Section 4.2 trains with Adam).
+ *   step scalars, computed on the host in binary64 from the binary32
+ *   arguments and rounded once to binary32:
+ *     c1 = 1 - b1;  c2 = 1 - b2;  st = lr / (1 - b1^t);  sb = sqrt(1 - b2^t);
+ *     dec = 1 - lr * wd;  b^t by binary exponentiation (square-and-multiply
+ *     from the lowest bit of t).
+ *   per element, binary32:
+ *     wd != 0: decoupled: p = p * dec;  coupled: g = fma(wd, p, g);
+ *     m = fma(b1, m, c1 * g);  v = fma(b2, v, c2 * (g * g));
+ *     p = p - st * (m / (sqrt(v) / sb + eps)).
+ *   param, exp_avg, exp_avg_sq   [n], updated in place; grad [n] read only;
+ *                                the four must not overlap.
+ *   step >= 1; 0 <= beta1, beta2 < 1; lr, eps, weight_decay finite; otherwise
+ *   REPOPS_ERR_VALUE.  Launch kinds as for gelu.
+ */
+repops_status_t repops_adam_step(const repops_order_t *order, int64_t n, float *param,
+                                 const float *grad, float *exp_avg, float *exp_avg_sq, float lr,
+                                 float beta1, float beta2, float eps, float weight_decay,
+                                 int64_t step, int32_t decoupled, const repops_launch_t *launch,
+                                 void *hip_stream);
 
 #ifdef __cplusplus
 }

@@ -1,14 +1,18 @@
 // C ABI of librepops: argument validation, order-descriptor checks and launch
 // selection.  Every error is detected before anything is enqueued.
 #include <hip/hip_runtime_api.h>
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 
 #include "../../include/repops.h"
 #include "repops_internal.h"
 
+using repops::AdamScalars;
 using repops::GemmArgs;
+using repops::LnParamArgs;
 using repops::RowArgs;
+using repops::RowBwdArgs;
 
 namespace {
 
@@ -222,6 +226,59 @@ repops_status_t check_elementwise(const repops_order_t* order, int64_t n, const 
   return REPOPS_OK;
 }
 
+// A rows x cols operand: null, stride and size checks.
+repops_status_t check_matrix(const float* p, int64_t rows, int64_t cols, int64_t ld) {
+  if (!p) return REPOPS_ERR_NULL;
+  if (ld < cols || ld < 1) return REPOPS_ERR_STRIDE;
+  (void)rows;
+  return REPOPS_OK;
+}
+
+// Output `out` may coincide exactly with `in` (same base and leading
+// dimension); any other overlap is an alias error.
+bool bad_overlap(const float* out, int64_t ldo, Extent oe, const float* in, int64_t ldi, Extent ie) {
+  if (out == in && ldo == ldi) return false;
+  return overlaps(oe, ie);
+}
+
+Extent vec_extent(const void* p, int64_t n_floats) {
+  return extent_of(static_cast<const float*>(p), 1, 0, 1, 0, 1, n_floats, n_floats);
+}
+
+// Adam step scalars, in binary64 from the binary32 arguments and rounded once
+// to binary32 (1 - b^t cancels in binary32 when b is near 1 and t is small).
+// b^t by binary exponentiation: the result is multiplied by the running power
+// for each set bit of t from the lowest, and the power squared after each bit.
+double pow_by_bits(double base, int64_t t) {
+  double result = 1.0;
+  while (t > 0) {
+    if (t & 1) result = result * base;
+    base = base * base;
+    t >>= 1;
+  }
+  return result;
+}
+
+AdamScalars adam_scalars(float lr, float b1, float b2, float eps, float wd, int64_t t,
+                         int decoupled) {
+  AdamScalars s{};
+  const double dlr = lr, db1 = b1, db2 = b2, dwd = wd;
+  s.c1 = static_cast<float>(1.0 - db1);
+  s.c2 = static_cast<float>(1.0 - db2);
+  const double bc1 = 1.0 - pow_by_bits(db1, t);
+  const double bc2 = 1.0 - pow_by_bits(db2, t);
+  s.step = static_cast<float>(dlr / bc1);
+  s.sbc2 = static_cast<float>(sqrt(bc2));
+  const double lw = dlr * dwd;
+  s.dec = static_cast<float>(1.0 - lw);
+  s.eps = eps;
+  s.wd = wd;
+  s.b1 = b1;
+  s.b2 = b2;
+  s.decay = wd != 0.0f ? (decoupled ? 1 : 2) : 0;
+  return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -247,6 +304,8 @@ const char* repops_status_str(repops_status_t s) {
     case REPOPS_ERR_ORDER: return "unsupported order descriptor";
     case REPOPS_ERR_LAUNCH: return "invalid launch configuration";
     case REPOPS_ERR_HIP: return "HIP launch failed";
+    case REPOPS_ERR_VALUE: return "invalid scalar argument";
+    case REPOPS_ERR_WORKSPACE: return "workspace missing or too small";
     default: return "unknown status";
   }
 }
@@ -376,6 +435,170 @@ repops_status_t repops_exp(const repops_order_t* order, int64_t n, const float* 
   if (st != REPOPS_OK || n == 0) return st;
   return hip_status(
       repops::launch_exp(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+// ---------------------------------------------------------------------------
+// Training-step operators
+// ---------------------------------------------------------------------------
+
+repops_status_t repops_softmax_backward_rows(const repops_order_t* order, int64_t rows,
+                                             int64_t cols, const float* Y, int64_t ldy,
+                                             const float* dY, int64_t lddy, float* dX,
+                                             int64_t lddx, int64_t causal_period,
+                                             const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (causal_period < 0) return REPOPS_ERR_SHAPE;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return REPOPS_ERR_SHAPE;
+  const bool empty = rows == 0 || cols == 0;
+  uint32_t kind;
+  int wpb;
+  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  if (st != REPOPS_OK || empty) return st;
+  if ((st = check_matrix(Y, rows, cols, ldy)) != REPOPS_OK) return st;
+  if ((st = check_matrix(dY, rows, cols, lddy)) != REPOPS_OK) return st;
+  if ((st = check_matrix(dX, rows, cols, lddx)) != REPOPS_OK) return st;
+  const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
+  const Extent de = extent_of(dY, 1, 0, 1, 0, rows, cols, lddy);
+  const Extent xe = extent_of(dX, 1, 0, 1, 0, rows, cols, lddx);
+  if (bad_overlap(dX, lddx, xe, Y, ldy, ye) || bad_overlap(dX, lddx, xe, dY, lddy, de))
+    return REPOPS_ERR_ALIAS;
+  RowBwdArgs a{};
+  a.rows = rows; a.cols = cols;
+  a.Y = Y; a.ldy = ldy; a.dY = dY; a.lddy = lddy; a.dX = dX; a.lddx = lddx;
+  a.W = static_cast<int>(order->row_width);
+  a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
+  a.period = causal_period;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_softmax_bwd_wave(a, wpb, s));
+  return hip_status(repops::launch_softmax_bwd_generic(a, s));
+}
+
+repops_status_t repops_layernorm_backward_workspace(const repops_order_t* order, int64_t rows,
+                                                    int64_t cols, uint64_t* bytes) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (!bytes) return REPOPS_ERR_NULL;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
+  const int64_t nblk = repops::layernorm_param_blocks(rows, order->k_block);
+  *bytes = nblk > 1 ? static_cast<uint64_t>(2 * nblk * cols) * sizeof(float) : 0;
+  return REPOPS_OK;
+}
+
+repops_status_t repops_layernorm_backward_rows(
+    const repops_order_t* order, int64_t rows, int64_t cols, const float* X, int64_t ldx,
+    const float* dY, int64_t lddy, const float* mean, const float* rstd, const float* gamma,
+    float* dX, int64_t lddx, float* dgamma, float* dbeta, void* workspace,
+    uint64_t workspace_bytes, const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
+  if (rows > 0 && cols == 0) return REPOPS_ERR_SHAPE;
+  uint32_t kind;
+  int wpb;
+  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  if (st != REPOPS_OK) return st;
+  const bool want_params = dgamma || dbeta;
+  if (cols == 0 || (rows == 0 && !want_params) || (!dX && !want_params)) return REPOPS_OK;
+  uint64_t need = 0;
+  if ((st = repops_layernorm_backward_workspace(order, rows, cols, &need)) != REPOPS_OK) return st;
+  if (!want_params) need = 0;
+  if (repops::layernorm_param_grid(rows, cols, order->k_block) > kMaxDim) return REPOPS_ERR_SHAPE;
+  if (need > 0 && (!workspace || workspace_bytes < need)) return REPOPS_ERR_WORKSPACE;
+  // Inputs and outputs as (extent, base, leading dimension).  No output may
+  // overlap another output or an input, except that dX may coincide exactly
+  // with X or with dY.
+  struct Span {
+    Extent e;
+    const float* base;
+    int64_t ld;
+  };
+  Span in[5], out[4];
+  int nin = 0, nout = 0;
+  if (rows > 0) {
+    if ((st = check_matrix(X, rows, cols, ldx)) != REPOPS_OK) return st;
+    if ((st = check_matrix(dY, rows, cols, lddy)) != REPOPS_OK) return st;
+    if (!mean || !rstd) return REPOPS_ERR_NULL;
+    in[nin++] = {extent_of(X, 1, 0, 1, 0, rows, cols, ldx), X, ldx};
+    in[nin++] = {extent_of(dY, 1, 0, 1, 0, rows, cols, lddy), dY, lddy};
+    in[nin++] = {vec_extent(mean, rows), mean, rows};
+    in[nin++] = {vec_extent(rstd, rows), rstd, rows};
+  }
+  if (gamma) in[nin++] = {vec_extent(gamma, cols), gamma, cols};
+  if (dX && rows > 0) {
+    if ((st = check_matrix(dX, rows, cols, lddx)) != REPOPS_OK) return st;
+    out[nout++] = {extent_of(dX, 1, 0, 1, 0, rows, cols, lddx), dX, lddx};
+  }
+  if (dgamma) out[nout++] = {vec_extent(dgamma, cols), dgamma, cols};
+  if (dbeta) out[nout++] = {vec_extent(dbeta, cols), dbeta, cols};
+  if (need > 0) {
+    const float* w = static_cast<const float*>(workspace);
+    const int64_t wn = static_cast<int64_t>(need / sizeof(float));
+    out[nout++] = {vec_extent(w, wn), w, wn};
+  }
+  for (int i = 0; i < nout; ++i) {
+    for (int j = i + 1; j < nout; ++j)
+      if (overlaps(out[i].e, out[j].e)) return REPOPS_ERR_ALIAS;
+    for (int j = 0; j < nin; ++j) {
+      const bool is_dx = dX && rows > 0 && i == 0;
+      const bool exact = out[i].base == in[j].base && out[i].ld == in[j].ld;
+      if (is_dx && j < 2 && exact) continue;  // dX in place of X or dY
+      if (overlaps(out[i].e, in[j].e)) return REPOPS_ERR_ALIAS;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  // Parameter gradients first: they read X and dY, which dX may overwrite.
+  if (want_params) {
+    LnParamArgs p{};
+    p.rows = rows; p.cols = cols; p.k_block = order->k_block;
+    p.X = X; p.ldx = ldx; p.dY = dY; p.lddy = lddy; p.mean = mean; p.rstd = rstd;
+    p.dgamma = dgamma; p.dbeta = dbeta; p.ws = static_cast<float*>(workspace);
+    if ((st = hip_status(repops::launch_layernorm_param(p, s))) != REPOPS_OK) return st;
+  }
+  if (!dX || rows == 0) return REPOPS_OK;
+  RowBwdArgs a{};
+  a.rows = rows; a.cols = cols;
+  a.Y = X; a.ldy = ldx; a.dY = dY; a.lddy = lddy; a.dX = dX; a.lddx = lddx;
+  a.W = static_cast<int>(order->row_width);
+  a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
+  a.mean = mean; a.rstd = rstd; a.gamma = gamma;
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_bwd_wave(a, wpb, s));
+  return hip_status(repops::launch_layernorm_bwd_generic(a, s));
+}
+
+repops_status_t repops_gelu_backward(const repops_order_t* order, int64_t n, const float* X,
+                                     const float* dY, float* dX, const repops_launch_t* launch,
+                                     void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, dX);
+  if (st != REPOPS_OK) return st;
+  if ((st = check_elementwise(order, n, dY, dX)) != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(repops::launch_gelu_bwd(n, X, dY, dX, threads, max_blocks,
+                                            static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_adam_step(const repops_order_t* order, int64_t n, float* param,
+                                 const float* grad, float* exp_avg, float* exp_avg_sq, float lr,
+                                 float beta1, float beta2, float eps, float weight_decay,
+                                 int64_t step, int32_t decoupled, const repops_launch_t* launch,
+                                 void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (n < 0 || n > kMaxDim) return REPOPS_ERR_SHAPE;
+  if (step < 1 || (decoupled != 0 && decoupled != 1)) return REPOPS_ERR_VALUE;
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+    return REPOPS_ERR_VALUE;
+  if (!isfinite(lr) || !isfinite(eps) || !isfinite(weight_decay)) return REPOPS_ERR_VALUE;
+  int threads, max_blocks;
+  repops_status_t st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  if (!param || !grad || !exp_avg || !exp_avg_sq) return REPOPS_ERR_NULL;
+  const Extent pe = vec_extent(param, n), ge = vec_extent(grad, n);
+  const Extent me = vec_extent(exp_avg, n), ve = vec_extent(exp_avg_sq, n);
+  if (overlaps(pe, ge) || overlaps(pe, me) || overlaps(pe, ve) || overlaps(me, ge) ||
+      overlaps(me, ve) || overlaps(ve, ge))
+    return REPOPS_ERR_ALIAS;
+  const AdamScalars sc = adam_scalars(lr, beta1, beta2, eps, weight_decay, step, decoupled);
+  return hip_status(repops::launch_adam(n, param, grad, exp_avg, exp_avg_sq, sc, threads,
+                                        max_blocks, static_cast<hipStream_t>(hip_stream)));
 }
 
 }  // extern "C"

@@ -10,6 +10,8 @@
 //       steps (RepOps rebuilds exp with a controlled order, Section 3.1 of the
 //       Verde paper; the method is Cody-Waite + Taylor).
 // gelu: tanh form through 0.5 (1 + tanh z) = 1 / (1 + exp(-2z)).
+// gelu': with s = 1 / (1 + exp(-2z)) the forward is x * s, so its derivative
+//       is s + x s (1 - s) * 2 sqrt(2/pi) (1 + 3 * 0.044715 x^2).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -33,6 +35,9 @@ constexpr float kInvFact7 = 0x1.a01a02p-13f;
 // Nearest binary32 values to 0.044715 and sqrt(2/pi).
 constexpr float kGeluCubic = 0x1.6e4e26p-5f;
 constexpr float kGeluScale = 0x1.988454p-1f;
+// Nearest binary32 value to 3 * 0.044715 = 0.134145, and 2 * kGeluScale (exact).
+constexpr float kGeluCubic3 = 0x1.12ba9ep-3f;
+constexpr float kGeluScale2 = 0x1.988454p+0f;
 
 __device__ __forceinline__ float pow2_exact(int e) {
   // 2^e for e in [-126, 127] from the exponent field alone.
@@ -72,6 +77,23 @@ __device__ __forceinline__ float rep_gelu(float x) {
   const float w = z * -2.0f;
   const float d = 1.0f + rep_exp(w);
   return x / d;  // correctly rounded division
+}
+
+// Derivative of rep_gelu, one fixed operation sequence.
+__device__ __forceinline__ float rep_gelu_grad(float x) {
+  const float u = x * x;
+  const float u3 = u * x;
+  float z = __builtin_fmaf(kGeluCubic, u3, x);
+  z = z * kGeluScale;
+  const float w = z * -2.0f;
+  const float d = 1.0f + rep_exp(w);
+  const float s = 1.0f / d;
+  const float om = 1.0f - s;
+  const float v = __builtin_fmaf(kGeluCubic3, u, 1.0f);
+  const float t1 = x * s;
+  const float t2 = t1 * om;
+  const float t3 = kGeluScale2 * v;
+  return __builtin_fmaf(t2, t3, s);
 }
 
 }  // namespace repops

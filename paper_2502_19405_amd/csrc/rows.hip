@@ -17,38 +17,12 @@
 
 #include "rep_math.h"
 #include "repops_internal.h"
+#include "row_reduce.h"
 
 #pragma clang fp contract(off)
 
 namespace repops {
 namespace {
-
-constexpr int kWave = 64;
-constexpr int kMaxPerLane = 32;  // register-resident rows: cols <= 64 * 32
-
-// Halving tree over the 64 lane partials: after the step with distance s, lane
-// l < s holds q[l] + q[l+s].  Lanes >= s keep stale values that no later step
-// reads.  Every lane returns q[0].
-__device__ __forceinline__ float wave_tree_sum(float q) {
-#pragma unroll
-  for (int s = kWave / 2; s >= 1; s >>= 1) {
-    const float other = __shfl_down(q, s, kWave);
-    q = q + other;
-  }
-  return __shfl(q, 0, kWave);
-}
-
-// Maximum over the wave (order-free up to the sign of a zero maximum, which
-// cannot change any softmax output: x - (+0) and x - (-0) differ only for
-// x = -0, and exp_rep(+0) = exp_rep(-0) = 1).
-__device__ __forceinline__ float wave_max(float m) {
-#pragma unroll
-  for (int s = kWave / 2; s >= 1; s >>= 1) {
-    const float other = __shfl_xor(m, s, kWave);
-    m = other > m ? other : m;
-  }
-  return m;
-}
 
 template <int T>
 __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
@@ -153,52 +127,6 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
 // ---------------------------------------------------------------------------
 // Generic path: one 64-lane workgroup per row, any W and combine mode.
 // ---------------------------------------------------------------------------
-
-// Sum of term(j), j in [0, n), in the descriptor's order.  qs is LDS holding at
-// least 1024 floats.  Every lane returns the sum.
-template <class Term>
-__device__ float generic_row_sum(int64_t n, int W, int blocked, Term term, float* qs) {
-  const int lane = threadIdx.x;
-  if (!blocked) {
-    for (int l = lane; l < W; l += kWave) {
-      float q = 0.0f;
-      for (int64_t j = l; j < n; j += W) q = term(q, j);
-      qs[l] = q;
-    }
-    __syncthreads();
-    for (int s = W / 2; s >= 1; s >>= 1) {
-      for (int l = lane; l < s; l += kWave) qs[l] = qs[l] + qs[l + s];
-      __syncthreads();
-    }
-    const float r = qs[0];
-    __syncthreads();
-    return r;
-  }
-  // Blocked: block partials are formed 64 at a time in parallel, then added
-  // left to right by lane 0.
-  const int64_t nblk = (n + W - 1) / W;
-  float acc = 0.0f;
-  for (int64_t b0 = 0; b0 < nblk; b0 += kWave) {
-    const int64_t b = b0 + lane;
-    if (b < nblk) {
-      float p = 0.0f;
-      const int64_t j1 = (b + 1) * W < n ? (b + 1) * W : n;
-      for (int64_t j = b * W; j < j1; ++j) p = term(p, j);
-      qs[lane] = p;
-    }
-    __syncthreads();
-    if (lane == 0) {
-      const int64_t cnt = nblk - b0 < kWave ? nblk - b0 : kWave;
-      for (int64_t c = 0; c < cnt; ++c) acc = acc + qs[c];
-    }
-    __syncthreads();
-  }
-  if (lane == 0) qs[0] = acc;
-  __syncthreads();
-  const float r = qs[0];
-  __syncthreads();
-  return r;
-}
 
 __global__ __launch_bounds__(64) void softmax_generic_kernel(RowArgs a) {
   __shared__ float qs[1024];

@@ -1,0 +1,439 @@
+// Reproducible training-step operators for gfx950: softmax, LayerNorm and
+// GELU backward, and the Adam / AdamW update.
+//
+// The training runs of the Verde paper (Section 4.2, Adam optimizer) execute
+// the extended graph of Section 2.2: forward nodes, their backward nodes and
+// the optimizer update.  Each backward operator below is one fixed sequence of
+// binary32 operations per output; its row reductions take the order
+// descriptor's row order, and the LayerNorm parameter gradients reduce over
+// rows with the contraction's blocked left-to-right rule.
+//
+// LayerNorm parameter gradients: for column j, dgamma_j = sum over rows i of
+// dy_ij * t_ij and dbeta_j = sum of dy_ij, with blocks of k_block consecutive
+// rows, each block a sequential chain from +0 (fma for dgamma, add for dbeta),
+// block partials added left to right.  One thread per (block, column) forms
+// the block partials -- every chain is independent, so the grid is as wide as
+// blocks x columns -- and a second kernel adds them left to right per column.
+// With a single block the first kernel writes the gradients directly (the left
+// to right sum of one partial P is +0 + P = P, since a chain started at +0 is
+// never -0).
+#include <hip/hip_runtime.h>
+
+#include "rep_math.h"
+#include "repops_internal.h"
+#include "row_reduce.h"
+
+#pragma clang fp contract(off)
+
+namespace repops {
+namespace {
+
+// ---------------------------------------------------------------------------
+// softmax backward: dx_j = y_j * (dy_j - s), s = rowsum of fma(y_j, dy_j, .)
+// over the unmasked columns; masked columns get +0.
+// ---------------------------------------------------------------------------
+
+template <int T>
+__global__ __launch_bounds__(512) void softmax_bwd_wave_kernel(RowBwdArgs a, int wpb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  const float* y = a.Y + row * a.ldy;
+  const float* dy = a.dY + row * a.lddy;
+  float* dx = a.dX + row * a.lddx;
+  int64_t valid = a.cols;
+  if (a.period > 0) {
+    const int64_t v = row % a.period + 1;
+    valid = v < valid ? v : valid;
+  }
+  const int64_t live = (valid + kWave - 1) / kWave;
+  float yv[T], dv[T];
+  float q = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int64_t j = lane + kWave * t;
+    yv[t] = 0.0f;
+    dv[t] = 0.0f;
+    if (t < live && j < valid) {  // masked entries are never read
+      yv[t] = y[j];
+      dv[t] = dy[j];
+    }
+    // A masked term is fma(+0, +0, q) = q: the chain never holds -0.
+    q = __builtin_fmaf(yv[t], dv[t], q);
+  }
+  const float s = wave_tree_sum(q);
+  auto out = [&](int t, int64_t j) {
+    const float diff = dv[t] - s;
+    return j < valid ? yv[t] * diff : 0.0f;
+  };
+  if (a.cols == kWave * T) {  // full-width row: unconditional stores
+#pragma unroll
+    for (int t = 0; t < T; ++t) dx[lane + kWave * t] = out(t, lane + kWave * t);
+  } else {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      if (j < a.cols) dx[j] = out(t, j);
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) void softmax_bwd_generic_kernel(RowBwdArgs a) {
+  __shared__ float qs[1024];
+  const int lane = threadIdx.x;
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* y = a.Y + row * a.ldy;
+    const float* dy = a.dY + row * a.lddy;
+    float* dx = a.dX + row * a.lddx;
+    int64_t valid = a.cols;
+    if (a.period > 0) {
+      const int64_t v = row % a.period + 1;
+      valid = v < valid ? v : valid;
+    }
+    auto term = [&](float q, int64_t j) { return j < valid ? __builtin_fmaf(y[j], dy[j], q) : q; };
+    const float s = generic_row_sum(a.cols, a.W, a.blocked, term, qs);
+    for (int64_t j = lane; j < a.cols; j += kWave) {
+      float o = 0.0f;
+      if (j < valid) {
+        const float diff = dy[j] - s;
+        o = y[j] * diff;
+      }
+      dx[j] = o;  // dX may equal Y or dY: element j is read before it is written
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm backward, input gradient.  With the forward's mean and rstd:
+//   t_j = (x_j - mean) * rstd;  g_j = dy_j * gamma_j (dy_j without gamma);
+//   a = rowsum(g) / n;  b = rowsum of fma(g_j, t_j, .) / n;
+//   dx_j = rstd * ((g_j - a) - t_j * b).
+// ---------------------------------------------------------------------------
+
+template <int T>
+__global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, int wpb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  const float* x = a.Y + row * a.ldy;
+  const float* dy = a.dY + row * a.lddy;
+  float* dx = a.dX + row * a.lddx;
+  const float mean = a.mean[row], rstd = a.rstd[row];
+  float tv[T], gv[T];
+  float q = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int64_t j = lane + kWave * t;
+    tv[t] = 0.0f;
+    gv[t] = 0.0f;
+    if (j < a.cols) {
+      const float d = x[j] - mean;
+      tv[t] = d * rstd;
+      gv[t] = a.gamma ? dy[j] * a.gamma[j] : dy[j];
+    }
+    q = q + gv[t];  // terms past the row are +0 and leave q unchanged
+  }
+  const float n = static_cast<float>(a.cols);
+  const float am = wave_tree_sum(q) / n;
+  float q2 = 0.0f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);
+  const float bm = wave_tree_sum(q2) / n;
+  auto out = [&](int t) {
+    const float u = gv[t] - am;
+    const float tb = tv[t] * bm;
+    const float w = u - tb;
+    return rstd * w;
+  };
+  if (a.cols == kWave * T) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) dx[lane + kWave * t] = out(t);
+  } else {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      if (j < a.cols) dx[j] = out(t);
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) void layernorm_bwd_generic_kernel(RowBwdArgs a) {
+  __shared__ float qs[1024];
+  const int lane = threadIdx.x;
+  const float n = static_cast<float>(a.cols);
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* x = a.Y + row * a.ldy;
+    const float* dy = a.dY + row * a.lddy;
+    float* dx = a.dX + row * a.lddx;
+    const float mean = a.mean[row], rstd = a.rstd[row];
+    auto g_at = [&](int64_t j) { return a.gamma ? dy[j] * a.gamma[j] : dy[j]; };
+    auto t_at = [&](int64_t j) {
+      const float d = x[j] - mean;
+      return d * rstd;
+    };
+    auto sum_g = [&](float q, int64_t j) { return q + g_at(j); };
+    const float am = generic_row_sum(a.cols, a.W, a.blocked, sum_g, qs) / n;
+    auto sum_gt = [&](float q, int64_t j) { return __builtin_fmaf(g_at(j), t_at(j), q); };
+    const float bm = generic_row_sum(a.cols, a.W, a.blocked, sum_gt, qs) / n;
+    for (int64_t j = lane; j < a.cols; j += kWave) {
+      const float gj = g_at(j), tj = t_at(j);
+      const float u = gj - am;
+      const float tb = tj * bm;
+      const float w = u - tb;
+      dx[j] = rstd * w;  // dX may equal X or dY: element j is read before it is written
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm parameter gradients.
+// ---------------------------------------------------------------------------
+
+constexpr int kParamThreads = 256;
+
+__global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
+    LnParamArgs a, int64_t col_groups, int64_t blk, int64_t nblk) {
+  const int64_t bid = blockIdx.x;
+  const int64_t beta = bid / col_groups;
+  const int64_t j = (bid - beta * col_groups) * kParamThreads + threadIdx.x;
+  if (j >= a.cols) return;
+  const int64_t i0 = beta * blk;
+  const int64_t i1 = (i0 + blk < a.rows) ? i0 + blk : a.rows;
+  const float* xp = a.X + j;
+  const float* dp = a.dY + j;
+  float pg = 0.0f, pb = 0.0f;
+  int64_t i = i0;
+  // Eight rows per step: the loads are independent of the chains and issue
+  // together; the chains themselves advance one row at a time.
+  for (; i + 8 <= i1; i += 8) {
+    float xv[8], dv[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      xv[r] = xp[(i + r) * a.ldx];
+      dv[r] = dp[(i + r) * a.lddy];
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const float d = xv[r] - a.mean[i + r];
+      const float t = d * a.rstd[i + r];
+      pg = __builtin_fmaf(dv[r], t, pg);
+      pb = pb + dv[r];
+    }
+  }
+  for (; i < i1; ++i) {
+    const float dv = dp[i * a.lddy];
+    const float d = xp[i * a.ldx] - a.mean[i];
+    const float t = d * a.rstd[i];
+    pg = __builtin_fmaf(dv, t, pg);
+    pb = pb + dv;
+  }
+  if (nblk == 1) {
+    if (a.dgamma) a.dgamma[j] = pg;
+    if (a.dbeta) a.dbeta[j] = pb;
+  } else {
+    a.ws[beta * a.cols + j] = pg;
+    a.ws[(nblk + beta) * a.cols + j] = pb;
+  }
+}
+
+__global__ __launch_bounds__(kParamThreads) void layernorm_param_combine_kernel(LnParamArgs a,
+                                                                             int64_t nblk) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * kParamThreads + threadIdx.x;
+  if (j >= a.cols) return;
+  float accg = 0.0f, accb = 0.0f;
+  for (int64_t b = 0; b < nblk; ++b) {
+    accg = accg + a.ws[b * a.cols + j];
+    accb = accb + a.ws[(nblk + b) * a.cols + j];
+  }
+  if (a.dgamma) a.dgamma[j] = accg;
+  if (a.dbeta) a.dbeta[j] = accb;
+}
+
+// ---------------------------------------------------------------------------
+// GELU backward and Adam: elementwise, 16-byte accesses where every operand
+// is 16-byte aligned.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(1024) void gelu_bwd_kernel(int64_t n, const float* x, const float* dy,
+                                                        float* dx, int vec) {
+  const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    const float4* d4 = reinterpret_cast<const float4*>(dy);
+    float4* o4 = reinterpret_cast<float4*>(dx);
+    for (int64_t i = tid; i < n4; i += stride) {
+      const float4 xv = x4[i];
+      const float4 dv = d4[i];
+      float4 o;
+      o.x = dv.x * rep_gelu_grad(xv.x);
+      o.y = dv.y * rep_gelu_grad(xv.y);
+      o.z = dv.z * rep_gelu_grad(xv.z);
+      o.w = dv.w * rep_gelu_grad(xv.w);
+      o4[i] = o;
+    }
+    done = n4 * 4;
+  }
+  for (int64_t i = done + tid; i < n; i += stride) dx[i] = dy[i] * rep_gelu_grad(x[i]);
+}
+
+// One element of the Adam / AdamW update (decay: 0 none, 1 decoupled, 2 coupled).
+__device__ __forceinline__ void adam_one(const AdamScalars& s, float& p, float g, float& m,
+                                         float& v) {
+  if (s.decay == 1) p = p * s.dec;
+  if (s.decay == 2) g = __builtin_fmaf(s.wd, p, g);
+  const float cg = s.c1 * g;
+  m = __builtin_fmaf(s.b1, m, cg);
+  const float gg = g * g;
+  const float cgg = s.c2 * gg;
+  v = __builtin_fmaf(s.b2, v, cgg);
+  const float rv = __builtin_sqrtf(v);
+  const float q = rv / s.sbc2;
+  const float den = q + s.eps;
+  const float upd = m / den;
+  const float su = s.step * upd;
+  p = p - su;
+}
+
+__global__ __launch_bounds__(1024) void adam_kernel(int64_t n, float* p, const float* g, float* m,
+                                                    float* v, AdamScalars s, int vec) {
+  const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  int64_t done = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    float4* p4 = reinterpret_cast<float4*>(p);
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+    float4* m4 = reinterpret_cast<float4*>(m);
+    float4* v4 = reinterpret_cast<float4*>(v);
+    for (int64_t i = tid; i < n4; i += stride) {
+      float4 pv = p4[i], mv = m4[i], vv = v4[i];
+      const float4 gv = g4[i];
+      adam_one(s, pv.x, gv.x, mv.x, vv.x);
+      adam_one(s, pv.y, gv.y, mv.y, vv.y);
+      adam_one(s, pv.z, gv.z, mv.z, vv.z);
+      adam_one(s, pv.w, gv.w, mv.w, vv.w);
+      p4[i] = pv;
+      m4[i] = mv;
+      v4[i] = vv;
+    }
+    done = n4 * 4;
+  }
+  for (int64_t i = done + tid; i < n; i += stride) {
+    float pv = p[i], mv = m[i], vv = v[i];
+    adam_one(s, pv, g[i], mv, vv);
+    p[i] = pv;
+    m[i] = mv;
+    v[i] = vv;
+  }
+}
+
+using WaveBwdKernel = void (*)(RowBwdArgs, int);
+
+WaveBwdKernel pick_softmax_bwd(int64_t cols) {
+  if (cols <= kWave * 1) return softmax_bwd_wave_kernel<1>;
+  if (cols <= kWave * 2) return softmax_bwd_wave_kernel<2>;
+  if (cols <= kWave * 4) return softmax_bwd_wave_kernel<4>;
+  if (cols <= kWave * 8) return softmax_bwd_wave_kernel<8>;
+  if (cols <= kWave * 16) return softmax_bwd_wave_kernel<16>;
+  return softmax_bwd_wave_kernel<32>;
+}
+
+WaveBwdKernel pick_layernorm_bwd(int64_t cols) {
+  if (cols <= kWave * 1) return layernorm_bwd_wave_kernel<1>;
+  if (cols <= kWave * 2) return layernorm_bwd_wave_kernel<2>;
+  if (cols <= kWave * 4) return layernorm_bwd_wave_kernel<4>;
+  if (cols <= kWave * 8) return layernorm_bwd_wave_kernel<8>;
+  if (cols <= kWave * 12) return layernorm_bwd_wave_kernel<12>;
+  if (cols <= kWave * 16) return layernorm_bwd_wave_kernel<16>;
+  return layernorm_bwd_wave_kernel<32>;
+}
+
+unsigned row_grid(int64_t rows) {
+  const int64_t cap = int64_t(1) << 30;
+  return static_cast<unsigned>(rows < cap ? rows : cap);
+}
+
+int64_t ew_blocks(int64_t items, int threads, int max_blocks) {
+  int64_t blocks = (items + threads - 1) / threads;
+  if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
+  const int64_t cap = int64_t(1) << 30;
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  return blocks;
+}
+
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+}  // namespace
+
+hipError_t launch_softmax_bwd_wave(const RowBwdArgs& a, int wpb, hipStream_t s) {
+  const int64_t blocks = (a.rows + wpb - 1) / wpb;
+  hipLaunchKernelGGL(pick_softmax_bwd(a.cols), dim3(static_cast<unsigned>(blocks)),
+                     dim3(kWave * wpb), 0, s, a, wpb);
+  return hipGetLastError();
+}
+
+hipError_t launch_softmax_bwd_generic(const RowBwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_bwd_generic_kernel, dim3(row_grid(a.rows)), dim3(kWave), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm_bwd_wave(const RowBwdArgs& a, int wpb, hipStream_t s) {
+  const int64_t blocks = (a.rows + wpb - 1) / wpb;
+  hipLaunchKernelGGL(pick_layernorm_bwd(a.cols), dim3(static_cast<unsigned>(blocks)),
+                     dim3(kWave * wpb), 0, s, a, wpb);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm_bwd_generic(const RowBwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(layernorm_bwd_generic_kernel, dim3(row_grid(a.rows)), dim3(kWave), 0, s, a);
+  return hipGetLastError();
+}
+
+int64_t layernorm_param_blocks(int64_t rows, int64_t k_block) {
+  if (k_block <= 0 || k_block >= rows) return 1;  // rows == 0: one empty block, gradients +0
+  return (rows + k_block - 1) / k_block;
+}
+
+int64_t layernorm_param_grid(int64_t rows, int64_t cols, int64_t k_block) {
+  const int64_t groups = (cols + kParamThreads - 1) / kParamThreads;
+  return layernorm_param_blocks(rows, k_block) * groups;
+}
+
+hipError_t launch_layernorm_param(const LnParamArgs& a, hipStream_t s) {
+  const int64_t nblk = layernorm_param_blocks(a.rows, a.k_block);
+  const int64_t blk = nblk == 1 ? a.rows : a.k_block;
+  const int64_t groups = (a.cols + kParamThreads - 1) / kParamThreads;
+  hipLaunchKernelGGL(layernorm_param_partial_kernel, dim3(static_cast<unsigned>(nblk * groups)),
+                     dim3(kParamThreads), 0, s, a, groups, blk, nblk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nblk == 1) return e;
+  hipLaunchKernelGGL(layernorm_param_combine_kernel, dim3(static_cast<unsigned>(groups)),
+                     dim3(kParamThreads), 0, s, a, nblk);
+  return hipGetLastError();
+}
+
+hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,
+                           int max_blocks, hipStream_t s) {
+  const bool vec = aligned16(x) && aligned16(dy) && aligned16(dx);
+  const int64_t blocks = ew_blocks(vec ? (n + 3) / 4 : n, threads, max_blocks);
+  hipLaunchKernelGGL(gelu_bwd_kernel, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0, s, n,
+                     x, dy, dx, vec ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam(int64_t n, float* p, const float* g, float* m, float* v,
+                       const AdamScalars& sc, int threads, int max_blocks, hipStream_t s) {
+  const bool vec = aligned16(p) && aligned16(g) && aligned16(m) && aligned16(v);
+  const int64_t blocks = ew_blocks(vec ? (n + 3) / 4 : n, threads, max_blocks);
+  hipLaunchKernelGGL(adam_kernel, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0, s, n, p, g,
+                     m, v, sc, vec ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace repops

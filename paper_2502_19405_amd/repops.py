@@ -16,7 +16,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librepops.so")
 
-OK, ERR_NULL, ERR_SHAPE, ERR_STRIDE, ERR_ALIAS, ERR_ORDER, ERR_LAUNCH, ERR_HIP = range(8)
+(OK, ERR_NULL, ERR_SHAPE, ERR_STRIDE, ERR_ALIAS, ERR_ORDER, ERR_LAUNCH, ERR_HIP, ERR_VALUE,
+ ERR_WORKSPACE) = range(10)
 K_FMA, K_MUL_ADD = 0, 1
 ROW_STRIDED_TREE, ROW_BLOCKED_LTR = 0, 1
 LAUNCH_AUTO = 0
@@ -92,6 +93,14 @@ _SIGNATURES = {
                                      _vp, _lp, _vp]),
     "repops_gelu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
     "repops_exp": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_softmax_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64,
+                                            _i64, _lp, _vp]),
+    "repops_layernorm_backward_workspace": (_i32, [_op, _i64, _i64, ctypes.POINTER(ctypes.c_uint64)]),
+    "repops_layernorm_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp,
+                                              _vp, _i64, _vp, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
+    "repops_gelu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
+    "repops_adam_step": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32, _f32, _f32, _i64,
+                                _i32, _lp, _vp]),
 }
 EXPORTS = tuple(_SIGNATURES)
 
@@ -302,3 +311,115 @@ def gelu(X: torch.Tensor, order: Order | None = None, launch: Launch | None = No
 def exp(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
         out: torch.Tensor | None = None) -> torch.Tensor:
     return _elementwise("repops_exp", X, order, launch, out)
+
+
+# ---------------------------------------------------------------------------
+# training-step operators
+# ---------------------------------------------------------------------------
+
+def softmax_backward_rows(Y: torch.Tensor, dY: torch.Tensor, causal_period: int = 0,
+                          order: Order | None = None, launch: Launch | None = None,
+                          out: torch.Tensor | None = None) -> torch.Tensor:
+    """dX = Y * (dY - rowsum(Y * dY)) from the forward output Y."""
+    rows, cols, ldy = _rows(Y, "Y")
+    r2, c2, lddy = _rows(dY, "dY")
+    if (r2, c2) != (rows, cols):
+        raise ValueError("Y and dY shapes differ")
+    if out is None:
+        out = torch.empty_like(Y, memory_format=torch.contiguous_format)
+    _, _, lddx = _rows(out, "out")
+    rc = load().repops_softmax_backward_rows(
+        ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols, _dev(Y, "Y"), ldy,
+        _dev(dY, "dY"), lddy, _dev(out, "out"), lddx, causal_period, _launch(launch), _stream(out))
+    _check(rc, "repops_softmax_backward_rows")
+    return out
+
+
+def layernorm_backward_workspace(rows: int, cols: int, order: Order | None = None) -> int:
+    """Bytes of workspace the LayerNorm backward needs for its parameter gradients."""
+    n = ctypes.c_uint64(0)
+    rc = load().repops_layernorm_backward_workspace(ctypes.byref((order or _DEFAULT_ORDER).c()),
+                                                    rows, cols, ctypes.byref(n))
+    _check(rc, "repops_layernorm_backward_workspace")
+    return n.value
+
+
+def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tensor,
+                            rstd: torch.Tensor, gamma: torch.Tensor | None = None,
+                            need_dx: bool = True, need_params: bool = True,
+                            order: Order | None = None, launch: Launch | None = None,
+                            dx_out: torch.Tensor | None = None,
+                            workspace: torch.Tensor | None = None):
+    """(dX, dgamma, dbeta) of the row LayerNorm from the forward's mean / rstd;
+    entries not requested are None.  The workspace is allocated here when
+    none is passed."""
+    order = order or _DEFAULT_ORDER
+    rows, cols, ldx = _rows(X, "X")
+    r2, c2, lddy = _rows(dY, "dY")
+    if (r2, c2) != (rows, cols):
+        raise ValueError("X and dY shapes differ")
+    for t, name in ((mean, "mean"), (rstd, "rstd")):
+        if t.numel() != rows or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [{rows}] tensor")
+    pg = None
+    if gamma is not None:
+        if gamma.numel() != cols or not gamma.is_contiguous():
+            raise ValueError(f"gamma must be a contiguous [{cols}] tensor")
+        pg = _dev(gamma, "gamma")
+    dx = dgamma = dbeta = None
+    lddx = cols
+    if need_dx:
+        dx = dx_out if dx_out is not None else torch.empty_like(X, memory_format=torch.contiguous_format)
+        _, _, lddx = _rows(dx, "dx_out")
+    wptr, wbytes = None, 0
+    if need_params:
+        dgamma = torch.empty(cols, dtype=torch.float32, device=X.device)
+        dbeta = torch.empty(cols, dtype=torch.float32, device=X.device)
+        need = layernorm_backward_workspace(rows, cols, order)
+        if need:
+            if workspace is None:
+                workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
+            wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
+    ptr = lambda t, n: None if t is None else _dev(t, n)  # noqa: E731
+    rc = load().repops_layernorm_backward_rows(
+        ctypes.byref(order.c()), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
+        _dev(mean, "mean"), _dev(rstd, "rstd"), pg, ptr(dx, "dX"), lddx, ptr(dgamma, "dgamma"),
+        ptr(dbeta, "dbeta"), wptr, wbytes, _launch(launch), _stream(X))
+    _check(rc, "repops_layernorm_backward_rows")
+    return dx, dgamma, dbeta
+
+
+def gelu_backward(X: torch.Tensor, dY: torch.Tensor, order: Order | None = None,
+                  launch: Launch | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """dX = dY * gelu'(X), elementwise over contiguous tensors."""
+    if not X.is_contiguous() or not dY.is_contiguous() or dY.numel() != X.numel():
+        raise ValueError("X and dY must be contiguous with equal element counts")
+    if out is None:
+        out = torch.empty_like(X)
+    if not out.is_contiguous() or out.numel() != X.numel():
+        raise ValueError("out must be contiguous with X's element count")
+    rc = load().repops_gelu_backward(ctypes.byref((order or _DEFAULT_ORDER).c()), X.numel(),
+                                     _dev(X, "X"), _dev(dY, "dY"), _dev(out, "out"),
+                                     _launch(launch), _stream(out))
+    _check(rc, "repops_gelu_backward")
+    return out
+
+
+def adam_step(param: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor,
+              exp_avg_sq: torch.Tensor, lr: float, beta1: float = 0.9, beta2: float = 0.999,
+              eps: float = 1e-8, weight_decay: float = 0.0, step: int = 1,
+              decoupled: bool = True, order: Order | None = None,
+              launch: Launch | None = None) -> None:
+    """One Adam / AdamW update of param, exp_avg and exp_avg_sq in place."""
+    n = param.numel()
+    for t, name in ((param, "param"), (grad, "grad"), (exp_avg, "exp_avg"),
+                    (exp_avg_sq, "exp_avg_sq")):
+        if not t.is_contiguous() or t.numel() != n:
+            raise ValueError(f"{name} must be contiguous with {n} elements")
+    rc = load().repops_adam_step(ctypes.byref((order or _DEFAULT_ORDER).c()), n,
+                                 _dev(param, "param"), _dev(grad, "grad"),
+                                 _dev(exp_avg, "exp_avg"), _dev(exp_avg_sq, "exp_avg_sq"),
+                                 float(lr), float(beta1), float(beta2), float(eps),
+                                 float(weight_decay), int(step), 1 if decoupled else 0,
+                                 _launch(launch), _stream(param))
+    _check(rc, "repops_adam_step")

@@ -29,7 +29,9 @@ def rp():
 def test_header_declares_the_operator_calls():
     names = declared_functions()
     for fn in ("repops_matmul", "repops_bmm", "repops_softmax_rows", "repops_layernorm_rows",
-               "repops_gelu", "repops_exp", "repops_order_default"):
+               "repops_gelu", "repops_exp", "repops_order_default",
+               "repops_softmax_backward_rows", "repops_layernorm_backward_rows",
+               "repops_layernorm_backward_workspace", "repops_gelu_backward", "repops_adam_step"):
         assert fn in names
 
 
@@ -158,6 +160,73 @@ def test_rows_and_elementwise_rejections(rp):
     ew = ctypes.byref(rp.Launch(rp.LAUNCH_ELEMENTWISE, (100,)).c())
     assert lib.repops_exp(o, 8, FAKE_A, FAKE_C, ew, None) == rp.ERR_LAUNCH
     assert lib.repops_exp(o, 0, None, None, None, None) == rp.OK
+
+
+FAKE_D, FAKE_M, FAKE_R, FAKE_G, FAKE_W = 0x400000, 0x500000, 0x600000, 0x700000, 0x800000
+
+
+@no_gpu_only
+def test_training_rejections(rp):
+    lib = rp.load()
+    o = _order()
+    sbw = lib.repops_softmax_backward_rows
+    assert sbw(o, 4, 8, FAKE_A, 8, FAKE_B, 8, FAKE_C, 7, 0, None, None) == rp.ERR_STRIDE
+    assert sbw(o, 4, 8, FAKE_A, 8, None, 8, FAKE_C, 8, 0, None, None) == rp.ERR_NULL
+    assert sbw(o, 4, 8, FAKE_A, 8, FAKE_B, 8, FAKE_A + 4, 8, 0, None, None) == rp.ERR_ALIAS
+    assert sbw(o, 4, 8, FAKE_A, 8, FAKE_B, 8, FAKE_B, 9, 0, None, None) == rp.ERR_ALIAS
+    assert sbw(o, 4, 8, FAKE_A, 8, FAKE_B, 8, FAKE_C, 8, -1, None, None) == rp.ERR_SHAPE
+    assert sbw(o, 0, 8, None, 8, None, 8, None, 8, 0, None, None) == rp.OK
+
+    ws = ctypes.c_uint64(1)
+    assert lib.repops_layernorm_backward_workspace(o, 4096, 768, ctypes.byref(ws)) == rp.OK
+    assert ws.value == 2 * 64 * 768 * 4
+    assert lib.repops_layernorm_backward_workspace(o, 64, 768, ctypes.byref(ws)) == rp.OK
+    assert ws.value == 0
+    assert lib.repops_layernorm_backward_workspace(_order(k_block=0), 4096, 768,
+                                                   ctypes.byref(ws)) == rp.OK
+    assert ws.value == 0
+    assert lib.repops_layernorm_backward_workspace(o, 64, 768, None) == rp.ERR_NULL
+
+    def lnb(rows=128, cols=8, X=FAKE_A, ldx=8, dY=FAKE_B, lddy=8, mean=FAKE_M, rstd=FAKE_R,
+            gamma=None, dX=FAKE_C, lddx=8, dg=FAKE_D, db=FAKE_D + 64, ws=FAKE_W, wsb=1 << 20,
+            order=None):
+        return lib.repops_layernorm_backward_rows(order or o, rows, cols, X, ldx, dY, lddy, mean,
+                                                  rstd, gamma, dX, lddx, dg, db, ws, wsb, None,
+                                                  None)
+    assert lnb(cols=0) == rp.ERR_SHAPE
+    assert lnb(ws=None) == rp.ERR_WORKSPACE
+    assert lnb(wsb=2 * 2 * 8 * 4 - 4) == rp.ERR_WORKSPACE
+    assert lnb(mean=None) == rp.ERR_NULL
+    assert lnb(lddx=7) == rp.ERR_STRIDE
+    assert lnb(dX=FAKE_A + 4) == rp.ERR_ALIAS           # dX partly over X
+    assert lnb(db=FAKE_D + 16) == rp.ERR_ALIAS          # dgamma and dbeta overlap
+    assert lnb(ws=FAKE_D) == rp.ERR_ALIAS               # workspace over dgamma
+    assert lnb(dg=FAKE_M) == rp.ERR_ALIAS               # dgamma over mean
+    assert lnb(gamma=FAKE_C + 8) == rp.ERR_ALIAS        # gamma inside dX
+    assert lnb(order=_order(version=0)) == rp.ERR_ORDER
+    assert lnb(rows=4, cols=0, dX=None, dg=None, db=None) == rp.ERR_SHAPE
+    assert lnb(rows=0, cols=0) == rp.OK
+
+    assert lib.repops_gelu_backward(o, 8, FAKE_A, FAKE_B, FAKE_A + 4, None, None) == rp.ERR_ALIAS
+    assert lib.repops_gelu_backward(o, 8, FAKE_A, FAKE_B, FAKE_B + 4, None, None) == rp.ERR_ALIAS
+    assert lib.repops_gelu_backward(o, 8, FAKE_A, None, FAKE_C, None, None) == rp.ERR_NULL
+    assert lib.repops_gelu_backward(o, -1, FAKE_A, FAKE_B, FAKE_C, None, None) == rp.ERR_SHAPE
+
+    def adam(n=8, p=FAKE_A, g=FAKE_B, m=FAKE_C, v=FAKE_D, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8,
+             wd=0.0, step=1, dec=1):
+        return lib.repops_adam_step(o, n, p, g, m, v, lr, b1, b2, eps, wd, step, dec, None, None)
+    assert adam(step=0) == rp.ERR_VALUE
+    assert adam(b1=1.0) == rp.ERR_VALUE
+    assert adam(b2=-0.1) == rp.ERR_VALUE
+    assert adam(lr=float("inf")) == rp.ERR_VALUE
+    assert adam(eps=float("nan")) == rp.ERR_VALUE
+    assert adam(dec=2) == rp.ERR_VALUE
+    assert adam(m=None) == rp.ERR_NULL
+    assert adam(m=FAKE_A + 16) == rp.ERR_ALIAS
+    assert adam(v=FAKE_C) == rp.ERR_ALIAS
+    assert adam(n=-1) == rp.ERR_SHAPE
+    assert adam(n=0, p=None, g=None, m=None, v=None) == rp.OK
+    assert rp.status_str(rp.ERR_WORKSPACE).startswith("workspace")
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
