@@ -146,7 +146,16 @@ def secondary(repops, steps):
     out["softmax_dense_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
     ms = event_time_ms(lambda: repops.exp(S, out=P), steps)
     out["exp_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
-    del S, P
+    # softmax backward on the same scores: reads Y and dY (unmasked part when
+    # causal), writes dX everywhere
+    Yp = repops.softmax_rows(S, causal_period=T)
+    dP = t(inputs.normal(g, (rows, T), var=1e-4))
+    ms = event_time_ms(lambda: repops.softmax_backward_rows(Yp, dP, causal_period=T, out=P), steps)
+    out["softmax_backward_causal_131072x1024"] = _rate(
+        ms, nbytes=4 * (rows // T) * (2 * T * (T + 1) // 2 + T * T))
+    ms = event_time_ms(lambda: repops.softmax_backward_rows(Yp, dP, out=P), steps)
+    out["softmax_backward_dense_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 3)
+    del S, P, Yp, dP
 
     d = inputs.distilbert_mlp()
     gam, bet = t(d["gamma"]), t(d["beta"])
@@ -155,11 +164,42 @@ def secondary(repops, steps):
         Y = torch.empty_like(Z)
         ms = event_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y), steps)
         out[name] = _rate(ms, nbytes=4 * Z.numel() * 2)
+    # LayerNorm backward: reads X and dY, writes dX (mean, rstd, gamma and the
+    # [cols] parameter gradients are negligible); dgamma/dbeta included
+    for name, shape in (("layernorm_backward_4096x768", (4096, 768)),
+                        ("layernorm_backward_65536x768", (65536, 768))):
+        Z = t(inputs.normal(g, shape, var=0.5))
+        mean = torch.empty(shape[0], device=dev)
+        rstd = torch.empty(shape[0], device=dev)
+        repops.layernorm_rows(Z, gam, bet, mean_out=mean, rstd_out=rstd)
+        dZ = t(inputs.normal(g, shape, var=1e-2))
+        dX = torch.empty_like(Z)
+        dg, db = torch.empty_like(gam), torch.empty_like(gam)
+        ws = torch.empty(max(repops.layernorm_backward_workspace(*shape) // 4, 1), device=dev)
+        ms = event_time_ms(lambda: repops.layernorm_backward_rows(
+            Z, dZ, mean, rstd, gam, dx_out=dX, dgamma_out=dg, dbeta_out=db, workspace=ws), steps)
+        out[name] = _rate(ms, nbytes=4 * Z.numel() * 3)
+        del Z, dZ, dX, ws
     H = t(inputs.normal(g, (4096, 3072), var=0.31))
     G = torch.empty_like(H)
     out["gelu_4096x3072"] = _rate(event_time_ms(lambda: repops.gelu(H, out=G), steps),
                                   nbytes=4 * H.numel() * 2)
-    del H, G
+    dG = t(inputs.normal(g, (4096, 3072), var=1e-2))
+    out["gelu_backward_4096x3072"] = _rate(
+        event_time_ms(lambda: repops.gelu_backward(H, dG, out=G), steps), nbytes=4 * H.numel() * 3)
+    del H, G, dG
+    # Adam: reads param, grad, exp_avg, exp_avg_sq and writes three of them
+    # (28 B per parameter); the DistilBERT feed-forward block's 4.72 M
+    # parameters, and a 64 M-parameter flat buffer
+    for name, n in (("adam_4723968", 2 * 768 * 3072 + 3072 + 3 * 768),
+                    ("adam_67108864", 1 << 26)):
+        p = t(inputs.normal(g, (n,), var=4e-4))
+        gr = t(inputs.normal(g, (n,), var=1e-4))
+        m, v = torch.zeros_like(p), torch.zeros_like(p)
+        ms = event_time_ms(lambda: repops.adam_step(p, gr, m, v, 1e-4, weight_decay=0.01, step=10),
+                           steps)
+        out[name] = _rate(ms, nbytes=28 * n)
+        del p, gr, m, v
 
     # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))

@@ -7,6 +7,7 @@
 
 #include "../../include/repops.h"
 #include "repops_internal.h"
+#include "train_internal.h"
 
 using repops::AdamScalars;
 using repops::GemmArgs;
@@ -544,21 +545,30 @@ repops_status_t repops_layernorm_backward_rows(
     }
   }
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
-  // Parameter gradients first: they read X and dY, which dX may overwrite.
-  if (want_params) {
-    LnParamArgs p{};
-    p.rows = rows; p.cols = cols; p.k_block = order->k_block;
-    p.X = X; p.ldx = ldx; p.dY = dY; p.lddy = lddy; p.mean = mean; p.rstd = rstd;
-    p.dgamma = dgamma; p.dbeta = dbeta; p.ws = static_cast<float*>(workspace);
-    if ((st = hip_status(repops::launch_layernorm_param(p, s))) != REPOPS_OK) return st;
-  }
-  if (!dX || rows == 0) return REPOPS_OK;
+  LnParamArgs p{};
+  p.rows = rows; p.cols = cols; p.k_block = order->k_block;
+  p.X = X; p.ldx = ldx; p.dY = dY; p.lddy = lddy; p.mean = mean; p.rstd = rstd;
+  p.dgamma = dgamma; p.dbeta = dbeta; p.ws = static_cast<float*>(workspace);
   RowBwdArgs a{};
   a.rows = rows; a.cols = cols;
   a.Y = X; a.ldy = ldx; a.dY = dY; a.lddy = lddy; a.dX = dX; a.lddx = lddx;
   a.W = static_cast<int>(order->row_width);
   a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
   a.mean = mean; a.rstd = rstd; a.gamma = gamma;
+  // Both gradients on the wave path with row blocks: one fused pass over X
+  // and dY (R rows staged per pass: the launch's waves per block, else a
+  // choice by size).
+  if (want_params && dX && rows > 0 && kind == REPOPS_LAUNCH_ROWS_WAVE && order->k_block >= 1) {
+    const bool explicit_wave = launch && launch->kind == REPOPS_LAUNCH_ROWS_WAVE;
+    const int R = repops::layernorm_fused_rows(rows, cols, order->k_block, explicit_wave ? wpb : 0);
+    if (R >= 1) return hip_status(repops::launch_layernorm_bwd_fused(a, p, R, s));
+  }
+  // Otherwise parameter gradients first: they read X and dY, which dX may
+  // overwrite.
+  if (want_params) {
+    if ((st = hip_status(repops::launch_layernorm_param(p, s))) != REPOPS_OK) return st;
+  }
+  if (!dX || rows == 0) return REPOPS_OK;
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_bwd_wave(a, wpb, s));
   return hip_status(repops::launch_layernorm_bwd_generic(a, s));
 }

@@ -40,6 +40,13 @@ __device__ __forceinline__ float wave_max(float m) {
   return m;
 }
 
+// Workgroup barrier that waits for this wave's LDS operations only: global
+// loads issued before it stay in flight (__syncthreads would also wait for
+// them).  The memory clobber keeps LDS accesses on their side of the barrier.
+__device__ __forceinline__ void lds_only_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Sum of term(j), j in [0, n), in the descriptor's order.  qs is LDS holding at
 // least 1024 floats.  Every lane returns the sum.
 template <class Term>

@@ -21,6 +21,7 @@
 
 #include "rep_math.h"
 #include "repops_internal.h"
+#include "train_internal.h"
 #include "row_reduce.h"
 
 #pragma clang fp contract(off)
@@ -238,17 +239,191 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
   }
 }
 
-__global__ __launch_bounds__(kParamThreads) void layernorm_param_combine_kernel(LnParamArgs a,
-                                                                             int64_t nblk) {
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * kParamThreads + threadIdx.x;
-  if (j >= a.cols) return;
-  float accg = 0.0f, accb = 0.0f;
-  for (int64_t b = 0; b < nblk; ++b) {
-    accg = accg + a.ws[b * a.cols + j];
-    accb = accb + a.ws[(nblk + b) * a.cols + j];
+// Left-to-right sum of the block partials, per column.  The chains are short
+// (one add per block) but their operands sit in HBM, so the workgroup first
+// stages a chunk of partials in LDS with every thread loading, then one lane
+// per chain adds the chunk in block order.  A workgroup owns 16 columns; each
+// chain (dgamma or dbeta of one column) lives in one lane of wave 0.
+constexpr int kCombCols = 16;
+constexpr int kCombThreads = 256;
+constexpr int kCombChunk = 256;  // blocks per LDS chunk
+constexpr int kCombRowsPerPass = kCombThreads / kCombCols;
+
+__global__ __launch_bounds__(kCombThreads) void layernorm_param_combine_kernel(LnParamArgs a,
+                                                                            int64_t nblk) {
+  __shared__ float buf[2][kCombChunk][kCombCols];
+  const int tid = threadIdx.x;
+  const int c = tid % kCombCols;
+  const int rb = tid / kCombCols;
+  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kCombCols;
+  const bool col_ok = j0 + c < a.cols;
+  const float* wg = a.ws + j0 + c;
+  const float* wb = a.ws + nblk * a.cols + j0 + c;
+  float acc = 0.0f;  // lanes 0..15: dgamma of column c, lanes 16..31: dbeta
+  for (int64_t b0 = 0; b0 < nblk; b0 += kCombChunk) {
+    const int nb = static_cast<int>(nblk - b0 < kCombChunk ? nblk - b0 : kCombChunk);
+    constexpr int kPer = kCombChunk / kCombRowsPerPass;
+    float vg[kPer], vb[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int b = rb + r * kCombRowsPerPass;
+      vg[r] = 0.0f;
+      vb[r] = 0.0f;
+      if (b < nb && col_ok) {
+        vg[r] = wg[(b0 + b) * a.cols];
+        vb[r] = wb[(b0 + b) * a.cols];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int b = rb + r * kCombRowsPerPass;
+      buf[0][b][c] = vg[r];
+      buf[1][b][c] = vb[r];
+    }
+    __syncthreads();
+    if (tid < 2 * kCombCols) {
+      const int arr = tid / kCombCols;
+      for (int b = 0; b < nb; ++b) acc = acc + buf[arr][b][c];
+    }
+    __syncthreads();
   }
-  if (a.dgamma) a.dgamma[j] = accg;
-  if (a.dbeta) a.dbeta[j] = accb;
+  if (tid < 2 * kCombCols && col_ok) {
+    if (tid < kCombCols) {
+      if (a.dgamma) a.dgamma[j0 + c] = acc;
+    } else {
+      if (a.dbeta) a.dbeta[j0 + c] = acc;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm backward, fused: input gradient and parameter-gradient block
+// partials from one read of X and dY.  One workgroup per block of k_block rows
+// with R waves.  The block's rows are taken R at a time: wave w computes the
+// input gradient of row chunk + w exactly as the wave kernel does and stages
+// t_j and dy_j of that row in LDS; then every thread advances the chains of
+// its columns through the R staged rows in row order.  At the end of the
+// block the partials go to the workspace (or to dgamma / dbeta directly when
+// the rows form a single block).
+// ---------------------------------------------------------------------------
+
+constexpr int kFusedChains = 4;  // columns per thread in the chain phase
+
+template <int T, int MAXT, bool PF>
+__global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a, LnParamArgs p,
+                                                                   int R, int64_t nblk) {
+  extern __shared__ float stage[];  // [R][cols] t, then [R][cols] dy
+  const int64_t cols = a.cols;
+  float* st = stage;
+  float* sd = stage + static_cast<int64_t>(R) * cols;
+  const int tid = threadIdx.x;
+  const int nthr = R * kWave;
+  const int lane = tid & (kWave - 1);
+  const int w = tid >> 6;
+  const int64_t beta = blockIdx.x;
+  const int64_t blk = nblk == 1 ? a.rows : p.k_block;
+  const int64_t r0 = beta * blk;
+  const int64_t r1 = (r0 + blk < a.rows) ? r0 + blk : a.rows;
+  const float n = static_cast<float>(cols);
+  float gam[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int64_t j = lane + kWave * t;
+    gam[t] = (a.gamma && j < cols) ? a.gamma[j] : 1.0f;
+  }
+  float pg[kFusedChains], pb[kFusedChains];
+#pragma unroll
+  for (int k = 0; k < kFusedChains; ++k) {
+    pg[k] = 0.0f;
+    pb[k] = 0.0f;
+  }
+  // Rows are software-pipelined (PF): the loads of a wave's next row are
+  // issued before the reductions, the barriers and the chain phase of this
+  // one.  The widest rows load at the top of each pass instead, to stay in
+  // registers.
+  float xv[T], dv[T];
+  auto load_row = [&](int64_t row) {
+    const float* x = a.Y + row * a.ldy;
+    const float* dy = a.dY + row * a.lddy;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      xv[t] = 0.0f;
+      dv[t] = 0.0f;
+      if (j < cols) {
+        xv[t] = x[j];
+        dv[t] = dy[j];
+      }
+    }
+  };
+  if (PF && r0 + w < r1) load_row(r0 + w);
+  for (int64_t c0 = r0; c0 < r1; c0 += R) {
+    const int64_t row = c0 + w;
+    if (row < r1) {
+      if (!PF) load_row(row);
+      float* dx = a.dX + row * a.lddx;
+      const float mean = a.mean[row], rstd = a.rstd[row];
+      float tv[T], gv[T];
+      float q = 0.0f;
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int64_t j = lane + kWave * t;
+        tv[t] = 0.0f;
+        gv[t] = 0.0f;
+        if (j < cols) {
+          const float d = xv[t] - mean;
+          tv[t] = d * rstd;
+          gv[t] = a.gamma ? dv[t] * gam[t] : dv[t];
+          st[w * cols + j] = tv[t];
+          sd[w * cols + j] = dv[t];
+        }
+        q = q + gv[t];
+      }
+      if (PF && row + R < r1) load_row(row + R);
+      const float am = wave_tree_sum(q) / n;
+      float q2 = 0.0f;
+#pragma unroll
+      for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);
+      const float bm = wave_tree_sum(q2) / n;
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int64_t j = lane + kWave * t;
+        if (j < cols) {
+          const float u = gv[t] - am;
+          const float tb = tv[t] * bm;
+          const float wv = u - tb;
+          dx[j] = rstd * wv;
+        }
+      }
+    }
+    lds_only_barrier();
+    const int nr = static_cast<int>(r1 - c0 < R ? r1 - c0 : R);
+#pragma unroll
+    for (int k = 0; k < kFusedChains; ++k) {
+      const int64_t j = tid + static_cast<int64_t>(k) * nthr;
+      if (j < cols) {
+        for (int rr = 0; rr < nr; ++rr) {
+          const float dyv = sd[rr * cols + j];
+          pg[k] = __builtin_fmaf(dyv, st[rr * cols + j], pg[k]);
+          pb[k] = pb[k] + dyv;
+        }
+      }
+    }
+    lds_only_barrier();
+  }
+#pragma unroll
+  for (int k = 0; k < kFusedChains; ++k) {
+    const int64_t j = tid + static_cast<int64_t>(k) * nthr;
+    if (j < cols) {
+      if (nblk == 1) {
+        if (p.dgamma) p.dgamma[j] = pg[k];
+        if (p.dbeta) p.dbeta[j] = pb[k];
+      } else {
+        p.ws[beta * cols + j] = pg[k];
+        p.ws[(nblk + beta) * cols + j] = pb[k];
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -353,6 +528,20 @@ WaveBwdKernel pick_layernorm_bwd(int64_t cols) {
   return layernorm_bwd_wave_kernel<32>;
 }
 
+using FusedKernel = void (*)(RowBwdArgs, LnParamArgs, int, int64_t);
+
+// Kernels for R <= 16 waves (1024 threads) up to 768 columns; wider rows
+// take R <= 8 so that they keep their registers.
+FusedKernel pick_layernorm_fused(int64_t cols) {
+  if (cols <= kWave * 1) return layernorm_bwd_fused_kernel<1, 1024, true>;
+  if (cols <= kWave * 2) return layernorm_bwd_fused_kernel<2, 1024, true>;
+  if (cols <= kWave * 4) return layernorm_bwd_fused_kernel<4, 1024, true>;
+  if (cols <= kWave * 8) return layernorm_bwd_fused_kernel<8, 1024, true>;
+  if (cols <= kWave * 12) return layernorm_bwd_fused_kernel<12, 1024, true>;
+  if (cols <= kWave * 16) return layernorm_bwd_fused_kernel<16, 512, true>;
+  return layernorm_bwd_fused_kernel<32, 512, false>;
+}
+
 unsigned row_grid(int64_t rows) {
   const int64_t cap = int64_t(1) << 30;
   return static_cast<unsigned>(rows < cap ? rows : cap);
@@ -405,6 +594,13 @@ int64_t layernorm_param_grid(int64_t rows, int64_t cols, int64_t k_block) {
   return layernorm_param_blocks(rows, k_block) * groups;
 }
 
+hipError_t launch_layernorm_param_combine(const LnParamArgs& a, int64_t nblk, hipStream_t s) {
+  const int64_t groups = (a.cols + kCombCols - 1) / kCombCols;
+  hipLaunchKernelGGL(layernorm_param_combine_kernel, dim3(static_cast<unsigned>(groups)),
+                     dim3(kCombThreads), 0, s, a, nblk);
+  return hipGetLastError();
+}
+
 hipError_t launch_layernorm_param(const LnParamArgs& a, hipStream_t s) {
   const int64_t nblk = layernorm_param_blocks(a.rows, a.k_block);
   const int64_t blk = nblk == 1 ? a.rows : a.k_block;
@@ -413,9 +609,46 @@ hipError_t launch_layernorm_param(const LnParamArgs& a, hipStream_t s) {
                      dim3(kParamThreads), 0, s, a, groups, blk, nblk);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nblk == 1) return e;
-  hipLaunchKernelGGL(layernorm_param_combine_kernel, dim3(static_cast<unsigned>(groups)),
-                     dim3(kParamThreads), 0, s, a, nblk);
-  return hipGetLastError();
+  return launch_layernorm_param_combine(a, nblk, s);
+}
+
+// Dynamic LDS a workgroup may use on the current device, at most 128 KiB.
+int64_t lds_budget_bytes() {
+  int dev = 0, v = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+      v <= 0)
+    return 64 * 1024;
+  return v < 128 * 1024 ? v : 128 * 1024;
+}
+
+int layernorm_fused_rows(int64_t rows, int64_t cols, int64_t k_block, int requested) {
+  // R rows staged per pass: LDS holds 2 * R * cols floats; the chain phase
+  // needs R * 64 * kFusedChains >= cols; R * 64 within the kernel's bound.
+  // Without a request: 16 rows per pass while there are fewer row blocks
+  // than two per compute unit, else 8 (smaller workgroups, more of them
+  // resident per compute unit).
+  const int64_t c = cols > 0 ? cols : 1;
+  const int64_t fit = lds_budget_bytes() / (8 * c);
+  const int64_t rmax = c <= kWave * 12 ? 16 : 8;
+  const int64_t rmin = (c + kWave * kFusedChains - 1) / (kWave * kFusedChains);
+  int64_t r = fit < rmax ? fit : rmax;
+  if (requested <= 0 && layernorm_param_blocks(rows, k_block) >= 512) requested = 8;
+  if (requested > 0 && requested < r) r = requested;
+  if (r < rmin) r = rmin;
+  if (r > fit || r > rmax) return 0;  // does not fit: use the unfused kernels
+  return static_cast<int>(r);
+}
+
+hipError_t launch_layernorm_bwd_fused(const RowBwdArgs& a, const LnParamArgs& p, int R,
+                                      hipStream_t s) {
+  const int64_t nblk = layernorm_param_blocks(a.rows, p.k_block);
+  const size_t lds = sizeof(float) * 2 * static_cast<size_t>(R) * static_cast<size_t>(a.cols);
+  hipLaunchKernelGGL(pick_layernorm_fused(a.cols), dim3(static_cast<unsigned>(nblk)),
+                     dim3(R * kWave), lds, s, a, p, R, nblk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nblk == 1) return e;
+  return launch_layernorm_param_combine(p, nblk, s);
 }
 
 hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,

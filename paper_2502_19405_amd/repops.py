@@ -174,8 +174,28 @@ def _mat(t: torch.Tensor, name: str):
     raise ValueError(f"{name}: needs unit stride along one dimension (got strides {t.stride()})")
 
 
+_STRUCTS: dict = {}
+
+
+def _ord(order):
+    """ctypes reference to the descriptor struct of `order` (default if None),
+    built once per distinct descriptor."""
+    o = order or _DEFAULT_ORDER
+    r = _STRUCTS.get(o)
+    if r is None:
+        c = o.c()
+        r = _STRUCTS[o] = (c, ctypes.byref(c))
+    return r[1]
+
+
 def _launch(launch):
-    return None if launch is None else ctypes.byref(launch.c())
+    if launch is None:
+        return None
+    r = _STRUCTS.get(launch)
+    if r is None:
+        c = launch.c()
+        r = _STRUCTS[launch] = (c, ctypes.byref(c))
+    return r[1]
 
 
 def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
@@ -196,7 +216,7 @@ def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
         if bias.shape != (n,) or not bias.is_contiguous():
             raise ValueError("bias must be a contiguous [n] tensor")
         pbias = _dev(bias, "bias")
-    rc = load().repops_matmul(ctypes.byref((order or _DEFAULT_ORDER).c()), m, n, k, pa, lda, ta,
+    rc = load().repops_matmul(_ord(order), m, n, k, pa, lda, ta,
                               pb, ldb, tb, pbias, _dev(out, "out"), max(out.stride(0), n, 1),
                               _launch(launch), _stream(out))
     _check(rc, "repops_matmul")
@@ -211,7 +231,7 @@ def bmm_raw(batch0: int, batch1: int, m: int, n: int, k: int,
             order: Order | None = None, launch: Launch | None = None):
     """The C-ABI bmm on raw element strides over the storage of A, B, C
     (offsets in elements from each tensor's data pointer)."""
-    rc = load().repops_bmm(ctypes.byref((order or _DEFAULT_ORDER).c()), batch0, batch1, m, n, k,
+    rc = load().repops_bmm(_ord(order), batch0, batch1, m, n, k,
                            _dev(A, "A") + 4 * a_offset, sa0, sa1, lda, trans_a,
                            _dev(B, "B") + 4 * b_offset, sb0, sb1, ldb, trans_b, alpha,
                            _dev(C, "C") + 4 * c_offset, sc0, sc1, ldc, _launch(launch), _stream(C))
@@ -236,7 +256,7 @@ def bmm(A: torch.Tensor, B: torch.Tensor, alpha: float = 1.0, order: Order | Non
         out = torch.empty((b0, b1, m, n), dtype=torch.float32, device=A.device)
     if out.stride(3) != 1:
         raise ValueError("out must be row-major in its last two dimensions")
-    rc = load().repops_bmm(ctypes.byref((order or _DEFAULT_ORDER).c()), b0, b1, m, n, k,
+    rc = load().repops_bmm(_ord(order), b0, b1, m, n, k,
                            _dev(A, "A"), A.stride(0), A.stride(1), lda, ta,
                            _dev(B, "B"), B.stride(0), B.stride(1), ldb, tb, float(alpha),
                            _dev(out, "out"), out.stride(0), out.stride(1),
@@ -257,7 +277,7 @@ def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = 
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
     _, _, ldy = _rows(out, "out")
-    rc = load().repops_softmax_rows(ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols,
+    rc = load().repops_softmax_rows(_ord(order), rows, cols,
                                     _dev(X, "X"), ldx, _dev(out, "out"), ldy, causal_period,
                                     _launch(launch), _stream(out))
     _check(rc, "repops_softmax_rows")
@@ -282,7 +302,7 @@ def layernorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None,
         if t.numel() != size or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous [{size}] tensor")
         ptrs.append(_dev(t, name))
-    rc = load().repops_layernorm_rows(ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols,
+    rc = load().repops_layernorm_rows(_ord(order), rows, cols,
                                       _dev(X, "X"), ldx, ptrs[0], ptrs[1], float(eps),
                                       _dev(out, "out"), ldy, ptrs[2], ptrs[3], _launch(launch),
                                       _stream(out))
@@ -297,7 +317,7 @@ def _elementwise(fn_name: str, X: torch.Tensor, order, launch, out):
         out = torch.empty_like(X)
     if not out.is_contiguous() or out.numel() != X.numel():
         raise ValueError("out must be contiguous with X's element count")
-    rc = getattr(load(), fn_name)(ctypes.byref((order or _DEFAULT_ORDER).c()), X.numel(),
+    rc = getattr(load(), fn_name)(_ord(order), X.numel(),
                                   _dev(X, "X"), _dev(out, "out"), _launch(launch), _stream(out))
     _check(rc, fn_name)
     return out
@@ -329,7 +349,7 @@ def softmax_backward_rows(Y: torch.Tensor, dY: torch.Tensor, causal_period: int 
         out = torch.empty_like(Y, memory_format=torch.contiguous_format)
     _, _, lddx = _rows(out, "out")
     rc = load().repops_softmax_backward_rows(
-        ctypes.byref((order or _DEFAULT_ORDER).c()), rows, cols, _dev(Y, "Y"), ldy,
+        _ord(order), rows, cols, _dev(Y, "Y"), ldy,
         _dev(dY, "dY"), lddy, _dev(out, "out"), lddx, causal_period, _launch(launch), _stream(out))
     _check(rc, "repops_softmax_backward_rows")
     return out
@@ -338,7 +358,7 @@ def softmax_backward_rows(Y: torch.Tensor, dY: torch.Tensor, causal_period: int 
 def layernorm_backward_workspace(rows: int, cols: int, order: Order | None = None) -> int:
     """Bytes of workspace the LayerNorm backward needs for its parameter gradients."""
     n = ctypes.c_uint64(0)
-    rc = load().repops_layernorm_backward_workspace(ctypes.byref((order or _DEFAULT_ORDER).c()),
+    rc = load().repops_layernorm_backward_workspace(_ord(order),
                                                     rows, cols, ctypes.byref(n))
     _check(rc, "repops_layernorm_backward_workspace")
     return n.value
@@ -349,11 +369,12 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
                             need_dx: bool = True, need_params: bool = True,
                             order: Order | None = None, launch: Launch | None = None,
                             dx_out: torch.Tensor | None = None,
+                            dgamma_out: torch.Tensor | None = None,
+                            dbeta_out: torch.Tensor | None = None,
                             workspace: torch.Tensor | None = None):
     """(dX, dgamma, dbeta) of the row LayerNorm from the forward's mean / rstd;
-    entries not requested are None.  The workspace is allocated here when
-    none is passed."""
-    order = order or _DEFAULT_ORDER
+    entries not requested are None.  Outputs and the workspace are allocated
+    here unless passed (the library checks the workspace's size)."""
     rows, cols, ldx = _rows(X, "X")
     r2, c2, lddy = _rows(dY, "dY")
     if (r2, c2) != (rows, cols):
@@ -373,16 +394,22 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
         _, _, lddx = _rows(dx, "dx_out")
     wptr, wbytes = None, 0
     if need_params:
-        dgamma = torch.empty(cols, dtype=torch.float32, device=X.device)
-        dbeta = torch.empty(cols, dtype=torch.float32, device=X.device)
-        need = layernorm_backward_workspace(rows, cols, order)
-        if need:
-            if workspace is None:
+        dgamma = dgamma_out if dgamma_out is not None else torch.empty(cols, dtype=torch.float32,
+                                                                       device=X.device)
+        dbeta = dbeta_out if dbeta_out is not None else torch.empty(cols, dtype=torch.float32,
+                                                                    device=X.device)
+        for t, name in ((dgamma, "dgamma_out"), (dbeta, "dbeta_out")):
+            if t.numel() != cols or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous [{cols}] tensor")
+        if workspace is None:
+            need = layernorm_backward_workspace(rows, cols, order)
+            if need:
                 workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
+        if workspace is not None:
             wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
     ptr = lambda t, n: None if t is None else _dev(t, n)  # noqa: E731
     rc = load().repops_layernorm_backward_rows(
-        ctypes.byref(order.c()), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
+        _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
         _dev(mean, "mean"), _dev(rstd, "rstd"), pg, ptr(dx, "dX"), lddx, ptr(dgamma, "dgamma"),
         ptr(dbeta, "dbeta"), wptr, wbytes, _launch(launch), _stream(X))
     _check(rc, "repops_layernorm_backward_rows")
@@ -398,7 +425,7 @@ def gelu_backward(X: torch.Tensor, dY: torch.Tensor, order: Order | None = None,
         out = torch.empty_like(X)
     if not out.is_contiguous() or out.numel() != X.numel():
         raise ValueError("out must be contiguous with X's element count")
-    rc = load().repops_gelu_backward(ctypes.byref((order or _DEFAULT_ORDER).c()), X.numel(),
+    rc = load().repops_gelu_backward(_ord(order), X.numel(),
                                      _dev(X, "X"), _dev(dY, "dY"), _dev(out, "out"),
                                      _launch(launch), _stream(out))
     _check(rc, "repops_gelu_backward")
@@ -416,7 +443,7 @@ def adam_step(param: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor,
                     (exp_avg_sq, "exp_avg_sq")):
         if not t.is_contiguous() or t.numel() != n:
             raise ValueError(f"{name} must be contiguous with {n} elements")
-    rc = load().repops_adam_step(ctypes.byref((order or _DEFAULT_ORDER).c()), n,
+    rc = load().repops_adam_step(_ord(order), n,
                                  _dev(param, "param"), _dev(grad, "grad"),
                                  _dev(exp_avg, "exp_avg"), _dev(exp_avg_sq, "exp_avg_sq"),
                                  float(lr), float(beta1), float(beta2), float(eps),
