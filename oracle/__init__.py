@@ -94,6 +94,20 @@ def _declare(lib):
         "repops_ref_adam_step": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _flt, _flt, _flt, _flt,
                                         _flt, _i64, _int, _int]),
         "repops_ref_adam_scalars": (_int, [_flt, _flt, _flt, _flt, _i64, _f32p]),
+        "repops_ref_sincos1": (None, [_flt, _f32p, _f32p]),
+        "repops_ref_sincos": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
+        "repops_ref_rope": (_int, [_i64, _i64, _i64, _f32p, _i64, _f32p, _i64, _i64, _int, _f32p,
+                                   _i64, _int]),
+        "repops_ref_rmsnorm_rows": (_int, [_int, _int, _i64, _i64, _f32p, _i64, _f32p, _flt,
+                                           _f32p, _i64, _f32p, _int]),
+        "repops_ref_rmsnorm_backward_rows": (_int, [_int, _int, _i64, _i64, _i64, _f32p, _i64,
+                                                    _f32p, _i64, _f32p, _f32p, _f32p, _i64, _f32p,
+                                                    _int]),
+        "repops_ref_silu1": (_flt, [_flt]),
+        "repops_ref_silu_grad1": (_flt, [_flt]),
+        "repops_ref_silu": (_int, [_i64, _f32p, _f32p, _int]),
+        "repops_ref_swiglu": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
+        "repops_ref_swiglu_backward": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _f32p, _int]),
     })
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -338,3 +352,93 @@ def adam_scalars(lr, beta1, beta2, weight_decay, step, lib=None):
                                                  int(step), _p(out))
     _check(rc, "adam_scalars")
     return out
+
+
+# --------------------------------------------------------------------------
+# Llama-block operators
+# --------------------------------------------------------------------------
+
+def sincos1(x, lib=None):
+    s, c = ctypes.c_float(), ctypes.c_float()
+    (lib or load()).repops_ref_sincos1(float(np.float32(x)), ctypes.byref(s), ctypes.byref(c))
+    return np.float32(s.value), np.float32(c.value)
+
+
+def sincos(x, nthreads=0, lib=None):
+    x = np.ascontiguousarray(x, np.float32)
+    s, c = np.empty_like(x), np.empty_like(x)
+    _check((lib or load()).repops_ref_sincos(x.size, _p(x), _p(s), _p(c), nthreads), "sincos")
+    return s, c
+
+
+def rope(X, heads, head_dim, inv_freq, period=0, offset=0, inverse=False, nthreads=0, lib=None):
+    """X [rows, heads * head_dim] (contiguous); returns the rotated copy."""
+    X = np.ascontiguousarray(X, np.float32)
+    rows = X.shape[0]
+    Y = np.empty_like(X)
+    rc = (lib or load()).repops_ref_rope(rows, heads, head_dim, _p(X), X.shape[1],
+                                         _p(np.ascontiguousarray(inv_freq, np.float32)), period,
+                                         offset, int(inverse), _p(Y), X.shape[1], nthreads)
+    _check(rc, "rope")
+    return Y
+
+
+def rmsnorm_rows(X, gamma=None, eps=1e-5, row_width=64, row_combine=ROW_TREE, nthreads=0,
+                 lib=None, with_stats=False):
+    X = np.ascontiguousarray(X, np.float32)
+    rows, cols = X.shape
+    Y = np.empty_like(X)
+    rstd = np.empty(rows, np.float32)
+    rc = (lib or load()).repops_ref_rmsnorm_rows(row_width, row_combine, rows, cols, _p(X), cols,
+                                                 _p(gamma), float(np.float32(eps)), _p(Y), cols,
+                                                 _p(rstd), nthreads)
+    _check(rc, "rmsnorm_rows")
+    return (Y, rstd) if with_stats else Y
+
+
+def rmsnorm_backward_rows(X, dY, rstd, gamma=None, row_width=64, row_combine=ROW_TREE,
+                          k_block=64, want_dx=True, want_params=True, nthreads=0, lib=None):
+    """Returns (dX, dgamma); entries not requested are None."""
+    X = np.ascontiguousarray(X, np.float32)
+    dY = np.ascontiguousarray(dY, np.float32)
+    rows, cols = X.shape
+    dX = np.empty_like(X) if want_dx else None
+    dg = np.empty(cols, np.float32) if want_params else None
+    rc = (lib or load()).repops_ref_rmsnorm_backward_rows(
+        row_width, row_combine, k_block, rows, cols, _p(X), cols, _p(dY), cols,
+        _p(np.ascontiguousarray(rstd, np.float32)), _p(gamma), _p(dX), cols, _p(dg), nthreads)
+    _check(rc, "rmsnorm_backward_rows")
+    return dX, dg
+
+
+def silu1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_silu1(float(np.float32(x))))
+
+
+def silu_grad1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_silu_grad1(float(np.float32(x))))
+
+
+def silu(x, nthreads=0, lib=None):
+    x = np.ascontiguousarray(x, np.float32)
+    y = np.empty_like(x)
+    _check((lib or load()).repops_ref_silu(x.size, _p(x), _p(y), nthreads), "silu")
+    return y
+
+
+def swiglu(g, u, nthreads=0, lib=None):
+    g = np.ascontiguousarray(g, np.float32)
+    u = np.ascontiguousarray(u, np.float32)
+    y = np.empty_like(g)
+    _check((lib or load()).repops_ref_swiglu(g.size, _p(g), _p(u), _p(y), nthreads), "swiglu")
+    return y
+
+
+def swiglu_backward(g, u, dy, nthreads=0, lib=None):
+    g = np.ascontiguousarray(g, np.float32)
+    u = np.ascontiguousarray(u, np.float32)
+    dy = np.ascontiguousarray(dy, np.float32)
+    dg, du = np.empty_like(g), np.empty_like(g)
+    _check((lib or load()).repops_ref_swiglu_backward(g.size, _p(g), _p(u), _p(dy), _p(dg),
+                                                      _p(du), nthreads), "swiglu_backward")
+    return dg, du

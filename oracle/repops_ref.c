@@ -649,6 +649,384 @@ int repops_ref_layernorm_rows(int row_width, int row_combine, int64_t rows, int6
 }
 
 /* ========================================================================= */
+/* Llama-block operators: sin/cos and rotary embedding, RMSNorm, SiLU/SwiGLU  */
+/* ========================================================================= */
+
+/*
+ * The Llama programs of Section 4.2 add rotary position embeddings, RMSNorm
+ * and the SiLU-gated feed-forward to the operators above.  Section 3.1 lists
+ * the math functions RepOps rebuilds with a controlled order; sin and cos are
+ * rebuilt here in the style of exp: Cody and Waite's additive reduction by
+ * pi/2 (pi/2 split in three binary32 parts), Taylor polynomials on
+ * |r| <= pi/4 by Horner's rule with fused multiply-adds, quadrant selection.
+ * Reading (op sequence):
+ *   non-finite x: both results NaN;  x = +-0: (sin, cos) = (x, 1);
+ *   n = rint(x * RN(2/pi)) (ties to even);
+ *   n = 0: r = x; else r = fma(n, -P1, x); r = fma(n, -P2, r); r = fma(n, -P3, r)
+ *     with P1 = RN(pi/2), P2 = RN(pi/2 - P1), P3 = RN(pi/2 - P1 - P2);
+ *   u = r*r;
+ *   sin part: p = fma(S9, u, S7); p = fma(p, u, S5); p = fma(p, u, S3);
+ *             s = fma(r*u, p, r)                 (S_k = RN((-1)^((k-1)/2) / k!));
+ *   cos part: p = fma(C10, u, C8); p = fma(p, u, C6); p = fma(p, u, C4);
+ *             p = fma(p, u, C2); c = fma(u, p, 1) (C_k = RN((-1)^(k/2) / k!));
+ *   q = n - 4 floor(n/4) (exact, in {0,1,2,3}):
+ *     (sin, cos) = (s, c), (c, -s), (-s, -c), (-c, s) for q = 0..3.
+ * Accurate to a few ulp for |x| <= 2^17 (the angles of rotary embeddings);
+ * beyond that the results stay reproducible but lose accuracy.
+ */
+static const float SC_TWO_OVER_PI = 0x1.45f306p-1f;
+static const float SC_P1 = 0x1.921fb6p+0f;
+static const float SC_P2 = -0x1.777a5cp-25f;
+static const float SC_P3 = -0x1.ee59dap-50f;
+static const float SC_S3 = -0x1.555556p-3f;  /* -1/3! */
+static const float SC_S5 = 0x1.111112p-7f;   /* 1/5! */
+static const float SC_S7 = -0x1.a01a02p-13f; /* -1/7! */
+static const float SC_S9 = 0x1.71de3ap-19f;  /* 1/9! */
+static const float SC_C2 = -0x1p-1f;         /* -1/2! */
+static const float SC_C4 = 0x1.555556p-5f;   /* 1/4! */
+static const float SC_C6 = -0x1.6c16c2p-10f; /* -1/6! */
+static const float SC_C8 = 0x1.a01a02p-16f;  /* 1/8! */
+static const float SC_C10 = -0x1.27e4fcp-22f; /* -1/10! */
+
+void repops_ref_sincos1(float x, float *sin_out, float *cos_out)
+{
+    if (!isfinite(x)) {
+        *sin_out = NAN;
+        *cos_out = NAN;
+        return;
+    }
+    if (x == 0.0f) { /* keeps the sign of zero, which the fused step would lose */
+        *sin_out = x;
+        *cos_out = 1.0f;
+        return;
+    }
+    const float t = x * SC_TWO_OVER_PI;
+    const float n = rintf(t);
+    float r = x;
+    if (n != 0.0f) {
+        r = fmaf(n, -SC_P1, x);
+        r = fmaf(n, -SC_P2, r);
+        r = fmaf(n, -SC_P3, r);
+    }
+    const float u = r * r;
+    float ps = fmaf(SC_S9, u, SC_S7);
+    ps = fmaf(ps, u, SC_S5);
+    ps = fmaf(ps, u, SC_S3);
+    const float r3 = r * u;
+    const float sv = fmaf(r3, ps, r);
+    float pc = fmaf(SC_C10, u, SC_C8);
+    pc = fmaf(pc, u, SC_C6);
+    pc = fmaf(pc, u, SC_C4);
+    pc = fmaf(pc, u, SC_C2);
+    const float cv = fmaf(u, pc, 1.0f);
+    const float quarter = n * 0.25f;
+    const float fq = n - 4.0f * floorf(quarter);
+    const int q = (int)fq;
+    if (q == 0) { *sin_out = sv; *cos_out = cv; }
+    else if (q == 1) { *sin_out = cv; *cos_out = -sv; }
+    else if (q == 2) { *sin_out = -sv; *cos_out = -cv; }
+    else { *sin_out = -cv; *cos_out = sv; }
+}
+
+typedef struct {
+    const float *x;
+    float *s, *c;
+} sc_ctx;
+
+static void sincos_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const sc_ctx *k = (const sc_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) {
+        float sv, cv;
+        repops_ref_sincos1(k->x[i], &sv, &cv);
+        if (k->s) k->s[i] = sv;
+        if (k->c) k->c[i] = cv;
+    }
+}
+
+int repops_ref_sincos(int64_t n, const float *x, float *s, float *c, int nthreads)
+{
+    if (n < 0) return -1;
+    sc_ctx k = {x, s, c};
+    parallel_for(nthreads, n, sincos_range, &k);
+    return 0;
+}
+
+/*
+ * Rotary position embedding (rotate-half pairing within each head): row r of
+ * X holds `heads` heads of `head_dim` (even) values; its position is
+ * p = r mod period (period 0: p = r) plus offset.  For i < head_dim/2:
+ *   angle = RN(p * inv_freq[i])  (p converted exactly: p < 2^24);
+ *   c, s = cos_rep(angle), sin_rep(angle);
+ *   x1 = X[.., i], x2 = X[.., i + head_dim/2];
+ *   forward: y1 = RN(RN(x1 c) - RN(x2 s)),  y2 = RN(RN(x2 c) + RN(x1 s));
+ *   inverse (the backward, rotation by -angle):
+ *            y1 = RN(RN(x1 c) + RN(x2 s)),  y2 = RN(RN(x2 c) - RN(x1 s)).
+ * inv_freq is the model's frequency table, an input like a weight.
+ */
+typedef struct {
+    int64_t heads, hd, period, offset;
+    const float *X; int64_t ldx;
+    const float *inv_freq;
+    float *Y; int64_t ldy;
+    int inverse;
+} rope_ctx;
+
+static void rope_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const rope_ctx *c = (const rope_ctx *)vctx;
+    const int64_t half = c->hd / 2;
+    for (int64_t r = r0; r < r1; ++r) {
+        const int64_t p = (c->period > 0 ? r % c->period : r) + c->offset;
+        const float pf = (float)p;
+        const float *x = c->X + r * c->ldx;
+        float *y = c->Y + r * c->ldy;
+        for (int64_t i = 0; i < half; ++i) {
+            const float angle = pf * c->inv_freq[i];
+            float sv, cv;
+            repops_ref_sincos1(angle, &sv, &cv);
+            for (int64_t h = 0; h < c->heads; ++h) {
+                const float x1 = x[h * c->hd + i], x2 = x[h * c->hd + i + half];
+                const float a = x1 * cv, b = x2 * sv, d = x2 * cv, e = x1 * sv;
+                if (!c->inverse) {
+                    y[h * c->hd + i] = a - b;
+                    y[h * c->hd + i + half] = d + e;
+                } else {
+                    y[h * c->hd + i] = a + b;
+                    y[h * c->hd + i + half] = d - e;
+                }
+            }
+        }
+    }
+}
+
+int repops_ref_rope(int64_t rows, int64_t heads, int64_t head_dim, const float *X, int64_t ldx,
+                    const float *inv_freq, int64_t period, int64_t offset, int inverse,
+                    float *Y, int64_t ldy, int nthreads)
+{
+    if (rows < 0 || heads < 0 || head_dim < 0 || (head_dim & 1) || period < 0 || offset < 0)
+        return -1;
+    if (rows > 0 && (period > 0 ? period - 1 : rows - 1) + offset >= (int64_t)1 << 24) return -1;
+    rope_ctx c = {heads, head_dim, period, offset, X, ldx, inv_freq, Y, ldy, inverse};
+    parallel_for(nthreads, rows, rope_range, &c);
+    return 0;
+}
+
+/*
+ * RMSNorm (Llama's normalisation), with the row order of c2:
+ *   ms = rowsum(fma(x_j, x_j, .)) / n;  rstd = 1 / sqrt(ms + eps);
+ *   t_j = x_j * rstd;  y_j = t_j * gamma_j (t_j when gamma is absent).
+ * Backward, from the forward's rstd:
+ *   g_j = dy_j * gamma_j (dy_j);  b = rowsum(fma(g_j, t_j, .)) / n;
+ *   dx_j = rstd * (g_j - t_j * b);
+ *   dgamma_j = sum over rows of dy_ij * t_ij with the contraction rule
+ *   (blocks of k_block rows, fma chains, block partials left to right).
+ */
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *X; int64_t ldx;
+    const float *gamma;
+    float eps;
+    float *Y; int64_t ldy;
+    float *rstd_out;
+} rms_ctx;
+
+static void rms_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const rms_ctx *c = (const rms_ctx *)vctx;
+    const float nf = (float)c->cols;
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *x = c->X + r * c->ldx;
+        float *y = c->Y + r * c->ldy;
+        const float q = rowsum_terms(c->W, c->combine, c->cols, c->cols, x, NULL, 1);
+        const float ms = q / nf;
+        const float ve = ms + c->eps;
+        const float sd = sqrtf(ve);
+        const float rstd = 1.0f / sd;
+        for (int64_t j = 0; j < c->cols; ++j) {
+            const float t = x[j] * rstd;
+            y[j] = c->gamma ? t * c->gamma[j] : t;
+        }
+        if (c->rstd_out) c->rstd_out[r] = rstd;
+    }
+}
+
+int repops_ref_rmsnorm_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                            const float *X, int64_t ldx, const float *gamma, float eps,
+                            float *Y, int64_t ldy, float *rstd_out, int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || rows < 0 || cols < 0) return -1;
+    if (rows > 0 && cols == 0) return -1;
+    rms_ctx c = {row_width, row_combine, cols, X, ldx, gamma, eps, Y, ldy, rstd_out};
+    parallel_for(nthreads, rows, rms_range, &c);
+    return 0;
+}
+
+typedef struct {
+    int W, combine;
+    int64_t cols;
+    const float *X; int64_t ldx;
+    const float *dY; int64_t lddy;
+    const float *rstd, *gamma;
+    float *dX; int64_t lddx;
+} rmsb_ctx;
+
+static void rms_bwd_range(void *vctx, int64_t r0, int64_t r1)
+{
+    const rmsb_ctx *c = (const rmsb_ctx *)vctx;
+    const size_t n = (size_t)(c->cols > 0 ? c->cols : 1);
+    float *t = (float *)malloc(sizeof(float) * n);
+    float *g = (float *)malloc(sizeof(float) * n);
+    if (!t || !g) abort();
+    const float nf = (float)c->cols;
+    for (int64_t r = r0; r < r1; ++r) {
+        const float *x = c->X + r * c->ldx;
+        const float *dy = c->dY + r * c->lddy;
+        float *dx = c->dX + r * c->lddx;
+        const float rstd = c->rstd[r];
+        for (int64_t j = 0; j < c->cols; ++j) {
+            t[j] = x[j] * rstd;
+            g[j] = c->gamma ? dy[j] * c->gamma[j] : dy[j];
+        }
+        const float b = rowsum_terms(c->W, c->combine, c->cols, c->cols, g, t, 2) / nf;
+        for (int64_t j = 0; j < c->cols; ++j) {
+            const float tb = t[j] * b;
+            const float w = g[j] - tb;
+            dx[j] = rstd * w;
+        }
+    }
+    free(t);
+    free(g);
+}
+
+typedef struct {
+    int64_t k_block, rows, cols;
+    const float *X; int64_t ldx;
+    const float *dY; int64_t lddy;
+    const float *rstd;
+    float *dgamma;
+} rmsp_ctx;
+
+static void rms_param_range(void *vctx, int64_t j0, int64_t j1)
+{
+    const rmsp_ctx *c = (const rmsp_ctx *)vctx;
+    const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;
+    for (int64_t j = j0; j < j1; ++j) {
+        float acc = 0.0f;
+        for (int64_t i0 = 0; i0 < c->rows; i0 += blk) {
+            const int64_t i1 = (i0 + blk < c->rows) ? i0 + blk : c->rows;
+            float pg = 0.0f;
+            for (int64_t i = i0; i < i1; ++i) {
+                const float t = c->X[i * c->ldx + j] * c->rstd[i];
+                pg = fmaf(c->dY[i * c->lddy + j], t, pg);
+            }
+            acc = acc + pg;
+        }
+        c->dgamma[j] = acc;
+    }
+}
+
+int repops_ref_rmsnorm_backward_rows(int row_width, int row_combine, int64_t k_block,
+                                     int64_t rows, int64_t cols, const float *X, int64_t ldx,
+                                     const float *dY, int64_t lddy, const float *rstd,
+                                     const float *gamma, float *dX, int64_t lddx, float *dgamma,
+                                     int nthreads)
+{
+    if (check_order_rows(row_width, row_combine) || k_block < 0 || rows < 0 || cols < 0)
+        return -1;
+    if (rows > 0 && cols == 0) return -1;
+    if (dX) {
+        rmsb_ctx c = {row_width, row_combine, cols, X, ldx, dY, lddy, rstd, gamma, dX, lddx};
+        parallel_for(nthreads, rows, rms_bwd_range, &c);
+    }
+    if (dgamma) {
+        rmsp_ctx p = {k_block, rows, cols, X, ldx, dY, lddy, rstd, dgamma};
+        parallel_for(nthreads, cols, rms_param_range, &p);
+    }
+    return 0;
+}
+
+/*
+ * SiLU and the SiLU-gated unit of Llama's feed-forward (op sequences):
+ *   silu(x) = x / (1 + exp_rep(-x));  swiglu(g, u) = RN(silu(g) * u);
+ *   backward: s = 1 / (1 + exp_rep(-g)); silu'(g) = fma(g*s, 1 - s, s)
+ *     (= s + g s (1 - s));  dgate = RN(RN(dy * u) * silu'(g));
+ *     dup = RN(dy * silu(g)) with silu(g) recomputed as in the forward.
+ */
+float repops_ref_silu1(float x)
+{
+    const float w = -x;
+    const float d = 1.0f + repops_ref_exp1(w);
+    return x / d;
+}
+
+float repops_ref_silu_grad1(float x)
+{
+    const float w = -x;
+    const float d = 1.0f + repops_ref_exp1(w);
+    const float s = 1.0f / d;
+    const float om = 1.0f - s;
+    const float xs = x * s;
+    return fmaf(xs, om, s);
+}
+
+typedef struct {
+    const float *g, *u, *dy;
+    float *y, *dg, *du;
+} sw_ctx;
+
+static void silu_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const sw_ctx *c = (const sw_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) c->y[i] = repops_ref_silu1(c->g[i]);
+}
+
+static void swiglu_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const sw_ctx *c = (const sw_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) c->y[i] = repops_ref_silu1(c->g[i]) * c->u[i];
+}
+
+static void swiglu_bwd_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const sw_ctx *c = (const sw_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) {
+        const float gi = c->g[i], ui = c->u[i], dyi = c->dy[i];
+        const float dyu = dyi * ui;
+        const float dgv = dyu * repops_ref_silu_grad1(gi);
+        const float duv = dyi * repops_ref_silu1(gi);
+        c->dg[i] = dgv;
+        c->du[i] = duv;
+    }
+}
+
+int repops_ref_silu(int64_t n, const float *x, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    sw_ctx c = {x, NULL, NULL, y, NULL, NULL};
+    parallel_for(nthreads, n, silu_range, &c);
+    return 0;
+}
+
+int repops_ref_swiglu(int64_t n, const float *g, const float *u, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    sw_ctx c = {g, u, NULL, y, NULL, NULL};
+    parallel_for(nthreads, n, swiglu_range, &c);
+    return 0;
+}
+
+int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const float *dy,
+                               float *dg, float *du, int nthreads)
+{
+    if (n < 0) return -1;
+    sw_ctx c = {g, u, dy, NULL, dg, du};
+    parallel_for(nthreads, n, swiglu_bwd_range, &c);
+    return 0;
+}
+
+/* ========================================================================= */
 /* Training-step operators                                                   */
 /* ========================================================================= */
 

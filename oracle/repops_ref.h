@@ -104,6 +104,39 @@ int repops_ref_layernorm_rows(int row_width, int row_combine, int64_t rows, int6
                               const float *beta, float eps, float *Y, int64_t ldy,
                               float *mean_out, float *rstd_out, int nthreads);
 
+/* ---- Llama-block operators ---- */
+
+/* Reproducible sin and cos of one argument (both results; NaN for non-finite x). */
+void repops_ref_sincos1(float x, float *sin_out, float *cos_out);
+/* Elementwise; s or c may be NULL. */
+int repops_ref_sincos(int64_t n, const float *x, float *s, float *c, int nthreads);
+
+/* Rotary embedding (rotate-half pairing) of `heads` heads of head_dim values per
+ * row; position of row r = (period > 0 ? r % period : r) + offset; inverse = 1
+ * rotates by -angle (the backward). */
+int repops_ref_rope(int64_t rows, int64_t heads, int64_t head_dim, const float *X, int64_t ldx,
+                    const float *inv_freq, int64_t period, int64_t offset, int inverse,
+                    float *Y, int64_t ldy, int nthreads);
+
+/* RMSNorm rows; gamma may be NULL; rstd_out may be NULL. */
+int repops_ref_rmsnorm_rows(int row_width, int row_combine, int64_t rows, int64_t cols,
+                            const float *X, int64_t ldx, const float *gamma, float eps,
+                            float *Y, int64_t ldy, float *rstd_out, int nthreads);
+/* RMSNorm backward from the forward's rstd; dX / dgamma may be NULL. */
+int repops_ref_rmsnorm_backward_rows(int row_width, int row_combine, int64_t k_block,
+                                     int64_t rows, int64_t cols, const float *X, int64_t ldx,
+                                     const float *dY, int64_t lddy, const float *rstd,
+                                     const float *gamma, float *dX, int64_t lddx, float *dgamma,
+                                     int nthreads);
+
+/* SiLU, the SiLU-gated unit silu(g) * u, and its backward. */
+float repops_ref_silu1(float x);
+float repops_ref_silu_grad1(float x);
+int repops_ref_silu(int64_t n, const float *x, float *y, int nthreads);
+int repops_ref_swiglu(int64_t n, const float *g, const float *u, float *y, int nthreads);
+int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const float *dy,
+                               float *dg, float *du, int nthreads);
+
 /* ---- training-step operators ---- */
 
 /* dX = Y * (dY - rowsum(Y * dY)) per row; masked columns (causal_period > 0:

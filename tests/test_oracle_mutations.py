@@ -13,6 +13,7 @@ import pytest
 import oracle
 import test_oracle as pins
 import test_oracle_training as tpins
+import test_oracle_llama as lpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")
 
@@ -48,7 +49,9 @@ MUTATIONS = {
     # c7: unbiased variance
     "ln_unbiased": ("const float var = q / nf;", "const float var = q / (nf - 1.0f);", ["ln"]),
     # c7: eps outside the square root
-    "ln_eps_outside": ("const float sd = sqrtf(ve);", "const float sd = sqrtf(var) + c->eps;", ["ln"]),
+    "ln_eps_outside": ("const float ve = var + c->eps;\n        const float sd = sqrtf(ve);",
+                       "const float ve = var + c->eps;\n        const float sd = sqrtf(var) + c->eps;",
+                       ["ln"]),
     # softmax backward: sign of the inner product flipped
     "smb_sign": ("const float diff = dy[j] - s;", "const float diff = dy[j] + s;", ["smb", "smb_onehot"]),
     # softmax backward: masked columns get the unmasked formula
@@ -56,10 +59,12 @@ MUTATIONS = {
     # LayerNorm backward: the t * b projection dropped
     "lnb_no_proj": ("const float w = u - tb;", "const float w = u;", ["lnb"]),
     # LayerNorm backward: gamma not applied to dy
-    "lnb_no_gamma": ("g[j] = c->gamma ? dy[j] * c->gamma[j] : dy[j];", "g[j] = dy[j];", ["lnb"]),
+    "lnb_no_gamma": ("t[j] = d * rstd;\n            g[j] = c->gamma ? dy[j] * c->gamma[j] : dy[j];",
+                     "t[j] = d * rstd;\n            g[j] = dy[j];", ["lnb"]),
     # LayerNorm parameter gradients: rows summed in one block
-    "lnp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;",
-                      "const int64_t blk = c->rows;", ["lnp_order"]),
+    "lnp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float accg",
+                      "const int64_t blk = c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float accg",
+                      ["lnp_order"]),
     # LayerNorm parameter gradients: dbeta weighted by t
     "lnp_dbeta_t": ("pb = pb + dy;", "pb = fmaf(dy, t, pb);", ["lnp_int"]),
     # GELU backward: (1 - s) factor replaced by s
@@ -75,6 +80,46 @@ MUTATIONS = {
     # Adam: binary exponentiation tests the wrong bit
     "adam_pow_bit": ("if (t & 1) result = result * base;", "if (t & 2) result = result * base;",
                      ["adam_sc"]),
+    # sin/cos: quadrant 1 mapped like quadrant 3
+    "sc_quadrant": ("else if (q == 1) { *sin_out = cv; *cos_out = -sv; }",
+                    "else if (q == 1) { *sin_out = -cv; *cos_out = sv; }", ["sc_acc"]),
+    # sin/cos: third part of pi/2 dropped
+    "sc_no_p3": ("        r = fmaf(n, -SC_P3, r);\n", "", ["sc_acc", "sc_near"]),
+    # sin/cos: second part added instead of subtracted
+    "sc_p2_sign": ("r = fmaf(n, -SC_P2, r);", "r = fmaf(n, SC_P2, r);", ["sc_acc", "sc_near"]),
+    # sin/cos: 1/5! with the exponent of 1/4!
+    "sc_coeff": ("SC_S5 = 0x1.111112p-7f;", "SC_S5 = 0x1.111112p-6f;", ["sc_acc"]),
+    # sin/cos: a coefficient one ulp off (only the constants check sees it)
+    "sc_coeff_ulp": ("SC_C8 = 0x1.a01a02p-16f;", "SC_C8 = 0x1.a01a04p-16f;", ["sc_const"]),
+    # rotary embedding: rotation sign flipped
+    "rope_sign": ("y[h * c->hd + i] = a - b;", "y[h * c->hd + i] = a + b;", ["rope_acc"]),
+    # rotary embedding: position offset ignored
+    "rope_offset": ("(c->period > 0 ? r % c->period : r) + c->offset;",
+                    "(c->period > 0 ? r % c->period : r);", ["rope_acc"]),
+    # rotary embedding: pairs (i, i+1) instead of (i, i + d/2)
+    "rope_pairing": ("const float x1 = x[h * c->hd + i], x2 = x[h * c->hd + i + half];",
+                     "const float x1 = x[h * c->hd + i], x2 = x[h * c->hd + (i + 1) % c->hd];",
+                     ["rope_pairs", "rope_acc"]),
+    # RMSNorm: mean of squares over n - 1
+    "rms_n1": ("const float ms = q / nf;", "const float ms = q / (nf - 1.0f);", ["rms"]),
+    # RMSNorm: eps outside the root
+    "rms_eps": ("const float ve = ms + c->eps;\n        const float sd = sqrtf(ve);",
+                "const float ve = ms;\n        const float sd = sqrtf(ve) + c->eps;", ["rms"]),
+    # RMSNorm backward: projection term dropped
+    "rmsb_proj": ("const float w = g[j] - tb;", "const float w = g[j];", ["rmsb"]),
+    # RMSNorm dgamma: rows in one block
+    "rmsp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for",
+                       "const int64_t blk = c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for",
+                       ["rmsp"]),
+    # SiLU: exp of +x
+    "silu_sign": ("    const float w = -x;\n    const float d = 1.0f + repops_ref_exp1(w);\n    return x / d;",
+                  "    const float w = x;\n    const float d = 1.0f + repops_ref_exp1(w);\n    return x / d;",
+                  ["silu"]),
+    # SiLU derivative: (1 - s) replaced by s
+    "silu_grad": ("return fmaf(xs, om, s);", "return fmaf(xs, s, s);", ["silu", "swiglu"]),
+    # SwiGLU backward: dup uses g instead of silu(g)
+    "swiglu_du": ("const float duv = dyi * repops_ref_silu1(gi);", "const float duv = dyi * gi;",
+                  ["swiglu"]),
 }
 
 CHECKS = {
@@ -101,6 +146,17 @@ CHECKS = {
     "adam_sc": lambda lib: tpins.test_adam_scalars(lib),
     "adam": lambda lib: tpins.test_adam_against_float64(lib, 0.0, False),
     "adam_coupled": lambda lib: tpins.test_adam_against_float64(lib, 0.01, False),
+    "sc_acc": lambda lib: lpins.test_sincos_accuracy(lib, 4096.0),
+    "sc_near": lambda lib: lpins.test_sincos_near_multiples_of_half_pi(lib),
+    "sc_const": lambda lib: lpins.check_sincos_constants(
+        open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
+    "rope_acc": lambda lib: lpins.test_rope_rotation_accuracy_and_inverse(lib),
+    "rope_pairs": lambda lib: lpins.test_rope_pairs_rotate_half(lib),
+    "rms": lambda lib: lpins.test_rmsnorm_bound(lib, 64, 0),
+    "rmsb": lambda lib: lpins.test_rmsnorm_backward_bound(lib),
+    "rmsp": lambda lib: lpins.test_rmsnorm_dgamma_order_witness_and_integers(lib),
+    "silu": lambda lib: lpins.test_silu_and_grad_bounds(lib),
+    "swiglu": lambda lib: lpins.test_swiglu_forward_and_backward(lib),
 }
 
 
