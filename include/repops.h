@@ -320,6 +320,105 @@ repops_status_t repops_adam_step(const repops_order_t *order, int64_t n, float *
                                  int64_t step, int32_t decoupled, const repops_launch_t *launch,
                                  void *hip_stream);
 
+/* ------------------------------------------------------------------------
+ * Llama-block operators (the Llama programs of Section 4.2): sin/cos for the
+ * rotary embedding, RMSNorm and the SiLU-gated unit.  Section 3.1 lists the
+ * math functions RepOps rebuilds with a controlled order; version 1 fixes the
+ * sequences below.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * repops_sincos -- reproducible sin and cos of n contiguous elements (used
+ * inside repops_rope; exported for testing).  Cody-Waite reduction by pi/2:
+ *     n = rint(x * RN(2/pi));  r = x if n = 0, else three fused steps
+ *     r = fma(n, -P_i, r) with P1 + P2 + P3 = pi/2 (each the binary32 value
+ *     nearest the remainder);  u = r*r;
+ *     s = fma(r*u, S(u), r), S by Horner over RN(-1/3!), RN(1/5!), RN(-1/7!), RN(1/9!);
+ *     c = fma(u, C(u), 1), C by Horner over -1/2, RN(1/4!), ..., RN(-1/10!);
+ *     quadrant n mod 4 selects (s, c), (c, -s), (-s, -c), (-c, s).
+ *   x = +-0 gives (x, 1); non-finite x gives NaN.  Accurate to 2 ulp for
+ *   |x| <= 2^17 (reproducible, less accurate, beyond).  S or C may be NULL (not
+ *   both); S may equal X when C is NULL, C may equal X.
+ */
+repops_status_t repops_sincos(const repops_order_t *order, int64_t n, const float *X, float *S,
+                              float *C, const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_rope -- rotary position embedding with rotate-half pairing.  Row r of
+ * X holds `heads` heads of head_dim (even) values at X + r*ldx; its position is
+ * p = (position_period > 0 ? r % position_period : r) + position_offset
+ * (p < 2^24).  For i < head_dim/2:
+ *     angle = RN(p * inv_freq[i]);  s, c = repops_sincos(angle);
+ *     x1 = x[h*head_dim + i], x2 = x[h*head_dim + i + head_dim/2];
+ *     inverse = 0: y1 = RN(x1 c) - RN(x2 s), y2 = RN(x2 c) + RN(x1 s);
+ *     inverse = 1 (the backward): y1 = RN(x1 c) + RN(x2 s), y2 = RN(x2 c) - RN(x1 s).
+ *   inv_freq   [head_dim/2], the model's frequency table (an input like a weight).
+ *   Y, ldy     output rows of heads*head_dim; may coincide exactly with X.
+ *   launch     AUTO or ROWS_WAVE (p[0] = rows per block: 1, 2, 4, 8).
+ */
+repops_status_t repops_rope(const repops_order_t *order, int64_t rows, int64_t heads,
+                            int64_t head_dim, const float *X, int64_t ldx, const float *inv_freq,
+                            int64_t position_period, int64_t position_offset, int32_t inverse,
+                            float *Y, int64_t ldy, const repops_launch_t *launch,
+                            void *hip_stream);
+
+/*
+ * repops_rmsnorm_rows -- RMSNorm over rows:
+ *     ms = rowsum(fma(x_j, x_j, .)) / n in the descriptor's row order;
+ *     rstd = 1 / sqrt(ms + eps);  y_j = RN(x_j rstd) * gamma_j (no product if
+ *     gamma is NULL).  rstd_out NULL or [rows].  In place as for LayerNorm;
+ *     cols >= 1 when rows > 0.  Launch kinds as for layernorm_rows.
+ */
+repops_status_t repops_rmsnorm_rows(const repops_order_t *order, int64_t rows, int64_t cols,
+                                    const float *X, int64_t ldx, const float *gamma, float eps,
+                                    float *Y, int64_t ldy, float *rstd_out,
+                                    const repops_launch_t *launch, void *hip_stream);
+
+/* Workspace bytes of repops_rmsnorm_backward_rows (same rule as LayerNorm's). */
+repops_status_t repops_rmsnorm_backward_workspace(const repops_order_t *order, int64_t rows,
+                                                  int64_t cols, uint64_t *bytes);
+
+/*
+ * repops_rmsnorm_backward_rows -- gradients of repops_rmsnorm_rows from its rstd:
+ *     t_j = x_j rstd;  g_j = dy_j gamma_j (dy_j);  b = rowsum(fma(g_j, t_j, .)) / n;
+ *     dx_j = rstd * (g_j - t_j b);
+ *     dgamma_j: per column, the contraction rule over rows with block k_block
+ *     (P = fma(dy_ij, t_ij, P), block partials left to right).
+ *   Arguments, workspace, aliasing and launch as for the LayerNorm backward
+ *   (no mean, no dbeta).
+ */
+repops_status_t repops_rmsnorm_backward_rows(
+    const repops_order_t *order, int64_t rows, int64_t cols, const float *X, int64_t ldx,
+    const float *dY, int64_t lddy, const float *rstd, const float *gamma, float *dX,
+    int64_t lddx, float *dgamma, void *workspace, uint64_t workspace_bytes,
+    const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_silu -- y = x / (1 + exp_rep(-x)) over n contiguous elements; Y may
+ * equal X.  Launch kinds as for gelu.
+ */
+repops_status_t repops_silu(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                            const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_swiglu -- the SiLU-gated unit of Llama's feed-forward:
+ *     y = RN(silu(g) * up).  Y may equal G or Up.
+ */
+repops_status_t repops_swiglu(const repops_order_t *order, int64_t n, const float *G,
+                              const float *Up, float *Y, const repops_launch_t *launch,
+                              void *hip_stream);
+
+/*
+ * repops_swiglu_backward -- gradients of repops_swiglu:
+ *     s = 1 / (1 + exp_rep(-g));  silu'(g) = fma(g*s, 1 - s, s);
+ *     dG = RN(RN(dy * up) * silu'(g));  dUp = RN(dy * silu(g)) with silu(g) as
+ *     in the forward.  dG and dUp may each coincide exactly with an input and
+ *     must not overlap each other.
+ */
+repops_status_t repops_swiglu_backward(const repops_order_t *order, int64_t n, const float *G,
+                                       const float *Up, const float *dY, float *dG, float *dUp,
+                                       const repops_launch_t *launch, void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

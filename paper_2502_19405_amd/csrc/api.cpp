@@ -8,6 +8,7 @@
 #include "../../include/repops.h"
 #include "repops_internal.h"
 #include "train_internal.h"
+#include "llama_internal.h"
 
 using repops::AdamScalars;
 using repops::GemmArgs;
@@ -170,10 +171,11 @@ repops_status_t check_rows(int64_t rows, int64_t cols, const float* X, int64_t l
 }
 
 repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch_t* launch,
-                                int64_t cols, uint32_t* kind, int* wpb) {
+                                int64_t cols, uint32_t* kind, int* wpb,
+                                int64_t wave_max = repops::rows_wave_max_cols()) {
   const bool wave_order =
       order->row_width == 64 && order->row_combine == REPOPS_ROW_STRIDED_TREE;
-  const bool wave_fits = cols <= repops::rows_wave_max_cols();
+  const bool wave_fits = cols <= wave_max;
   *wpb = 4;
   if (!launch || launch->kind == REPOPS_LAUNCH_AUTO) {
     if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
@@ -484,10 +486,11 @@ repops_status_t repops_layernorm_backward_workspace(const repops_order_t* order,
   return REPOPS_OK;
 }
 
-repops_status_t repops_layernorm_backward_rows(
-    const repops_order_t* order, int64_t rows, int64_t cols, const float* X, int64_t ldx,
-    const float* dY, int64_t lddy, const float* mean, const float* rstd, const float* gamma,
-    float* dX, int64_t lddx, float* dgamma, float* dbeta, void* workspace,
+// LayerNorm and RMSNorm backward (rms: no mean input, no dbeta).
+static repops_status_t norm_backward(
+    bool rms, const repops_order_t* order, int64_t rows, int64_t cols, const float* X,
+    int64_t ldx, const float* dY, int64_t lddy, const float* mean, const float* rstd,
+    const float* gamma, float* dX, int64_t lddx, float* dgamma, float* dbeta, void* workspace,
     uint64_t workspace_bytes, const repops_launch_t* launch, void* hip_stream) {
   if (!order_valid(order)) return REPOPS_ERR_ORDER;
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
@@ -516,10 +519,10 @@ repops_status_t repops_layernorm_backward_rows(
   if (rows > 0) {
     if ((st = check_matrix(X, rows, cols, ldx)) != REPOPS_OK) return st;
     if ((st = check_matrix(dY, rows, cols, lddy)) != REPOPS_OK) return st;
-    if (!mean || !rstd) return REPOPS_ERR_NULL;
+    if ((!rms && !mean) || !rstd) return REPOPS_ERR_NULL;
     in[nin++] = {extent_of(X, 1, 0, 1, 0, rows, cols, ldx), X, ldx};
     in[nin++] = {extent_of(dY, 1, 0, 1, 0, rows, cols, lddy), dY, lddy};
-    in[nin++] = {vec_extent(mean, rows), mean, rows};
+    if (!rms) in[nin++] = {vec_extent(mean, rows), mean, rows};
     in[nin++] = {vec_extent(rstd, rows), rstd, rows};
   }
   if (gamma) in[nin++] = {vec_extent(gamma, cols), gamma, cols};
@@ -549,12 +552,14 @@ repops_status_t repops_layernorm_backward_rows(
   p.rows = rows; p.cols = cols; p.k_block = order->k_block;
   p.X = X; p.ldx = ldx; p.dY = dY; p.lddy = lddy; p.mean = mean; p.rstd = rstd;
   p.dgamma = dgamma; p.dbeta = dbeta; p.ws = static_cast<float*>(workspace);
+  p.rms = rms ? 1 : 0;
   RowBwdArgs a{};
   a.rows = rows; a.cols = cols;
   a.Y = X; a.ldy = ldx; a.dY = dY; a.lddy = lddy; a.dX = dX; a.lddx = lddx;
   a.W = static_cast<int>(order->row_width);
   a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
   a.mean = mean; a.rstd = rstd; a.gamma = gamma;
+  a.rms = rms ? 1 : 0;
   // Both gradients on the wave path with row blocks: one fused pass over X
   // and dY (R rows staged per pass: the launch's waves per block, else a
   // choice by size).
@@ -571,6 +576,29 @@ repops_status_t repops_layernorm_backward_rows(
   if (!dX || rows == 0) return REPOPS_OK;
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_bwd_wave(a, wpb, s));
   return hip_status(repops::launch_layernorm_bwd_generic(a, s));
+}
+
+repops_status_t repops_layernorm_backward_rows(
+    const repops_order_t* order, int64_t rows, int64_t cols, const float* X, int64_t ldx,
+    const float* dY, int64_t lddy, const float* mean, const float* rstd, const float* gamma,
+    float* dX, int64_t lddx, float* dgamma, float* dbeta, void* workspace,
+    uint64_t workspace_bytes, const repops_launch_t* launch, void* hip_stream) {
+  return norm_backward(false, order, rows, cols, X, ldx, dY, lddy, mean, rstd, gamma, dX, lddx,
+                       dgamma, dbeta, workspace, workspace_bytes, launch, hip_stream);
+}
+
+repops_status_t repops_rmsnorm_backward_workspace(const repops_order_t* order, int64_t rows,
+                                                  int64_t cols, uint64_t* bytes) {
+  return repops_layernorm_backward_workspace(order, rows, cols, bytes);
+}
+
+repops_status_t repops_rmsnorm_backward_rows(
+    const repops_order_t* order, int64_t rows, int64_t cols, const float* X, int64_t ldx,
+    const float* dY, int64_t lddy, const float* rstd, const float* gamma, float* dX,
+    int64_t lddx, float* dgamma, void* workspace, uint64_t workspace_bytes,
+    const repops_launch_t* launch, void* hip_stream) {
+  return norm_backward(true, order, rows, cols, X, ldx, dY, lddy, nullptr, rstd, gamma, dX, lddx,
+                       dgamma, nullptr, workspace, workspace_bytes, launch, hip_stream);
 }
 
 repops_status_t repops_gelu_backward(const repops_order_t* order, int64_t n, const float* X,
@@ -609,6 +637,150 @@ repops_status_t repops_adam_step(const repops_order_t* order, int64_t n, float* 
   const AdamScalars sc = adam_scalars(lr, beta1, beta2, eps, weight_decay, step, decoupled);
   return hip_status(repops::launch_adam(n, param, grad, exp_avg, exp_avg_sq, sc, threads,
                                         max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+// ---------------------------------------------------------------------------
+// Llama-block operators
+// ---------------------------------------------------------------------------
+
+repops_status_t repops_sincos(const repops_order_t* order, int64_t n, const float* X, float* S,
+                              float* C, const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (n < 0 || n > kMaxDim) return REPOPS_ERR_SHAPE;
+  int threads, max_blocks;
+  repops_status_t st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  if (!X || (!S && !C)) return REPOPS_ERR_NULL;
+  const Extent xe = vec_extent(X, n);
+  if (S && S != X && overlaps(vec_extent(S, n), xe)) return REPOPS_ERR_ALIAS;
+  if (C && C != X && overlaps(vec_extent(C, n), xe)) return REPOPS_ERR_ALIAS;
+  if (S && C && overlaps(vec_extent(S, n), vec_extent(C, n))) return REPOPS_ERR_ALIAS;
+  if (S == X && C) return REPOPS_ERR_ALIAS;  // the second output would read a written input
+  return hip_status(repops::launch_sincos(n, X, S, C, threads, max_blocks,
+                                          static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_rope(const repops_order_t* order, int64_t rows, int64_t heads,
+                            int64_t head_dim, const float* X, int64_t ldx, const float* inv_freq,
+                            int64_t position_period, int64_t position_offset, int32_t inverse,
+                            float* Y, int64_t ldy, const repops_launch_t* launch,
+                            void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (rows < 0 || heads < 0 || head_dim < 0 || rows > kMaxDim || heads > kMaxDim ||
+      head_dim > kMaxDim || (head_dim & 1) || position_period < 0 || position_offset < 0)
+    return REPOPS_ERR_SHAPE;
+  if (inverse != 0 && inverse != 1) return REPOPS_ERR_VALUE;
+  const int64_t cols = heads * head_dim;
+  if (cols > kMaxDim) return REPOPS_ERR_SHAPE;
+  const int64_t last = position_period > 0 ? position_period - 1 : rows - 1;
+  if (rows > 0 && last + position_offset >= (int64_t(1) << 24))
+    return REPOPS_ERR_SHAPE;  // positions must convert to binary32 exactly
+  int wpb = 4;
+  if (launch && launch->kind != REPOPS_LAUNCH_AUTO) {
+    const uint32_t w = launch->p[0];
+    if (launch->kind != REPOPS_LAUNCH_ROWS_WAVE || !(w == 1 || w == 2 || w == 4 || w == 8) ||
+        !launch_params_zero_from(launch, 1))
+      return REPOPS_ERR_LAUNCH;
+    wpb = static_cast<int>(w);
+  } else if (launch && !launch_params_zero_from(launch, 0)) {
+    return REPOPS_ERR_LAUNCH;
+  }
+  if (rows == 0 || cols == 0) return REPOPS_OK;
+  repops_status_t st;
+  if ((st = check_matrix(X, rows, cols, ldx)) != REPOPS_OK) return st;
+  if ((st = check_matrix(Y, rows, cols, ldy)) != REPOPS_OK) return st;
+  if (!inv_freq) return REPOPS_ERR_NULL;
+  const Extent xe = extent_of(X, 1, 0, 1, 0, rows, cols, ldx);
+  const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
+  if (bad_overlap(Y, ldy, ye, X, ldx, xe)) return REPOPS_ERR_ALIAS;
+  if (overlaps(ye, vec_extent(inv_freq, head_dim / 2))) return REPOPS_ERR_ALIAS;
+  repops::RopeArgs a{};
+  a.rows = rows; a.heads = heads; a.head_dim = head_dim;
+  a.X = X; a.ldx = ldx; a.inv_freq = inv_freq;
+  a.period = position_period; a.offset = position_offset; a.inverse = inverse;
+  a.Y = Y; a.ldy = ldy;
+  return hip_status(repops::launch_rope(a, wpb, static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_rmsnorm_rows(const repops_order_t* order, int64_t rows, int64_t cols,
+                                    const float* X, int64_t ldx, const float* gamma, float eps,
+                                    float* Y, int64_t ldy, float* rstd_out,
+                                    const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (rows > 0 && cols == 0) return REPOPS_ERR_SHAPE;
+  if (cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
+  bool empty = false;
+  repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
+  if (st != REPOPS_OK) return st;
+  uint32_t kind;
+  int wpb;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rmsnorm_wave_max_cols());
+  if (st != REPOPS_OK || empty) return st;
+  const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
+  if (gamma && overlaps(ye, vec_extent(gamma, cols))) return REPOPS_ERR_ALIAS;
+  if (rstd_out) {
+    const Extent re = vec_extent(rstd_out, rows);
+    if (overlaps(re, ye) || overlaps(re, extent_of(X, 1, 0, 1, 0, rows, cols, ldx)) ||
+        (gamma && overlaps(re, vec_extent(gamma, cols))))
+      return REPOPS_ERR_ALIAS;
+  }
+  repops::RmsArgs a{};
+  a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
+  a.W = static_cast<int>(order->row_width);
+  a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
+  a.gamma = gamma; a.eps = eps; a.rstd_out = rstd_out;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_rmsnorm_wave(a, wpb, s));
+  return hip_status(repops::launch_rmsnorm_generic(a, s));
+}
+
+repops_status_t repops_silu(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                            const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(
+      repops::launch_silu(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_swiglu(const repops_order_t* order, int64_t n, const float* G,
+                              const float* Up, float* Y, const repops_launch_t* launch,
+                              void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, G, Y);
+  if (st != REPOPS_OK) return st;
+  if ((st = check_elementwise(order, n, Up, Y)) != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(repops::launch_swiglu(n, G, Up, Y, threads, max_blocks,
+                                          static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_swiglu_backward(const repops_order_t* order, int64_t n, const float* G,
+                                       const float* Up, const float* dY, float* dG, float* dUp,
+                                       const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (n < 0 || n > kMaxDim) return REPOPS_ERR_SHAPE;
+  int threads, max_blocks;
+  repops_status_t st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  if (!G || !Up || !dY || !dG || !dUp) return REPOPS_ERR_NULL;
+  // Outputs may coincide exactly with one input each (element i is read before
+  // it is written); partial overlaps and dG/dUp overlapping each other are not
+  // allowed.
+  const Extent ge = vec_extent(G, n), ue = vec_extent(Up, n), de = vec_extent(dY, n);
+  const Extent oge = vec_extent(dG, n), oue = vec_extent(dUp, n);
+  if (overlaps(oge, oue)) return REPOPS_ERR_ALIAS;
+  const float* ins[3] = {G, Up, dY};
+  const Extent ine[3] = {ge, ue, de};
+  for (int i = 0; i < 3; ++i) {
+    if (dG != ins[i] && overlaps(oge, ine[i])) return REPOPS_ERR_ALIAS;
+    if (dUp != ins[i] && overlaps(oue, ine[i])) return REPOPS_ERR_ALIAS;
+  }
+  return hip_status(repops::launch_swiglu_bwd(n, G, Up, dY, dG, dUp, threads, max_blocks,
+                                              static_cast<hipStream_t>(hip_stream)));
 }
 
 }  // extern "C"

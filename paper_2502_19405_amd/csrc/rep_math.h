@@ -12,6 +12,10 @@
 // gelu: tanh form through 0.5 (1 + tanh z) = 1 / (1 + exp(-2z)).
 // gelu': with s = 1 / (1 + exp(-2z)) the forward is x * s, so its derivative
 //       is s + x s (1 - s) * 2 sqrt(2/pi) (1 + 3 * 0.044715 x^2).
+// sin/cos: Cody and Waite's additive reduction by pi/2 (pi/2 split in three
+//       binary32 parts), Taylor polynomials of degree 9 and 10 on |r| <= pi/4
+//       by Horner's rule, quadrant selection.
+// silu: x / (1 + exp(-x)); silu' = s + x s (1 - s) with s = 1 / (1 + exp(-x)).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -77,6 +81,76 @@ __device__ __forceinline__ float rep_gelu(float x) {
   const float w = z * -2.0f;
   const float d = 1.0f + rep_exp(w);
   return x / d;  // correctly rounded division
+}
+
+// Nearest binary32 value to 2/pi; pi/2 = kHalfPi1 + kHalfPi2 + kHalfPi3 + O(2^-76),
+// each part the binary32 value nearest the remainder.
+constexpr float kTwoOverPi = 0x1.45f306p-1f;
+constexpr float kHalfPi1 = 0x1.921fb6p+0f;
+constexpr float kHalfPi2 = -0x1.777a5cp-25f;
+constexpr float kHalfPi3 = -0x1.ee59dap-50f;
+// (-1)^k / (2k+1)! and (-1)^k / (2k)! rounded to binary32.
+constexpr float kSin3 = -0x1.555556p-3f;
+constexpr float kSin5 = 0x1.111112p-7f;
+constexpr float kSin7 = -0x1.a01a02p-13f;
+constexpr float kSin9 = 0x1.71de3ap-19f;
+constexpr float kCos2 = -0x1p-1f;
+constexpr float kCos4 = 0x1.555556p-5f;
+constexpr float kCos6 = -0x1.6c16c2p-10f;
+constexpr float kCos8 = 0x1.a01a02p-16f;
+constexpr float kCos10 = -0x1.27e4fcp-22f;
+
+// sin and cos of x.  n = rint(x * 2/pi); r = x - n pi/2 in three fused steps
+// (r = x when n = 0); u = r*r; s = r + (r u) P(u), c = 1 + u Q(u); the quadrant
+// n mod 4 picks (s, c), (c, -s), (-s, -c) or (-c, s).  x = +-0 gives (x, 1);
+// non-finite x gives NaN.  Straight-line code: every lane takes the same path.
+__device__ __forceinline__ void rep_sincos(float x, float& sin_out, float& cos_out) {
+  const bool finite = __builtin_isfinite(x);
+  const float xs = finite ? x : 0.0f;
+  const float t = xs * kTwoOverPi;
+  const float n = __builtin_rintf(t);
+  float r = __builtin_fmaf(n, -kHalfPi1, xs);
+  r = __builtin_fmaf(n, -kHalfPi2, r);
+  r = __builtin_fmaf(n, -kHalfPi3, r);
+  r = (n != 0.0f) ? r : xs;
+  const float u = r * r;
+  float ps = __builtin_fmaf(kSin9, u, kSin7);
+  ps = __builtin_fmaf(ps, u, kSin5);
+  ps = __builtin_fmaf(ps, u, kSin3);
+  const float r3 = r * u;
+  const float sv = __builtin_fmaf(r3, ps, r);
+  float pc = __builtin_fmaf(kCos10, u, kCos8);
+  pc = __builtin_fmaf(pc, u, kCos6);
+  pc = __builtin_fmaf(pc, u, kCos4);
+  pc = __builtin_fmaf(pc, u, kCos2);
+  const float cv = __builtin_fmaf(u, pc, 1.0f);
+  const float quarter = n * 0.25f;
+  const float fq = n - 4.0f * __builtin_floorf(quarter);  // exact, in {0, 1, 2, 3}
+  const int q = static_cast<int>(fq);
+  float so = (q & 1) ? cv : sv;
+  float co = (q & 1) ? sv : cv;
+  so = (q & 2) ? -so : so;
+  co = (q == 1 || q == 2) ? -co : co;
+  so = (x == 0.0f) ? x : so;
+  co = (x == 0.0f) ? 1.0f : co;
+  const float qnan = __builtin_nanf("");
+  sin_out = finite ? so : qnan;
+  cos_out = finite ? co : qnan;
+}
+
+__device__ __forceinline__ float rep_silu(float x) {
+  const float w = -x;
+  const float d = 1.0f + rep_exp(w);
+  return x / d;
+}
+
+__device__ __forceinline__ float rep_silu_grad(float x) {
+  const float w = -x;
+  const float d = 1.0f + rep_exp(w);
+  const float s = 1.0f / d;
+  const float om = 1.0f - s;
+  const float xs = x * s;
+  return __builtin_fmaf(xs, om, s);
 }
 
 // Derivative of rep_gelu, one fixed operation sequence.

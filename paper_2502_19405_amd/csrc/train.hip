@@ -120,7 +120,7 @@ __global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, i
   const float* x = a.Y + row * a.ldy;
   const float* dy = a.dY + row * a.lddy;
   float* dx = a.dX + row * a.lddx;
-  const float mean = a.mean[row], rstd = a.rstd[row];
+  const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
   float tv[T], gv[T];
   float q = 0.0f;
 #pragma unroll
@@ -136,7 +136,7 @@ __global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, i
     q = q + gv[t];  // terms past the row are +0 and leave q unchanged
   }
   const float n = static_cast<float>(a.cols);
-  const float am = wave_tree_sum(q) / n;
+  const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
   float q2 = 0.0f;
 #pragma unroll
   for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);
@@ -167,14 +167,14 @@ __global__ __launch_bounds__(64) void layernorm_bwd_generic_kernel(RowBwdArgs a)
     const float* x = a.Y + row * a.ldy;
     const float* dy = a.dY + row * a.lddy;
     float* dx = a.dX + row * a.lddx;
-    const float mean = a.mean[row], rstd = a.rstd[row];
+    const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
     auto g_at = [&](int64_t j) { return a.gamma ? dy[j] * a.gamma[j] : dy[j]; };
     auto t_at = [&](int64_t j) {
       const float d = x[j] - mean;
       return d * rstd;
     };
     auto sum_g = [&](float q, int64_t j) { return q + g_at(j); };
-    const float am = generic_row_sum(a.cols, a.W, a.blocked, sum_g, qs) / n;
+    const float am = a.rms ? 0.0f : generic_row_sum(a.cols, a.W, a.blocked, sum_g, qs) / n;
     auto sum_gt = [&](float q, int64_t j) { return __builtin_fmaf(g_at(j), t_at(j), q); };
     const float bm = generic_row_sum(a.cols, a.W, a.blocked, sum_gt, qs) / n;
     for (int64_t j = lane; j < a.cols; j += kWave) {
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const float d = xv[r] - a.mean[i + r];
+      const float d = xv[r] - (a.rms ? 0.0f : a.mean[i + r]);
       const float t = d * a.rstd[i + r];
       pg = __builtin_fmaf(dv[r], t, pg);
       pb = pb + dv[r];
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
   }
   for (; i < i1; ++i) {
     const float dv = dp[i * a.lddy];
-    const float d = xp[i * a.ldx] - a.mean[i];
+    const float d = xp[i * a.ldx] - (a.rms ? 0.0f : a.mean[i]);
     const float t = d * a.rstd[i];
     pg = __builtin_fmaf(dv, t, pg);
     pb = pb + dv;
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
     if (row < r1) {
       if (!PF) load_row(row);
       float* dx = a.dX + row * a.lddx;
-      const float mean = a.mean[row], rstd = a.rstd[row];
+      const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
       float tv[T], gv[T];
       float q = 0.0f;
 #pragma unroll
@@ -380,7 +380,7 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
         q = q + gv[t];
       }
       if (PF && row + R < r1) load_row(row + R);
-      const float am = wave_tree_sum(q) / n;
+      const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
       float q2 = 0.0f;
 #pragma unroll
       for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);

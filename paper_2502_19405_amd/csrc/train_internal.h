@@ -9,6 +9,9 @@ namespace repops {
 
 // Backward row operators.  Softmax: Y = forward output.  LayerNorm: Y = the
 // forward input X, with the forward's mean / rstd and gamma (nullable).
+// RMSNorm (rms = 1) runs the LayerNorm kernels with mean = +0 and the mean of
+// g taken as +0: x - 0 = x and g - 0 = g exactly, which leaves
+// t = x rstd and dx = rstd (g - t b), the RMSNorm gradient.
 struct RowBwdArgs {
   int64_t rows, cols;
   const float* Y; int64_t ldy;
@@ -18,6 +21,7 @@ struct RowBwdArgs {
   int blocked;
   int64_t period;     // softmax causal period, 0 = none
   const float* mean; const float* rstd; const float* gamma;
+  int rms;            // RMSNorm: no mean, no a term
 };
 
 hipError_t launch_softmax_bwd_wave(const RowBwdArgs& a, int waves_per_block, hipStream_t s);
@@ -34,6 +38,7 @@ struct LnParamArgs {
   const float* mean; const float* rstd;
   float* dgamma; float* dbeta;  // nullable
   float* ws;
+  int rms;            // RMSNorm: t = x * rstd (no mean)
 };
 
 int64_t layernorm_param_blocks(int64_t rows, int64_t k_block);

@@ -101,6 +101,17 @@ _SIGNATURES = {
     "repops_gelu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
     "repops_adam_step": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32, _f32, _f32, _i64,
                                 _i32, _lp, _vp]),
+    "repops_sincos": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
+    "repops_rope": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _i32, _vp, _i64,
+                           _lp, _vp]),
+    "repops_rmsnorm_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _f32, _vp, _i64, _vp, _lp,
+                                   _vp]),
+    "repops_rmsnorm_backward_workspace": (_i32, [_op, _i64, _i64, ctypes.POINTER(ctypes.c_uint64)]),
+    "repops_rmsnorm_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp,
+                                            _i64, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
+    "repops_silu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_swiglu": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
+    "repops_swiglu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _vp, _lp, _vp]),
 }
 EXPORTS = tuple(_SIGNATURES)
 
@@ -450,3 +461,140 @@ def adam_step(param: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor,
                                  float(weight_decay), int(step), 1 if decoupled else 0,
                                  _launch(launch), _stream(param))
     _check(rc, "repops_adam_step")
+
+
+# ---------------------------------------------------------------------------
+# Llama-block operators
+# ---------------------------------------------------------------------------
+
+def _flat(t: torch.Tensor, n: int, name: str):
+    if not t.is_contiguous() or t.numel() != n:
+        raise ValueError(f"{name} must be contiguous with {n} elements")
+    return _dev(t, name)
+
+
+def sincos(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None):
+    """(sin X, cos X) elementwise (the reproducible sin/cos inside the rotary
+    embedding, exported for testing)."""
+    n = X.numel()
+    S, C = torch.empty_like(X), torch.empty_like(X)
+    rc = load().repops_sincos(_ord(order), n, _flat(X, n, "X"), _dev(S, "S"), _dev(C, "C"),
+                              _launch(launch), _stream(X))
+    _check(rc, "repops_sincos")
+    return S, C
+
+
+def rope(X: torch.Tensor, heads: int, head_dim: int, inv_freq: torch.Tensor,
+         position_period: int = 0, position_offset: int = 0, inverse: bool = False,
+         order: Order | None = None, launch: Launch | None = None,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    """Rotary embedding of X [rows, >= heads * head_dim] (rotate-half pairs);
+    row r sits at position (r % period if period else r) + offset."""
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be a 2-D tensor with unit column stride")
+    rows = X.shape[0]
+    if X.shape[1] < heads * head_dim:
+        raise ValueError("X is narrower than heads * head_dim")
+    if out is None:
+        out = torch.empty((rows, heads * head_dim), dtype=torch.float32, device=X.device)
+    if out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be a 2-D tensor with unit column stride")
+    pinv = _flat(inv_freq, head_dim // 2, "inv_freq")
+    rc = load().repops_rope(_ord(order), rows, heads, head_dim, _dev(X, "X"),
+                            max(X.stride(0), 1), pinv, position_period, position_offset,
+                            1 if inverse else 0, _dev(out, "out"), max(out.stride(0), 1),
+                            _launch(launch), _stream(X))
+    _check(rc, "repops_rope")
+    return out
+
+
+def rmsnorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None, eps: float = 1e-5,
+                 order: Order | None = None, launch: Launch | None = None,
+                 out: torch.Tensor | None = None,
+                 rstd_out: torch.Tensor | None = None) -> torch.Tensor:
+    rows, cols, ldx = _rows(X, "X")
+    if out is None:
+        out = torch.empty_like(X, memory_format=torch.contiguous_format)
+    _, _, ldy = _rows(out, "out")
+    pg = None if gamma is None else _flat(gamma, cols, "gamma")
+    pr = None if rstd_out is None else _flat(rstd_out, rows, "rstd_out")
+    rc = load().repops_rmsnorm_rows(_ord(order), rows, cols, _dev(X, "X"), ldx, pg, float(eps),
+                                    _dev(out, "out"), ldy, pr, _launch(launch), _stream(out))
+    _check(rc, "repops_rmsnorm_rows")
+    return out
+
+
+def rmsnorm_backward_workspace(rows: int, cols: int, order: Order | None = None) -> int:
+    n = ctypes.c_uint64(0)
+    rc = load().repops_rmsnorm_backward_workspace(_ord(order), rows, cols, ctypes.byref(n))
+    _check(rc, "repops_rmsnorm_backward_workspace")
+    return n.value
+
+
+def rmsnorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, rstd: torch.Tensor,
+                          gamma: torch.Tensor | None = None, need_dx: bool = True,
+                          need_dgamma: bool = True, order: Order | None = None,
+                          launch: Launch | None = None, dx_out: torch.Tensor | None = None,
+                          dgamma_out: torch.Tensor | None = None,
+                          workspace: torch.Tensor | None = None):
+    """(dX, dgamma) of the RMSNorm from the forward's rstd; entries not
+    requested are None."""
+    rows, cols, ldx = _rows(X, "X")
+    r2, c2, lddy = _rows(dY, "dY")
+    if (r2, c2) != (rows, cols):
+        raise ValueError("X and dY shapes differ")
+    prs = _flat(rstd, rows, "rstd")
+    pg = None if gamma is None else _flat(gamma, cols, "gamma")
+    dx = dgamma = None
+    lddx = cols
+    if need_dx:
+        dx = dx_out if dx_out is not None else torch.empty_like(X, memory_format=torch.contiguous_format)
+        _, _, lddx = _rows(dx, "dx_out")
+    wptr, wbytes = None, 0
+    if need_dgamma:
+        dgamma = dgamma_out if dgamma_out is not None else torch.empty(cols, dtype=torch.float32,
+                                                                       device=X.device)
+        if workspace is None:
+            need = rmsnorm_backward_workspace(rows, cols, order)
+            if need:
+                workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
+        if workspace is not None:
+            wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
+    rc = load().repops_rmsnorm_backward_rows(
+        _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy, prs, pg,
+        None if dx is None else _dev(dx, "dX"), lddx,
+        None if dgamma is None else _flat(dgamma, cols, "dgamma"), wptr, wbytes,
+        _launch(launch), _stream(X))
+    _check(rc, "repops_rmsnorm_backward_rows")
+    return dx, dgamma
+
+
+def silu(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    return _elementwise("repops_silu", X, order, launch, out)
+
+
+def swiglu(G: torch.Tensor, Up: torch.Tensor, order: Order | None = None,
+           launch: Launch | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """silu(G) * Up elementwise."""
+    n = G.numel()
+    if out is None:
+        out = torch.empty_like(G)
+    rc = load().repops_swiglu(_ord(order), n, _flat(G, n, "G"), _flat(Up, n, "Up"),
+                              _flat(out, n, "out"), _launch(launch), _stream(out))
+    _check(rc, "repops_swiglu")
+    return out
+
+
+def swiglu_backward(G: torch.Tensor, Up: torch.Tensor, dY: torch.Tensor,
+                    order: Order | None = None, launch: Launch | None = None,
+                    dg_out: torch.Tensor | None = None, du_out: torch.Tensor | None = None):
+    """(dG, dUp) of silu(G) * Up."""
+    n = G.numel()
+    dG = dg_out if dg_out is not None else torch.empty_like(G)
+    dU = du_out if du_out is not None else torch.empty_like(G)
+    rc = load().repops_swiglu_backward(_ord(order), n, _flat(G, n, "G"), _flat(Up, n, "Up"),
+                                       _flat(dY, n, "dY"), _flat(dG, n, "dG"), _flat(dU, n, "dUp"),
+                                       _launch(launch), _stream(G))
+    _check(rc, "repops_swiglu_backward")
+    return dG, dU

@@ -229,6 +229,56 @@ def test_training_rejections(rp):
     assert rp.status_str(rp.ERR_WORKSPACE).startswith("workspace")
 
 
+@no_gpu_only
+def test_llama_rejections(rp):
+    lib = rp.load()
+    o = _order()
+    assert lib.repops_sincos(o, 8, FAKE_A, None, None, None, None) == rp.ERR_NULL
+    assert lib.repops_sincos(o, 8, FAKE_A, FAKE_B, FAKE_B + 4, None, None) == rp.ERR_ALIAS
+    assert lib.repops_sincos(o, 8, FAKE_A, FAKE_A, FAKE_C, None, None) == rp.ERR_ALIAS
+    assert lib.repops_sincos(o, -1, FAKE_A, FAKE_B, None, None, None) == rp.ERR_SHAPE
+
+    def rope(rows=4, heads=2, hd=8, X=FAKE_A, ldx=16, inv=FAKE_D, period=0, offset=0, inverse=0,
+             Y=FAKE_C, ldy=16, launch=None):
+        return lib.repops_rope(o, rows, heads, hd, X, ldx, inv, period, offset, inverse, Y, ldy,
+                               launch, None)
+    assert rope(hd=7) == rp.ERR_SHAPE
+    assert rope(ldx=15) == rp.ERR_STRIDE
+    assert rope(inv=None) == rp.ERR_NULL
+    assert rope(Y=FAKE_A + 4) == rp.ERR_ALIAS
+    assert rope(inv=FAKE_C + 8) == rp.ERR_ALIAS
+    assert rope(inverse=2) == rp.ERR_VALUE
+    assert rope(offset=1 << 24) == rp.ERR_SHAPE
+    assert rope(period=-1) == rp.ERR_SHAPE
+    assert rope(launch=ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (3,)).c())) == rp.ERR_LAUNCH
+    assert rope(launch=ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_GENERIC).c())) == rp.ERR_LAUNCH
+    assert rope(rows=0, X=None, Y=None, inv=None) == rp.OK
+
+    rms = lib.repops_rmsnorm_rows
+    assert rms(o, 4, 0, FAKE_A, 8, None, 1e-5, FAKE_C, 8, None, None, None) == rp.ERR_SHAPE
+    assert rms(o, 4, 8, FAKE_A, 8, FAKE_C + 4, 1e-5, FAKE_C, 8, None, None, None) == rp.ERR_ALIAS
+    assert rms(o, 4, 8, FAKE_A, 8, None, 1e-5, FAKE_C, 8, FAKE_A + 8, None, None) == rp.ERR_ALIAS
+    ws = ctypes.c_uint64(0)
+    assert lib.repops_rmsnorm_backward_workspace(o, 4096, 4096, ctypes.byref(ws)) == rp.OK
+    assert ws.value == 2 * 64 * 4096 * 4
+    rb = lib.repops_rmsnorm_backward_rows
+    assert rb(o, 128, 8, FAKE_A, 8, FAKE_B, 8, None, None, FAKE_C, 8, FAKE_D, FAKE_W, 1 << 20,
+              None, None) == rp.ERR_NULL
+    assert rb(o, 128, 8, FAKE_A, 8, FAKE_B, 8, FAKE_R, None, FAKE_C, 8, FAKE_D, None, 0,
+              None, None) == rp.ERR_WORKSPACE
+    assert rb(o, 128, 8, FAKE_A, 8, FAKE_B, 8, FAKE_R, None, FAKE_C, 8, FAKE_R, FAKE_W, 1 << 20,
+              None, None) == rp.ERR_ALIAS
+
+    assert lib.repops_silu(o, 8, FAKE_A, FAKE_A + 4, None, None) == rp.ERR_ALIAS
+    assert lib.repops_swiglu(o, 8, FAKE_A, None, FAKE_C, None, None) == rp.ERR_NULL
+    assert lib.repops_swiglu(o, 8, FAKE_A, FAKE_B, FAKE_B + 4, None, None) == rp.ERR_ALIAS
+    sb = lib.repops_swiglu_backward
+    assert sb(o, 8, FAKE_A, FAKE_B, FAKE_D, FAKE_C, FAKE_C + 4, None, None) == rp.ERR_ALIAS
+    assert sb(o, 8, FAKE_A, FAKE_B, FAKE_D, FAKE_A + 4, FAKE_C, None, None) == rp.ERR_ALIAS
+    assert sb(o, 8, FAKE_A, FAKE_B, None, FAKE_C, FAKE_W, None, None) == rp.ERR_NULL
+    assert sb(o, 0, None, None, None, None, None, None, None) == rp.OK
+
+
 def test_binding_fails_loudly_without_library(tmp_path):
     from paper_2502_19405_amd import repops
     with pytest.raises(RuntimeError, match="not found"):
