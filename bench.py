@@ -119,6 +119,7 @@ def secondary(repops, steps):
     element read once and written once; causal softmax reads only the
     unmasked part), GEMM-shaped steps and the model-shaped pipelines in
     TFLOP/s of 2*M*N*K."""
+    import numpy as np
     import torch
     from paper_2502_19405_amd import inputs, pipelines
 
@@ -200,6 +201,37 @@ def secondary(repops, steps):
                            steps)
         out[name] = _rate(ms, nbytes=28 * n)
         del p, gr, m, v
+
+    # Llama-block operators: rotary embedding of Q (4 x 1024 tokens, 32 heads of
+    # 128; 8 B per element), RMSNorm over 4096 x 4096 (forward 8 B, backward with
+    # dgamma 12 B per element), SwiGLU over 4096 x 14336 (forward 12 B,
+    # backward 20 B per element)
+    Q = t(inputs.normal(g, (4096, 4096)))
+    Qo = torch.empty_like(Q)
+    inv = t((500000.0 ** (-np.arange(0, 128, 2) / 128)).astype(np.float32))
+    ms = event_time_ms(lambda: repops.rope(Q, 32, 128, inv, 1024, 0, out=Qo), steps)
+    out["rope_4096x32x128"] = _rate(ms, nbytes=4 * Q.numel() * 2)
+    gw = t((1 + inputs.uniform(g, (4096,), -0.1, 0.1)).astype(np.float32))
+    rs = torch.empty(4096, device=dev)
+    ms = event_time_ms(lambda: repops.rmsnorm_rows(Q, gw, out=Qo, rstd_out=rs), steps)
+    out["rmsnorm_4096x4096"] = _rate(ms, nbytes=4 * Q.numel() * 2)
+    dQ = t(inputs.normal(g, (4096, 4096), var=1e-2))
+    dgw = torch.empty_like(gw)
+    wsr = torch.empty(max(repops.rmsnorm_backward_workspace(4096, 4096) // 4, 1), device=dev)
+    ms = event_time_ms(lambda: repops.rmsnorm_backward_rows(
+        Q, dQ, rs, gw, dx_out=Qo, dgamma_out=dgw, workspace=wsr), steps)
+    out["rmsnorm_backward_4096x4096"] = _rate(ms, nbytes=4 * Q.numel() * 3)
+    del Q, Qo, dQ, wsr
+    Gt = t(inputs.normal(g, (4096 * 14336,), var=4.0))
+    Ut = t(inputs.normal(g, (4096 * 14336,)))
+    Yt = torch.empty_like(Gt)
+    ms = event_time_ms(lambda: repops.swiglu(Gt, Ut, out=Yt), steps)
+    out["swiglu_4096x14336"] = _rate(ms, nbytes=4 * Gt.numel() * 3)
+    Dt = t(inputs.normal(g, (4096 * 14336,), var=1e-2))
+    Et = torch.empty_like(Gt)
+    ms = event_time_ms(lambda: repops.swiglu_backward(Gt, Ut, Dt, dg_out=Yt, du_out=Et), steps)
+    out["swiglu_backward_4096x14336"] = _rate(ms, nbytes=4 * Gt.numel() * 5)
+    del Gt, Ut, Yt, Dt, Et
 
     # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
