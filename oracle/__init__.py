@@ -108,6 +108,9 @@ def _declare(lib):
         "repops_ref_silu": (_int, [_i64, _f32p, _f32p, _int]),
         "repops_ref_swiglu": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
         "repops_ref_swiglu_backward": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _f32p, _int]),
+        "repops_ref_sha256": (None, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]),
+        "repops_ref_commit": (_int, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
+                                     ctypes.c_void_p]),
     })
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -442,3 +445,29 @@ def swiglu_backward(g, u, dy, nthreads=0, lib=None):
     _check((lib or load()).repops_ref_swiglu_backward(g.size, _p(g), _p(u), _p(dy), _p(dg),
                                                       _p(du), nthreads), "swiglu_backward")
     return dg, du
+
+
+# --------------------------------------------------------------------------
+# tensor commitments
+# --------------------------------------------------------------------------
+
+def _bytes_of(data):
+    if isinstance(data, (bytes, bytearray)):
+        return np.frombuffer(bytes(data), np.uint8)
+    return np.ascontiguousarray(data).view(np.uint8).ravel()
+
+
+def sha256(data, lib=None) -> bytes:
+    b = _bytes_of(data)
+    out = (ctypes.c_uint8 * 32)()
+    (lib or load()).repops_ref_sha256(b.ctypes.data if b.size else None, b.size, out)
+    return bytes(out)
+
+
+def commit(data, chunk_bytes=1024, lib=None) -> bytes:
+    """RFC 6962 Merkle Tree Hash of the data's bytes in chunks of chunk_bytes."""
+    b = _bytes_of(data)
+    out = (ctypes.c_uint8 * 32)()
+    _check((lib or load()).repops_ref_commit(b.ctypes.data if b.size else None, b.size,
+                                             chunk_bytes, out), "commit")
+    return bytes(out)

@@ -1027,6 +1027,134 @@ int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const 
 }
 
 /* ========================================================================= */
+/* Tensor commitments: SHA-256 and a Merkle tree over chunks                  */
+/* ========================================================================= */
+
+/*
+ * The protocol commits to checkpoints and to the tensors entering and leaving
+ * each graph node with a collision-resistant hash such as SHA-256 (Sections
+ * 3.1 and 3.3), and combines node hashes with a binary Merkle tree (Section
+ * 3.3, checkpoint hash format).  Reading for a tensor: its bytes as stored
+ * (row-major, little-endian binary32) are cut into chunks of C bytes (the last
+ * one shorter); the commitment is the Merkle Tree Hash of RFC 6962 over the
+ * chunks:  MTH({}) = SHA-256(empty);  MTH({d}) = SHA-256(0x00 || d);
+ * MTH(D[0:n]) = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])) with k the largest
+ * power of two below n.  SHA-256 is FIPS 180-4 (Section 6.2), written out
+ * below from the standard.
+ */
+static const uint32_t SHA_K[64] = {
+    0x428a2f98u, 0x71374491u, 0xb5c0fbcfu, 0xe9b5dba5u, 0x3956c25bu, 0x59f111f1u, 0x923f82a4u,
+    0xab1c5ed5u, 0xd807aa98u, 0x12835b01u, 0x243185beu, 0x550c7dc3u, 0x72be5d74u, 0x80deb1feu,
+    0x9bdc06a7u, 0xc19bf174u, 0xe49b69c1u, 0xefbe4786u, 0x0fc19dc6u, 0x240ca1ccu, 0x2de92c6fu,
+    0x4a7484aau, 0x5cb0a9dcu, 0x76f988dau, 0x983e5152u, 0xa831c66du, 0xb00327c8u, 0xbf597fc7u,
+    0xc6e00bf3u, 0xd5a79147u, 0x06ca6351u, 0x14292967u, 0x27b70a85u, 0x2e1b2138u, 0x4d2c6dfcu,
+    0x53380d13u, 0x650a7354u, 0x766a0abbu, 0x81c2c92eu, 0x92722c85u, 0xa2bfe8a1u, 0xa81a664bu,
+    0xc24b8b70u, 0xc76c51a3u, 0xd192e819u, 0xd6990624u, 0xf40e3585u, 0x106aa070u, 0x19a4c116u,
+    0x1e376c08u, 0x2748774cu, 0x34b0bcb5u, 0x391c0cb3u, 0x4ed8aa4au, 0x5b9cca4fu, 0x682e6ff3u,
+    0x748f82eeu, 0x78a5636fu, 0x84c87814u, 0x8cc70208u, 0x90befffau, 0xa4506cebu, 0xbef9a3f7u,
+    0xc67178f2u};
+static const uint32_t SHA_H0[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0xa54ff53au,
+                                   0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
+
+static uint32_t rotr32(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
+
+/* One application of the compression function to a 64-byte block. */
+static void sha_block(uint32_t H[8], const uint8_t blk[64])
+{
+    uint32_t W[64];
+    for (int t = 0; t < 16; ++t)
+        W[t] = ((uint32_t)blk[4 * t] << 24) | ((uint32_t)blk[4 * t + 1] << 16) |
+               ((uint32_t)blk[4 * t + 2] << 8) | (uint32_t)blk[4 * t + 3];
+    for (int t = 16; t < 64; ++t) {
+        const uint32_t s0 = rotr32(W[t - 15], 7) ^ rotr32(W[t - 15], 18) ^ (W[t - 15] >> 3);
+        const uint32_t s1 = rotr32(W[t - 2], 17) ^ rotr32(W[t - 2], 19) ^ (W[t - 2] >> 10);
+        W[t] = W[t - 16] + s0 + W[t - 7] + s1;
+    }
+    uint32_t a = H[0], b = H[1], c = H[2], d = H[3], e = H[4], f = H[5], g = H[6], h = H[7];
+    for (int t = 0; t < 64; ++t) {
+        const uint32_t S1 = rotr32(e, 6) ^ rotr32(e, 11) ^ rotr32(e, 25);
+        const uint32_t ch = (e & f) ^ (~e & g);
+        const uint32_t T1 = h + S1 + ch + SHA_K[t] + W[t];
+        const uint32_t S0 = rotr32(a, 2) ^ rotr32(a, 13) ^ rotr32(a, 22);
+        const uint32_t maj = (a & b) ^ (a & c) ^ (b & c);
+        const uint32_t T2 = S0 + maj;
+        h = g; g = f; f = e; e = d + T1;
+        d = c; c = b; b = a; a = T1 + T2;
+    }
+    H[0] += a; H[1] += b; H[2] += c; H[3] += d;
+    H[4] += e; H[5] += f; H[6] += g; H[7] += h;
+}
+
+/* SHA-256 of (prefix byte if has_prefix) || msg[0..len). */
+static void sha256_prefixed(int has_prefix, uint8_t prefix, const uint8_t *msg, uint64_t len,
+                            uint8_t out[32])
+{
+    uint32_t H[8];
+    memcpy(H, SHA_H0, sizeof H);
+    const uint64_t total = len + (has_prefix ? 1 : 0);
+    uint8_t blk[64];
+    uint64_t pos = 0; /* bytes of the whole message consumed */
+    int fill = 0;
+    if (has_prefix) blk[fill++] = prefix;
+    for (uint64_t i = 0; i < len; ++i) {
+        blk[fill++] = msg[i];
+        if (fill == 64) { sha_block(H, blk); fill = 0; }
+    }
+    pos = total;
+    blk[fill++] = 0x80; /* padding: one bit, zeros, 64-bit big-endian bit length */
+    if (fill > 56) {
+        while (fill < 64) blk[fill++] = 0;
+        sha_block(H, blk);
+        fill = 0;
+    }
+    while (fill < 56) blk[fill++] = 0;
+    const uint64_t bits = pos * 8;
+    for (int i = 0; i < 8; ++i) blk[56 + i] = (uint8_t)(bits >> (56 - 8 * i));
+    sha_block(H, blk);
+    for (int i = 0; i < 8; ++i) {
+        out[4 * i] = (uint8_t)(H[i] >> 24);
+        out[4 * i + 1] = (uint8_t)(H[i] >> 16);
+        out[4 * i + 2] = (uint8_t)(H[i] >> 8);
+        out[4 * i + 3] = (uint8_t)H[i];
+    }
+}
+
+void repops_ref_sha256(const void *msg, uint64_t len, uint8_t out[32])
+{
+    sha256_prefixed(0, 0, (const uint8_t *)msg, len, out);
+}
+
+/* MTH over the chunks [first, first + count) of data. */
+static void mth_range(const uint8_t *data, uint64_t nbytes, uint64_t chunk, uint64_t first,
+                      uint64_t count, uint8_t out[32])
+{
+    if (count == 1) {
+        const uint64_t off = first * chunk;
+        const uint64_t len = (off + chunk <= nbytes) ? chunk : nbytes - off;
+        sha256_prefixed(1, 0x00, data + off, len, out);
+        return;
+    }
+    uint64_t k = 1;
+    while (k * 2 < count) k *= 2; /* largest power of two below count */
+    uint8_t node[64];
+    mth_range(data, nbytes, chunk, first, k, node);
+    mth_range(data, nbytes, chunk, first + k, count - k, node + 32);
+    sha256_prefixed(1, 0x01, node, 64, out);
+}
+
+int repops_ref_commit(const void *data, uint64_t nbytes, uint64_t chunk_bytes, uint8_t out[32])
+{
+    if (chunk_bytes == 0) return -1;
+    if (nbytes == 0) {
+        sha256_prefixed(0, 0, NULL, 0, out);
+        return 0;
+    }
+    const uint64_t leaves = (nbytes + chunk_bytes - 1) / chunk_bytes;
+    mth_range((const uint8_t *)data, nbytes, chunk_bytes, 0, leaves, out);
+    return 0;
+}
+
+/* ========================================================================= */
 /* Training-step operators                                                   */
 /* ========================================================================= */
 

@@ -137,6 +137,14 @@ int repops_ref_swiglu(int64_t n, const float *g, const float *u, float *y, int n
 int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const float *dy,
                                float *dg, float *du, int nthreads);
 
+/* ---- tensor commitments ---- */
+
+/* SHA-256 (FIPS 180-4) of len bytes. */
+void repops_ref_sha256(const void *msg, uint64_t len, uint8_t out[32]);
+/* RFC 6962 Merkle Tree Hash over the chunk_bytes-sized chunks of data (last
+ * chunk shorter); nbytes = 0 gives SHA-256 of the empty string. */
+int repops_ref_commit(const void *data, uint64_t nbytes, uint64_t chunk_bytes, uint8_t out[32]);
+
 /* ---- training-step operators ---- */
 
 /* dX = Y * (dY - rowsum(Y * dY)) per row; masked columns (causal_period > 0:

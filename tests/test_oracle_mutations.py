@@ -14,6 +14,7 @@ import oracle
 import test_oracle as pins
 import test_oracle_training as tpins
 import test_oracle_llama as lpins
+import test_oracle_commit as cpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")
 
@@ -120,6 +121,17 @@ MUTATIONS = {
     # SwiGLU backward: dup uses g instead of silu(g)
     "swiglu_du": ("const float duv = dyi * repops_ref_silu1(gi);", "const float duv = dyi * gi;",
                   ["swiglu"]),
+    # SHA-256: a round constant off by one
+    "sha_k": ("0xc67178f2u};", "0xc67178f3u};", ["sha_const", "sha"]),
+    # SHA-256: small sigma 0 with the wrong rotation
+    "sha_sigma": ("rotr32(W[t - 15], 7)", "rotr32(W[t - 15], 8)", ["sha"]),
+    # SHA-256: message length in bytes instead of bits
+    "sha_len": ("const uint64_t bits = pos * 8;", "const uint64_t bits = pos;", ["sha"]),
+    # commitment: leaves with the internal-node prefix
+    "leaf_prefix": ("sha256_prefixed(1, 0x00, data + off, len, out);",
+                    "sha256_prefixed(1, 0x01, data + off, len, out);", ["mth"]),
+    # commitment: tree split in halves instead of at a power of two
+    "mth_split": ("while (k * 2 < count) k *= 2;", "k = count / 2;", ["mth"]),
 }
 
 CHECKS = {
@@ -157,6 +169,10 @@ CHECKS = {
     "rmsp": lambda lib: lpins.test_rmsnorm_dgamma_order_witness_and_integers(lib),
     "silu": lambda lib: lpins.test_silu_and_grad_bounds(lib),
     "swiglu": lambda lib: lpins.test_swiglu_forward_and_backward(lib),
+    "sha": lambda lib: cpins.test_sha256_every_length_against_hashlib(lib),
+    "sha_const": lambda lib: cpins.check_sha_constants(
+        open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
+    "mth": lambda lib: cpins.test_commit_against_rfc6962(lib, 64),
 }
 
 
