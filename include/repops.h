@@ -419,6 +419,37 @@ repops_status_t repops_swiglu_backward(const repops_order_t *order, int64_t n, c
                                        const float *Up, const float *dY, float *dG, float *dUp,
                                        const repops_launch_t *launch, void *hip_stream);
 
+/* ------------------------------------------------------------------------
+ * Tensor commitments.  The protocol commits to checkpoints and to the tensors
+ * entering and leaving every graph node with a collision-resistant hash such
+ * as SHA-256, and combines node hashes in a binary Merkle tree (Sections 3.1
+ * and 3.3).  A tensor is committed as the RFC 6962 Merkle Tree Hash of its
+ * bytes cut into chunks:
+ *     MTH({}) = SHA-256(empty);  MTH({d}) = SHA-256(0x00 || d);
+ *     MTH(D[0:n]) = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])), k the largest
+ *     power of two below n;
+ * with SHA-256 as in FIPS 180-4.
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes repops_commit needs for nbytes of data in chunks of
+ * chunk_bytes (1 <= chunk_bytes <= 2^30): 32 per chunk plus 32 per pair. */
+repops_status_t repops_commit_workspace(uint64_t nbytes, uint32_t chunk_bytes, uint64_t *bytes);
+
+/*
+ * repops_commit -- the commitment of nbytes at `data` (device; a tensor's
+ * storage as it lies in memory, e.g. row-major little-endian binary32),
+ * chunks of chunk_bytes (the last one shorter).  The 32-byte digest goes to
+ * `digest` (device memory, SHA-256 byte order).  16-byte-aligned data with a
+ * chunk size that is a multiple of 64 takes the vector path; anything else is
+ * hashed byte by byte, with the same result.  workspace: device memory of at
+ * least repops_commit_workspace bytes, 4-byte aligned, contents on return
+ * unspecified.  digest, data and workspace must not overlap.  launch: NULL
+ * or AUTO.
+ */
+repops_status_t repops_commit(const void *data, uint64_t nbytes, uint32_t chunk_bytes,
+                              uint8_t *digest, void *workspace, uint64_t workspace_bytes,
+                              const repops_launch_t *launch, void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

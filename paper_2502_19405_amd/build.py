@@ -19,7 +19,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "gemm.hip", "gemm_mfma.hip", "rows.hip", "elementwise.hip", "train.hip", "llama.hip"]
+SOURCES = ["api.cpp", "gemm.hip", "gemm_mfma.hip", "rows.hip", "elementwise.hip", "train.hip", "llama.hip", "commit.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -9,6 +9,7 @@
 #include "repops_internal.h"
 #include "train_internal.h"
 #include "llama_internal.h"
+#include "commit_internal.h"
 
 using repops::AdamScalars;
 using repops::GemmArgs;
@@ -781,6 +782,45 @@ repops_status_t repops_swiglu_backward(const repops_order_t* order, int64_t n, c
   }
   return hip_status(repops::launch_swiglu_bwd(n, G, Up, dY, dG, dUp, threads, max_blocks,
                                               static_cast<hipStream_t>(hip_stream)));
+}
+
+// ---------------------------------------------------------------------------
+// Tensor commitments
+// ---------------------------------------------------------------------------
+
+repops_status_t repops_commit_workspace(uint64_t nbytes, uint32_t chunk_bytes, uint64_t* bytes) {
+  if (!bytes) return REPOPS_ERR_NULL;
+  if (chunk_bytes == 0 || chunk_bytes > (1u << 30)) return REPOPS_ERR_SHAPE;
+  if (nbytes > (uint64_t(1) << 46)) return REPOPS_ERR_SHAPE;
+  *bytes = repops::commit_workspace_bytes(nbytes, chunk_bytes);
+  return REPOPS_OK;
+}
+
+repops_status_t repops_commit(const void* data, uint64_t nbytes, uint32_t chunk_bytes,
+                              uint8_t* digest, void* workspace, uint64_t workspace_bytes,
+                              const repops_launch_t* launch, void* hip_stream) {
+  uint64_t need = 0;
+  repops_status_t st = repops_commit_workspace(nbytes, chunk_bytes, &need);
+  if (st != REPOPS_OK) return st;
+  if (launch && (launch->kind != REPOPS_LAUNCH_AUTO || !launch_params_zero_from(launch, 0)))
+    return REPOPS_ERR_LAUNCH;
+  if (!digest || (nbytes > 0 && !data)) return REPOPS_ERR_NULL;
+  if (need > 0 && (!workspace || workspace_bytes < need)) return REPOPS_ERR_WORKSPACE;
+  auto span = [](const void* p, uint64_t n) {
+    const uintptr_t b = reinterpret_cast<uintptr_t>(p);
+    return Extent{b, b + static_cast<uintptr_t>(n)};
+  };
+  const Extent de = span(digest, 32);
+  if (nbytes > 0 && overlaps(de, span(data, nbytes))) return REPOPS_ERR_ALIAS;
+  if (need > 0) {
+    const Extent we = span(workspace, need);
+    if (overlaps(we, de) || (nbytes > 0 && overlaps(we, span(data, nbytes))))
+      return REPOPS_ERR_ALIAS;
+  }
+  if (reinterpret_cast<uintptr_t>(workspace) % 4 != 0) return REPOPS_ERR_STRIDE;
+  return hip_status(repops::launch_commit(static_cast<const uint8_t*>(data), nbytes, chunk_bytes,
+                                          digest, static_cast<uint32_t*>(workspace),
+                                          static_cast<hipStream_t>(hip_stream)));
 }
 
 }  // extern "C"

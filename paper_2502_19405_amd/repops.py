@@ -112,6 +112,8 @@ _SIGNATURES = {
     "repops_silu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
     "repops_swiglu": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
     "repops_swiglu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _vp, _lp, _vp]),
+    "repops_commit_workspace": (_i32, [ctypes.c_uint64, _u32, ctypes.POINTER(ctypes.c_uint64)]),
+    "repops_commit": (_i32, [_vp, ctypes.c_uint64, _u32, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
 }
 EXPORTS = tuple(_SIGNATURES)
 
@@ -598,3 +600,33 @@ def swiglu_backward(G: torch.Tensor, Up: torch.Tensor, dY: torch.Tensor,
                                        _launch(launch), _stream(G))
     _check(rc, "repops_swiglu_backward")
     return dG, dU
+
+
+# ---------------------------------------------------------------------------
+# tensor commitments
+# ---------------------------------------------------------------------------
+
+def commit_workspace(nbytes: int, chunk_bytes: int = 1024) -> int:
+    n = ctypes.c_uint64(0)
+    _check(load().repops_commit_workspace(nbytes, chunk_bytes, ctypes.byref(n)),
+           "repops_commit_workspace")
+    return n.value
+
+
+def commit(t: torch.Tensor, chunk_bytes: int = 1024, digest: torch.Tensor | None = None,
+           workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """RFC 6962 Merkle commitment of a contiguous device tensor's bytes; returns
+    the 32-byte digest as a uint8 device tensor."""
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("commit takes a contiguous device tensor")
+    nbytes = t.numel() * t.element_size()
+    if digest is None:
+        digest = torch.empty(32, dtype=torch.uint8, device=t.device)
+    if workspace is None:
+        need = commit_workspace(nbytes, chunk_bytes)
+        workspace = torch.empty(max(need // 4, 1), dtype=torch.int32, device=t.device)
+    rc = load().repops_commit(t.data_ptr() if nbytes else None, nbytes, chunk_bytes,
+                              digest.data_ptr(), workspace.data_ptr(),
+                              workspace.numel() * workspace.element_size(), None, _stream(t))
+    _check(rc, "repops_commit")
+    return digest

@@ -279,6 +279,27 @@ def test_llama_rejections(rp):
     assert sb(o, 0, None, None, None, None, None, None, None) == rp.OK
 
 
+@no_gpu_only
+def test_commit_rejections(rp):
+    lib = rp.load()
+    n = ctypes.c_uint64(0)
+    assert lib.repops_commit_workspace(1 << 20, 1024, ctypes.byref(n)) == rp.OK
+    assert n.value == 32 * (1024 + 512)
+    assert lib.repops_commit_workspace(0, 1024, ctypes.byref(n)) == rp.OK and n.value == 0
+    assert lib.repops_commit_workspace(10, 0, ctypes.byref(n)) == rp.ERR_SHAPE
+    assert lib.repops_commit_workspace(10, 64, None) == rp.ERR_NULL
+    c = lib.repops_commit
+    assert c(FAKE_A, 4096, 1024, None, FAKE_W, 1 << 20, None, None) == rp.ERR_NULL
+    assert c(None, 4096, 1024, FAKE_C, FAKE_W, 1 << 20, None, None) == rp.ERR_NULL
+    assert c(FAKE_A, 4096, 1024, FAKE_C, None, 0, None, None) == rp.ERR_WORKSPACE
+    assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_W, 32 * 6 - 1, None, None) == rp.ERR_WORKSPACE
+    assert c(FAKE_A, 4096, 1024, FAKE_A + 100, FAKE_W, 1 << 20, None, None) == rp.ERR_ALIAS
+    assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_A + 64, 1 << 20, None, None) == rp.ERR_ALIAS
+    assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_W + 2, 1 << 20, None, None) == rp.ERR_STRIDE
+    wave = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (4,)).c())
+    assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_W, 1 << 20, wave, None) == rp.ERR_LAUNCH
+
+
 def test_binding_fails_loudly_without_library(tmp_path):
     from paper_2502_19405_amd import repops
     with pytest.raises(RuntimeError, match="not found"):
