@@ -9,10 +9,12 @@
 // left || right), the tree split at the largest power of two (RFC 6962).
 //
 // Schedule: one lane per leaf chunk (the chunk's blocks in sequence); then
-// one launch per tree level while a level is wide, each lane hashing one pair
-// (an odd last node is carried up unchanged, which reproduces RFC 6962's
-// split); the last levels (at most kTopNodes nodes) run in one workgroup with
-// the digests in LDS, and the root is written as 32 bytes.
+// the tree level by level, pairs hashed and an odd last node carried up
+// unchanged (which reproduces RFC 6962's split): one launch per level while a
+// level is wider than 512 nodes, then the rest in one workgroup from LDS, which
+// writes the root as 32 bytes.  A level costs at least one two-block hash of
+// latency (about 6 us), so a tensor's commitment has a floor of about that
+// times the tree depth; wide levels and the leaves are integer-ALU bound.
 //
 // Digests travel between kernels as eight 32-bit words (SHA-256's big-endian
 // word view); data bytes are read as little-endian dwords and reassembled into
@@ -43,10 +45,17 @@ constexpr uint32_t kK[64] = {
 constexpr uint32_t kH0[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u, 0xa54ff53au,
                              0x510e527fu, 0x9b05688cu, 0x1f83d9abu, 0x5be0cd19u};
 
-constexpr int kTopNodes = 512;     // levels at or below this width finish in one workgroup
+constexpr int kTopNodes = 512;     // nodes one workgroup reduces to one (nine levels)
 constexpr int kTopThreads = 256;
 
 __device__ __forceinline__ uint32_t rotr(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
+
+// Three-input XOR in one instruction: gfx950's three-input bitwise operation
+// with the parity truth table 0x96 (the compiler otherwise splits the Sigma /
+// sigma functions into two-input XORs).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
 
 // The compression function on one block; W holds the block's 16 words and is
 // consumed as the rolling message schedule.  Fully unrolled: every round
@@ -60,15 +69,15 @@ __device__ __forceinline__ void compress(uint32_t H[8], uint32_t W[16]) {
       w = W[t];
     } else {
       const uint32_t w15 = W[(t - 15) & 15], w2 = W[(t - 2) & 15];
-      const uint32_t s0 = rotr(w15, 7) ^ rotr(w15, 18) ^ (w15 >> 3);
-      const uint32_t s1 = rotr(w2, 17) ^ rotr(w2, 19) ^ (w2 >> 10);
+      const uint32_t s0 = xor3(rotr(w15, 7), rotr(w15, 18), w15 >> 3);
+      const uint32_t s1 = xor3(rotr(w2, 17), rotr(w2, 19), w2 >> 10);
       w = W[t & 15] + s0 + W[(t - 7) & 15] + s1;
       W[t & 15] = w;
     }
-    const uint32_t S1 = rotr(e, 6) ^ rotr(e, 11) ^ rotr(e, 25);
+    const uint32_t S1 = xor3(rotr(e, 6), rotr(e, 11), rotr(e, 25));
     const uint32_t ch = (e & f) ^ (~e & g);
     const uint32_t T1 = h + S1 + ch + kK[t] + w;
-    const uint32_t S0 = rotr(a, 2) ^ rotr(a, 13) ^ rotr(a, 22);
+    const uint32_t S0 = xor3(rotr(a, 2), rotr(a, 13), rotr(a, 22));
     const uint32_t maj = (a & b) ^ (a & c) ^ (b & c);
     const uint32_t T2 = S0 + maj;
     h = g;
@@ -221,16 +230,24 @@ __global__ __launch_bounds__(256) void node_kernel(const uint32_t* in, uint64_t 
   for (int k = 0; k < 8; ++k) out[i * 8 + k] = H[k];
 }
 
-// The remaining levels (n_in <= kTopNodes) in one workgroup, digests in LDS;
-// the root goes to `digest` as 32 bytes in SHA-256's byte order.
-__global__ __launch_bounds__(kTopThreads) void top_kernel(const uint32_t* in, uint64_t n_in,
-                                                          uint8_t* digest) {
+// The last levels (at most kTopNodes nodes) in one workgroup, level by level
+// in LDS; the root is written as 32 bytes in SHA-256's byte order.  (The
+// kernel also reduces aligned slices of kTopNodes nodes when launched with
+// several workgroups -- inside such a slice the pairs (2i, 2i + 1) are those
+// of the whole level and only the last slice can hold the odd last node -- but
+// wide levels run faster one launch per level: inside a workgroup every level
+// after the first leaves half of the remaining lanes idle, while a level costs
+// about one two-block hash of latency either way.)
+__global__ __launch_bounds__(kTopThreads) void tree_kernel(const uint32_t* in, uint64_t n_in,
+                                                           uint32_t* out, uint8_t* digest) {
   __shared__ uint32_t buf[2][kTopNodes * 8];
   const int tid = threadIdx.x;
-  for (uint64_t i = tid; i < n_in * 8; i += kTopThreads) buf[0][i] = in[i];
+  const uint64_t first = static_cast<uint64_t>(blockIdx.x) * kTopNodes;
+  const uint64_t left = n_in - first;
+  uint64_t n = left < static_cast<uint64_t>(kTopNodes) ? left : kTopNodes;
+  for (uint64_t i = tid; i < n * 8; i += kTopThreads) buf[0][i] = in[first * 8 + i];
   __syncthreads();
   int cur = 0;
-  uint64_t n = n_in;
   while (n > 1) {
     const uint64_t n_out = (n + 1) / 2;
     for (uint64_t i = tid; i < n_out; i += kTopThreads) {
@@ -254,9 +271,13 @@ __global__ __launch_bounds__(kTopThreads) void top_kernel(const uint32_t* in, ui
     cur ^= 1;
     n = n_out;
   }
-  if (tid < 32) {
-    const uint32_t w = buf[cur][tid / 4];
-    digest[tid] = static_cast<uint8_t>(w >> (24 - 8 * (tid % 4)));
+  if (digest) {
+    if (tid < 32) {
+      const uint32_t w = buf[cur][tid / 4];
+      digest[tid] = static_cast<uint8_t>(w >> (24 - 8 * (tid % 4)));
+    }
+  } else if (tid < 8) {
+    out[static_cast<uint64_t>(blockIdx.x) * 8 + tid] = buf[cur][tid];
   }
 }
 
@@ -297,8 +318,8 @@ hipError_t launch_commit(const uint8_t* data, uint64_t nbytes, uint32_t chunk, u
     return hipGetLastError();
   }
   const bool vec = reinterpret_cast<uintptr_t>(data) % 16 == 0 && chunk % 64 == 0;
-  uint32_t* a = ws;                // level 0 and every even level
-  uint32_t* b = ws + leaves * 8;   // odd levels
+  uint32_t* a = ws;                // leaf digests, then every second reduced level
+  uint32_t* b = ws + leaves * 8;   // the other reduced levels
   hipLaunchKernelGGL(leaf_kernel, dim3(grid_for(leaves, 256)), dim3(256), 0, s, data, nbytes,
                      chunk, leaves, a, vec ? 1 : 0);
   hipError_t e = hipGetLastError();
@@ -312,7 +333,8 @@ hipError_t launch_commit(const uint8_t* data, uint64_t nbytes, uint32_t chunk, u
     n = (n + 1) / 2;
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(top_kernel, dim3(1), dim3(kTopThreads), 0, s, a, n, digest);
+  hipLaunchKernelGGL(tree_kernel, dim3(1), dim3(kTopThreads), 0, s, a, n,
+                     static_cast<uint32_t*>(nullptr), digest);
   return hipGetLastError();
 }
 

@@ -232,7 +232,7 @@ int64_t ew_grid(int64_t items, int threads, int max_blocks) {
 }  // namespace
 
 // RMSNorm rows stay in registers up to 64 values per lane (Llama's 4096).
-int64_t rmsnorm_wave_max_cols() { return int64_t(kWave) * 64; }
+int64_t rmsnorm_wave_max_cols() { return int64_t(kWave) * kMaxPerLane; }
 
 hipError_t launch_sincos(int64_t n, const float* x, float* s, float* c, int threads,
                          int max_blocks, hipStream_t st) {

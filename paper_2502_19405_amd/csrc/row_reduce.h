@@ -14,7 +14,7 @@
 namespace repops {
 
 constexpr int kWave = 64;
-constexpr int kMaxPerLane = 32;  // register-resident rows: cols <= 64 * 32
+constexpr int kMaxPerLane = 64;  // register-resident rows: cols <= 64 * 64
 
 // Halving tree over the 64 lane partials: after the step with distance s, lane
 // l < s holds q[l] + q[l+s].  Lanes >= s keep stale values that no later step

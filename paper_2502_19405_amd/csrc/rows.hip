@@ -195,7 +195,8 @@ WaveKernel pick_softmax(int64_t cols) {
   if (cols <= kWave * 4) return softmax_wave_kernel<4>;
   if (cols <= kWave * 8) return softmax_wave_kernel<8>;
   if (cols <= kWave * 16) return softmax_wave_kernel<16>;
-  return softmax_wave_kernel<32>;
+  if (cols <= kWave * 32) return softmax_wave_kernel<32>;
+  return softmax_wave_kernel<64>;
 }
 
 WaveKernel pick_layernorm(int64_t cols) {
@@ -205,7 +206,8 @@ WaveKernel pick_layernorm(int64_t cols) {
   if (cols <= kWave * 8) return layernorm_wave_kernel<8>;
   if (cols <= kWave * 12) return layernorm_wave_kernel<12>;
   if (cols <= kWave * 16) return layernorm_wave_kernel<16>;
-  return layernorm_wave_kernel<32>;
+  if (cols <= kWave * 32) return layernorm_wave_kernel<32>;
+  return layernorm_wave_kernel<64>;
 }
 
 unsigned generic_grid(int64_t rows) {

@@ -34,8 +34,11 @@ namespace {
 // over the unmasked columns; masked columns get +0.
 // ---------------------------------------------------------------------------
 
+// The widest rows (T = 64) keep 128 row values per lane and run at most four
+// waves per workgroup, which leaves them a full register file.
 template <int T>
-__global__ __launch_bounds__(512) void softmax_bwd_wave_kernel(RowBwdArgs a, int wpb) {
+__global__ __launch_bounds__(T > 32 ? 256 : 512) void softmax_bwd_wave_kernel(RowBwdArgs a,
+                                                                              int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
   if (row >= a.rows) return;
@@ -515,7 +518,8 @@ WaveBwdKernel pick_softmax_bwd(int64_t cols) {
   if (cols <= kWave * 4) return softmax_bwd_wave_kernel<4>;
   if (cols <= kWave * 8) return softmax_bwd_wave_kernel<8>;
   if (cols <= kWave * 16) return softmax_bwd_wave_kernel<16>;
-  return softmax_bwd_wave_kernel<32>;
+  if (cols <= kWave * 32) return softmax_bwd_wave_kernel<32>;
+  return softmax_bwd_wave_kernel<64>;
 }
 
 WaveBwdKernel pick_layernorm_bwd(int64_t cols) {
@@ -525,7 +529,8 @@ WaveBwdKernel pick_layernorm_bwd(int64_t cols) {
   if (cols <= kWave * 8) return layernorm_bwd_wave_kernel<8>;
   if (cols <= kWave * 12) return layernorm_bwd_wave_kernel<12>;
   if (cols <= kWave * 16) return layernorm_bwd_wave_kernel<16>;
-  return layernorm_bwd_wave_kernel<32>;
+  if (cols <= kWave * 32) return layernorm_bwd_wave_kernel<32>;
+  return layernorm_bwd_wave_kernel<64>;
 }
 
 using FusedKernel = void (*)(RowBwdArgs, LnParamArgs, int, int64_t);
@@ -561,6 +566,7 @@ bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0;
 }  // namespace
 
 hipError_t launch_softmax_bwd_wave(const RowBwdArgs& a, int wpb, hipStream_t s) {
+  if (a.cols > kWave * 32 && wpb > 4) wpb = 4;
   const int64_t blocks = (a.rows + wpb - 1) / wpb;
   hipLaunchKernelGGL(pick_softmax_bwd(a.cols), dim3(static_cast<unsigned>(blocks)),
                      dim3(kWave * wpb), 0, s, a, wpb);

@@ -26,7 +26,7 @@ def rp():
 
 def row_launches(rp, W=64, combine=0, cols=0):
     out = [("generic", rp.Launch(rp.LAUNCH_ROWS_GENERIC)), ("auto", None)]
-    if W == 64 and combine == 0 and cols <= 2048:
+    if W == 64 and combine == 0 and cols <= 4096:
         out += [(f"wave{w}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (w,))) for w in (1, 2, 4, 8)]
     return out
 
@@ -37,7 +37,7 @@ def ew_launches(rp):
             ("t256b7", rp.Launch(rp.LAUNCH_ELEMENTWISE, (256, 7)))]
 
 
-COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000]
+COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000, 4096, 4097]
 
 
 # --------------------------------------------------------------------------
