@@ -422,8 +422,8 @@ repops_status_t repops_swiglu_backward(const repops_order_t *order, int64_t n, c
 /* ------------------------------------------------------------------------
  * Tensor commitments.  The protocol commits to checkpoints and to the tensors
  * entering and leaving every graph node with a collision-resistant hash such
- * as SHA-256, and combines node hashes in a binary Merkle tree (Sections 3.1
- * and 3.3).  A tensor is committed as the RFC 6962 Merkle Tree Hash of its
+ * as SHA-256, and combines node hashes in a binary Merkle tree (Sections 2.1
+ * and 2.2).  A tensor is committed as the RFC 6962 Merkle Tree Hash of its
  * bytes cut into chunks:
  *     MTH({}) = SHA-256(empty);  MTH({d}) = SHA-256(0x00 || d);
  *     MTH(D[0:n]) = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])), k the largest

@@ -1033,8 +1033,8 @@ int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const 
 /*
  * The protocol commits to checkpoints and to the tensors entering and leaving
  * each graph node with a collision-resistant hash such as SHA-256 (Sections
- * 3.1 and 3.3), and combines node hashes with a binary Merkle tree (Section
- * 3.3, checkpoint hash format).  Reading for a tensor: its bytes as stored
+ * 2.1 and 2.2), and combines node hashes with a binary Merkle tree (Section
+ * 2.2, checkpoint hash format).  Reading for a tensor: its bytes as stored
  * (row-major, little-endian binary32) are cut into chunks of C bytes (the last
  * one shorter); the commitment is the Merkle Tree Hash of RFC 6962 over the
  * chunks:  MTH({}) = SHA-256(empty);  MTH({d}) = SHA-256(0x00 || d);

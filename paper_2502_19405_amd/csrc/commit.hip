@@ -3,7 +3,7 @@
 //
 // The Verde protocol commits to checkpoints and to the tensors entering and
 // leaving every graph node with a collision-resistant hash such as SHA-256,
-// and combines node hashes in a binary Merkle tree (Sections 3.1 and 3.3).  A
+// and combines node hashes in a binary Merkle tree (Sections 2.1 and 2.2).  A
 // single SHA-256 stream is sequential, so a tensor is committed as a Merkle
 // tree of its chunks: leaf = SHA-256(0x00 || chunk), node = SHA-256(0x01 ||
 // left || right), the tree split at the largest power of two (RFC 6962).
