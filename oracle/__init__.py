@@ -108,6 +108,12 @@ def _declare(lib):
         "repops_ref_silu": (_int, [_i64, _f32p, _f32p, _int]),
         "repops_ref_swiglu": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
         "repops_ref_swiglu_backward": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _f32p, _int]),
+        "repops_ref_erf1": (_flt, [_flt]),
+        "repops_ref_gelu_erf1": (_flt, [_flt]),
+        "repops_ref_gelu_erf_grad1": (_flt, [_flt]),
+        "repops_ref_erf": (_int, [_i64, _f32p, _f32p, _int]),
+        "repops_ref_gelu_erf": (_int, [_i64, _f32p, _f32p, _int]),
+        "repops_ref_gelu_erf_backward": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
         "repops_ref_sha256": (None, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]),
         "repops_ref_commit": (_int, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
                                      ctypes.c_void_p]),
@@ -445,6 +451,42 @@ def swiglu_backward(g, u, dy, nthreads=0, lib=None):
     _check((lib or load()).repops_ref_swiglu_backward(g.size, _p(g), _p(u), _p(dy), _p(dg),
                                                       _p(du), nthreads), "swiglu_backward")
     return dg, du
+
+
+def erf1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_erf1(float(np.float32(x))))
+
+
+def gelu_erf1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_gelu_erf1(float(np.float32(x))))
+
+
+def gelu_erf_grad1(x, lib=None) -> np.float32:
+    return np.float32((lib or load()).repops_ref_gelu_erf_grad1(float(np.float32(x))))
+
+
+def _unary(fn, x, nthreads, lib):
+    x = np.ascontiguousarray(x, np.float32)
+    y = np.empty_like(x)
+    _check(getattr(lib or load(), fn)(x.size, _p(x), _p(y), nthreads), fn)
+    return y
+
+
+def erf(x, nthreads=0, lib=None):
+    return _unary("repops_ref_erf", x, nthreads, lib)
+
+
+def gelu_erf(x, nthreads=0, lib=None):
+    return _unary("repops_ref_gelu_erf", x, nthreads, lib)
+
+
+def gelu_erf_backward(x, dy, nthreads=0, lib=None):
+    x = np.ascontiguousarray(x, np.float32)
+    dy = np.ascontiguousarray(dy, np.float32)
+    dx = np.empty_like(x)
+    _check((lib or load()).repops_ref_gelu_erf_backward(x.size, _p(x), _p(dy), _p(dx), nthreads),
+           "gelu_erf_backward")
+    return dx
 
 
 # --------------------------------------------------------------------------

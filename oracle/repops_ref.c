@@ -1026,6 +1026,168 @@ int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const 
     return 0;
 }
 
+/*
+ * erf and the erf-form ("exact") GELU, x * Phi(x) with Phi the standard normal
+ * distribution function, as DistilBERT's activation (Section 4.2; Section 3.1
+ * lists the math functions RepOps rebuilds).  Reading (op sequence):
+ *   small arguments |z| < 0.5: erf(z) = z * S(z*z), S by Horner with fma over
+ *     RN(2/sqrt(pi) (-1)^n / (n! (2n+1))), n = 0..7;
+ *   otherwise erfc(z) = exp(-z^2) R(z), R(z) = exp(z^2) erfc(z) on
+ *     [0.5, 2.5]: degree-12 polynomial in s = z - 1.5 (exact),
+ *     [2.5, 10.5]: degree-8 polynomial in s = (1/(1 + z) - 3/16) * 9.5;
+ *     each the binary32-rounded monomial coefficients of the polynomial that
+ *     interpolates R at the Chebyshev points cos(pi (2k+1) / (2(d+1))) of s;
+ *     erfc(z) = 0 for z >= 10.5;
+ *   exp(-c x^2) (c = 1 or 1/2) without rounding x^2: h = x with the low 12
+ *     bits of its significand cleared (h*h is exact), d = (x - h) * (x + h),
+ *     exp(-c x^2) = exp_rep(-(h h) c) * exp_rep(-d c);
+ *   erf(x) = sign(x) (1 - erfc(|x|)) for |x| >= 0.5;
+ *   Phi(x): z = |x| * RN(1/sqrt 2); z < 0.5: fma(0.5, erf(x * RN(1/sqrt 2)), 0.5);
+ *     else q = RN(exp(-x^2/2) R(z)) * 0.5 (0 for z >= 10.5) and
+ *     Phi = 1 - q for x > 0, q otherwise (no cancellation in the lower tail);
+ *   gelu(x) = x * Phi(x);  gelu'(x) = fma(x, exp(-x^2/2) * RN(1/sqrt(2 pi)), Phi(x)).
+ */
+static const float ERF_SMALL[8] = {
+    0x1.20dd76p+0f, -0x1.812746p-2f, 0x1.ce2f22p-4f, -0x1.b82ce4p-6f,
+    0x1.565bcep-8f, -0x1.c02db4p-11f, 0x1.f9a326p-14f, -0x1.f4d25cp-17f};
+static const float ERFC_P1[13] = {
+    0x1.494db0p-2f, -0x1.4f1988p-3f, 0x1.37ea26p-4f, -0x1.0dc542p-5f, 0x1.b6596ep-7f,
+    -0x1.5135c2p-8f, 0x1.ee6646p-10f, -0x1.5c00ccp-11f, 0x1.d5624ap-13f, -0x1.243bd4p-14f,
+    0x1.71a8d4p-16f, -0x1.364e28p-17f, 0x1.6a86acp-19f};
+static const float ERFC_P2[9] = {
+    0x1.040c3ap-3f, 0x1.565eecp-4f, 0x1.c46bacp-8f, -0x1.24aa48p-13f, -0x1.44b7dap-14f,
+    0x1.7d0926p-19f, 0x1.82a7a8p-20f, -0x1.1ebc20p-23f, -0x1.dd0088p-26f};
+static const float ERF_INV_SQRT2 = 0x1.6a09e6p-1f;
+static const float ERF_INV_SQRT_2PI = 0x1.988454p-2f;
+
+static float erf_small(float z)
+{
+    const float u = z * z;
+    float p = ERF_SMALL[7];
+    for (int n = 6; n >= 0; --n) p = fmaf(p, u, ERF_SMALL[n]);
+    return z * p;
+}
+
+static float clear_low12(float x)
+{
+    uint32_t b;
+    memcpy(&b, &x, 4);
+    b &= 0xFFFFF000u;
+    float h;
+    memcpy(&h, &b, 4);
+    return h;
+}
+
+static float exp_neg_sq(float x, float c)
+{
+    const float h = clear_low12(x);
+    const float hh = h * h;
+    const float a = -(hh * c);
+    const float dl = x - h;
+    const float ds = x + h;
+    const float d = dl * ds;
+    const float b = -(d * c);
+    return repops_ref_exp1(a) * repops_ref_exp1(b);
+}
+
+static float erfc_scaled(float z)
+{
+    if (z < 2.5f) {
+        const float s = z - 1.5f;
+        float p = ERFC_P1[12];
+        for (int j = 11; j >= 0; --j) p = fmaf(p, s, ERFC_P1[j]);
+        return p;
+    }
+    const float t = 1.0f / (1.0f + z);
+    const float s = (t - 0.1875f) * 9.5f;
+    float p = ERFC_P2[8];
+    for (int j = 7; j >= 0; --j) p = fmaf(p, s, ERFC_P2[j]);
+    return p;
+}
+
+float repops_ref_erf1(float x)
+{
+    if (isnan(x)) return x;
+    const float a = fabsf(x);
+    if (a < 0.5f) return erf_small(x);
+    const float q = (a >= 10.5f) ? 0.0f : exp_neg_sq(a, 1.0f) * erfc_scaled(a);
+    const float r = 1.0f - q;
+    return x < 0.0f ? -r : r;
+}
+
+static float normal_cdf(float x)
+{
+    const float a = fabsf(x);
+    const float z = a * ERF_INV_SQRT2;
+    if (z < 0.5f) {
+        const float xs = x * ERF_INV_SQRT2;
+        return fmaf(0.5f, erf_small(xs), 0.5f);
+    }
+    float q = 0.0f;
+    if (!(z >= 10.5f)) {
+        const float er = exp_neg_sq(a, 0.5f) * erfc_scaled(z);
+        q = er * 0.5f;
+    }
+    return x > 0.0f ? 1.0f - q : q;
+}
+
+float repops_ref_gelu_erf1(float x)
+{
+    if (isnan(x)) return x;
+    return x * normal_cdf(x);
+}
+
+float repops_ref_gelu_erf_grad1(float x)
+{
+    if (isnan(x)) return x;
+    const float a = fabsf(x);
+    const float e = exp_neg_sq(a, 0.5f);
+    const float phi = e * ERF_INV_SQRT_2PI;
+    return fmaf(x, phi, normal_cdf(x));
+}
+
+typedef struct {
+    const float *x, *dy;
+    float *y;
+    int which; /* 0 erf, 1 gelu, 2 gelu backward */
+} erf_ctx;
+
+static void erf_range(void *vctx, int64_t i0, int64_t i1)
+{
+    const erf_ctx *c = (const erf_ctx *)vctx;
+    for (int64_t i = i0; i < i1; ++i) {
+        const float x = c->x[i];
+        if (c->which == 0) c->y[i] = repops_ref_erf1(x);
+        else if (c->which == 1) c->y[i] = repops_ref_gelu_erf1(x);
+        else c->y[i] = c->dy[i] * repops_ref_gelu_erf_grad1(x);
+    }
+}
+
+int repops_ref_erf(int64_t n, const float *x, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    erf_ctx c = {x, NULL, y, 0};
+    parallel_for(nthreads, n, erf_range, &c);
+    return 0;
+}
+
+int repops_ref_gelu_erf(int64_t n, const float *x, float *y, int nthreads)
+{
+    if (n < 0) return -1;
+    erf_ctx c = {x, NULL, y, 1};
+    parallel_for(nthreads, n, erf_range, &c);
+    return 0;
+}
+
+int repops_ref_gelu_erf_backward(int64_t n, const float *x, const float *dy, float *dx,
+                                 int nthreads)
+{
+    if (n < 0) return -1;
+    erf_ctx c = {x, dy, dx, 2};
+    parallel_for(nthreads, n, erf_range, &c);
+    return 0;
+}
+
 /* ========================================================================= */
 /* Tensor commitments: SHA-256 and a Merkle tree over chunks                  */
 /* ========================================================================= */

@@ -137,6 +137,15 @@ int repops_ref_swiglu(int64_t n, const float *g, const float *u, float *y, int n
 int repops_ref_swiglu_backward(int64_t n, const float *g, const float *u, const float *dy,
                                float *dg, float *du, int nthreads);
 
+/* erf and the erf-form GELU x * Phi(x) with its derivative (elementwise). */
+float repops_ref_erf1(float x);
+float repops_ref_gelu_erf1(float x);
+float repops_ref_gelu_erf_grad1(float x);
+int repops_ref_erf(int64_t n, const float *x, float *y, int nthreads);
+int repops_ref_gelu_erf(int64_t n, const float *x, float *y, int nthreads);
+int repops_ref_gelu_erf_backward(int64_t n, const float *x, const float *dy, float *dx,
+                                 int nthreads);
+
 /* ---- tensor commitments ---- */
 
 /* SHA-256 (FIPS 180-4) of len bytes. */

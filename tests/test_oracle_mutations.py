@@ -15,6 +15,7 @@ import test_oracle as pins
 import test_oracle_training as tpins
 import test_oracle_llama as lpins
 import test_oracle_commit as cpins
+import test_oracle_erf as epins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "repops_ref.c")
 
@@ -132,6 +133,23 @@ MUTATIONS = {
                     "sha256_prefixed(1, 0x01, data + off, len, out);", ["mth"]),
     # commitment: tree split in halves instead of at a power of two
     "mth_split": ("while (k * 2 < count) k *= 2;", "k = count / 2;", ["mth"]),
+    # erf: Taylor coefficient with a wrong exponent
+    "erf_small_coeff": ("0x1.ce2f22p-4f, -0x1.b82ce4p-6f,", "0x1.ce2f22p-3f, -0x1.b82ce4p-6f,",
+                        ["erf"]),
+    # erf: one interpolant coefficient one ulp off (only the constants check sees it)
+    "erfc_coeff_ulp": ("0x1.71a8d4p-16f", "0x1.71a8d6p-16f", ["erf_const"]),
+    # erf: second interval's variable shifted
+    "erfc_var": ("const float s = (t - 0.1875f) * 9.5f;", "const float s = (t - 0.1875f) * 9.0f;",
+                 ["erf", "gelu_erf"]),
+    # exact GELU: x^2 rounded before exp (no split) -- the lower tail loses accuracy
+    "erf_no_split": ("    return repops_ref_exp1(a) * repops_ref_exp1(b);",
+                     "    return repops_ref_exp1(-(x * x) * c);", ["gelu_erf"]),
+    # exact GELU: lower tail through 1 - q
+    "phi_branch": ("return x > 0.0f ? 1.0f - q : q;", "return x > 0.0f ? 1.0f - q : 1.0f - (1.0f - q);",
+                   ["gelu_erf"]),
+    # exact GELU derivative: pdf term without the 1/sqrt(2 pi)
+    "gelu_erf_grad": ("const float phi = e * ERF_INV_SQRT_2PI;", "const float phi = e;",
+                      ["gelu_erf_grad"]),
 }
 
 CHECKS = {
@@ -173,6 +191,11 @@ CHECKS = {
     "sha_const": lambda lib: cpins.check_sha_constants(
         open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
     "mth": lambda lib: cpins.test_commit_against_rfc6962(lib, 64),
+    "erf": lambda lib: epins.test_erf_accuracy_and_symmetry(lib),
+    "erf_const": lambda lib: epins.check_erf_constants(
+        open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
+    "gelu_erf": lambda lib: epins.test_gelu_erf_accuracy(lib),
+    "gelu_erf_grad": lambda lib: epins.test_gelu_erf_grad(lib),
 }
 
 
