@@ -450,6 +450,42 @@ repops_status_t repops_commit(const void *data, uint64_t nbytes, uint32_t chunk_
                               uint8_t *digest, void *workspace, uint64_t workspace_bytes,
                               const repops_launch_t *launch, void *hip_stream);
 
+/*
+ * repops_erf -- reproducible erf of n contiguous elements (used inside the
+ * erf-form GELU; exported for testing).  |x| < 0.5: x * S(x*x), S by Horner
+ * with fma over RN(2/sqrt(pi) (-1)^n / (n! (2n+1))), n = 0..7.  Otherwise
+ * sign(x) (1 - erfc(|x|)) with erfc(z) = exp(-z^2) R(z), 0 for z >= 10.5:
+ *     R on [0.5, 2.5]: degree-12 polynomial in s = z - 1.5; on [2.5, 10.5]:
+ *     degree-8 polynomial in s = (1/(1 + z) - 3/16) * 9.5; each the
+ *     binary32-rounded monomial coefficients of the Chebyshev interpolant of
+ *     exp(z^2) erfc(z) (points cos(pi (2k+1) / (2(d+1))) in s), by Horner with fma;
+ *     exp(-c x^2) = exp_rep(-(h*h) c) * exp_rep(-((x - h)(x + h)) c), h = x with
+ *     its low 12 significand bits cleared.
+ *   Y may equal X.
+ */
+repops_status_t repops_erf(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                           const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_gelu_erf -- the erf form of GELU (DistilBERT's activation, Section
+ * 4.2): y = x * Phi(x), with z = |x| RN(1/sqrt 2):
+ *     z < 0.5: Phi = fma(0.5, erf(x RN(1/sqrt 2)), 0.5);
+ *     else q = RN(exp(-x^2/2) R(z)) * 0.5 (0 for z >= 10.5), Phi = 1 - q for
+ *     x > 0 and q otherwise.
+ *   Y may equal X.
+ */
+repops_status_t repops_gelu_erf(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                                const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_gelu_erf_backward -- dx = dy * (Phi(x) + x phi(x)) with
+ * phi(x) = RN(exp(-x^2/2) * RN(1/sqrt(2 pi))):  gelu' = fma(x, phi, Phi(x)).
+ *   dX may coincide exactly with X or dY.
+ */
+repops_status_t repops_gelu_erf_backward(const repops_order_t *order, int64_t n, const float *X,
+                                         const float *dY, float *dX, const repops_launch_t *launch,
+                                         void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -612,7 +612,7 @@ repops_status_t repops_gelu_backward(const repops_order_t* order, int64_t n, con
   st = ew_launch(launch, &threads, &max_blocks);
   if (st != REPOPS_OK || n == 0) return st;
   return hip_status(repops::launch_gelu_bwd(n, X, dY, dX, threads, max_blocks,
-                                            static_cast<hipStream_t>(hip_stream)));
+                                            static_cast<hipStream_t>(hip_stream), false));
 }
 
 repops_status_t repops_adam_step(const repops_order_t* order, int64_t n, float* param,
@@ -821,6 +821,45 @@ repops_status_t repops_commit(const void* data, uint64_t nbytes, uint32_t chunk_
   return hip_status(repops::launch_commit(static_cast<const uint8_t*>(data), nbytes, chunk_bytes,
                                           digest, static_cast<uint32_t*>(workspace),
                                           static_cast<hipStream_t>(hip_stream)));
+}
+
+// ---------------------------------------------------------------------------
+// erf and the erf-form GELU
+// ---------------------------------------------------------------------------
+
+repops_status_t repops_erf(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                           const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(
+      repops::launch_erf(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_gelu_erf(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                                const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(repops::launch_gelu_erf(n, X, Y, threads, max_blocks,
+                                            static_cast<hipStream_t>(hip_stream)));
+}
+
+repops_status_t repops_gelu_erf_backward(const repops_order_t* order, int64_t n, const float* X,
+                                         const float* dY, float* dX, const repops_launch_t* launch,
+                                         void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, dX);
+  if (st != REPOPS_OK) return st;
+  if ((st = check_elementwise(order, n, dY, dX)) != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(repops::launch_gelu_bwd(n, X, dY, dX, threads, max_blocks,
+                                            static_cast<hipStream_t>(hip_stream), true));
 }
 
 }  // extern "C"

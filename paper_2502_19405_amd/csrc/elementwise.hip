@@ -1,4 +1,4 @@
-// Reproducible elementwise exp and tanh-form GELU for gfx950.
+// Reproducible elementwise exp, erf, tanh-form and erf-form GELU for gfx950.
 //
 // Each element is independent, so the launch only decides which lane computes
 // which element.  Aligned, vectorisable spans go through 16-byte loads and
@@ -19,6 +19,12 @@ struct ExpOp {
 };
 struct GeluOp {
   __device__ __forceinline__ float operator()(float x) const { return rep_gelu(x); }
+};
+struct ErfOp {
+  __device__ __forceinline__ float operator()(float x) const { return rep_erf(x); }
+};
+struct GeluErfOp {
+  __device__ __forceinline__ float operator()(float x) const { return rep_gelu_erf(x); }
 };
 
 template <class Op>
@@ -71,6 +77,16 @@ hipError_t launch_gelu(int64_t n, const float* x, float* y, int threads, int max
 hipError_t launch_exp(int64_t n, const float* x, float* y, int threads, int max_blocks,
                       hipStream_t s) {
   return launch<ExpOp>(n, x, y, threads, max_blocks, s);
+}
+
+hipError_t launch_erf(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                      hipStream_t s) {
+  return launch<ErfOp>(n, x, y, threads, max_blocks, s);
+}
+
+hipError_t launch_gelu_erf(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                           hipStream_t s) {
+  return launch<GeluErfOp>(n, x, y, threads, max_blocks, s);
 }
 
 }  // namespace repops

@@ -26,6 +26,12 @@ struct RmsArgs {
   float* rstd_out;     // nullable
 };
 
+// erf and the erf-form GELU (elementwise.hip).
+hipError_t launch_erf(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                      hipStream_t s);
+hipError_t launch_gelu_erf(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                           hipStream_t s);
+
 hipError_t launch_sincos(int64_t n, const float* x, float* s, float* c, int threads,
                          int max_blocks, hipStream_t st);
 hipError_t launch_rope(const RopeArgs& a, int waves_per_block, hipStream_t s);

@@ -16,6 +16,10 @@
 //       binary32 parts), Taylor polynomials of degree 9 and 10 on |r| <= pi/4
 //       by Horner's rule, quadrant selection.
 // silu: x / (1 + exp(-x)); silu' = s + x s (1 - s) with s = 1 / (1 + exp(-x)).
+// erf: Taylor series below 0.5; beyond, erfc(z) = exp(-z^2) R(z) with R =
+//       exp(z^2) erfc(z) from Chebyshev interpolants on [0.5, 2.5] and
+//       [2.5, 10.5]; exp(-c x^2) from a split of x so that x^2 is never rounded.
+// gelu_erf: x Phi(x), Phi's lower tail taken directly (no 1 + erf).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -136,6 +140,100 @@ __device__ __forceinline__ void rep_sincos(float x, float& sin_out, float& cos_o
   const float qnan = __builtin_nanf("");
   sin_out = finite ? so : qnan;
   cos_out = finite ? co : qnan;
+}
+
+// Taylor coefficients 2/sqrt(pi) (-1)^n / (n! (2n + 1)), n = 0..7.
+constexpr float kErfT0 = 0x1.20dd76p+0f, kErfT1 = -0x1.812746p-2f, kErfT2 = 0x1.ce2f22p-4f,
+                kErfT3 = -0x1.b82ce4p-6f, kErfT4 = 0x1.565bcep-8f, kErfT5 = -0x1.c02db4p-11f,
+                kErfT6 = 0x1.f9a326p-14f, kErfT7 = -0x1.f4d25cp-17f;
+// exp(z^2) erfc(z): degree-12 Chebyshev interpolant in s = z - 1.5 on [0.5, 2.5]
+// and degree-8 interpolant in s = (1/(1+z) - 3/16) * 9.5 on [2.5, 10.5],
+// binary32-rounded monomial coefficients, constant term first.
+constexpr float kErfcA[13] = {
+    0x1.494db0p-2f, -0x1.4f1988p-3f, 0x1.37ea26p-4f, -0x1.0dc542p-5f, 0x1.b6596ep-7f,
+    -0x1.5135c2p-8f, 0x1.ee6646p-10f, -0x1.5c00ccp-11f, 0x1.d5624ap-13f, -0x1.243bd4p-14f,
+    0x1.71a8d4p-16f, -0x1.364e28p-17f, 0x1.6a86acp-19f};
+constexpr float kErfcB[9] = {
+    0x1.040c3ap-3f, 0x1.565eecp-4f, 0x1.c46bacp-8f, -0x1.24aa48p-13f, -0x1.44b7dap-14f,
+    0x1.7d0926p-19f, 0x1.82a7a8p-20f, -0x1.1ebc20p-23f, -0x1.dd0088p-26f};
+constexpr float kInvSqrt2 = 0x1.6a09e6p-1f;
+constexpr float kInvSqrt2Pi = 0x1.988454p-2f;
+
+__device__ __forceinline__ float rep_erf_small(float z) {
+  const float u = z * z;
+  float p = __builtin_fmaf(kErfT7, u, kErfT6);
+  p = __builtin_fmaf(p, u, kErfT5);
+  p = __builtin_fmaf(p, u, kErfT4);
+  p = __builtin_fmaf(p, u, kErfT3);
+  p = __builtin_fmaf(p, u, kErfT2);
+  p = __builtin_fmaf(p, u, kErfT1);
+  p = __builtin_fmaf(p, u, kErfT0);
+  return z * p;
+}
+
+// exp(-c x^2), c = 1 or 1/2: h = x with its low 12 significand bits cleared,
+// so h*h is exact; exp(-c x^2) = exp(-(h h) c) exp(-(x - h)(x + h) c).
+__device__ __forceinline__ float rep_exp_neg_sq(float x, float c) {
+  const float h = __uint_as_float(__float_as_uint(x) & 0xFFFFF000u);
+  const float hh = h * h;
+  const float a = -(hh * c);
+  const float dl = x - h;
+  const float ds = x + h;
+  const float d = dl * ds;
+  const float b = -(d * c);
+  return rep_exp(a) * rep_exp(b);
+}
+
+// exp(z^2) erfc(z) for z >= 0.5.  Both intervals run one degree-12 Horner
+// chain: the second interval's coefficients are preceded by four zeros, which
+// keeps the chain at +0 until its own leading coefficient, so the result is
+// that of its degree-8 chain bit for bit.
+__device__ __forceinline__ float rep_erfc_scaled(float z) {
+  const bool lo = z < 2.5f;
+  const float t = 1.0f / (1.0f + z);
+  const float s = lo ? z - 1.5f : (t - 0.1875f) * 9.5f;
+  float p = lo ? kErfcA[12] : 0.0f;
+#pragma unroll
+  for (int j = 11; j >= 0; --j) {
+    const float c = lo ? kErfcA[j] : (j <= 8 ? kErfcB[j] : 0.0f);
+    p = __builtin_fmaf(p, s, c);
+  }
+  return p;
+}
+
+__device__ __forceinline__ float rep_erf(float x) {
+  const float a = __builtin_fabsf(x);
+  const float small = rep_erf_small(x);
+  const float q = (a >= 10.5f) ? 0.0f : rep_exp_neg_sq(a, 1.0f) * rep_erfc_scaled(a);
+  const float r = 1.0f - q;
+  float y = (x < 0.0f) ? -r : r;
+  y = (a < 0.5f) ? small : y;
+  return (x != x) ? x : y;
+}
+
+// Phi(x), the standard normal distribution function.
+__device__ __forceinline__ float rep_normal_cdf(float x, float a, float e) {
+  const float z = a * kInvSqrt2;
+  const float xs = x * kInvSqrt2;
+  const float mid = __builtin_fmaf(0.5f, rep_erf_small(xs), 0.5f);
+  const float er = e * rep_erfc_scaled(z);
+  const float q = (z >= 10.5f) ? 0.0f : er * 0.5f;
+  const float tail = (x > 0.0f) ? 1.0f - q : q;
+  return (z < 0.5f) ? mid : tail;
+}
+
+__device__ __forceinline__ float rep_gelu_erf(float x) {
+  const float a = __builtin_fabsf(x);
+  const float y = x * rep_normal_cdf(x, a, rep_exp_neg_sq(a, 0.5f));
+  return (x != x) ? x : y;
+}
+
+__device__ __forceinline__ float rep_gelu_erf_grad(float x) {
+  const float a = __builtin_fabsf(x);
+  const float e = rep_exp_neg_sq(a, 0.5f);
+  const float phi = e * kInvSqrt2Pi;
+  const float g = __builtin_fmaf(x, phi, rep_normal_cdf(x, a, e));
+  return (x != x) ? x : g;
 }
 
 __device__ __forceinline__ float rep_silu(float x) {

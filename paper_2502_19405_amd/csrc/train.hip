@@ -434,8 +434,17 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
 // is 16-byte aligned.
 // ---------------------------------------------------------------------------
 
+struct GeluTanhGrad {
+  __device__ __forceinline__ float operator()(float x) const { return rep_gelu_grad(x); }
+};
+struct GeluErfGrad {
+  __device__ __forceinline__ float operator()(float x) const { return rep_gelu_erf_grad(x); }
+};
+
+template <class Grad>
 __global__ __launch_bounds__(1024) void gelu_bwd_kernel(int64_t n, const float* x, const float* dy,
                                                         float* dx, int vec) {
+  const Grad grad;
   const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   int64_t done = 0;
@@ -448,15 +457,15 @@ __global__ __launch_bounds__(1024) void gelu_bwd_kernel(int64_t n, const float* 
       const float4 xv = x4[i];
       const float4 dv = d4[i];
       float4 o;
-      o.x = dv.x * rep_gelu_grad(xv.x);
-      o.y = dv.y * rep_gelu_grad(xv.y);
-      o.z = dv.z * rep_gelu_grad(xv.z);
-      o.w = dv.w * rep_gelu_grad(xv.w);
+      o.x = dv.x * grad(xv.x);
+      o.y = dv.y * grad(xv.y);
+      o.z = dv.z * grad(xv.z);
+      o.w = dv.w * grad(xv.w);
       o4[i] = o;
     }
     done = n4 * 4;
   }
-  for (int64_t i = done + tid; i < n; i += stride) dx[i] = dy[i] * rep_gelu_grad(x[i]);
+  for (int64_t i = done + tid; i < n; i += stride) dx[i] = dy[i] * grad(x[i]);
 }
 
 // One element of the Adam / AdamW update (decay: 0 none, 1 decoupled, 2 coupled).
@@ -658,11 +667,15 @@ hipError_t launch_layernorm_bwd_fused(const RowBwdArgs& a, const LnParamArgs& p,
 }
 
 hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,
-                           int max_blocks, hipStream_t s) {
+                           int max_blocks, hipStream_t s, bool erf_form) {
   const bool vec = aligned16(x) && aligned16(dy) && aligned16(dx);
   const int64_t blocks = ew_blocks(vec ? (n + 3) / 4 : n, threads, max_blocks);
-  hipLaunchKernelGGL(gelu_bwd_kernel, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0, s, n,
-                     x, dy, dx, vec ? 1 : 0);
+  if (erf_form)
+    hipLaunchKernelGGL(gelu_bwd_kernel<GeluErfGrad>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(threads), 0, s, n, x, dy, dx, vec ? 1 : 0);
+  else
+    hipLaunchKernelGGL(gelu_bwd_kernel<GeluTanhGrad>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(threads), 0, s, n, x, dy, dx, vec ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -51,7 +51,7 @@ hipError_t launch_layernorm_bwd_fused(const RowBwdArgs& a, const LnParamArgs& p,
                                       hipStream_t s);
 
 hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,
-                           int max_blocks, hipStream_t s);
+                           int max_blocks, hipStream_t s, bool erf_form);
 
 // Step scalars of the Adam update, computed on the host.
 struct AdamScalars {

@@ -112,6 +112,9 @@ _SIGNATURES = {
     "repops_silu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
     "repops_swiglu": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
     "repops_swiglu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _vp, _lp, _vp]),
+    "repops_erf": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_gelu_erf": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_gelu_erf_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
     "repops_commit_workspace": (_i32, [ctypes.c_uint64, _u32, ctypes.POINTER(ctypes.c_uint64)]),
     "repops_commit": (_i32, [_vp, ctypes.c_uint64, _u32, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
 }
@@ -442,6 +445,30 @@ def gelu_backward(X: torch.Tensor, dY: torch.Tensor, order: Order | None = None,
                                      _dev(X, "X"), _dev(dY, "dY"), _dev(out, "out"),
                                      _launch(launch), _stream(out))
     _check(rc, "repops_gelu_backward")
+    return out
+
+
+def erf(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+        out: torch.Tensor | None = None) -> torch.Tensor:
+    return _elementwise("repops_erf", X, order, launch, out)
+
+
+def gelu_erf(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+             out: torch.Tensor | None = None) -> torch.Tensor:
+    """x * Phi(x), the erf form of GELU."""
+    return _elementwise("repops_gelu_erf", X, order, launch, out)
+
+
+def gelu_erf_backward(X: torch.Tensor, dY: torch.Tensor, order: Order | None = None,
+                      launch: Launch | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    if not X.is_contiguous() or not dY.is_contiguous() or dY.numel() != X.numel():
+        raise ValueError("X and dY must be contiguous with equal element counts")
+    if out is None:
+        out = torch.empty_like(X)
+    rc = load().repops_gelu_erf_backward(_ord(order), X.numel(), _dev(X, "X"), _dev(dY, "dY"),
+                                         _flat(out, X.numel(), "out"), _launch(launch),
+                                         _stream(out))
+    _check(rc, "repops_gelu_erf_backward")
     return out
 
 
