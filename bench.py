@@ -188,6 +188,11 @@ def secondary(repops, steps):
     dG = t(inputs.normal(g, (4096, 3072), var=1e-2))
     out["gelu_backward_4096x3072"] = _rate(
         event_time_ms(lambda: repops.gelu_backward(H, dG, out=G), steps), nbytes=4 * H.numel() * 3)
+    out["gelu_erf_4096x3072"] = _rate(event_time_ms(lambda: repops.gelu_erf(H, out=G), steps),
+                                      nbytes=4 * H.numel() * 2)
+    out["gelu_erf_backward_4096x3072"] = _rate(
+        event_time_ms(lambda: repops.gelu_erf_backward(H, dG, out=G), steps),
+        nbytes=4 * H.numel() * 3)
     del H, G, dG
     # Adam: reads param, grad, exp_avg, exp_avg_sq and writes three of them
     # (28 B per parameter); the DistilBERT feed-forward block's 4.72 M
@@ -232,6 +237,17 @@ def secondary(repops, steps):
     ms = event_time_ms(lambda: repops.swiglu_backward(Gt, Ut, Dt, dg_out=Yt, du_out=Et), steps)
     out["swiglu_backward_4096x14336"] = _rate(ms, nbytes=4 * Gt.numel() * 5)
     del Gt, Ut, Yt, Dt, Et
+
+    # tensor commitment (SHA-256 Merkle tree, 1 KiB leaves) of a Llama-8B
+    # feed-forward weight, 4096 x 14336 fp32: bytes read once; SHA-256 is
+    # integer-ALU bound (about 22.5 VALU instructions per byte)
+    Wc = t(inputs.normal(g, (4096, 14336), var=4e-4))
+    dig = torch.empty(32, dtype=torch.uint8, device=dev)
+    wsc = torch.empty(repops.commit_workspace(Wc.numel() * 4, 1024) // 4 + 1, dtype=torch.int32,
+                      device=dev)
+    ms = event_time_ms(lambda: repops.commit(Wc, 1024, digest=dig, workspace=wsc), steps)
+    out["commit_4096x14336"] = _rate(ms, nbytes=Wc.numel() * 4)
+    del Wc, wsc
 
     # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
