@@ -253,7 +253,14 @@ def secondary(repops, steps):
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
     ms = event_time_ms(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet), steps)
     out["distilbert_mlp_block"] = _rate(ms, flops=2 * 2 * 4096 * 768 * 3072)
-    del X, W1, W2, b1, b2
+    # one whole training step of the block: forward, every gradient, AdamW over
+    # all 4.72 M parameters (six GEMMs of 2 * 4096 * 768 * 3072 flop each)
+    st = pipelines.MlpTrainState(W1, b1, W2, b2, gam, bet)
+    dYb = t(inputs.normal(g, (4096, 768), var=1e-4))
+    sbufs = {}
+    ms = event_time_ms(lambda: pipelines.mlp_train_step(st, X, dYb, bufs=sbufs), steps)
+    out["distilbert_mlp_train_step"] = _rate(ms, flops=6 * 2 * 4096 * 768 * 3072)
+    del X, W1, W2, b1, b2, st, dYb, sbufs
 
     # Llama attention block: 4 x 1024 tokens, d 4096, 32 heads
     d = inputs.llama_attention()

@@ -284,6 +284,23 @@ repops_status_t repops_layernorm_backward_rows(
     uint64_t workspace_bytes, const repops_launch_t *launch, void *hip_stream);
 
 /*
+ * repops_colsum_rows -- column sums over rows, the bias gradient of a linear
+ * layer (db = ones^T dY).  The row index is a contraction index, so the
+ * matmul rule applies with block length k_block: per column, chains
+ * P = P + x_ij over blocks of rows from +0, block partials left to right
+ * (bit-identical to repops_matmul of a ones row with X, since
+ * fma(1, x, P) = P + x).  rows = 0 gives +0.
+ *   X, ldx     rows x cols input; out [cols], must not overlap X.
+ *   workspace  as for repops_layernorm_backward_rows (its workspace query
+ *              gives the size for the same rows, cols and order).
+ *   launch     NULL or AUTO.
+ */
+repops_status_t repops_colsum_rows(const repops_order_t *order, int64_t rows, int64_t cols,
+                                   const float *X, int64_t ldx, float *out, void *workspace,
+                                   uint64_t workspace_bytes, const repops_launch_t *launch,
+                                   void *hip_stream);
+
+/*
  * repops_gelu_backward -- dx = dy * gelu'(x) over n contiguous elements, the
  * derivative of repops_gelu.  With s = 1 / (1 + exp_rep(w)) from the forward's
  * sequence (y = x * s), one fixed sequence:

@@ -89,6 +89,7 @@ def _declare(lib):
         "repops_ref_layernorm_backward_rows": (_int, [_int, _int, _i64, _i64, _i64, _f32p, _i64,
                                                       _f32p, _i64, _f32p, _f32p, _f32p, _f32p,
                                                       _i64, _f32p, _f32p, _int]),
+        "repops_ref_colsum_rows": (_int, [_i64, _i64, _i64, _f32p, _i64, _f32p, _int]),
         "repops_ref_gelu_grad1": (_flt, [_flt]),
         "repops_ref_gelu_backward": (_int, [_i64, _f32p, _f32p, _f32p, _int]),
         "repops_ref_adam_step": (_int, [_i64, _f32p, _f32p, _f32p, _f32p, _flt, _flt, _flt, _flt,
@@ -324,6 +325,16 @@ def layernorm_backward_rows(X, dY, mean, rstd, gamma=None, row_width=64, row_com
         _p(gamma), _p(dX), cols, _p(dg), _p(db), nthreads)
     _check(rc, "layernorm_backward_rows")
     return dX, dg, db
+
+
+def colsum_rows(X, k_block=64, nthreads=0, lib=None):
+    """Column sums over rows with the contraction rule (a linear layer's bias gradient)."""
+    X = np.ascontiguousarray(X, np.float32)
+    rows, cols = X.shape
+    out = np.empty(cols, np.float32)
+    _check((lib or load()).repops_ref_colsum_rows(k_block, rows, cols, _p(X), cols, _p(out),
+                                                  nthreads), "colsum_rows")
+    return out
 
 
 def gelu_grad1(x, lib=None) -> np.float32:

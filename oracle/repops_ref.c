@@ -1482,6 +1482,44 @@ int repops_ref_layernorm_backward_rows(int row_width, int row_combine, int64_t k
 }
 
 /*
+ * Bias gradient of a linear layer: db_j = sum over rows i of dY_ij.  Reading:
+ * the row index is a contraction index (the product ones^T dY), so the
+ * contraction rule applies with block length k_block: per column, chains
+ * P = P + dY_ij over blocks of rows from +0, block partials added left to
+ * right.  Rows = 0 gives +0.
+ */
+typedef struct {
+    int64_t k_block, rows;
+    const float *X; int64_t ldx;
+    float *out;
+} colsum_ctx;
+
+static void colsum_range(void *vctx, int64_t j0, int64_t j1)
+{
+    const colsum_ctx *c = (const colsum_ctx *)vctx;
+    const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;
+    for (int64_t j = j0; j < j1; ++j) {
+        float acc = 0.0f;
+        for (int64_t i0 = 0; i0 < c->rows; i0 += blk) {
+            const int64_t i1 = (i0 + blk < c->rows) ? i0 + blk : c->rows;
+            float p = 0.0f;
+            for (int64_t i = i0; i < i1; ++i) p = p + c->X[i * c->ldx + j];
+            acc = acc + p;
+        }
+        c->out[j] = acc;
+    }
+}
+
+int repops_ref_colsum_rows(int64_t k_block, int64_t rows, int64_t cols, const float *X,
+                           int64_t ldx, float *out, int nthreads)
+{
+    if (k_block < 0 || rows < 0 || cols < 0) return -1;
+    colsum_ctx c = {k_block, rows, X, ldx, out};
+    parallel_for(nthreads, cols, colsum_range, &c);
+    return 0;
+}
+
+/*
  * GELU backward (tanh form): with s = 1 / (1 + exp_rep(-2z)) the forward is
  * x * s, so d/dx = s + x s (1 - s) * 2 sqrt(2/pi) (1 + 3 * 0.044715 x^2).
  * Reading (op sequence): u = x*x; z = fma(c, u*x, x) * sq; e = exp_rep(-2z);

@@ -172,6 +172,10 @@ int repops_ref_layernorm_backward_rows(int row_width, int row_combine, int64_t k
                                        float *dX, int64_t lddx, float *dgamma, float *dbeta,
                                        int nthreads);
 
+/* Column sums over rows with the contraction rule (the bias gradient). */
+int repops_ref_colsum_rows(int64_t k_block, int64_t rows, int64_t cols, const float *X,
+                           int64_t ldx, float *out, int nthreads);
+
 /* d gelu(x) / dx and dX = dY * gelu'(X). */
 float repops_ref_gelu_grad1(float x);
 int repops_ref_gelu_backward(int64_t n, const float *x, const float *dy, float *dx, int nthreads);

@@ -602,6 +602,39 @@ repops_status_t repops_rmsnorm_backward_rows(
                        dgamma, nullptr, workspace, workspace_bytes, launch, hip_stream);
 }
 
+repops_status_t repops_colsum_rows(const repops_order_t* order, int64_t rows, int64_t cols,
+                                   const float* X, int64_t ldx, float* out, void* workspace,
+                                   uint64_t workspace_bytes, const repops_launch_t* launch,
+                                   void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
+  if (launch && (launch->kind != REPOPS_LAUNCH_AUTO || !launch_params_zero_from(launch, 0)))
+    return REPOPS_ERR_LAUNCH;
+  if (cols == 0) return REPOPS_OK;
+  uint64_t need = 0;
+  repops_status_t st = repops_layernorm_backward_workspace(order, rows, cols, &need);
+  if (st != REPOPS_OK) return st;
+  if (repops::layernorm_param_grid(rows, cols, order->k_block) > kMaxDim) return REPOPS_ERR_SHAPE;
+  if (!out) return REPOPS_ERR_NULL;
+  if (need > 0 && (!workspace || workspace_bytes < need)) return REPOPS_ERR_WORKSPACE;
+  const Extent oe = vec_extent(out, cols);
+  if (rows > 0) {
+    if ((st = check_matrix(X, rows, cols, ldx)) != REPOPS_OK) return st;
+    if (overlaps(oe, extent_of(X, 1, 0, 1, 0, rows, cols, ldx))) return REPOPS_ERR_ALIAS;
+  }
+  if (need > 0) {
+    const Extent we = vec_extent(workspace, static_cast<int64_t>(need / sizeof(float)));
+    if (overlaps(we, oe) || (rows > 0 && overlaps(we, extent_of(X, 1, 0, 1, 0, rows, cols, ldx))))
+      return REPOPS_ERR_ALIAS;
+  }
+  LnParamArgs p{};
+  p.rows = rows; p.cols = cols; p.k_block = order->k_block;
+  p.X = X; p.ldx = ldx; p.dY = X; p.lddy = ldx;
+  p.dbeta = out; p.ws = static_cast<float*>(workspace);
+  p.sum_only = 1;
+  return hip_status(repops::launch_layernorm_param(p, static_cast<hipStream_t>(hip_stream)));
+}
+
 repops_status_t repops_gelu_backward(const repops_order_t* order, int64_t n, const float* X,
                                      const float* dY, float* dX, const repops_launch_t* launch,
                                      void* hip_stream) {

@@ -211,6 +211,16 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
   int64_t i = i0;
   // Eight rows per step: the loads are independent of the chains and issue
   // together; the chains themselves advance one row at a time.
+  if (a.sum_only) {  // bias gradient: dY's column chains only
+    for (; i + 8 <= i1; i += 8) {
+      float dv[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) dv[r] = dp[(i + r) * a.lddy];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) pb = pb + dv[r];
+    }
+    for (; i < i1; ++i) pb = pb + dp[i * a.lddy];
+  }
   for (; i + 8 <= i1; i += 8) {
     float xv[8], dv[8];
 #pragma unroll

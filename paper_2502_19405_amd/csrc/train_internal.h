@@ -39,6 +39,7 @@ struct LnParamArgs {
   float* dgamma; float* dbeta;  // nullable
   float* ws;
   int rms;            // RMSNorm: t = x * rstd (no mean)
+  int sum_only;       // column sums of dY only (the bias gradient): no X, mean, rstd
 };
 
 int64_t layernorm_param_blocks(int64_t rows, int64_t k_block);

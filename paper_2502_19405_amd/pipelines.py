@@ -77,3 +77,72 @@ def linear_backward(X, dY, W, order=None, gemm_launch=None, out_dx=None, out_dw=
     dX = repops.matmul(dY, W.t(), order=order, launch=gemm_launch, out=out_dx)
     dW = repops.matmul(X.t(), dY, order=order, launch=gemm_launch, out=out_dw)
     return dX, dW
+
+
+class MlpTrainState:
+    """Parameters, gradients and Adam moments of the feed-forward block in flat
+    device buffers (one Adam launch updates everything); W1 [h, f], b1 [f],
+    W2 [f, h], b2 [h], gamma [h], beta [h] are views into `param`, and the
+    gradients are written straight into the matching views of `grad`."""
+
+    def __init__(self, W1, b1, W2, b2, gamma, beta):
+        h, f = W1.shape
+        sizes = [h * f, f, f * h, h, h, h]
+        self.shapes = [(h, f), (f,), (f, h), (h,), (h,), (h,)]
+        n = sum(sizes)
+        dev = W1.device
+        self.param = torch.empty(n, dtype=torch.float32, device=dev)
+        self.grad = torch.empty_like(self.param)
+        self.exp_avg = torch.zeros_like(self.param)
+        self.exp_avg_sq = torch.zeros_like(self.param)
+        self.p, self.g = [], []
+        off = 0
+        for t, size, shape in zip((W1, b1, W2, b2, gamma, beta), sizes, self.shapes):
+            self.p.append(self.param[off:off + size].view(shape))
+            self.g.append(self.grad[off:off + size].view(shape))
+            self.p[-1].copy_(t)
+            off += size
+        self.step = 0
+
+
+def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps=1e-8,
+                   weight_decay=0.01, ln_eps=1e-5, order=None, gemm_launch=None, bufs=None):
+    """One training step of the feed-forward block Y = LayerNorm(gelu(X W1 + b1) W2 + b2)
+    given the loss gradient dY: forward, backward (every gradient), AdamW update
+    of all parameters.  Returns (Y, dX).  Every operation is a library call, so
+    the step is bitwise reproducible."""
+    W1, b1, W2, b2, gamma, beta = state.p
+    gW1, gb1, gW2, gb2, ggamma, gbeta = state.g
+    t, h = X.shape
+    f = W1.shape[1]
+    dev = X.device
+    b = bufs if bufs is not None else {}
+
+    def buf(name, *shape):
+        if name not in b:
+            b[name] = torch.empty(shape, dtype=torch.float32, device=dev)
+        return b[name]
+
+    # forward (the LayerNorm statistics are the backward's saved tensors)
+    H1 = repops.matmul(X, W1, b1, order=order, launch=gemm_launch, out=buf("H1", t, f))
+    G = repops.gelu(H1, order=order, out=buf("G", t, f))
+    H2 = repops.matmul(G, W2, b2, order=order, launch=gemm_launch, out=buf("H2", t, h))
+    mean, rstd = buf("mean", t), buf("rstd", t)
+    Y = repops.layernorm_rows(H2, gamma, beta, eps=ln_eps, order=order, out=buf("Y", t, h),
+                              mean_out=mean, rstd_out=rstd)
+    # backward
+    dH2, _, _ = repops.layernorm_backward_rows(H2, dY, mean, rstd, gamma, order=order,
+                                               dx_out=buf("dH2", t, h), dgamma_out=ggamma,
+                                               dbeta_out=gbeta)
+    repops.matmul(G.t(), dH2, order=order, launch=gemm_launch, out=gW2)
+    repops.colsum_rows(dH2, order=order, out=gb2)
+    dG = repops.matmul(dH2, W2.t(), order=order, launch=gemm_launch, out=buf("dG", t, f))
+    dH1 = repops.gelu_backward(H1, dG, order=order, out=dG)
+    repops.matmul(X.t(), dH1, order=order, launch=gemm_launch, out=gW1)
+    repops.colsum_rows(dH1, order=order, out=gb1)
+    dX = repops.matmul(dH1, W1.t(), order=order, launch=gemm_launch, out=buf("dX", t, h))
+    # optimizer
+    state.step += 1
+    repops.adam_step(state.param, state.grad, state.exp_avg, state.exp_avg_sq, lr, betas[0],
+                     betas[1], eps, weight_decay, state.step, decoupled=True, order=order)
+    return Y, dX

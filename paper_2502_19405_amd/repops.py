@@ -99,6 +99,7 @@ _SIGNATURES = {
     "repops_layernorm_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp,
                                               _vp, _i64, _vp, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
     "repops_gelu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
+    "repops_colsum_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
     "repops_adam_step": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32, _f32, _f32, _i64,
                                 _i32, _lp, _vp]),
     "repops_sincos": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
@@ -430,6 +431,25 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
         ptr(dbeta, "dbeta"), wptr, wbytes, _launch(launch), _stream(X))
     _check(rc, "repops_layernorm_backward_rows")
     return dx, dgamma, dbeta
+
+
+def colsum_rows(X: torch.Tensor, order: Order | None = None, out: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Column sums of X [rows, cols] over rows (a linear layer's bias gradient)."""
+    rows, cols, ldx = _rows(X, "X")
+    if out is None:
+        out = torch.empty(cols, dtype=torch.float32, device=X.device)
+    wptr, wbytes = None, 0
+    if workspace is None:
+        need = layernorm_backward_workspace(rows, cols, order)
+        if need:
+            workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
+    if workspace is not None:
+        wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
+    rc = load().repops_colsum_rows(_ord(order), rows, cols, X.data_ptr() if rows else None, ldx,
+                                   _flat(out, cols, "out"), wptr, wbytes, None, _stream(out))
+    _check(rc, "repops_colsum_rows")
+    return out
 
 
 def gelu_backward(X: torch.Tensor, dY: torch.Tensor, order: Order | None = None,

@@ -222,6 +222,28 @@ def test_layernorm_backward_distilbert_shape(rp):
 
 
 # --------------------------------------------------------------------------
+# bias gradient (column sums)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,cols,k_block", [(75, 100, 64), (4096, 768, 64), (4096, 3072, 64),
+                                               (300, 77, 0), (300, 77, 7), (0, 40, 64),
+                                               (64, 5000, 64), (1, 3, 64)])
+def test_colsum_rows(rp, rows, cols, k_block):
+    import torch
+    g = inputs.rng(1050 + rows + k_block)
+    X = inputs.normal(g, (rows, cols))
+    want = oracle.colsum_rows(X, k_block)
+    announce("colsum", rows, cols, k_block)
+    got = rp.colsum_rows(dev(X) if rows else torch.empty((0, cols), device="cuda:0"),
+                         order=rp.Order(k_block=k_block))
+    assert_bits_equal(host(got), want, f"{rows}x{cols} k_block={k_block}")
+    if rows:  # the same as the product ones^T X
+        ones = torch.ones((1, rows), device="cuda:0")
+        via = rp.matmul(ones, dev(X), order=rp.Order(k_block=k_block))
+        assert_bits_equal(host(via)[0], want, "ones^T X")
+
+
+# --------------------------------------------------------------------------
 # GELU backward
 # --------------------------------------------------------------------------
 

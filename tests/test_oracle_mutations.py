@@ -69,6 +69,10 @@ MUTATIONS = {
                       ["lnp_order"]),
     # LayerNorm parameter gradients: dbeta weighted by t
     "lnp_dbeta_t": ("pb = pb + dy;", "pb = fmaf(dy, t, pb);", ["lnp_int"]),
+    # bias gradient: block partial not reset between row blocks
+    "colsum_no_reset": ("            float p = 0.0f;\n            for (int64_t i = i0; i < i1; ++i) p = p + c->X",
+                        "            static __thread float p; if (i0 == 0) p = 0.0f;\n            for (int64_t i = i0; i < i1; ++i) p = p + c->X",
+                        ["colsum"]),
     # GELU backward: (1 - s) factor replaced by s
     "gelu_grad_om": ("const float t2 = t1 * om;", "const float t2 = t1 * s;", ["gelu_grad"]),
     # GELU backward: 3 * 0.044715 coefficient one ulp off
@@ -110,8 +114,8 @@ MUTATIONS = {
     # RMSNorm backward: projection term dropped
     "rmsb_proj": ("const float w = g[j] - tb;", "const float w = g[j];", ["rmsb"]),
     # RMSNorm dgamma: rows in one block
-    "rmsp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for",
-                       "const int64_t blk = c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for",
+    "rmsp_unblocked": ("const int64_t blk = c->k_block > 0 ? c->k_block : c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for (int64_t i0 = 0; i0 < c->rows; i0 += blk) {\n            const int64_t i1 = (i0 + blk < c->rows) ? i0 + blk : c->rows;\n            float pg",
+                       "const int64_t blk = c->rows;\n    for (int64_t j = j0; j < j1; ++j) {\n        float acc = 0.0f;\n        for (int64_t i0 = 0; i0 < c->rows; i0 += blk) {\n            const int64_t i1 = (i0 + blk < c->rows) ? i0 + blk : c->rows;\n            float pg",
                        ["rmsp"]),
     # SiLU: exp of +x
     "silu_sign": ("    const float w = -x;\n    const float d = 1.0f + repops_ref_exp1(w);\n    return x / d;",
@@ -171,6 +175,7 @@ CHECKS = {
     "lnp_order": lambda lib: tpins.test_layernorm_param_grads_order_witness(lib),
     "lnp_int": lambda lib: tpins.test_layernorm_param_grads_integer_exact(lib),
     "gelu_grad": lambda lib: tpins.test_gelu_grad_bound(lib),
+    "colsum": lambda lib: tpins.test_colsum_witness_and_integers(lib),
     "tconst": lambda lib: tpins.check_training_constants(
         open(lib._name[:-len("mutant.so")] + "repops_ref.c").read()),
     "adam_sc": lambda lib: tpins.test_adam_scalars(lib),

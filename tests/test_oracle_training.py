@@ -184,6 +184,32 @@ def test_layernorm_backward_gamma_none_equals_ones_for_dx(ref):
 
 
 # --------------------------------------------------------------------------
+# bias gradient (column sums)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k_block", [64, 0, 7, 1])
+def test_colsum_equals_the_contraction_with_ones(ref, k_block):
+    """fma(1, y, P) rounds once, exactly as P + y: the column sums equal the
+    oracle's matrix product ones^T dY bit for bit under every block length."""
+    g = inputs.rng(140 + k_block)
+    dY = inputs.normal(g, (300, 77))
+    ones = np.ones((1, 300), np.float32)
+    want = oracle.matmul(ones, dY, k_block=k_block, lib=ref)[0]
+    assert_bits_equal(oracle.colsum_rows(dY, k_block, lib=ref), want, f"k_block={k_block}")
+
+
+def test_colsum_witness_and_integers(ref):
+    dY = np.zeros((128, 3), np.float32)
+    dY[0] = 2.0 ** 24
+    dY[64:] = 1.0
+    assert (oracle.colsum_rows(dY, 64, lib=ref) == np.float32(2 ** 24 + 64)).all()
+    assert (oracle.colsum_rows(dY, 0, lib=ref) == np.float32(2 ** 24)).all()
+    dYi = inputs.integers(inputs.rng(141), (500, 9), -100, 100)
+    assert np.array_equal(oracle.colsum_rows(dYi, lib=ref), dYi.astype(np.int64).sum(0).astype(np.float32))
+    assert (oracle.colsum_rows(np.zeros((0, 5), np.float32), lib=ref).view(np.uint32) == 0).all()
+
+
+# --------------------------------------------------------------------------
 # GELU backward
 # --------------------------------------------------------------------------
 
