@@ -276,6 +276,15 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_kernel(GemmArgs 
 // rows 16-byte aligned and the k-major operand's row count (N of row-major B,
 // M of transposed A) a multiple of 4; otherwise the register-staged kernel of
 // the same tile shape runs.
+//
+// Pipelining (a wave may be the only one on its SIMD, so whatever it does
+// between two matrix steps idles the matrix unit unless it fits inside the
+// 16 passes of the step before): each group of 4 k issues the LDS reads of
+// the next group right after its own first step; one workgroup barrier per
+// slice, placed inside the slice's last group, publishes the next slice and
+// frees the slot just read for the slice NS ahead; slot and block positions
+// are counters, not divisions.  With the default 64-deep k blocks the loop
+// body is one turn of the ring, unrolled, with no branches (see slice<>).
 // ---------------------------------------------------------------------------
 typedef float v4f __attribute__((ext_vector_type(4)));
 
@@ -315,36 +324,66 @@ struct StagedTile {
     float b[NS][B_FLOATS];
   };
 
-  // Issue this wave's share of the direct loads of slice k0 into ring slot.
-  // k-packed chunk q of an operand with R rows: [q][R][4]; wave load t covers
-  // rows 64t' .. 64t'+63 of chunk t / (R/64).  k-major with R rows: wave load
-  // t covers floats [256t, 256t+256) = k rows 256t/R ...
+  // Sources of this wave's direct loads at k = 0, and how far (in floats)
+  // each moves per unit of k.  k-packed chunk q of an operand with R rows:
+  // [q][R][4]; wave load t covers rows 64t' .. 64t'+63 of chunk t / (R/64).
+  // k-major with R rows: wave load t covers floats [256t, 256t+256) = k rows
+  // 256t/R ...
+  static constexpr int AU = A_LOADS / NW, BU = B_LOADS / NW;  // wave loads per slice
+  struct Src {
+    const float* a[AU];
+    const float* b[BU];
+    int64_t astep, bstep;
+  };
+
   template <bool KPACKED, int R>
-  __device__ static void issue(const float* base, int64_t ld, int64_t r0, int64_t rmax,
-                               int64_t k0, float* slot, int wave, int lane) {
-    constexpr int LOADS = R * BK / 256;
-#pragma unroll
-    for (int u = 0; u < LOADS / NW; ++u) {
-      const int t = wave + u * NW;
-      const float* src;
-      if constexpr (KPACKED) {
-        const int q = t / (R / 64);                 // k group of 4
-        const int row = (t % (R / 64)) * 64 + lane;
-        int64_t gr = r0 + row;
-        gr = gr < rmax ? gr : rmax - 1;
-        src = base + gr * ld + k0 + 4 * q;
-      } else {
-        const int flat = t * 256 + lane * 4;        // = k * R + row
-        const int kk = flat / R, row = flat % R;
-        // rmax is a multiple of 4 here, so a group is either wholly inside
-        // or wholly past the edge (then it re-reads the last group)
-        int64_t gr = r0 + row;
-        gr = gr < rmax ? gr : rmax - 4;
-        src = base + (k0 + kk) * ld + gr;
-      }
-      __builtin_amdgcn_global_load_lds((global_void_ptr)src, (lds_void_ptr)(slot + t * 256), 16,
-                                       0, 0);
+  __device__ static const float* src_at_k0(const float* base, int64_t ld, int64_t r0,
+                                           int64_t rmax, int t, int lane) {
+    if constexpr (KPACKED) {
+      const int q = t / (R / 64);                 // k group of 4
+      const int row = (t % (R / 64)) * 64 + lane;
+      int64_t gr = r0 + row;
+      gr = gr < rmax ? gr : rmax - 1;
+      return base + gr * ld + 4 * q;
+    } else {
+      const int flat = t * 256 + lane * 4;        // = k * R + row
+      const int kk = flat / R, row = flat % R;
+      // rmax is a multiple of 4 here, so a group is either wholly inside
+      // or wholly past the edge (then it re-reads the last group)
+      int64_t gr = r0 + row;
+      gr = gr < rmax ? gr : rmax - 4;
+      return base + kk * ld + gr;
     }
+  }
+
+  __device__ static Src sources(const GemmArgs& g, const float* A, const float* B, int64_t m0,
+                                int64_t n0, int wave, int lane) {
+    Src src;
+#pragma unroll
+    for (int u = 0; u < AU; ++u)
+      src.a[u] = src_at_k0<!TA, BM>(A, g.lda, m0, g.m, wave + u * NW, lane);
+#pragma unroll
+    for (int u = 0; u < BU; ++u)
+      src.b[u] = src_at_k0<TB, BN>(B, g.ldb, n0, g.n, wave + u * NW, lane);
+    src.astep = TA ? g.lda : 1;
+    src.bstep = TB ? 1 : g.ldb;
+    return src;
+  }
+
+  // Issue this wave's share of the direct loads of slice s into ring slot.
+  __device__ static void issue_slice(Smem& sm, const Src& src, int s, int slot, int wave) {
+    const int64_t k0 = static_cast<int64_t>(s) * BK;
+    const int64_t ao = k0 * src.astep, bo = k0 * src.bstep;
+#pragma unroll
+    for (int u = 0; u < AU; ++u)
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(src.a[u] + ao),
+                                       (lds_void_ptr)(sm.a[slot] + (wave + u * NW) * 256), 16, 0,
+                                       0);
+#pragma unroll
+    for (int u = 0; u < BU; ++u)
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(src.b[u] + bo),
+                                       (lds_void_ptr)(sm.b[slot] + (wave + u * NW) * 256), 16, 0,
+                                       0);
   }
 
   struct Pack {
@@ -377,31 +416,82 @@ struct StagedTile {
     }
   }
 
-  template <bool OPEN>
-  __device__ static void mfma_pack(const Pack& pk, v32f (&P)[IM][IN]) {
+  // Matrix steps [LO, HI) of one group of 4 k, in the order (c, i, j); step
+  // c of every tile comes before step c + 1.  OPEN: step c = 0 starts the
+  // block partials from +0.
+  template <bool OPEN, int LO, int HI>
+  __device__ static void mfma_steps(const Pack& pk, v32f (&P)[IM][IN]) {
     const v32f zero = {};
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-      for (int i = 0; i < IM; ++i)
-#pragma unroll
-        for (int j = 0; j < IN; ++j)
-          P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(pk.a[i][c], pk.b[j][c],
-                                                         (OPEN && c == 0) ? zero : P[i][j], 0,
-                                                         0, 0);
+    for (int t = LO; t < HI; ++t) {
+      const int c = t / (IM * IN), i = (t / IN) % IM, j = t % IN;
+      P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(pk.a[i][c], pk.b[j][c],
+                                                     (OPEN && c == 0) ? zero : P[i][j], 0, 0, 0);
+    }
   }
 
-  // One BK-deep slice.  FIRST: the slice opens a k block (its first update
-  // starts the block partial from +0).
-  template <bool FIRST>
-  __device__ static void compute(const float* sa, const float* sb, int lane, int wm0, int wn0,
-                                 v32f (&P)[IM][IN]) {
+  // Waits until this wave's loads of a slice have landed, given how many
+  // later slices of this wave were issued after it (at most MAXL).
+  template <int MAXL>
+  __device__ static void wait_landed(int later) {
+    constexpr int PER = (A_LOADS + B_LOADS) / NW;  // wave loads per slice
+    static_assert(PER * MAXL < 64, "vmcnt range");
+    if constexpr (MAXL == 0) {
+      wait_vmcnt<0>();
+    } else {
+      if (later >= MAXL) wait_vmcnt<MAXL * PER>();
+      else wait_landed<MAXL - 1>(later);
+    }
+  }
+
+  // Slice s from ring slot `slot`; pk[0] already holds its first group of 4 k.
+  // Each group's matrix steps are split after the first one: the LDS reads
+  // of the next group go out there, so the remaining steps (each occupying
+  // the matrix unit for 16 passes) cover their latency.  (While global-to-LDS
+  // loads are in flight the compiler only waits for all LDS reads at once,
+  // so the reads must be issued early rather than waited for selectively.)
+  // In the last group the next slice is published at that point instead:
+  // this wave waits for its share of slice s + 1; the barrier (every wave has
+  // read all of slot `slot`, every share of slice s + 1 has landed) lets the
+  // slot be refilled with slice s + NS; then the next slice's first group is
+  // read.  OPEN: the slice opens a k block.
+  //
+  // FAST: every slice keeps the ring full -- past the last slice it re-loads
+  // the last slice into the freed slot (in bounds; never read as data) -- so
+  // every slice waits for the same load count and takes no branch; plain
+  // ALU work may then be scheduled between the matrix steps.
+  template <bool OPEN, bool FAST>
+  __device__ static void slice(Smem& sm, const Src& src, int s, int nslices, int slot, int nslot,
+                               int lane, int wave, int wm0, int wn0, Pack (&pk)[2],
+                               v32f (&P)[IM][IN]) {
+    constexpr int QN = BK / 4;
+    constexpr int STEPS = 4 * IM * IN;
+    constexpr int PER = (A_LOADS + B_LOADS) / NW;
+    constexpr int CROSS = FAST ? 0x2 : 0;  // sched_barrier mask: plain VALU work may cross
+    static_assert(QN % 2 == 0, "the next slice's first group must land in pk[0]");
 #pragma unroll
-    for (int q = 0; q < BK / 4; ++q) {
-      Pack pk;
-      read_pack(sa, sb, lane, wm0, wn0, q, pk);
-      if (FIRST && q == 0) mfma_pack<true>(pk, P);
-      else mfma_pack<false>(pk, P);
+    for (int q = 0; q < QN; ++q) {
+      if (OPEN && q == 0) mfma_steps<true, 0, 1>(pk[0], P);
+      else mfma_steps<false, 0, 1>(pk[q & 1], P);
+      __builtin_amdgcn_sched_barrier(CROSS);
+      if (q + 1 < QN) {
+        read_pack(sm.a[slot], sm.b[slot], lane, wm0, wn0, q + 1, pk[(q + 1) & 1]);
+      } else if (FAST) {
+        wait_vmcnt<(NS - 2) * PER>();
+        lds_barrier();
+        issue_slice(sm, src, s + NS < nslices ? s + NS : nslices - 1, slot, wave);
+        read_pack(sm.a[nslot], sm.b[nslot], lane, wm0, wn0, 0, pk[0]);
+      } else if (s + 1 < nslices) {
+        const int later = nslices - 2 - s;  // slices after s + 1, capped by the ring
+        wait_landed<NS - 2>(later < NS - 2 ? later : NS - 2);
+        lds_barrier();
+        if (s + NS < nslices) issue_slice(sm, src, s + NS, slot, wave);
+        read_pack(sm.a[nslot], sm.b[nslot], lane, wm0, wn0, 0, pk[0]);
+      }
+      __builtin_amdgcn_sched_barrier(CROSS);
+      if (OPEN && q == 0) mfma_steps<true, 1, STEPS>(pk[0], P);
+      else mfma_steps<false, 1, STEPS>(pk[q & 1], P);
+      __builtin_amdgcn_sched_barrier(CROSS);
     }
   }
 
@@ -409,19 +499,14 @@ struct StagedTile {
                              int64_t n0) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform in the wave
     const int wm0 = (wave / WN) * TWM;
     const int wn0 = (wave % WN) * TWN;
-    const int64_t nslices = g.k / BK;
-    const int64_t spb = g.k_block > 0 ? g.k_block / BK : (nslices > 0 ? nslices : 1);
-    const float* A = g.A + b0 * g.sa0 + b1 * g.sa1;
-    const float* B = g.B + b0 * g.sb0 + b1 * g.sb1;
-
-    auto issue_slice = [&](int64_t s) {
-      const int slot = static_cast<int>(s % NS);
-      issue<!TA, BM>(A, g.lda, m0, g.m, s * BK, sm.a[slot], wave, lane);
-      issue<TB, BN>(B, g.ldb, n0, g.n, s * BK, sm.b[slot], wave, lane);
-    };
+    // the host guarantees K / BK and k_block / BK fit in int
+    const int nslices = static_cast<int>(g.k / BK);
+    const int spb = g.k_block > 0 ? static_cast<int>(g.k_block / BK) : (nslices > 0 ? nslices : 1);
+    const Src src = sources(g, g.A + b0 * g.sa0 + b1 * g.sa1, g.B + b0 * g.sb0 + b1 * g.sb1, m0,
+                            n0, wave, lane);
 
     v32f P[IM][IN], acc[IM][IN];
 #pragma unroll
@@ -431,29 +516,56 @@ struct StagedTile {
         P[i][j] = v32f{};
         acc[i][j] = v32f{};
       }
-    // Prologue: NS - 1 slices in flight.
+    // Prologue: the ring's NS slots filled with slices 0 .. NS - 1; slice 0
+    // published and its first group read.
+    Pack pk[2];
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < nslices) issue_slice(s);
-    for (int64_t s = 0; s < nslices; ++s) {
-      // Slice s has landed once at most (NS - 2) later slices' loads of this
-      // wave are outstanding; the barrier then publishes every wave's part
-      // and guarantees that slot (s - 1) % NS is no longer read.
-      const int64_t later = (nslices - 1 - s) < (NS - 2) ? (nslices - 1 - s) : (NS - 2);
-      constexpr int PER = (A_LOADS + B_LOADS) / NW;
-      if (later >= 2) wait_vmcnt<2 * PER>();
-      else if (later == 1) wait_vmcnt<PER>();
-      else wait_vmcnt<0>();
+    for (int s = 0; s < NS; ++s)
+      if (s < nslices) issue_slice(sm, src, s, s, wave);
+    if (nslices > 0) {
+      wait_landed<NS - 1>(nslices - 1 < NS - 1 ? nslices - 1 : NS - 1);
       lds_barrier();
-      if (s + NS - 1 < nslices) issue_slice(s + NS - 1);
-      const int slot = static_cast<int>(s % NS);
-      if (s % spb == 0) compute<true>(sm.a[slot], sm.b[slot], lane, wm0, wn0, P);
-      else compute<false>(sm.a[slot], sm.b[slot], lane, wm0, wn0, P);
-      if ((s + 1) % spb == 0 || s + 1 == nslices) {
+      read_pack(sm.a[0], sm.b[0], lane, wm0, wn0, 0, pk[0]);
+    }
+    // Fast path: 64-deep k blocks (FSPB slices each) that tile the ring, and a
+    // whole number of ring turns: one loop iteration is one turn, with the
+    // ring slots and the block boundaries known at compile time.
+    constexpr int FSPB = BK <= 64 ? 64 / BK : 0;
+    if (FSPB > 0 && NS % FSPB == 0 && spb == FSPB && nslices % NS == 0) {
+      for (int s0 = 0; s0 < nslices; s0 += NS) {
 #pragma unroll
-        for (int i = 0; i < IM; ++i)
+        for (int t = 0; t < NS; ++t) {
+          if (t % FSPB == 0)
+            slice<true, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
+                              pk, P);
+          else
+            slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
+                               pk, P);
+          if (t % FSPB == FSPB - 1) {
 #pragma unroll
-          for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+            for (int i = 0; i < IM; ++i)
+#pragma unroll
+              for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+          }
+        }
+      }
+      wait_vmcnt<0>();  // the re-loads past the end
+    } else {
+      int slot = 0, pos = 0;  // ring slot of slice s; s's place inside its k block
+      for (int s = 0; s < nslices; ++s) {
+        const int nslot = slot + 1 == NS ? 0 : slot + 1;
+        if (pos == 0)
+          slice<true, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P);
+        else
+          slice<false, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P);
+        if (++pos == spb || s + 1 == nslices) {
+          pos = 0;
+#pragma unroll
+          for (int i = 0; i < IM; ++i)
+#pragma unroll
+            for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+        }
+        slot = nslot;
       }
     }
     __syncthreads();
@@ -506,6 +618,9 @@ struct MfmaEntry {
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>},                                  \
    {nullptr, nullptr, nullptr, nullptr}}
 
+// MINW: waves per SIMD the register allocation must leave room for; FWM x FWN:
+// the wave grid of the register-staged fallback of the same tile (as many
+// waves, each owning whole 64 x 32 instruction tiles).
 #define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN)                                \
   {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW "/s" #NS, BM, BN, BK},                    \
    64 * WM * WN,                                                                              \
@@ -519,12 +634,14 @@ struct MfmaEntry {
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
 
 const MfmaEntry kMfma[] = {
-    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 0: default for large outputs
-    REPOPS_STAGED(128, 128, 64, 2, 2, 2, 1, 2, 2),  // 1
+    REPOPS_STAGED(128, 128, 16, 4, 2, 4, 2, 2, 4),  // 0: default for large outputs
+    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 1: one wave per SIMD
     REPOPS_MFMA(128, 128, 16, 2, 2, 2),             // 2: short k (attention scores)
     REPOPS_STAGED(128, 128, 32, 2, 2, 4, 1, 2, 2),  // 3
     REPOPS_STAGED(256, 128, 16, 4, 2, 3, 1, 4, 2),  // 4
     REPOPS_MFMA(64, 64, 32, 1, 2, 2),               // 5: small outputs
+    REPOPS_STAGED(128, 128, 32, 4, 2, 4, 2, 2, 4),  // 6
+    REPOPS_STAGED(256, 128, 16, 4, 2, 4, 2, 4, 2),  // 7
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
@@ -549,7 +666,9 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
                      aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
   auto kernel = e.kernel[g.ta * 2 + g.tb];
   // the staged kernel takes whole slices only: K a multiple of its depth
-  const bool staged_ok = vec_ok && g.k % e.cfg.bk == 0 && (!g.ta || g.m % 4 == 0) &&
+  // (and slice counts that fit in int)
+  const bool staged_ok = vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
+                         g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) &&
                          (g.tb || g.n % 4 == 0);
   if (e.staged[0] && staged_ok) kernel = e.staged[g.ta * 2 + g.tb];
   hipLaunchKernelGGL(kernel, dim3(grid), dim3(e.threads), 0, s, g, tiles_m, tiles_n, ntiles,
