@@ -430,6 +430,15 @@ struct StagedTile {
     }
   }
 
+  // Matrix step t (in the order of mfma_steps); t and open fold to constants.
+  __device__ static __forceinline__ void mfma_step(const Pack& pk, v32f (&P)[IM][IN], int t,
+                                                   bool open) {
+    const v32f zero = {};
+    const int c = t / (IM * IN), i = (t / IN) % IM, j = t % IN;
+    P[i][j] = __builtin_amdgcn_mfma_f32_32x32x1f32(pk.a[i][c], pk.b[j][c],
+                                                   (open && c == 0) ? zero : P[i][j], 0, 0, 0);
+  }
+
   // Waits until this wave's loads of a slice have landed, given how many
   // later slices of this wave were issued after it (at most MAXL).
   template <int MAXL>
@@ -460,10 +469,15 @@ struct StagedTile {
   // the last slice into the freed slot (in bounds; never read as data) -- so
   // every slice waits for the same load count and takes no branch; plain
   // ALU work may then be scheduled between the matrix steps.
-  template <bool OPEN, bool FAST>
+  //
+  // ADD: acc = acc + done (the previous k block's partials, held in a second
+  // register set) is spread in small shares between this slice's matrix
+  // steps, where it costs no matrix-unit time.
+  template <bool OPEN, bool FAST, bool ADD = false>
   __device__ static void slice(Smem& sm, const Src& src, int s, int nslices, int slot, int nslot,
                                int lane, int wave, int wm0, int wn0, Pack (&pk)[2],
-                               v32f (&P)[IM][IN]) {
+                               v32f (&P)[IM][IN], v32f (&acc)[IM][IN],
+                               const v32f (&done)[IM][IN]) {
     constexpr int QN = BK / 4;
     constexpr int STEPS = 4 * IM * IN;
     constexpr int PER = (A_LOADS + B_LOADS) / NW;
@@ -489,9 +503,42 @@ struct StagedTile {
         read_pack(sm.a[nslot], sm.b[nslot], lane, wm0, wn0, 0, pk[0]);
       }
       __builtin_amdgcn_sched_barrier(CROSS);
-      if (OPEN && q == 0) mfma_steps<true, 1, STEPS>(pk[0], P);
-      else mfma_steps<false, 1, STEPS>(pk[q & 1], P);
+      if constexpr (ADD) {
+        constexpr int NCH = QN * (STEPS - 1), TOT = IM * IN * 32;
+#pragma unroll
+        for (int t = 1; t < STEPS; ++t) {
+          mfma_step(pk[q & 1], P, t, OPEN && q == 0);
+          __builtin_amdgcn_sched_barrier(0);
+          const int ch = q * (STEPS - 1) + t - 1;
+#pragma unroll
+          for (int f = TOT * ch / NCH; f < TOT * (ch + 1) / NCH; ++f) {
+            const int u = f / 32, r = f % 32;
+            acc[u / IN][u % IN][r] = acc[u / IN][u % IN][r] + done[u / IN][u % IN][r];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+        if (OPEN && q == 0) mfma_steps<true, 1, STEPS>(pk[0], P);
+        else mfma_steps<false, 1, STEPS>(pk[q & 1], P);
+      }
       __builtin_amdgcn_sched_barrier(CROSS);
+    }
+  }
+
+  // One turn of the ring (NS slices, one k block) of the fast path,
+  // accumulating the block in X while the previous block's partials in Y join
+  // acc during the first slice.
+  __device__ static void turn(Smem& sm, const Src& src, int s0, int nslices, int lane, int wave,
+                              int wm0, int wn0, Pack (&pk)[2], v32f (&X)[IM][IN],
+                              v32f (&acc)[IM][IN], const v32f (&Y)[IM][IN]) {
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      if (t == 0)
+        slice<true, true, true>(sm, src, s0, nslices, 0, 1 % NS, lane, wave, wm0, wn0, pk, X,
+                                acc, Y);
+      else
+        slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0, pk,
+                           X, acc, Y);
     }
   }
 
@@ -532,20 +579,40 @@ struct StagedTile {
     // ring slots and the block boundaries known at compile time.
     constexpr int FSPB = BK <= 64 ? 64 / BK : 0;
     if (FSPB > 0 && NS % FSPB == 0 && spb == FSPB && nslices % NS == 0) {
-      for (int s0 = 0; s0 < nslices; s0 += NS) {
+      if constexpr (IM * IN == 1 && FSPB == NS) {
+        // One instruction tile per wave leaves room for a second partial set:
+        // one ring turn is one k block, alternating between P and Q, and each
+        // block's partials join acc during the next block's first slice.  Q
+        // starts at +0, so the first block adds +0 to +0.
+        v32f Q[IM][IN];
+        Q[0][0] = v32f{};
+        int s0 = 0;
+        for (; s0 + 2 * NS <= nslices; s0 += 2 * NS) {
+          turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
+          turn(sm, src, s0 + NS, nslices, lane, wave, wm0, wn0, pk, Q, acc, P);
+        }
+        if (s0 < nslices) {
+          turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
+          acc[0][0] = acc[0][0] + P[0][0];
+        } else {
+          acc[0][0] = acc[0][0] + Q[0][0];
+        }
+      } else {
+        for (int s0 = 0; s0 < nslices; s0 += NS) {
 #pragma unroll
-        for (int t = 0; t < NS; ++t) {
-          if (t % FSPB == 0)
-            slice<true, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
-                              pk, P);
-          else
-            slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
-                               pk, P);
-          if (t % FSPB == FSPB - 1) {
+          for (int t = 0; t < NS; ++t) {
+            if (t % FSPB == 0)
+              slice<true, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
+                                pk, P, acc, P);
+            else
+              slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0,
+                                 wn0, pk, P, acc, P);
+            if (t % FSPB == FSPB - 1) {
 #pragma unroll
-            for (int i = 0; i < IM; ++i)
+              for (int i = 0; i < IM; ++i)
 #pragma unroll
-              for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+                for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+            }
           }
         }
       }
@@ -555,9 +622,11 @@ struct StagedTile {
       for (int s = 0; s < nslices; ++s) {
         const int nslot = slot + 1 == NS ? 0 : slot + 1;
         if (pos == 0)
-          slice<true, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P);
+          slice<true, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P, acc,
+                             P);
         else
-          slice<false, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P);
+          slice<false, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P, acc,
+                              P);
         if (++pos == spb || s + 1 == nslices) {
           pos = 0;
 #pragma unroll
