@@ -76,6 +76,35 @@ def event_time_ms(fn, reps, warmup=2):
     return start.elapsed_time(stop) / reps
 
 
+def graph_time_ms(fn, calls=20, reps=10):
+    """Average duration of fn() with `calls` of them captured in one HIP graph
+    and the graph replayed `reps` times: the kernels' own time without host
+    launch gaps (none of the library's calls allocates or clears memory, so
+    they capture as they run)."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(calls):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        graph.replay()
+    stop.record()
+    stop.synchronize()
+    return start.elapsed_time(stop) / (calls * reps)
+
+
 def cpu_baseline(d, flops_per_row_unit, target_s=12.0):
     """The oracle, as it stands, on a bounded row sample of the same GEMM."""
     import numpy as np
@@ -100,6 +129,11 @@ def cpu_baseline(d, flops_per_row_unit, target_s=12.0):
     return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} of 2048 output rows of the 2048^3 GEMM (+bias), "
                       f"{dt:.2f} s wall on {threads} threads"}
+
+
+def _graph_rate(ms, nbytes=None, flops=None):
+    """The same figures for graph-replayed calls, keys prefixed graph_."""
+    return {"graph_" + k: v for k, v in _rate(ms, nbytes, flops).items()}
 
 
 def _rate(ms, nbytes=None, flops=None):
@@ -134,8 +168,12 @@ def secondary(repops, steps):
     C, P = torch.empty_like(A), torch.empty_like(S)
     out["gemm_256"] = _rate(event_time_ms(lambda: repops.matmul(A, B, out=C), steps * 5),
                             flops=2 * 256 ** 3)
+    out["gemm_256"].update(_graph_rate(graph_time_ms(lambda: repops.matmul(A, B, out=C)),
+                                       flops=2 * 256 ** 3))
     out["softmax_256x256"] = _rate(event_time_ms(lambda: repops.softmax_rows(S, out=P), steps * 5),
                                    nbytes=8 * 256 * 256)
+    out["softmax_256x256"].update(_graph_rate(graph_time_ms(lambda: repops.softmax_rows(S, out=P)),
+                                              nbytes=8 * 256 * 256))
 
     # causal softmax, Llama attention scores: 4 x 32 heads x 1024 rows of 1024
     T, rows = 1024, 4 * 32 * 1024
@@ -147,6 +185,11 @@ def secondary(repops, steps):
     out["softmax_dense_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
     ms = event_time_ms(lambda: repops.exp(S, out=P), steps)
     out["exp_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 2)
+    # 4096-wide rows (one row per workgroup, split over waves)
+    S4 = S.view(-1)[:4096 * 4096].view(4096, 4096)
+    P4 = P.view(-1)[:4096 * 4096].view(4096, 4096)
+    ms = event_time_ms(lambda: repops.softmax_rows(S4, out=P4), steps)
+    out["softmax_4096x4096"] = _rate(ms, nbytes=4 * S4.numel() * 2)
     # softmax backward on the same scores: reads Y and dY (unmasked part when
     # causal), writes dX everywhere
     Yp = repops.softmax_rows(S, causal_period=T)
@@ -165,6 +208,10 @@ def secondary(repops, steps):
         Y = torch.empty_like(Z)
         ms = event_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y), steps)
         out[name] = _rate(ms, nbytes=4 * Z.numel() * 2)
+        if shape[0] == 4096:  # launch-bound: also without host launch gaps
+            out[name].update(_graph_rate(
+                graph_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y)),
+                nbytes=4 * Z.numel() * 2))
     # LayerNorm backward: reads X and dY, writes dX (mean, rstd, gamma and the
     # [cols] parameter gradients are negligible); dgamma/dbeta included
     for name, shape in (("layernorm_backward_4096x768", (4096, 768)),
@@ -177,9 +224,11 @@ def secondary(repops, steps):
         dX = torch.empty_like(Z)
         dg, db = torch.empty_like(gam), torch.empty_like(gam)
         ws = torch.empty(max(repops.layernorm_backward_workspace(*shape) // 4, 1), device=dev)
-        ms = event_time_ms(lambda: repops.layernorm_backward_rows(
-            Z, dZ, mean, rstd, gam, dx_out=dX, dgamma_out=dg, dbeta_out=db, workspace=ws), steps)
-        out[name] = _rate(ms, nbytes=4 * Z.numel() * 3)
+        call = lambda: repops.layernorm_backward_rows(  # noqa: E731
+            Z, dZ, mean, rstd, gam, dx_out=dX, dgamma_out=dg, dbeta_out=db, workspace=ws)
+        out[name] = _rate(event_time_ms(call, steps), nbytes=4 * Z.numel() * 3)
+        if shape[0] == 4096:
+            out[name].update(_graph_rate(graph_time_ms(call), nbytes=4 * Z.numel() * 3))
         del Z, dZ, dX, ws
     H = t(inputs.normal(g, (4096, 3072), var=0.31))
     G = torch.empty_like(H)

@@ -10,6 +10,7 @@
 #include "train_internal.h"
 #include "llama_internal.h"
 #include "commit_internal.h"
+#include "rows_internal.h"
 
 using repops::AdamScalars;
 using repops::GemmArgs;
@@ -171,16 +172,30 @@ repops_status_t check_rows(int64_t rows, int64_t cols, const float* X, int64_t l
   return REPOPS_OK;
 }
 
+// ROWS_WAVE: p[0] = rows per block (1, 2, 4, 8); p[1] = waves per row: 0 or 1
+// for one, or 2, 4, 8, 16 for one row per block split over that many waves (needs
+// p[0] = 1 and an operation with a split kernel: `split_max` non-null, giving
+// the widest row it takes for a split).  *split receives the waves per row.
 repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch_t* launch,
                                 int64_t cols, uint32_t* kind, int* wpb,
-                                int64_t wave_max = repops::rows_wave_max_cols()) {
+                                int64_t wave_max = repops::rows_wave_max_cols(),
+                                int* split = nullptr, int64_t (*split_max)(int) = nullptr) {
   const bool wave_order =
       order->row_width == 64 && order->row_combine == REPOPS_ROW_STRIDED_TREE;
   const bool wave_fits = cols <= wave_max;
   *wpb = 4;
+  if (split) *split = 1;
   if (!launch || launch->kind == REPOPS_LAUNCH_AUTO) {
     if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
     *kind = (wave_order && wave_fits) ? REPOPS_LAUNCH_ROWS_WAVE : REPOPS_LAUNCH_ROWS_GENERIC;
+    if (wave_order && split && split_max) {
+      const int S = repops::auto_row_split(cols);
+      if (S > 1 && cols <= split_max(S)) {
+        *kind = REPOPS_LAUNCH_ROWS_WAVE;
+        *wpb = 1;
+        *split = S;
+      }
+    }
     return REPOPS_OK;
   }
   if (launch->kind == REPOPS_LAUNCH_ROWS_GENERIC) {
@@ -189,10 +204,18 @@ repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch
     return REPOPS_OK;
   }
   if (launch->kind == REPOPS_LAUNCH_ROWS_WAVE) {
-    const uint32_t w = launch->p[0];
-    if (!(w == 1 || w == 2 || w == 4 || w == 8) || !launch_params_zero_from(launch, 1))
+    const uint32_t w = launch->p[0], S = launch->p[1];
+    if (!(w == 1 || w == 2 || w == 4 || w == 8) || !launch_params_zero_from(launch, 2))
       return REPOPS_ERR_LAUNCH;
-    if (!wave_order || !wave_fits) return REPOPS_ERR_LAUNCH;
+    if (!wave_order) return REPOPS_ERR_LAUNCH;
+    if (S <= 1) {
+      if (!wave_fits) return REPOPS_ERR_LAUNCH;
+    } else {
+      if (!(S == 2 || S == 4 || S == 8 || S == 16) || w != 1 || !split || !split_max ||
+          cols > split_max(static_cast<int>(S)))
+        return REPOPS_ERR_LAUNCH;
+      *split = static_cast<int>(S);
+    }
     *kind = REPOPS_LAUNCH_ROWS_WAVE;
     *wpb = static_cast<int>(w);
     return REPOPS_OK;
@@ -377,8 +400,9 @@ repops_status_t repops_softmax_rows(const repops_order_t* order, int64_t rows, i
   repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
   if (st != REPOPS_OK) return st;
   uint32_t kind;
-  int wpb;
-  st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  int wpb, split;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rows_wave_max_cols(), &split,
+                       repops::rows_split_max_cols);
   if (st != REPOPS_OK || empty) return st;
   RowArgs a{};
   a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
@@ -386,6 +410,8 @@ repops_status_t repops_softmax_rows(const repops_order_t* order, int64_t rows, i
   a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
   a.period = causal_period;
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1)
+    return hip_status(repops::launch_softmax_split(a, split, s));
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_softmax_wave(a, wpb, s));
   return hip_status(repops::launch_softmax_generic(a, s));
 }
@@ -402,8 +428,9 @@ repops_status_t repops_layernorm_rows(const repops_order_t* order, int64_t rows,
   repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
   if (st != REPOPS_OK) return st;
   uint32_t kind;
-  int wpb;
-  st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  int wpb, split;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rows_wave_max_cols(), &split,
+                       repops::rows_split_max_cols);
   if (st != REPOPS_OK || empty) return st;
   const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
   if (gamma && overlaps(ye, extent_of(gamma, 1, 0, 1, 0, 1, cols, cols))) return REPOPS_ERR_ALIAS;
@@ -415,6 +442,8 @@ repops_status_t repops_layernorm_rows(const repops_order_t* order, int64_t rows,
   a.gamma = gamma; a.beta = beta; a.eps = eps;
   a.mean_out = mean_out; a.rstd_out = rstd_out;
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1)
+    return hip_status(repops::launch_layernorm_split(a, split, s));
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_wave(a, wpb, s));
   return hip_status(repops::launch_layernorm_generic(a, s));
 }
@@ -747,8 +776,9 @@ repops_status_t repops_rmsnorm_rows(const repops_order_t* order, int64_t rows, i
   repops_status_t st = check_rows(rows, cols, X, ldx, Y, ldy, &empty);
   if (st != REPOPS_OK) return st;
   uint32_t kind;
-  int wpb;
-  st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rmsnorm_wave_max_cols());
+  int wpb, split;
+  st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rmsnorm_wave_max_cols(), &split,
+                       repops::rmsnorm_split_max_cols);
   if (st != REPOPS_OK || empty) return st;
   const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
   if (gamma && overlaps(ye, vec_extent(gamma, cols))) return REPOPS_ERR_ALIAS;
@@ -764,6 +794,8 @@ repops_status_t repops_rmsnorm_rows(const repops_order_t* order, int64_t rows, i
   a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
   a.gamma = gamma; a.eps = eps; a.rstd_out = rstd_out;
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1)
+    return hip_status(repops::launch_rmsnorm_split(a, split, s));
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_rmsnorm_wave(a, wpb, s));
   return hip_status(repops::launch_rmsnorm_generic(a, s));
 }

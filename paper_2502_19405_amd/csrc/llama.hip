@@ -16,6 +16,7 @@
 #include "llama_internal.h"
 #include "rep_math.h"
 #include "row_reduce.h"
+#include "rows_internal.h"
 
 #pragma clang fp contract(off)
 
@@ -87,12 +88,22 @@ __global__ __launch_bounds__(512) void rmsnorm_wave_kernel(RmsArgs a, int wpb) {
     v[t] = (j < a.cols) ? x[j] : 0.0f;
     q = __builtin_fmaf(v[t], v[t], q);  // terms past the row: fma(0, 0, q) = q
   }
+  constexpr bool kPre = T <= 16;  // gamma joins the row's loads when a lane holds few values
+  float gv[kPre ? T : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      gv[t] = (a.gamma && j < a.cols) ? a.gamma[j] : 0.0f;
+    }
+  }
   const float n = static_cast<float>(a.cols);
   const float ms = wave_tree_sum(q) / n;
   const float rstd = 1.0f / __builtin_sqrtf(ms + a.eps);
   auto out = [&](int t, int64_t j) {
     const float tv = v[t] * rstd;
-    return a.gamma ? tv * a.gamma[j] : tv;
+    if constexpr (kPre) return a.gamma ? tv * gv[t] : tv;
+    else return a.gamma ? tv * a.gamma[j] : tv;
   };
   if (a.cols == kWave * T) {
 #pragma unroll
@@ -105,6 +116,58 @@ __global__ __launch_bounds__(512) void rmsnorm_wave_kernel(RmsArgs a, int wpb) {
     }
   }
   if (lane == 0 && a.rstd_out) a.rstd_out[row] = rstd;
+}
+
+// Wide rows: one row per workgroup of S waves.  Wave w holds the values
+// j = lane + 64 * (w * T + t), t < T; the lane's chain passes from wave to
+// wave in order through LDS (wave w continues where wave w - 1 stopped), so
+// every lane sees its values in exactly the order of the one-wave kernel.
+// After the last wave's turn every wave reduces the finished chains itself.
+template <int T>
+__global__ __launch_bounds__(1024) void rmsnorm_split_kernel(RmsArgs a) {
+  __shared__ float chain[kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x >> 6;
+  const int S = static_cast<int>(blockDim.x >> 6);
+  const float n = static_cast<float>(a.cols);
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* x = a.X + row * a.ldx;
+    float* y = a.Y + row * a.ldy;
+    const int64_t j0 = lane + int64_t(kWave) * T * w;  // this wave's first column
+    float v[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      v[t] = (j < a.cols) ? x[j] : 0.0f;
+    }
+    constexpr bool kPre = T <= 16;  // gamma joins the row's loads
+    float gv[kPre ? T : 1];
+    if constexpr (kPre) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int64_t j = j0 + kWave * t;
+        gv[t] = (a.gamma && j < a.cols) ? a.gamma[j] : 0.0f;
+      }
+    }
+    const float q = chain_across_waves(chain, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = __builtin_fmaf(v[t], v[t], c);  // past the row: c
+      return c;
+    });
+    const float ms = wave_tree_sum(q) / n;
+    const float rstd = 1.0f / __builtin_sqrtf(ms + a.eps);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      if (j < a.cols) {
+        const float tv = v[t] * rstd;
+        if constexpr (kPre) y[j] = a.gamma ? tv * gv[t] : tv;
+        else y[j] = a.gamma ? tv * a.gamma[j] : tv;
+      }
+    }
+    if (w == 0 && lane == 0 && a.rstd_out) a.rstd_out[row] = rstd;
+    __syncthreads();  // every wave has read the chains before the next row
+  }
 }
 
 __global__ __launch_bounds__(64) void rmsnorm_generic_kernel(RmsArgs a) {
@@ -233,6 +296,7 @@ int64_t ew_grid(int64_t items, int threads, int max_blocks) {
 
 // RMSNorm rows stay in registers up to 64 values per lane (Llama's 4096).
 int64_t rmsnorm_wave_max_cols() { return int64_t(kWave) * kMaxPerLane; }
+int64_t rmsnorm_split_max_cols(int S) { return split_max_cols(S); }
 
 hipError_t launch_sincos(int64_t n, const float* x, float* s, float* c, int threads,
                          int max_blocks, hipStream_t st) {
@@ -252,6 +316,22 @@ hipError_t launch_rmsnorm_wave(const RmsArgs& a, int wpb, hipStream_t s) {
   const int64_t blocks = (a.rows + wpb - 1) / wpb;
   hipLaunchKernelGGL(pick_rmsnorm(a.cols), dim3(static_cast<unsigned>(blocks)), dim3(kWave * wpb),
                      0, s, a, wpb);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_split(const RmsArgs& a, int S, hipStream_t s) {
+  const int64_t per_wave = (a.cols + int64_t(kWave) * S - 1) / (int64_t(kWave) * S);
+  void (*k)(RmsArgs) = nullptr;
+  if (per_wave <= 1) k = rmsnorm_split_kernel<1>;
+  else if (per_wave <= 2) k = rmsnorm_split_kernel<2>;
+  else if (per_wave <= 4) k = rmsnorm_split_kernel<4>;
+  else if (per_wave <= 8) k = rmsnorm_split_kernel<8>;
+  else if (per_wave <= 16) k = rmsnorm_split_kernel<16>;
+  else if (per_wave <= 32) k = rmsnorm_split_kernel<32>;
+  else return hipErrorInvalidValue;
+  const int64_t cap = int64_t(1) << 30;
+  hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(a.rows < cap ? a.rows : cap)),
+                     dim3(kWave * S), 0, s, a);
   return hipGetLastError();
 }
 

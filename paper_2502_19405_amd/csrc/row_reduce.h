@@ -40,6 +40,22 @@ __device__ __forceinline__ float wave_max(float m) {
   return m;
 }
 
+// Per-lane chains continued across the S waves of a workgroup, in wave order:
+// wave k starts from what wave k - 1 left in chain[lane] (+0 for wave 0),
+// folds its own terms in with `step`, and leaves the result there.  Every
+// wave returns the finished chains.  All waves of the workgroup must call it
+// (it holds S barriers); a following use of the same array needs a barrier
+// first, since waves read the finished chains after the last one.
+template <class Step>
+__device__ __forceinline__ float chain_across_waves(float* chain, int lane, int w, int S,
+                                                    Step step) {
+  for (int k = 0; k < S; ++k) {
+    if (w == k) chain[lane] = step(k > 0 ? chain[lane] : 0.0f);
+    __syncthreads();
+  }
+  return chain[lane];
+}
+
 // Workgroup barrier that waits for this wave's LDS operations only: global
 // loads issued before it stay in flight (__syncthreads would also wait for
 // them).  The memory clobber keeps LDS accesses on their side of the barrier.

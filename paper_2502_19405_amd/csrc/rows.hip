@@ -18,6 +18,7 @@
 #include "rep_math.h"
 #include "repops_internal.h"
 #include "row_reduce.h"
+#include "rows_internal.h"
 
 #pragma clang fp contract(off)
 
@@ -88,6 +89,17 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
     v[t] = (j < a.cols) ? x[j] : 0.0f;
     q = q + v[t];
   }
+  // gamma and beta join the row's loads when a lane holds few values
+  constexpr bool kPre = T <= 16;
+  float gv[kPre ? T : 1], bv[kPre ? T : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * t;
+      gv[t] = (a.gamma && j < a.cols) ? a.gamma[j] : 0.0f;
+      bv[t] = (a.beta && j < a.cols) ? a.beta[j] : 0.0f;
+    }
+  }
   const float n = static_cast<float>(a.cols);
   const float mean = wave_tree_sum(q) / n;
   float q2 = 0.0f;
@@ -101,10 +113,18 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
   const float rstd = 1.0f / __builtin_sqrtf(var + a.eps);
   auto out = [&](int t, int64_t j) {
     const float tv = v[t] * rstd;
+    float gj, bj;
+    if constexpr (kPre) {
+      gj = gv[t];
+      bj = bv[t];
+    } else {
+      gj = a.gamma ? a.gamma[j] : 0.0f;
+      bj = a.beta ? a.beta[j] : 0.0f;
+    }
     float o;
-    if (a.gamma && a.beta) o = __builtin_fmaf(tv, a.gamma[j], a.beta[j]);
-    else if (a.gamma) o = tv * a.gamma[j];
-    else if (a.beta) o = tv + a.beta[j];
+    if (a.gamma && a.beta) o = __builtin_fmaf(tv, gj, bj);
+    else if (a.gamma) o = tv * gj;
+    else if (a.beta) o = tv + bj;
     else o = tv;
     y[j] = o;
   };
@@ -121,6 +141,144 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
   if (lane == 0) {
     if (a.mean_out) a.mean_out[row] = mean;
     if (a.rstd_out) a.rstd_out[row] = rstd;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Wide rows: one row per workgroup of S waves.  Wave w holds the columns
+// j = lane + 64 * (w * T + t), t < T; the lane chains run through the waves in
+// order (chain_across_waves), so every lane sees its terms in exactly the
+// order of the one-wave kernels above and the results are the same bits.
+// ---------------------------------------------------------------------------
+
+template <int T>
+__global__ __launch_bounds__(1024) void softmax_split_kernel(RowArgs a) {
+  __shared__ float chain[kWave];
+  __shared__ float wave_maxima[16];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x >> 6;
+  const int S = static_cast<int>(blockDim.x >> 6);
+  const float ninf = -__builtin_huge_valf();
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* x = a.X + row * a.ldx;
+    float* y = a.Y + row * a.ldy;
+    int64_t valid = a.cols;
+    if (a.period > 0) {
+      const int64_t v = row % a.period + 1;
+      valid = v < valid ? v : valid;
+    }
+    const int64_t live = (valid + kWave - 1) / kWave;  // segments holding unmasked entries
+    const int64_t s0 = int64_t(T) * w;                 // this wave's first segment
+    float v[T];
+    float m = ninf;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * (s0 + t);
+      v[t] = ninf;
+      if (s0 + t < live) v[t] = (j < valid) ? x[j] : ninf;  // masked entries are never read
+      m = v[t] > m ? v[t] : m;
+    }
+    // The maximum is a value of the row whatever the order of comparison (see
+    // wave_max), so the waves' maxima may be combined in any order.
+    m = wave_max(m);
+    if (lane == 0) wave_maxima[w] = m;
+    __syncthreads();
+    m = wave_maxima[0];
+    for (int k = 1; k < S; ++k) m = wave_maxima[k] > m ? wave_maxima[k] : m;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * (s0 + t);
+      float e = 0.0f;
+      if (s0 + t < live) e = (j < valid) ? rep_exp(v[t] - m) : 0.0f;
+      v[t] = e;
+    }
+    const float q = chain_across_waves(chain, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = c + v[t];  // masked terms are +0
+      return c;
+    });
+    const float r = 1.0f / wave_tree_sum(q);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * (s0 + t);
+      if (j < a.cols) y[j] = v[t] * r;
+    }
+    __syncthreads();  // chains and maxima read before the next row
+  }
+}
+
+template <int T>
+__global__ __launch_bounds__(1024) void layernorm_split_kernel(RowArgs a) {
+  __shared__ float chain_sum[kWave];
+  __shared__ float chain_sq[kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x >> 6;
+  const int S = static_cast<int>(blockDim.x >> 6);
+  const float n = static_cast<float>(a.cols);
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* x = a.X + row * a.ldx;
+    float* y = a.Y + row * a.ldy;
+    const int64_t j0 = lane + int64_t(kWave) * T * w;
+    float v[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      v[t] = (j < a.cols) ? x[j] : 0.0f;
+    }
+    constexpr bool kPre = T <= 16;  // gamma and beta join the row's loads
+    float gv[kPre ? T : 1], bv[kPre ? T : 1];
+    if constexpr (kPre) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int64_t j = j0 + kWave * t;
+        gv[t] = (a.gamma && j < a.cols) ? a.gamma[j] : 0.0f;
+        bv[t] = (a.beta && j < a.cols) ? a.beta[j] : 0.0f;
+      }
+    }
+    const float q = chain_across_waves(chain_sum, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = c + v[t];
+      return c;
+    });
+    const float mean = wave_tree_sum(q) / n;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      v[t] = (j < a.cols) ? v[t] - mean : 0.0f;
+    }
+    const float q2 = chain_across_waves(chain_sq, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = __builtin_fmaf(v[t], v[t], c);
+      return c;
+    });
+    const float var = wave_tree_sum(q2) / n;
+    const float rstd = 1.0f / __builtin_sqrtf(var + a.eps);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      if (j < a.cols) {
+        const float tv = v[t] * rstd;
+        float gj, bj;
+        if constexpr (kPre) {
+          gj = gv[t];
+          bj = bv[t];
+        } else {
+          gj = a.gamma ? a.gamma[j] : 0.0f;
+          bj = a.beta ? a.beta[j] : 0.0f;
+        }
+        float o;
+        if (a.gamma && a.beta) o = __builtin_fmaf(tv, gj, bj);
+        else if (a.gamma) o = tv * gj;
+        else if (a.beta) o = tv + bj;
+        else o = tv;
+        y[j] = o;
+      }
+    }
+    if (w == 0 && lane == 0) {
+      if (a.mean_out) a.mean_out[row] = mean;
+      if (a.rstd_out) a.rstd_out[row] = rstd;
+    }
+    __syncthreads();  // chains read before the next row
   }
 }
 
@@ -218,6 +376,40 @@ unsigned generic_grid(int64_t rows) {
 }  // namespace
 
 int64_t rows_wave_max_cols() { return int64_t(kWave) * kMaxPerLane; }
+int64_t rows_split_max_cols(int S) { return split_max_cols(S); }
+
+namespace {
+using SplitKernel = void (*)(RowArgs);
+template <template <int> class K>
+SplitKernel pick_split(int64_t cols, int S) {
+  const int64_t per_lane = (cols + int64_t(kWave) * S - 1) / (int64_t(kWave) * S);
+  if (per_lane <= 1) return K<1>::fn;
+  if (per_lane <= 2) return K<2>::fn;
+  if (per_lane <= 4) return K<4>::fn;
+  if (per_lane <= 8) return K<8>::fn;
+  if (per_lane <= 16) return K<16>::fn;
+  if (per_lane <= 32) return K<32>::fn;
+  return nullptr;
+}
+template <int T> struct SoftmaxSplit { static constexpr SplitKernel fn = softmax_split_kernel<T>; };
+template <int T> struct LayernormSplit { static constexpr SplitKernel fn = layernorm_split_kernel<T>; };
+
+hipError_t launch_split(SplitKernel k, const RowArgs& a, int S, hipStream_t s) {
+  if (!k) return hipErrorInvalidValue;
+  const int64_t cap = int64_t(1) << 30;
+  hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(a.rows < cap ? a.rows : cap)),
+                     dim3(kWave * S), 0, s, a);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_softmax_split(const RowArgs& a, int S, hipStream_t s) {
+  return launch_split(pick_split<SoftmaxSplit>(a.cols, S), a, S, s);
+}
+
+hipError_t launch_layernorm_split(const RowArgs& a, int S, hipStream_t s) {
+  return launch_split(pick_split<LayernormSplit>(a.cols, S), a, S, s);
+}
 
 hipError_t launch_softmax_wave(const RowArgs& a, int wpb, hipStream_t s) {
   const int64_t blocks = (a.rows + wpb - 1) / wpb;

@@ -24,10 +24,14 @@ def rp():
     return repops
 
 
-def row_launches(rp, cols, wave_max=2048, W=64, combine=0):
+def row_launches(rp, cols, wave_max=2048, W=64, combine=0, split=False):
     out = [("generic", rp.Launch(rp.LAUNCH_ROWS_GENERIC)), ("auto", None)]
     if W == 64 and combine == 0 and cols <= wave_max:
         out += [(f"wave{w}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (w,))) for w in (1, 2, 4, 8)]
+    if W == 64 and combine == 0 and split:
+        # one row per workgroup, split over S waves (at most 32 values per lane)
+        out += [(f"split{S}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, S)))
+                for S in (2, 4, 8, 16) if cols <= S * 64 * 32]
     return out
 
 
@@ -133,7 +137,7 @@ def test_rope_llama_shape(rp):
 # RMSNorm
 # --------------------------------------------------------------------------
 
-COLS = [1, 2, 63, 64, 65, 100, 768, 1000, 2048, 2049, 4096, 5000]
+COLS = [1, 2, 63, 64, 65, 100, 768, 1000, 2048, 2049, 4096, 5000, 8192, 16384]
 
 
 @pytest.mark.parametrize("cols", COLS)
@@ -143,7 +147,7 @@ def test_rmsnorm_forward_all_launches(rp, cols):
     gam = 1 + inputs.normal(g, (cols,), var=0.01)
     for gamma in (gam, None):
         want, wr = oracle.rmsnorm_rows(X, gamma, eps=1e-6, with_stats=True)
-        for name, launch in row_launches(rp, cols, wave_max=4096):
+        for name, launch in row_launches(rp, cols, wave_max=4096, split=True):
             announce("rmsnorm", cols, gamma is None, name)
             import torch
             r = torch.empty(75, device="cuda:0")

@@ -25,10 +25,14 @@ def row_launches(rp, W=64, combine=0, cols=0):
     out = [("generic", rp.Launch(rp.LAUNCH_ROWS_GENERIC)), ("auto", None)]
     if W == 64 and combine == 0 and cols <= 4096:
         out += [(f"wave{w}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (w,))) for w in (1, 2, 4, 8)]
+    if W == 64 and combine == 0:
+        # one row per workgroup, split over S waves (at most 32 values per lane)
+        out += [(f"split{S}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, S)))
+                for S in (2, 4, 8, 16) if cols <= S * 64 * 32]
     return out
 
 
-COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000, 4096, 5000]
+COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000, 4096, 5000, 8192, 20000]
 
 
 @pytest.mark.parametrize("cols", COLS)
@@ -101,7 +105,7 @@ def test_softmax_closed_forms(rp):
     assert got[0, 0] == 1 and (got[0, 1:] == 0).all()
 
 
-@pytest.mark.parametrize("cols", [1, 2, 5, 64, 100, 768, 1024, 2048, 3000])
+@pytest.mark.parametrize("cols", [1, 2, 5, 64, 100, 768, 1024, 2048, 3000, 4096, 8192, 9000])
 @pytest.mark.parametrize("affine", ["both", "gamma", "beta", "none"])
 def test_layernorm_ragged_all_launches(rp, cols, affine):
     g = inputs.rng(cols + len(affine))
