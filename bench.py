@@ -199,6 +199,11 @@ def secondary(repops, steps):
         ms, nbytes=4 * (rows // T) * (2 * T * (T + 1) // 2 + T * T))
     ms = event_time_ms(lambda: repops.softmax_backward_rows(Yp, dP, out=P), steps)
     out["softmax_backward_dense_131072x1024"] = _rate(ms, nbytes=4 * rows * T * 3)
+    Y4 = Yp.view(-1)[:4096 * 4096].view(4096, 4096)
+    dP4 = dP.view(-1)[:4096 * 4096].view(4096, 4096)
+    P4 = P.view(-1)[:4096 * 4096].view(4096, 4096)
+    ms = event_time_ms(lambda: repops.softmax_backward_rows(Y4, dP4, out=P4), steps)
+    out["softmax_backward_4096x4096"] = _rate(ms, nbytes=4 * Y4.numel() * 3)
     del S, P, Yp, dP
 
     d = inputs.distilbert_mlp()

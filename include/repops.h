@@ -103,11 +103,11 @@ enum { REPOPS_ROW_STRIDED_TREE = 0, REPOPS_ROW_BLOCKED_LTR = 1 };
  *     ROWS_WAVE    (2): STRIDED_TREE with W = 64; rows held in registers.
  *         p[0] = rows per block, one of 1, 2, 4, 8; p[1] = waves per row:
  *         0 or 1 for one 64-lane wave per row (rows up to 4096 columns), or
- *         2, 4, 8, 16 for one row per block split over that many waves (then
+ *         2, 4, 8 for one row per block split over that many waves (then
  *         p[0] = 1, and a row takes at most 2048 * p[1] columns).  Each lane
  *         still folds its terms in column order, so the bits do not depend on
  *         p[].  AUTO takes one wave per row up to 1024 columns and splits
- *         wider rows (at most 8 values per lane, at most 16 waves).
+ *         wider rows (at most 16 values per lane where 8 waves allow it).
  *   gelu / exp:
  *     ELEMENTWISE (1): p[0] = threads per block (multiple of 64, <= 1024),
  *         p[1] = maximum number of blocks (0 = as many as needed).

@@ -173,13 +173,14 @@ repops_status_t check_rows(int64_t rows, int64_t cols, const float* X, int64_t l
 }
 
 // ROWS_WAVE: p[0] = rows per block (1, 2, 4, 8); p[1] = waves per row: 0 or 1
-// for one, or 2, 4, 8, 16 for one row per block split over that many waves (needs
+// for one, or 2, 4, 8 for one row per block split over that many waves (needs
 // p[0] = 1 and an operation with a split kernel: `split_max` non-null, giving
 // the widest row it takes for a split).  *split receives the waves per row.
 repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch_t* launch,
                                 int64_t cols, uint32_t* kind, int* wpb,
                                 int64_t wave_max = repops::rows_wave_max_cols(),
-                                int* split = nullptr, int64_t (*split_max)(int) = nullptr) {
+                                int* split = nullptr, int64_t (*split_max)(int) = nullptr,
+                                int auto_per_lane = 16) {
   const bool wave_order =
       order->row_width == 64 && order->row_combine == REPOPS_ROW_STRIDED_TREE;
   const bool wave_fits = cols <= wave_max;
@@ -189,7 +190,7 @@ repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch
     if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
     *kind = (wave_order && wave_fits) ? REPOPS_LAUNCH_ROWS_WAVE : REPOPS_LAUNCH_ROWS_GENERIC;
     if (wave_order && split && split_max) {
-      const int S = repops::auto_row_split(cols);
+      const int S = repops::auto_row_split(cols, auto_per_lane);
       if (S > 1 && cols <= split_max(S)) {
         *kind = REPOPS_LAUNCH_ROWS_WAVE;
         *wpb = 1;
@@ -211,7 +212,7 @@ repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch
     if (S <= 1) {
       if (!wave_fits) return REPOPS_ERR_LAUNCH;
     } else {
-      if (!(S == 2 || S == 4 || S == 8 || S == 16) || w != 1 || !split || !split_max ||
+      if (!(S == 2 || S == 4 || S == 8) || w != 1 || !split || !split_max ||
           cols > split_max(static_cast<int>(S)))
         return REPOPS_ERR_LAUNCH;
       *split = static_cast<int>(S);
@@ -485,7 +486,10 @@ repops_status_t repops_softmax_backward_rows(const repops_order_t* order, int64_
   const bool empty = rows == 0 || cols == 0;
   uint32_t kind;
   int wpb;
-  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  int split;
+  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb,
+                                       repops::rows_wave_max_cols(), &split,
+                                       repops::rows_split_max_cols, 8);
   if (st != REPOPS_OK || empty) return st;
   if ((st = check_matrix(Y, rows, cols, ldy)) != REPOPS_OK) return st;
   if ((st = check_matrix(dY, rows, cols, lddy)) != REPOPS_OK) return st;
@@ -502,6 +506,8 @@ repops_status_t repops_softmax_backward_rows(const repops_order_t* order, int64_
   a.blocked = order->row_combine == REPOPS_ROW_BLOCKED_LTR;
   a.period = causal_period;
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1)
+    return hip_status(repops::launch_softmax_bwd_split(a, split, s));
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_softmax_bwd_wave(a, wpb, s));
   return hip_status(repops::launch_softmax_bwd_generic(a, s));
 }
@@ -526,8 +532,10 @@ static repops_status_t norm_backward(
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > (int64_t(1) << 24)) return REPOPS_ERR_SHAPE;
   if (rows > 0 && cols == 0) return REPOPS_ERR_SHAPE;
   uint32_t kind;
-  int wpb;
-  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb);
+  int wpb, split;
+  repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb,
+                                       repops::rows_wave_max_cols(), &split,
+                                       repops::rows_split_max_cols);
   if (st != REPOPS_OK) return st;
   const bool want_params = dgamma || dbeta;
   if (cols == 0 || (rows == 0 && !want_params) || (!dX && !want_params)) return REPOPS_OK;
@@ -593,7 +601,10 @@ static repops_status_t norm_backward(
   // Both gradients on the wave path with row blocks: one fused pass over X
   // and dY (R rows staged per pass: the launch's waves per block, else a
   // choice by size).
-  if (want_params && dX && rows > 0 && kind == REPOPS_LAUNCH_ROWS_WAVE && order->k_block >= 1) {
+  // (A launch that asks for split rows takes the split kernel for dX.)
+  const bool explicit_split = launch && launch->kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1;
+  if (want_params && dX && rows > 0 && kind == REPOPS_LAUNCH_ROWS_WAVE && order->k_block >= 1 &&
+      !explicit_split) {
     const bool explicit_wave = launch && launch->kind == REPOPS_LAUNCH_ROWS_WAVE;
     const int R = repops::layernorm_fused_rows(rows, cols, order->k_block, explicit_wave ? wpb : 0);
     if (R >= 1) return hip_status(repops::launch_layernorm_bwd_fused(a, p, R, s));
@@ -604,6 +615,8 @@ static repops_status_t norm_backward(
     if ((st = hip_status(repops::launch_layernorm_param(p, s))) != REPOPS_OK) return st;
   }
   if (!dX || rows == 0) return REPOPS_OK;
+  if (kind == REPOPS_LAUNCH_ROWS_WAVE && split > 1)
+    return hip_status(repops::launch_layernorm_bwd_split(a, split, s));
   if (kind == REPOPS_LAUNCH_ROWS_WAVE) return hip_status(repops::launch_layernorm_bwd_wave(a, wpb, s));
   return hip_status(repops::launch_layernorm_bwd_generic(a, s));
 }

@@ -124,7 +124,7 @@ __global__ __launch_bounds__(512) void rmsnorm_wave_kernel(RmsArgs a, int wpb) {
 // every lane sees its values in exactly the order of the one-wave kernel.
 // After the last wave's turn every wave reduces the finished chains itself.
 template <int T>
-__global__ __launch_bounds__(1024) void rmsnorm_split_kernel(RmsArgs a) {
+__global__ __launch_bounds__(512) void rmsnorm_split_kernel(RmsArgs a) {
   __shared__ float chain[kWave];
   const int lane = threadIdx.x & (kWave - 1);
   const int w = threadIdx.x >> 6;

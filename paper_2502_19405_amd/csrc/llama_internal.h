@@ -38,7 +38,7 @@ hipError_t launch_rope(const RopeArgs& a, int waves_per_block, hipStream_t s);
 int64_t rmsnorm_wave_max_cols();
 hipError_t launch_rmsnorm_wave(const RmsArgs& a, int waves_per_block, hipStream_t s);
 hipError_t launch_rmsnorm_generic(const RmsArgs& a, hipStream_t s);
-// One row per workgroup of S waves (S = 2, 4, 8, 16); cols <= S * 64 * 32.
+// One row per workgroup of S waves (S = 2, 4, 8); cols <= S * 64 * 32.
 hipError_t launch_rmsnorm_split(const RmsArgs& a, int S, hipStream_t s);
 int64_t rmsnorm_split_max_cols(int S);
 hipError_t launch_silu(int64_t n, const float* x, float* y, int threads, int max_blocks,

@@ -152,9 +152,9 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
 // ---------------------------------------------------------------------------
 
 template <int T>
-__global__ __launch_bounds__(1024) void softmax_split_kernel(RowArgs a) {
+__global__ __launch_bounds__(512) void softmax_split_kernel(RowArgs a) {
   __shared__ float chain[kWave];
-  __shared__ float wave_maxima[16];
+  __shared__ float wave_maxima[8];
   const int lane = threadIdx.x & (kWave - 1);
   const int w = threadIdx.x >> 6;
   const int S = static_cast<int>(blockDim.x >> 6);
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(1024) void softmax_split_kernel(RowArgs a) {
 }
 
 template <int T>
-__global__ __launch_bounds__(1024) void layernorm_split_kernel(RowArgs a) {
+__global__ __launch_bounds__(512) void layernorm_split_kernel(RowArgs a) {
   __shared__ float chain_sum[kWave];
   __shared__ float chain_sq[kWave];
   const int lane = threadIdx.x & (kWave - 1);

@@ -1,5 +1,5 @@
 // Split-row launchers of the forward row operations (rows.hip): one row per
-// workgroup of S waves (S = 2, 4, 8, 16), at most 32 values per lane.
+// workgroup of S waves (S = 2, 4, 8), at most 32 values per lane.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -10,13 +10,14 @@ namespace repops {
 
 // Waves per row that a wide row is split over when the launch leaves the
 // choice open: rows up to 1024 columns stay on one wave; wider rows get the
-// fewest waves (2, 4, 8) that leave at most 16 values per lane, or 8.
+// fewest waves (2, 4, 8) that leave at most `per_lane` values per lane (16,
+// or 8 for the softmax backward, which measured best there), or 8.
 // (Measured on 4096- and 8192-wide rows: 16 values per lane is within a few
-// percent of 8, 32 values per lane or 16 waves per row are far slower.)
-inline int auto_row_split(int64_t cols) {
+// percent of 8, 16 waves per row is far slower.)
+inline int auto_row_split(int64_t cols, int per_lane = 16) {
   if (cols <= 1024) return 1;
   int S = 2;
-  while (S < 8 && cols > int64_t(64) * 16 * S) S *= 2;
+  while (S < 8 && cols > int64_t(64) * per_lane * S) S *= 2;
   return S;
 }
 

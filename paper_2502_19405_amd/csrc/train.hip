@@ -162,6 +162,110 @@ __global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, i
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide rows: one row per workgroup of S waves (wave w holds the columns
+// lane + 64 * (w * T + t)); each lane's chains pass from wave to wave through
+// LDS in wave order, so the terms meet in the one-wave kernels' order and the
+// results are the same bits.
+// ---------------------------------------------------------------------------
+
+template <int T>
+__global__ __launch_bounds__(512) void softmax_bwd_split_kernel(RowBwdArgs a) {
+  __shared__ float chain[kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x >> 6;
+  const int S = static_cast<int>(blockDim.x >> 6);
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* y = a.Y + row * a.ldy;
+    const float* dy = a.dY + row * a.lddy;
+    float* dx = a.dX + row * a.lddx;
+    int64_t valid = a.cols;
+    if (a.period > 0) {
+      const int64_t v = row % a.period + 1;
+      valid = v < valid ? v : valid;
+    }
+    const int64_t live = (valid + kWave - 1) / kWave;
+    const int64_t s0 = int64_t(T) * w;  // this wave's first segment
+    float yv[T], dv[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * (s0 + t);
+      yv[t] = 0.0f;
+      dv[t] = 0.0f;
+      if (s0 + t < live && j < valid) {  // masked entries are never read
+        yv[t] = y[j];
+        dv[t] = dy[j];
+      }
+    }
+    const float q = chain_across_waves(chain, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = __builtin_fmaf(yv[t], dv[t], c);  // masked: c
+      return c;
+    });
+    const float sum = wave_tree_sum(q);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = lane + kWave * (s0 + t);
+      if (j < a.cols) dx[j] = j < valid ? yv[t] * (dv[t] - sum) : 0.0f;
+    }
+    __syncthreads();  // chains read before the next row
+  }
+}
+
+template <int T>
+__global__ __launch_bounds__(512) void layernorm_bwd_split_kernel(RowBwdArgs a) {
+  __shared__ float chain_g[kWave];
+  __shared__ float chain_gt[kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x >> 6;
+  const int S = static_cast<int>(blockDim.x >> 6);
+  const float n = static_cast<float>(a.cols);
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* x = a.Y + row * a.ldy;
+    const float* dy = a.dY + row * a.lddy;
+    float* dx = a.dX + row * a.lddx;
+    const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
+    const int64_t j0 = lane + int64_t(kWave) * T * w;
+    float tv[T], gv[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      tv[t] = 0.0f;
+      gv[t] = 0.0f;
+      if (j < a.cols) {
+        const float d = x[j] - mean;
+        tv[t] = d * rstd;
+        gv[t] = a.gamma ? dy[j] * a.gamma[j] : dy[j];
+      }
+    }
+    float am = 0.0f;
+    if (!a.rms) {  // uniform over the workgroup
+      const float q = chain_across_waves(chain_g, lane, w, S, [&](float c) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) c = c + gv[t];  // past the row: +0
+        return c;
+      });
+      am = wave_tree_sum(q) / n;
+    }
+    const float q2 = chain_across_waves(chain_gt, lane, w, S, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = __builtin_fmaf(gv[t], tv[t], c);
+      return c;
+    });
+    const float bm = wave_tree_sum(q2) / n;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      if (j < a.cols) {
+        const float u = gv[t] - am;
+        const float tb = tv[t] * bm;
+        dx[j] = rstd * (u - tb);
+      }
+    }
+    __syncthreads();  // chains read before the next row
+  }
+}
+
 __global__ __launch_bounds__(64) void layernorm_bwd_generic_kernel(RowBwdArgs a) {
   __shared__ float qs[1024];
   const int lane = threadIdx.x;
@@ -552,6 +656,30 @@ WaveBwdKernel pick_layernorm_bwd(int64_t cols) {
   return layernorm_bwd_wave_kernel<64>;
 }
 
+using SplitBwdKernel = void (*)(RowBwdArgs);
+
+template <template <int> class K>
+SplitBwdKernel pick_split_bwd(int64_t cols, int S) {
+  const int64_t per_lane = (cols + int64_t(kWave) * S - 1) / (int64_t(kWave) * S);
+  if (per_lane <= 1) return K<1>::fn;
+  if (per_lane <= 2) return K<2>::fn;
+  if (per_lane <= 4) return K<4>::fn;
+  if (per_lane <= 8) return K<8>::fn;
+  if (per_lane <= 16) return K<16>::fn;
+  if (per_lane <= 32) return K<32>::fn;
+  return nullptr;
+}
+template <int T> struct SoftmaxBwdSplit { static constexpr SplitBwdKernel fn = softmax_bwd_split_kernel<T>; };
+template <int T> struct LayernormBwdSplit { static constexpr SplitBwdKernel fn = layernorm_bwd_split_kernel<T>; };
+
+hipError_t launch_split_bwd(SplitBwdKernel k, const RowBwdArgs& a, int S, hipStream_t s) {
+  if (!k) return hipErrorInvalidValue;
+  const int64_t cap = int64_t(1) << 30;
+  hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(a.rows < cap ? a.rows : cap)),
+                     dim3(kWave * S), 0, s, a);
+  return hipGetLastError();
+}
+
 using FusedKernel = void (*)(RowBwdArgs, LnParamArgs, int, int64_t);
 
 // Kernels for R <= 16 waves (1024 threads) up to 768 columns; wider rows
@@ -602,6 +730,14 @@ hipError_t launch_layernorm_bwd_wave(const RowBwdArgs& a, int wpb, hipStream_t s
   hipLaunchKernelGGL(pick_layernorm_bwd(a.cols), dim3(static_cast<unsigned>(blocks)),
                      dim3(kWave * wpb), 0, s, a, wpb);
   return hipGetLastError();
+}
+
+hipError_t launch_softmax_bwd_split(const RowBwdArgs& a, int S, hipStream_t s) {
+  return launch_split_bwd(pick_split_bwd<SoftmaxBwdSplit>(a.cols, S), a, S, s);
+}
+
+hipError_t launch_layernorm_bwd_split(const RowBwdArgs& a, int S, hipStream_t s) {
+  return launch_split_bwd(pick_split_bwd<LayernormBwdSplit>(a.cols, S), a, S, s);
 }
 
 hipError_t launch_layernorm_bwd_generic(const RowBwdArgs& a, hipStream_t s) {

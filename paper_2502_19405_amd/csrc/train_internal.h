@@ -28,6 +28,9 @@ hipError_t launch_softmax_bwd_wave(const RowBwdArgs& a, int waves_per_block, hip
 hipError_t launch_softmax_bwd_generic(const RowBwdArgs& a, hipStream_t s);
 hipError_t launch_layernorm_bwd_wave(const RowBwdArgs& a, int waves_per_block, hipStream_t s);
 hipError_t launch_layernorm_bwd_generic(const RowBwdArgs& a, hipStream_t s);
+// One row per workgroup of S waves (2, 4, 8), at most 32 values per lane.
+hipError_t launch_softmax_bwd_split(const RowBwdArgs& a, int S, hipStream_t s);
+hipError_t launch_layernorm_bwd_split(const RowBwdArgs& a, int S, hipStream_t s);
 
 // LayerNorm parameter gradients over rows, blocks of k_block rows (0 = one
 // block).  ws holds 2 * blocks * cols floats when there is more than one block.

@@ -150,9 +150,9 @@ def test_rows_and_elementwise_rejections(rp):
     wave4 = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (4,)).c())
     assert lib.repops_softmax_rows(_order(row_width=32), 4, 8, FAKE_A, 8, FAKE_C, 8, 0, wave4,
                                    None) == rp.ERR_LAUNCH
-    # split rows (ROWS_WAVE p[1] = waves per row): 2, 4, 8 or 16, one row per block, and a
+    # split rows (ROWS_WAVE p[1] = waves per row): 2, 4 or 8, one row per block, and a
     # row of at most 32 values per lane
-    for p in ((1, 3), (1, 32), (2, 4), (4, 2)):
+    for p in ((1, 3), (1, 16), (1, 32), (2, 4), (4, 2)):
         bad = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, p).c())
         assert lib.repops_softmax_rows(o, 4, 8, FAKE_A, 8, FAKE_C, 8, 0, bad, None) == \
             rp.ERR_LAUNCH, p
@@ -164,9 +164,9 @@ def test_rows_and_elementwise_rejections(rp):
     assert lib.repops_layernorm_rows(o, 4, 8, FAKE_A, 8, None, None, 1e-5, FAKE_C, 8, None, None,
                                      ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, 5)).c()),
                                      None) == rp.ERR_LAUNCH
-    # operations without a split kernel refuse it
-    assert lib.repops_softmax_backward_rows(o, 4, 8, FAKE_A, 8, FAKE_B, 8, FAKE_C, 8, 0, wide,
-                                            None) == rp.ERR_LAUNCH
+    # the backward row operations take splits too, under the same rules
+    assert lib.repops_softmax_backward_rows(o, 4, 4097, FAKE_A, 4097, FAKE_B, 4097, FAKE_C, 4097,
+                                            0, wide, None) == rp.ERR_LAUNCH
     assert lib.repops_layernorm_rows(o, 4, 0, FAKE_A, 8, None, None, 1e-5, FAKE_C, 8, None, None,
                                      None, None) == rp.ERR_SHAPE
     assert lib.repops_layernorm_rows(o, 4, 8, FAKE_A, 8, FAKE_C + 4, None, 1e-5, FAKE_C, 8, None,
@@ -268,6 +268,8 @@ def test_llama_rejections(rp):
     assert rope(offset=1 << 24) == rp.ERR_SHAPE
     assert rope(period=-1) == rp.ERR_SHAPE
     assert rope(launch=ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (3,)).c())) == rp.ERR_LAUNCH
+    # no split kernel for the rotary embedding
+    assert rope(launch=ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, 2)).c())) == rp.ERR_LAUNCH
     assert rope(launch=ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_GENERIC).c())) == rp.ERR_LAUNCH
     assert rope(rows=0, X=None, Y=None, inv=None) == rp.OK
 

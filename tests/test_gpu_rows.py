@@ -28,7 +28,7 @@ def row_launches(rp, W=64, combine=0, cols=0):
     if W == 64 and combine == 0:
         # one row per workgroup, split over S waves (at most 32 values per lane)
         out += [(f"split{S}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, S)))
-                for S in (2, 4, 8, 16) if cols <= S * 64 * 32]
+                for S in (2, 4, 8) if cols <= S * 64 * 32]
     return out
 
 

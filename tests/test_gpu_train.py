@@ -28,6 +28,10 @@ def row_launches(rp, W=64, combine=0, cols=0):
     out = [("generic", rp.Launch(rp.LAUNCH_ROWS_GENERIC)), ("auto", None)]
     if W == 64 and combine == 0 and cols <= 4096:
         out += [(f"wave{w}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (w,))) for w in (1, 2, 4, 8)]
+    if W == 64 and combine == 0:
+        # one row per workgroup, split over S waves (at most 32 values per lane)
+        out += [(f"split{S}", rp.Launch(rp.LAUNCH_ROWS_WAVE, (1, S)))
+                for S in (2, 4, 8) if cols <= S * 64 * 32]
     return out
 
 
@@ -37,7 +41,7 @@ def ew_launches(rp):
             ("t256b7", rp.Launch(rp.LAUNCH_ELEMENTWISE, (256, 7)))]
 
 
-COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000, 4096, 4097]
+COLS = [1, 2, 63, 64, 65, 100, 256, 768, 1000, 1024, 2048, 2049, 3000, 4096, 4097, 8192, 20000]
 
 
 # --------------------------------------------------------------------------
