@@ -331,7 +331,13 @@ def secondary(repops, steps):
                                               K, 1024 * 4096, 128, 4096, 1, 0.08838835, S,
                                               32 * 1024 * 1024, 1024 * 1024, 1024), steps)
     out["bmm_qkT_4x32x1024x1024x128"] = _rate(ms, flops=2 * 4 * 32 * 1024 * 1024 * 128)
-    del X, Wq, Wk, Wv, Wo, bufs, Q, K, S
+    # PV: P [4*32*1024, 1024] times V's head columns, written in place into O
+    P, V, O = bufs["P"], bufs["V"], bufs["O"]
+    ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 128, 1024, P, 32 * 1024 * 1024,
+                                              1024 * 1024, 1024, 0, V, 1024 * 4096, 128, 4096, 0,
+                                              1.0, O, 1024 * 4096, 128, 4096), steps)
+    out["bmm_pv_4x32x1024x128x1024"] = _rate(ms, flops=2 * 4 * 32 * 1024 * 128 * 1024)
+    del X, Wq, Wk, Wv, Wo, bufs, Q, K, S, P, V, O
 
     # Llama linear backward: dX = dY W^T, dW = X^T dY (8192 tokens, 4096 -> 14336)
     d = inputs.llama_linear_backward()
@@ -341,6 +347,18 @@ def secondary(repops, steps):
     ms = event_time_ms(lambda: pipelines.linear_backward(X, dY, W, out_dx=gx, out_dw=gw),
                        max(steps // 4, 3))
     out["llama_linear_backward"] = _rate(ms, flops=2 * 2 * 8192 * 4096 * 14336)
+    # one rank's share of dW under 8-way data parallelism: the same GEMM over
+    # 1024 of the 8192 tokens (the ordered cross-rank combine is not built)
+    ms = event_time_ms(lambda: repops.matmul(X[:1024].t(), dY[:1024], out=gw), steps)
+    out["llama_dW_rank_share_4096x14336x1024"] = _rate(ms, flops=2 * 4096 * 14336 * 1024)
+    del X, dY, W, gx, gw
+
+    # achievable streaming ceiling: a device-to-device copy of 512 MiB
+    src = torch.empty(1 << 27, device=dev)
+    dst = torch.empty_like(src)
+    ms = event_time_ms(lambda: dst.copy_(src), steps)
+    out["copy_ceiling_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
+    del src, dst
     return out
 
 

@@ -356,59 +356,79 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
   }
 }
 
-// Left-to-right sum of the block partials, per column.  The chains are short
-// (one add per block) but their operands sit in HBM, so the workgroup first
-// stages a chunk of partials in LDS with every thread loading, then one lane
-// per chain adds the chunk in block order.  A workgroup owns 16 columns; each
-// chain (dgamma or dbeta of one column) lives in one lane of wave 0.
-constexpr int kCombCols = 16;
+// Left-to-right sum of the block partials, per column.  The chains are long
+// (one add per row block) and each add depends on the previous one, so the
+// operands must be at hand: a workgroup owns kCombCols columns, stages up to
+// kCombChunk blocks of both partial arrays in LDS chain-major ([chain][block],
+// rows padded so that 16-byte reads stay aligned and spread over the banks),
+// and then one lane per chain reads four consecutive partials per LDS read
+// and adds them in block order.  Chains past the last block are padded with
+// +0, which leaves a chain that started at +0 unchanged.
 constexpr int kCombThreads = 256;
-constexpr int kCombChunk = 256;  // blocks per LDS chunk
-constexpr int kCombRowsPerPass = kCombThreads / kCombCols;
+constexpr int kCombChunk = 1024;  // blocks per LDS pass
 
+// COLS columns per workgroup: few row blocks favour wide workgroups (fewer
+// of them), many blocks narrow ones (more loads in flight per chain).
+template <int COLS>
 __global__ __launch_bounds__(kCombThreads) void layernorm_param_combine_kernel(LnParamArgs a,
-                                                                            int64_t nblk) {
-  __shared__ float buf[2][kCombChunk][kCombCols];
+                                                                            int64_t nblk,
+                                                                            int pitch) {
+  constexpr int kChains = 2 * COLS;  // dgamma and dbeta of each column
+  extern __shared__ float buf[];     // [kChains][pitch]
   const int tid = threadIdx.x;
-  const int c = tid % kCombCols;
-  const int rb = tid / kCombCols;
-  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kCombCols;
-  const bool col_ok = j0 + c < a.cols;
-  const float* wg = a.ws + j0 + c;
-  const float* wb = a.ws + nblk * a.cols + j0 + c;
-  float acc = 0.0f;  // lanes 0..15: dgamma of column c, lanes 16..31: dbeta
-  for (int64_t b0 = 0; b0 < nblk; b0 += kCombChunk) {
-    const int nb = static_cast<int>(nblk - b0 < kCombChunk ? nblk - b0 : kCombChunk);
-    constexpr int kPer = kCombChunk / kCombRowsPerPass;
-    float vg[kPer], vb[kPer];
+  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * COLS;
+  const int chunk = pitch - 4;  // blocks per pass (a multiple of 4)
+  float acc = 0.0f;             // thread ch < kChains: chain ch
+  const int ch = tid;
+  for (int64_t b0 = 0; b0 < nblk; b0 += chunk) {
+    const int nb = static_cast<int>(nblk - b0 < chunk ? nblk - b0 : chunk);
+    const int nb4 = (nb + 3) & ~3;
+    // stage: thread (k, b1) loads chain k's blocks b1, b1 + R, ... (R block
+    // rows per pass), kBatch loads in flight per thread; consecutive threads
+    // take consecutive columns
+    {
+      constexpr int kRowsPerPass = kCombThreads / kChains;
+      constexpr int kBatch = 32;
+      const int k = tid % kChains, b1 = tid / kChains;
+      const int arr = k / COLS, c = k % COLS;
+      const bool col_ok = j0 + c < a.cols;
+      const float* src = a.ws + (arr * nblk + b0) * a.cols + j0 + c;
+      for (int base = 0; base < nb4; base += kRowsPerPass * kBatch) {
+        float v[kBatch];
 #pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int b = rb + r * kCombRowsPerPass;
-      vg[r] = 0.0f;
-      vb[r] = 0.0f;
-      if (b < nb && col_ok) {
-        vg[r] = wg[(b0 + b) * a.cols];
-        vb[r] = wb[(b0 + b) * a.cols];
+        for (int r = 0; r < kBatch; ++r) {
+          const int b = base + b1 + r * kRowsPerPass;
+          v[r] = (b < nb && col_ok) ? src[static_cast<int64_t>(b) * a.cols] : 0.0f;
+        }
+#pragma unroll
+        for (int r = 0; r < kBatch; ++r) {
+          const int b = base + b1 + r * kRowsPerPass;
+          if (b < nb4) buf[k * pitch + b] = v[r];
+        }
       }
     }
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int b = rb + r * kCombRowsPerPass;
-      buf[0][b][c] = vg[r];
-      buf[1][b][c] = vb[r];
-    }
     __syncthreads();
-    if (tid < 2 * kCombCols) {
-      const int arr = tid / kCombCols;
-      for (int b = 0; b < nb; ++b) acc = acc + buf[arr][b][c];
+    if (ch < kChains) {
+      const float4* row = reinterpret_cast<const float4*>(buf + ch * pitch);
+#pragma unroll 8
+      for (int q = 0; q < nb4 / 4; ++q) {
+        const float4 v = row[q];
+        acc = acc + v.x;
+        acc = acc + v.y;
+        acc = acc + v.z;
+        acc = acc + v.w;
+      }
     }
     __syncthreads();
   }
-  if (tid < 2 * kCombCols && col_ok) {
-    if (tid < kCombCols) {
-      if (a.dgamma) a.dgamma[j0 + c] = acc;
-    } else {
-      if (a.dbeta) a.dbeta[j0 + c] = acc;
+  if (ch < kChains) {
+    const int arr = ch / COLS, c = ch % COLS;
+    if (j0 + c < a.cols) {
+      if (arr == 0) {
+        if (a.dgamma) a.dgamma[j0 + c] = acc;
+      } else {
+        if (a.dbeta) a.dbeta[j0 + c] = acc;
+      }
     }
   }
 }
@@ -756,9 +776,17 @@ int64_t layernorm_param_grid(int64_t rows, int64_t cols, int64_t k_block) {
 }
 
 hipError_t launch_layernorm_param_combine(const LnParamArgs& a, int64_t nblk, hipStream_t s) {
-  const int64_t groups = (a.cols + kCombCols - 1) / kCombCols;
-  hipLaunchKernelGGL(layernorm_param_combine_kernel, dim3(static_cast<unsigned>(groups)),
-                     dim3(kCombThreads), 0, s, a, nblk);
+  const int cols_per_group = nblk <= 256 ? 16 : 4;
+  const int64_t groups = (a.cols + cols_per_group - 1) / cols_per_group;
+  const int64_t chunk = nblk < kCombChunk ? (nblk + 3) & ~int64_t(3) : kCombChunk;
+  const int pitch = static_cast<int>(chunk) + 4;
+  const size_t lds = sizeof(float) * 2 * cols_per_group * static_cast<size_t>(pitch);
+  if (cols_per_group == 16)
+    hipLaunchKernelGGL(layernorm_param_combine_kernel<16>, dim3(static_cast<unsigned>(groups)),
+                       dim3(kCombThreads), lds, s, a, nblk, pitch);
+  else
+    hipLaunchKernelGGL(layernorm_param_combine_kernel<4>, dim3(static_cast<unsigned>(groups)),
+                       dim3(kCombThreads), lds, s, a, nblk, pitch);
   return hipGetLastError();
 }
 
