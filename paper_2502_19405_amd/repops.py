@@ -171,7 +171,15 @@ def _dev(t: torch.Tensor, name: str):
     return t.data_ptr()
 
 
+try:  # the raw handle of the current stream, without building a Stream object
+    _raw_stream = torch._C._cuda_getCurrentRawStream
+except AttributeError:  # pragma: no cover - older torch
+    _raw_stream = None
+
+
 def _stream(t: torch.Tensor):
+    if _raw_stream is not None:
+        return _raw_stream(t.get_device())
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
