@@ -16,28 +16,62 @@ namespace repops {
 constexpr int kWave = 64;
 constexpr int kMaxPerLane = 64;  // register-resident rows: cols <= 64 * 64
 
+// Cross-lane reads done in registers.  After lane_hi32(v), lane l < 32 holds
+// v[l + 32]; after lane_hi16(v), lane l of lanes 0..15 (and 32..47) holds
+// v[l + 16] (the gfx950 permute-swaps exchange the upper half of one operand
+// with the lower half of the other).  lane_down<D>(v), D in {1, 2, 4, 8},
+// gives lane l the value of lane l + D within its row of 16 lanes (a DPP row
+// shift; lanes whose source leaves the row read +0).  Unlike __shfl these
+// never go through the LDS crossbar.  The wave must have all 64 lanes active.
+__device__ __forceinline__ float lane_hi32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                  false, false);
+  return __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float lane_hi16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                  false, false);
+  return __uint_as_float(r[1]);
+}
+template <int D>
+__device__ __forceinline__ float lane_down(float v) {
+  static_assert(D == 1 || D == 2 || D == 4 || D == 8, "row shift of 1, 2, 4 or 8 lanes");
+  // DPP control 0x100 + D: row_shl by D; all rows and banks written.
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + D, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_broadcast0(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
 // Halving tree over the 64 lane partials: after the step with distance s, lane
-// l < s holds q[l] + q[l+s].  Lanes >= s keep stale values that no later step
-// reads.  Every lane returns q[0].
+// l < s holds q[l] + q[l+s].  Lanes >= s keep values that no later step reads.
+// Every lane returns q[0].  (An IEEE sum is commutative, so the compiler may
+// place the moved operand first.)  Called with all 64 lanes active.
 __device__ __forceinline__ float wave_tree_sum(float q) {
-#pragma unroll
-  for (int s = kWave / 2; s >= 1; s >>= 1) {
-    const float other = __shfl_down(q, s, kWave);
-    q = q + other;
-  }
-  return __shfl(q, 0, kWave);
+  q = q + lane_hi32(q);
+  q = q + lane_hi16(q);
+  q = q + lane_down<8>(q);
+  q = q + lane_down<4>(q);
+  q = q + lane_down<2>(q);
+  q = q + lane_down<1>(q);
+  return wave_broadcast0(q);
 }
 
 // Maximum over the wave (order-free up to the sign of a zero maximum, which
 // cannot change any softmax output: x - (+0) and x - (-0) differ only for
-// x = -0, and exp_rep(+0) = exp_rep(-0) = 1).
+// x = -0, and exp_rep(+0) = exp_rep(-0) = 1).  Same data movement as the tree
+// sum, so lane 0 ends with the maximum of all 64 lanes; every lane returns it.
+// Called with all 64 lanes active.
 __device__ __forceinline__ float wave_max(float m) {
-#pragma unroll
-  for (int s = kWave / 2; s >= 1; s >>= 1) {
-    const float other = __shfl_xor(m, s, kWave);
-    m = other > m ? other : m;
-  }
-  return m;
+  auto mx = [](float a, float b) { return b > a ? b : a; };
+  m = mx(m, lane_hi32(m));
+  m = mx(m, lane_hi16(m));
+  m = mx(m, lane_down<8>(m));
+  m = mx(m, lane_down<4>(m));
+  m = mx(m, lane_down<2>(m));
+  m = mx(m, lane_down<1>(m));
+  return wave_broadcast0(m);
 }
 
 // Per-lane chains continued across the S waves of a workgroup, in wave order:
