@@ -606,6 +606,12 @@ static repops_status_t norm_backward(
   if (want_params && dX && rows > 0 && kind == REPOPS_LAUNCH_ROWS_WAVE && order->k_block >= 1 &&
       !explicit_split) {
     const bool explicit_wave = launch && launch->kind == REPOPS_LAUNCH_ROWS_WAVE;
+    // Few row blocks: the blocks' rows and columns spread over about 512
+    // workgroups (not in place: other workgroups read the rows dX replaces).
+    repops::ColsplitPlan pl{};
+    if (!explicit_wave && dX != X && dX != dY &&
+        repops::layernorm_colsplit_plan(rows, cols, order->k_block, &pl))
+      return hip_status(repops::launch_layernorm_bwd_colsplit(a, p, pl, s));
     const int R = repops::layernorm_fused_rows(rows, cols, order->k_block, explicit_wave ? wpb : 0);
     if (R >= 1) return hip_status(repops::launch_layernorm_bwd_fused(a, p, R, s));
   }

@@ -115,11 +115,9 @@ __global__ __launch_bounds__(64) void softmax_bwd_generic_kernel(RowBwdArgs a) {
 //   dx_j = rstd * ((g_j - a) - t_j * b).
 // ---------------------------------------------------------------------------
 
+// dX of one row by one wave (row < a.rows; all 64 lanes active).
 template <int T>
-__global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, int wpb) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
-  if (row >= a.rows) return;
+__device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t row, int lane) {
   const float* x = a.Y + row * a.ldy;
   const float* dy = a.dY + row * a.lddy;
   float* dx = a.dX + row * a.lddx;
@@ -160,6 +158,14 @@ __global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, i
       if (j < a.cols) dx[j] = out(t);
     }
   }
+}
+
+template <int T>
+__global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, int wpb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  layernorm_bwd_row<T>(a, row, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -564,6 +570,114 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
 }
 
 // ---------------------------------------------------------------------------
+// LayerNorm backward, fused, for few row blocks: the G workgroups of a block
+// share its work.  Workgroup (beta, g) computes dX for its share of the
+// block's rows (whole rows, one wave each, as the wave kernel does) and the
+// chains of its column slice over all of the block's rows: chunks of rows are
+// loaded by all waves (t formed on the way) into LDS and one thread per
+// column advances its two chains through each chunk in row order, while the
+// next chunk's loads are in flight.  Every row is read twice (whole for dX,
+// by slices for the chains); the G workgroups of a block are placed on one
+// XCD so the second read finds the rows in that XCD's L2.  The rows are read
+// by workgroups other than the one writing their dX, so dX may not take the
+// place of X or dY here.
+// ---------------------------------------------------------------------------
+
+constexpr int kSplitWaves = 8;
+
+template <int T, int SWU>
+__global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_kernel(
+    RowBwdArgs a, LnParamArgs p, int G, int slice, int64_t nblk) {
+  constexpr int SW = kWave * SWU;            // LDS pitch: slice columns at most
+  constexpr int RPW = SWU <= 2 ? 8 : 4;      // chunk rows per wave
+  constexpr int RC = kSplitWaves * RPW;      // rows per chunk
+  __shared__ float st[RC * SW], sd[RC * SW];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int w = tid >> 6;
+  int64_t beta;
+  int g;
+  const int64_t bid = blockIdx.x;
+  if ((nblk & 7) == 0) {  // workgroups are dealt to the 8 XCDs in turn
+    const int64_t xcd = bid & 7, s = bid >> 3;
+    beta = (s / G) * 8 + xcd;
+    g = static_cast<int>(s % G);
+  } else {
+    beta = bid / G;
+    g = static_cast<int>(bid % G);
+  }
+  const int64_t blk = nblk == 1 ? a.rows : p.k_block;
+  const int64_t r0 = beta * blk;
+  const int64_t r1 = (r0 + blk < a.rows) ? r0 + blk : a.rows;
+  const int64_t c0 = static_cast<int64_t>(g) * slice;
+  const int sw = static_cast<int>(c0 + slice < a.cols ? slice : a.cols - c0);
+
+  float xr[RPW][SWU], dr[RPW][SWU];
+  auto load_chunk = [&](int64_t i0) {
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int64_t i = i0 + w + kSplitWaves * r;
+#pragma unroll
+      for (int u = 0; u < SWU; ++u) {
+        const int c = lane + kWave * u;
+        xr[r][u] = 0.0f;
+        dr[r][u] = 0.0f;
+        if (i < r1 && c < sw) {
+          xr[r][u] = p.X[i * p.ldx + c0 + c];
+          dr[r][u] = p.dY[i * p.lddy + c0 + c];
+        }
+      }
+    }
+  };
+  load_chunk(r0);
+
+  // dX for rows [d0, d1) of the block, one wave per row.
+  const int64_t per = (r1 - r0 + G - 1) / G;
+  const int64_t d0 = r0 + g * per;
+  const int64_t d1 = (d0 + per < r1) ? d0 + per : r1;
+  for (int64_t row = d0 + w; row < d1; row += kSplitWaves) layernorm_bwd_row<T>(a, row, lane);
+
+  float pg = 0.0f, pb = 0.0f;
+  for (int64_t i0 = r0; i0 < r1; i0 += RC) {
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int rr = w + kSplitWaves * r;
+      const int64_t i = i0 + rr;
+      if (i < r1) {
+        const float mean = p.rms ? 0.0f : p.mean[i], rstd = p.rstd[i];
+#pragma unroll
+        for (int u = 0; u < SWU; ++u) {
+          const float d = xr[r][u] - mean;
+          st[rr * SW + lane + kWave * u] = d * rstd;
+          sd[rr * SW + lane + kWave * u] = dr[r][u];
+        }
+      }
+    }
+    __syncthreads();
+    if (i0 + RC < r1) load_chunk(i0 + RC);
+    const int nr = static_cast<int>(r1 - i0 < RC ? r1 - i0 : RC);
+    if (tid < sw) {
+      for (int rr = 0; rr < nr; ++rr) {
+        const float dyv = sd[rr * SW + tid];
+        pg = __builtin_fmaf(dyv, st[rr * SW + tid], pg);
+        pb = pb + dyv;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid < sw) {
+    const int64_t j = c0 + tid;
+    if (nblk == 1) {
+      if (p.dgamma) p.dgamma[j] = pg;
+      if (p.dbeta) p.dbeta[j] = pb;
+    } else {
+      p.ws[beta * a.cols + j] = pg;
+      p.ws[(nblk + beta) * a.cols + j] = pb;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // GELU backward and Adam: elementwise, 16-byte accesses where every operand
 // is 16-byte aligned.
 // ---------------------------------------------------------------------------
@@ -835,6 +949,50 @@ hipError_t launch_layernorm_bwd_fused(const RowBwdArgs& a, const LnParamArgs& p,
   const size_t lds = sizeof(float) * 2 * static_cast<size_t>(R) * static_cast<size_t>(a.cols);
   hipLaunchKernelGGL(pick_layernorm_fused(a.cols), dim3(static_cast<unsigned>(nblk)),
                      dim3(R * kWave), lds, s, a, p, R, nblk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nblk == 1) return e;
+  return launch_layernorm_param_combine(p, nblk, s);
+}
+
+using ColsplitKernel = void (*)(RowBwdArgs, LnParamArgs, int, int, int64_t);
+
+template <int SWU>
+ColsplitKernel pick_colsplit_t(int64_t cols) {
+  if (cols <= kWave * 1) return layernorm_bwd_colsplit_kernel<1, SWU>;
+  if (cols <= kWave * 2) return layernorm_bwd_colsplit_kernel<2, SWU>;
+  if (cols <= kWave * 4) return layernorm_bwd_colsplit_kernel<4, SWU>;
+  if (cols <= kWave * 8) return layernorm_bwd_colsplit_kernel<8, SWU>;
+  if (cols <= kWave * 12) return layernorm_bwd_colsplit_kernel<12, SWU>;
+  return layernorm_bwd_colsplit_kernel<16, SWU>;
+}
+
+bool layernorm_colsplit_plan(int64_t rows, int64_t cols, int64_t k_block, ColsplitPlan* pl) {
+  // Few row blocks (fewer than one per compute unit) and rows a wave holds
+  // in registers; about 512 workgroups, slices of 16 to 256 columns.
+  if (rows < 1 || cols < 1 || cols > kWave * 16 || k_block < 1) return false;
+  const int64_t nblk = layernorm_param_blocks(rows, k_block);
+  if (nblk >= 256) return false;
+  int64_t g0 = (512 + nblk - 1) / nblk;
+  const int64_t gcol = (cols + kWave - 1) / kWave;
+  if (g0 > gcol) g0 = gcol;
+  int64_t slice = (cols + g0 - 1) / g0;
+  slice = (slice + 15) & ~int64_t(15);
+  if (slice > kWave * 4) slice = kWave * 4;
+  pl->slice = static_cast<int>(slice);
+  pl->G = static_cast<int>((cols + slice - 1) / slice);
+  pl->swu = static_cast<int>((slice + kWave - 1) / kWave);
+  return true;
+}
+
+hipError_t launch_layernorm_bwd_colsplit(const RowBwdArgs& a, const LnParamArgs& p,
+                                         const ColsplitPlan& pl, hipStream_t s) {
+  const int64_t nblk = layernorm_param_blocks(a.rows, p.k_block);
+  ColsplitKernel k = pl.swu == 1   ? pick_colsplit_t<1>(a.cols)
+                     : pl.swu == 2 ? pick_colsplit_t<2>(a.cols)
+                     : pl.swu == 3 ? pick_colsplit_t<3>(a.cols)
+                                   : pick_colsplit_t<4>(a.cols);
+  hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(nblk * pl.G)), dim3(kSplitWaves * kWave), 0,
+                     s, a, p, pl.G, pl.slice, nblk);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nblk == 1) return e;
   return launch_layernorm_param_combine(p, nblk, s);

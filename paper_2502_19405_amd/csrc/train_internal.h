@@ -54,6 +54,14 @@ int layernorm_fused_rows(int64_t rows, int64_t cols, int64_t k_block, int reques
 hipError_t launch_layernorm_bwd_fused(const RowBwdArgs& a, const LnParamArgs& p, int R,
                                       hipStream_t s);
 
+// Fused input and parameter gradients for few row blocks (W = 64 strided
+// tree, cols <= 1024): G workgroups per block, each with a column slice of
+// the chains and a share of the rows' dX.  dX must not alias X or dY.
+struct ColsplitPlan { int G, slice, swu; };
+bool layernorm_colsplit_plan(int64_t rows, int64_t cols, int64_t k_block, ColsplitPlan* pl);
+hipError_t launch_layernorm_bwd_colsplit(const RowBwdArgs& a, const LnParamArgs& p,
+                                         const ColsplitPlan& pl, hipStream_t s);
+
 hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,
                            int max_blocks, hipStream_t s, bool erf_form);
 

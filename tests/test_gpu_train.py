@@ -225,6 +225,31 @@ def test_layernorm_backward_distilbert_shape(rp):
         assert_bits_equal(a, b, f"distilbert {what}")
 
 
+# Few row blocks (fewer than 256): the automatic launch spreads each block's
+# rows and columns over several workgroups; block counts with and without a
+# multiple of 8, k_block 1 and k_block past the last row, RMSNorm, and the
+# single-wave fused kernel on the same inputs.
+@pytest.mark.parametrize("rows,cols,k_block", [(512, 1024, 64), (1000, 96, 16), (2048, 300, 128),
+                                               (130, 1000, 1), (777, 64, 4096), (4096, 17, 64),
+                                               (8 * 64, 768, 64), (255 * 16 - 3, 200, 16),
+                                               (110 * 64 - 5, 768, 64)])
+def test_layernorm_backward_few_row_blocks(rp, rows, cols, k_block):
+    X, dY, mean, rstd, gamma = ln_case(rows + cols + k_block, rows, cols)
+    order = rp.Order(k_block=k_block)
+    want = oracle.layernorm_backward_rows(X, dY, mean, rstd, gamma, k_block=k_block)
+    for name, launch in (("auto", None), ("wave4", rp.Launch(rp.LAUNCH_ROWS_WAVE, (4,)))):
+        announce("layernorm_backward few blocks", rows, cols, k_block, name)
+        got = run_lnb(rp, X, dY, mean, rstd, gamma, order=order, launch=launch)
+        for a, b, what in zip(got, want, ("dX", "dgamma", "dbeta")):
+            assert_bits_equal(a, b, f"{name} {what} {rows}x{cols} k_block={k_block}")
+    announce("rmsnorm_backward few blocks", rows, cols, k_block)
+    _, rstd2 = oracle.rmsnorm_rows(X, gamma, with_stats=True)
+    want = oracle.rmsnorm_backward_rows(X, dY, rstd2, gamma, k_block=k_block)
+    dx, dg = rp.rmsnorm_backward_rows(dev(X), dev(dY), dev(rstd2), dev(gamma), order=order)
+    assert_bits_equal(host(dx), want[0], f"rms dX {rows}x{cols} k_block={k_block}")
+    assert_bits_equal(host(dg), want[1], f"rms dgamma {rows}x{cols} k_block={k_block}")
+
+
 # --------------------------------------------------------------------------
 # bias gradient (column sums)
 # --------------------------------------------------------------------------
