@@ -353,11 +353,15 @@ def secondary(repops, steps):
     out["llama_dW_rank_share_4096x14336x1024"] = _rate(ms, flops=2 * 4096 * 14336 * 1024)
     del X, dY, W, gx, gw
 
-    # achievable streaming ceiling: a device-to-device copy of 512 MiB
+    # streaming ceilings: a device-to-device copy of 512 MiB by torch's copy kernel
     src = torch.empty(1 << 27, device=dev)
     dst = torch.empty_like(src)
     ms = event_time_ms(lambda: dst.copy_(src), steps)
     out["copy_ceiling_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
+    # The library's own elementwise kernel with no arithmetic: the streaming
+    # rate the bandwidth-bound operators can reach.
+    ms = event_time_ms(lambda: repops.copy(src, out=dst), steps)
+    out["copy_repops_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
     del src, dst
     return out
 

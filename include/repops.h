@@ -226,6 +226,16 @@ repops_status_t repops_gelu(const repops_order_t *order, int64_t n, const float 
 repops_status_t repops_exp(const repops_order_t *order, int64_t n, const float *X, float *Y,
                            const repops_launch_t *launch, void *hip_stream);
 
+/*
+ * repops_copy -- Y = X over n contiguous elements through the elementwise
+ *   kernel with no arithmetic: the streaming rate that kernel reaches, the
+ *   ceiling against which the bandwidth-bound operators are measured (not an
+ *   operator of the method).  Same checks, launch options and errors as
+ *   repops_exp; Y == X is allowed.
+ */
+repops_status_t repops_copy(const repops_order_t *order, int64_t n, const float *X, float *Y,
+                            const repops_launch_t *launch, void *hip_stream);
+
 /* ------------------------------------------------------------------------
  * Training-step operators.  The training runs of Section 4.2 (Adam optimizer)
  * execute the extended graph of Section 2.2: every forward node, its backward

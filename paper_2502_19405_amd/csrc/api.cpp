@@ -460,6 +460,17 @@ repops_status_t repops_gelu(const repops_order_t* order, int64_t n, const float*
       repops::launch_gelu(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
 }
 
+repops_status_t repops_copy(const repops_order_t* order, int64_t n, const float* X, float* Y,
+                            const repops_launch_t* launch, void* hip_stream) {
+  repops_status_t st = check_elementwise(order, n, X, Y);
+  if (st != REPOPS_OK) return st;
+  int threads, max_blocks;
+  st = ew_launch(launch, &threads, &max_blocks);
+  if (st != REPOPS_OK || n == 0) return st;
+  return hip_status(
+      repops::launch_copy(n, X, Y, threads, max_blocks, static_cast<hipStream_t>(hip_stream)));
+}
+
 repops_status_t repops_exp(const repops_order_t* order, int64_t n, const float* X, float* Y,
                            const repops_launch_t* launch, void* hip_stream) {
   repops_status_t st = check_elementwise(order, n, X, Y);

@@ -8,12 +8,16 @@
 
 #include "rep_math.h"
 #include "repops_internal.h"
+#include "stream_store.h"
 
 #pragma clang fp contract(off)
 
 namespace repops {
 namespace {
 
+struct CopyOp {  // no arithmetic: the streaming ceiling of this kernel
+  __device__ __forceinline__ float operator()(float x) const { return x; }
+};
 struct ExpOp {
   __device__ __forceinline__ float operator()(float x) const { return rep_exp(x); }
 };
@@ -45,11 +49,11 @@ __global__ __launch_bounds__(1024) void elementwise_kernel(int64_t n, const floa
       o.y = op(v.y);
       o.z = op(v.z);
       o.w = op(v.w);
-      y4[i] = o;
+      st_stream(y4 + i, o);
     }
     done = n4 * 4;
   }
-  for (int64_t i = done + tid; i < n; i += stride) y[i] = op(x[i]);
+  for (int64_t i = done + tid; i < n; i += stride) st_stream(y + i, op(x[i]));
 }
 
 template <class Op>
@@ -72,6 +76,11 @@ hipError_t launch(int64_t n, const float* x, float* y, int threads, int max_bloc
 hipError_t launch_gelu(int64_t n, const float* x, float* y, int threads, int max_blocks,
                        hipStream_t s) {
   return launch<GeluOp>(n, x, y, threads, max_blocks, s);
+}
+
+hipError_t launch_copy(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                       hipStream_t s) {
+  return launch<CopyOp>(n, x, y, threads, max_blocks, s);
 }
 
 hipError_t launch_exp(int64_t n, const float* x, float* y, int threads, int max_blocks,

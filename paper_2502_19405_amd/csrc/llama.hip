@@ -17,6 +17,7 @@
 #include "rep_math.h"
 #include "row_reduce.h"
 #include "rows_internal.h"
+#include "stream_store.h"
 
 #pragma clang fp contract(off)
 
@@ -62,8 +63,8 @@ __global__ __launch_bounds__(512) void rope_kernel(RopeArgs a, int wpb) {
       const float x1 = x[j], x2 = x[j + half];
       const float p1 = x1 * cv, p2 = x2 * sv, p3 = x2 * cv, p4 = x1 * sv;
       // Y may equal X: both elements of the pair are read before either is written
-      y[j] = a.inverse ? p1 + p2 : p1 - p2;
-      y[j + half] = a.inverse ? p3 - p4 : p3 + p4;
+      st_stream(y + j, a.inverse ? p1 + p2 : p1 - p2);
+      st_stream(y + j + half, a.inverse ? p3 - p4 : p3 + p4);
     }
   }
 }
@@ -107,12 +108,12 @@ __global__ __launch_bounds__(512) void rmsnorm_wave_kernel(RmsArgs a, int wpb) {
   };
   if (a.cols == kWave * T) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) y[lane + kWave * t] = out(t, lane + kWave * t);
+    for (int t = 0; t < T; ++t) st_stream(y + lane + kWave * t, out(t, lane + kWave * t));
   } else {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * t;
-      if (j < a.cols) y[j] = out(t, j);
+      if (j < a.cols) st_stream(y + j, out(t, j));
     }
   }
   if (lane == 0 && a.rstd_out) a.rstd_out[row] = rstd;
@@ -161,8 +162,8 @@ __global__ __launch_bounds__(512) void rmsnorm_split_kernel(RmsArgs a) {
       const int64_t j = j0 + kWave * t;
       if (j < a.cols) {
         const float tv = v[t] * rstd;
-        if constexpr (kPre) y[j] = a.gamma ? tv * gv[t] : tv;
-        else y[j] = a.gamma ? tv * a.gamma[j] : tv;
+        if constexpr (kPre) st_stream(y + j, a.gamma ? tv * gv[t] : tv);
+        else st_stream(y + j, a.gamma ? tv * a.gamma[j] : tv);
       }
     }
     if (w == 0 && lane == 0 && a.rstd_out) a.rstd_out[row] = rstd;
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(64) void rmsnorm_generic_kernel(RmsArgs a) {
     const float rstd = 1.0f / __builtin_sqrtf(ms + a.eps);
     for (int64_t j = lane; j < a.cols; j += kWave) {
       const float tv = x[j] * rstd;
-      y[j] = a.gamma ? tv * a.gamma[j] : tv;  // Y may equal X: x[j] is read first
+      st_stream(y + j, a.gamma ? tv * a.gamma[j] : tv);  // Y may equal X: x[j] is read first
     }
     if (lane == 0 && a.rstd_out) a.rstd_out[row] = rstd;
     __syncthreads();
@@ -221,11 +222,11 @@ __global__ __launch_bounds__(1024) void gated_kernel(int64_t n, const float* g, 
       o.y = op(gv.y, uv.y);
       o.z = op(gv.z, uv.z);
       o.w = op(gv.w, uv.w);
-      y4[i] = o;
+      st_stream(y4 + i, o);
     }
     done = n4 * 4;
   }
-  for (int64_t i = done + tid; i < n; i += stride) y[i] = op(g[i], TWO ? u[i] : 0.0f);
+  for (int64_t i = done + tid; i < n; i += stride) st_stream(y + i, op(g[i], TWO ? u[i] : 0.0f));
 }
 
 // dgate = (dy * u) * silu'(g); dup = dy * silu(g).
@@ -255,16 +256,16 @@ __global__ __launch_bounds__(1024) void swiglu_bwd_kernel(int64_t n, const float
       swiglu_bwd_one(gv.y, uv.y, dv.y, a.y, b.y);
       swiglu_bwd_one(gv.z, uv.z, dv.z, a.z, b.z);
       swiglu_bwd_one(gv.w, uv.w, dv.w, a.w, b.w);
-      dg4[i] = a;
-      du4[i] = b;
+      st_stream(dg4 + i, a);
+      st_stream(du4 + i, b);
     }
     done = n4 * 4;
   }
   for (int64_t i = done + tid; i < n; i += stride) {
     float a, b;
     swiglu_bwd_one(g[i], u[i], dy[i], a, b);
-    dg[i] = a;
-    du[i] = b;
+    st_stream(dg + i, a);
+    st_stream(du + i, b);
   }
 }
 

@@ -55,6 +55,8 @@ int64_t rows_wave_max_cols();
 
 hipError_t launch_gelu(int64_t n, const float* x, float* y, int threads, int max_blocks,
                        hipStream_t s);
+hipError_t launch_copy(int64_t n, const float* x, float* y, int threads, int max_blocks,
+                      hipStream_t s);
 hipError_t launch_exp(int64_t n, const float* x, float* y, int threads, int max_blocks,
                       hipStream_t s);
 

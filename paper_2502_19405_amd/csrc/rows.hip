@@ -19,6 +19,7 @@
 #include "repops_internal.h"
 #include "row_reduce.h"
 #include "rows_internal.h"
+#include "stream_store.h"
 
 #pragma clang fp contract(off)
 
@@ -64,12 +65,12 @@ __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
   const float r = 1.0f / s;
   if (a.cols == kWave * T) {  // full-width row: unconditional stores
 #pragma unroll
-    for (int t = 0; t < T; ++t) y[lane + kWave * t] = v[t] * r;
+    for (int t = 0; t < T; ++t) st_stream(y + lane + kWave * t, v[t] * r);
   } else {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * t;
-      if (j < a.cols) y[j] = v[t] * r;
+      if (j < a.cols) st_stream(y + j, v[t] * r);
     }
   }
 }
@@ -126,7 +127,7 @@ __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb)
     else if (a.gamma) o = tv * gj;
     else if (a.beta) o = tv + bj;
     else o = tv;
-    y[j] = o;
+    st_stream(y + j, o);
   };
   if (a.cols == kWave * T) {  // full-width row: unconditional stores
 #pragma unroll
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(512) void softmax_split_kernel(RowArgs a) {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * (s0 + t);
-      if (j < a.cols) y[j] = v[t] * r;
+      if (j < a.cols) st_stream(y + j, v[t] * r);
     }
     __syncthreads();  // chains and maxima read before the next row
   }
@@ -271,7 +272,7 @@ __global__ __launch_bounds__(512) void layernorm_split_kernel(RowArgs a) {
         else if (a.gamma) o = tv * gj;
         else if (a.beta) o = tv + bj;
         else o = tv;
-        y[j] = o;
+        st_stream(y + j, o);
       }
     }
     if (w == 0 && lane == 0) {
@@ -307,7 +308,7 @@ __global__ __launch_bounds__(64) void softmax_generic_kernel(RowArgs a) {
     const float r = 1.0f / s;
     for (int64_t j = lane; j < a.cols; j += kWave) {
       const float e = j < valid ? rep_exp(x[j] - m) : 0.0f;
-      y[j] = e * r;  // X may alias Y: x[j] is read before y[j] is written
+      st_stream(y + j, e * r);  // X may alias Y: x[j] is read before y[j] is written
     }
     __syncthreads();
   }
@@ -335,7 +336,7 @@ __global__ __launch_bounds__(64) void layernorm_generic_kernel(RowArgs a) {
       else if (a.gamma) o = tv * a.gamma[j];
       else if (a.beta) o = tv + a.beta[j];
       else o = tv;
-      y[j] = o;
+      st_stream(y + j, o);
     }
     if (lane == 0) {
       if (a.mean_out) a.mean_out[row] = mean;

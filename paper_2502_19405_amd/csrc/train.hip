@@ -23,6 +23,7 @@
 #include "repops_internal.h"
 #include "train_internal.h"
 #include "row_reduce.h"
+#include "stream_store.h"
 
 #pragma clang fp contract(off)
 
@@ -72,12 +73,12 @@ __global__ __launch_bounds__(T > 32 ? 256 : 512) void softmax_bwd_wave_kernel(Ro
   };
   if (a.cols == kWave * T) {  // full-width row: unconditional stores
 #pragma unroll
-    for (int t = 0; t < T; ++t) dx[lane + kWave * t] = out(t, lane + kWave * t);
+    for (int t = 0; t < T; ++t) st_stream(dx + lane + kWave * t, out(t, lane + kWave * t));
   } else {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * t;
-      if (j < a.cols) dx[j] = out(t, j);
+      if (j < a.cols) st_stream(dx + j, out(t, j));
     }
   }
 }
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(64) void softmax_bwd_generic_kernel(RowBwdArgs a) {
         const float diff = dy[j] - s;
         o = y[j] * diff;
       }
-      dx[j] = o;  // dX may equal Y or dY: element j is read before it is written
+      st_stream(dx + j, o);  // dX may equal Y or dY: element j is read before it is written
     }
     __syncthreads();
   }
@@ -150,12 +151,12 @@ __device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t r
   };
   if (a.cols == kWave * T) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) dx[lane + kWave * t] = out(t);
+    for (int t = 0; t < T; ++t) st_stream(dx + lane + kWave * t, out(t));
   } else {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * t;
-      if (j < a.cols) dx[j] = out(t);
+      if (j < a.cols) st_stream(dx + j, out(t));
     }
   }
 }
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(512) void softmax_bwd_split_kernel(RowBwdArgs a) {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int64_t j = lane + kWave * (s0 + t);
-      if (j < a.cols) dx[j] = j < valid ? yv[t] * (dv[t] - sum) : 0.0f;
+      if (j < a.cols) st_stream(dx + j, j < valid ? yv[t] * (dv[t] - sum) : 0.0f);
     }
     __syncthreads();  // chains read before the next row
   }
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(512) void layernorm_bwd_split_kernel(RowBwdArgs a) 
       if (j < a.cols) {
         const float u = gv[t] - am;
         const float tb = tv[t] * bm;
-        dx[j] = rstd * (u - tb);
+        st_stream(dx + j, rstd * (u - tb));
       }
     }
     __syncthreads();  // chains read before the next row
@@ -295,7 +296,7 @@ __global__ __launch_bounds__(64) void layernorm_bwd_generic_kernel(RowBwdArgs a)
       const float u = gj - am;
       const float tb = tj * bm;
       const float w = u - tb;
-      dx[j] = rstd * w;  // dX may equal X or dY: element j is read before it is written
+      st_stream(dx + j, rstd * w);  // dX may equal X or dY: element j is read before it is written
     }
     __syncthreads();
   }
@@ -535,7 +536,7 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
           const float u = gv[t] - am;
           const float tb = tv[t] * bm;
           const float wv = u - tb;
-          dx[j] = rstd * wv;
+          st_stream(dx + j, rstd * wv);
         }
       }
     }
@@ -709,11 +710,11 @@ __global__ __launch_bounds__(1024) void gelu_bwd_kernel(int64_t n, const float* 
       o.y = dv.y * grad(xv.y);
       o.z = dv.z * grad(xv.z);
       o.w = dv.w * grad(xv.w);
-      o4[i] = o;
+      st_stream(o4 + i, o);
     }
     done = n4 * 4;
   }
-  for (int64_t i = done + tid; i < n; i += stride) dx[i] = dy[i] * grad(x[i]);
+  for (int64_t i = done + tid; i < n; i += stride) st_stream(dx + i, dy[i] * grad(x[i]));
 }
 
 // One element of the Adam / AdamW update (decay: 0 none, 1 decoupled, 2 coupled).
@@ -752,18 +753,18 @@ __global__ __launch_bounds__(1024) void adam_kernel(int64_t n, float* p, const f
       adam_one(s, pv.y, gv.y, mv.y, vv.y);
       adam_one(s, pv.z, gv.z, mv.z, vv.z);
       adam_one(s, pv.w, gv.w, mv.w, vv.w);
-      p4[i] = pv;
-      m4[i] = mv;
-      v4[i] = vv;
+      st_stream(p4 + i, pv);
+      st_stream(m4 + i, mv);
+      st_stream(v4 + i, vv);
     }
     done = n4 * 4;
   }
   for (int64_t i = done + tid; i < n; i += stride) {
     float pv = p[i], mv = m[i], vv = v[i];
     adam_one(s, pv, g[i], mv, vv);
-    p[i] = pv;
-    m[i] = mv;
-    v[i] = vv;
+    st_stream(p + i, pv);
+    st_stream(m + i, mv);
+    st_stream(v + i, vv);
   }
 }
 

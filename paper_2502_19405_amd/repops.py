@@ -93,6 +93,7 @@ _SIGNATURES = {
                                      _vp, _lp, _vp]),
     "repops_gelu": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
     "repops_exp": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
+    "repops_copy": (_i32, [_op, _i64, _vp, _vp, _lp, _vp]),
     "repops_softmax_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64,
                                             _i64, _lp, _vp]),
     "repops_layernorm_backward_workspace": (_i32, [_op, _i64, _i64, ctypes.POINTER(ctypes.c_uint64)]),
@@ -351,6 +352,12 @@ def _elementwise(fn_name: str, X: torch.Tensor, order, launch, out):
 def gelu(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
          out: torch.Tensor | None = None) -> torch.Tensor:
     return _elementwise("repops_gelu", X, order, launch, out)
+
+
+def copy(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = X through the elementwise kernel (the streaming ceiling it reaches)."""
+    return _elementwise("repops_copy", X, order, launch, out)
 
 
 def exp(X: torch.Tensor, order: Order | None = None, launch: Launch | None = None,

@@ -75,6 +75,30 @@ def test_launch_shapes_and_alignment(rp, fn):
     assert getattr(rp, fn)(torch.empty(0, device="cuda:0")).numel() == 0
 
 
+def test_copy_keeps_every_bit(rp):
+    """The streaming-ceiling copy returns its input bit for bit (signed zeros,
+    infinities, NaN payloads, subnormals) for every launch shape, ragged
+    lengths, a misaligned view and in place."""
+    import torch
+    x = np.concatenate([SPECIALS, sweep(65537, 11),
+                        np.array([0x7FC00001, 0xFFBADBAD, 0x7F800001, 0x00000001],
+                                 np.uint32).view(np.float32)])
+    dx = dev(x)
+    launches = [None] + [rp.Launch(rp.LAUNCH_ELEMENTWISE, (t, b)) for t, b in
+                         ((64, 0), (256, 7), (1024, 0), (512, 1))]
+    for launch in launches:
+        announce("copy", launch)
+        for n in (1, 3, 4, 5, x.size):
+            assert_bits_equal(host(rp.copy(dx[:n], launch=launch)), x[:n], f"{launch} n={n}",
+                              nan_equal=False)
+        assert_bits_equal(host(rp.copy(dx[1:], launch=launch)), x[1:], "offset view",
+                          nan_equal=False)
+        d = dev(x)
+        rp.copy(d, launch=launch, out=d)
+        assert_bits_equal(host(d), x, "in place", nan_equal=False)
+    assert rp.copy(torch.empty(0, device="cuda:0")).numel() == 0
+
+
 @pytest.mark.parametrize("fn", ["exp", "gelu"])
 def test_exhaustive_all_bit_patterns(rp, fn):
     """Every one of the 2^32 binary32 inputs, in 16 chunks of 2^28: the GPU
