@@ -46,7 +46,7 @@ __global__ __launch_bounds__(1024) void sincos_kernel(int64_t n, const float* x,
 
 __global__ __launch_bounds__(512) void rope_kernel(RopeArgs a, int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   const int64_t pos = (a.period > 0 ? row % a.period : row) + a.offset;
   const float pf = static_cast<float>(pos);  // exact: pos < 2^24
@@ -77,7 +77,7 @@ __global__ __launch_bounds__(512) void rope_kernel(RopeArgs a, int wpb) {
 template <int T>
 __global__ __launch_bounds__(512) void rmsnorm_wave_kernel(RmsArgs a, int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   const float* x = a.X + row * a.ldx;
   float* y = a.Y + row * a.ldy;
@@ -128,7 +128,7 @@ template <int T>
 __global__ __launch_bounds__(512) void rmsnorm_split_kernel(RmsArgs a) {
   __shared__ float chain[kWave];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int S = static_cast<int>(blockDim.x >> 6);
   const float n = static_cast<float>(a.cols);
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {

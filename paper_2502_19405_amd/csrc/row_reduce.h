@@ -16,6 +16,13 @@ namespace repops {
 constexpr int kWave = 64;
 constexpr int kMaxPerLane = 64;  // register-resident rows: cols <= 64 * 64
 
+// This thread's wave within the workgroup, as a value the compiler knows to be
+// uniform over the wave: per-row scalars indexed by it are then read with
+// scalar loads, which the vector-load counter does not wait for.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+}
+
 // Cross-lane reads done in registers.  After lane_hi32(v), lane l < 32 holds
 // v[l + 32]; after lane_hi16(v), lane l of lanes 0..15 (and 32..47) holds
 // v[l + 16] (the gfx950 permute-swaps exchange the upper half of one operand

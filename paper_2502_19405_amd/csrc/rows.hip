@@ -29,7 +29,7 @@ namespace {
 template <int T>
 __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   const float* x = a.X + row * a.ldx;
   float* y = a.Y + row * a.ldy;
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(512) void softmax_wave_kernel(RowArgs a, int wpb) {
 template <int T>
 __global__ __launch_bounds__(512) void layernorm_wave_kernel(RowArgs a, int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   const float* x = a.X + row * a.ldx;
   float* y = a.Y + row * a.ldy;
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(512) void softmax_split_kernel(RowArgs a) {
   __shared__ float chain[kWave];
   __shared__ float wave_maxima[8];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int S = static_cast<int>(blockDim.x >> 6);
   const float ninf = -__builtin_huge_valf();
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(512) void layernorm_split_kernel(RowArgs a) {
   __shared__ float chain_sum[kWave];
   __shared__ float chain_sq[kWave];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int S = static_cast<int>(blockDim.x >> 6);
   const float n = static_cast<float>(a.cols);
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {

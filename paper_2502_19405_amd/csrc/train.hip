@@ -41,7 +41,7 @@ template <int T>
 __global__ __launch_bounds__(T > 32 ? 256 : 512) void softmax_bwd_wave_kernel(RowBwdArgs a,
                                                                               int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   const float* y = a.Y + row * a.ldy;
   const float* dy = a.dY + row * a.lddy;
@@ -116,7 +116,46 @@ __global__ __launch_bounds__(64) void softmax_bwd_generic_kernel(RowBwdArgs a) {
 //   dx_j = rstd * ((g_j - a) - t_j * b).
 // ---------------------------------------------------------------------------
 
-// dX of one row by one wave (row < a.rows; all 64 lanes active).
+// t_j = (x_j - mean) * rstd and g_j = dy_j * gamma_j (dy_j without gamma) of
+// the columns j0 + 64 t, t < T, +0 past the row.  Every load is issued before
+// any arithmetic (a load and its use in one conditional block would wait for
+// each element in turn).
+template <int T>
+__device__ __forceinline__ void ln_bwd_terms(const RowBwdArgs& a, const float* x, const float* dy,
+                                             int64_t j0, float mean, float rstd, float (&tv)[T],
+                                             float (&gv)[T]) {
+  float xv[T], dv[T], gm[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int64_t j = j0 + kWave * t;
+    xv[t] = 0.0f;
+    dv[t] = 0.0f;
+    if (j < a.cols) {
+      xv[t] = x[j];
+      dv[t] = dy[j];
+    }
+  }
+  if (a.gamma) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int64_t j = j0 + kWave * t;
+      gm[t] = 0.0f;
+      if (j < a.cols) gm[t] = a.gamma[j];
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const bool in = j0 + kWave * t < a.cols;
+    const float d = xv[t] - mean;
+    const float tt = d * rstd;
+    const float g = a.gamma ? dv[t] * gm[t] : dv[t];
+    tv[t] = in ? tt : 0.0f;
+    gv[t] = in ? g : 0.0f;
+  }
+}
+
+// dX of one row by one wave (row < a.rows, uniform over the wave; all 64
+// lanes active).
 template <int T>
 __device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t row, int lane) {
   const float* x = a.Y + row * a.ldy;
@@ -124,19 +163,10 @@ __device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t r
   float* dx = a.dX + row * a.lddx;
   const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
   float tv[T], gv[T];
+  ln_bwd_terms<T>(a, x, dy, lane, mean, rstd, tv, gv);
   float q = 0.0f;
 #pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const int64_t j = lane + kWave * t;
-    tv[t] = 0.0f;
-    gv[t] = 0.0f;
-    if (j < a.cols) {
-      const float d = x[j] - mean;
-      tv[t] = d * rstd;
-      gv[t] = a.gamma ? dy[j] * a.gamma[j] : dy[j];
-    }
-    q = q + gv[t];  // terms past the row are +0 and leave q unchanged
-  }
+  for (int t = 0; t < T; ++t) q = q + gv[t];  // terms past the row are +0 and leave q unchanged
   const float n = static_cast<float>(a.cols);
   const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
   float q2 = 0.0f;
@@ -164,7 +194,7 @@ __device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t r
 template <int T>
 __global__ __launch_bounds__(512) void layernorm_bwd_wave_kernel(RowBwdArgs a, int wpb) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + (threadIdx.x >> 6);
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * wpb + wave_id();
   if (row >= a.rows) return;
   layernorm_bwd_row<T>(a, row, lane);
 }
@@ -180,7 +210,7 @@ template <int T>
 __global__ __launch_bounds__(512) void softmax_bwd_split_kernel(RowBwdArgs a) {
   __shared__ float chain[kWave];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int S = static_cast<int>(blockDim.x >> 6);
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
     const float* y = a.Y + row * a.ldy;
@@ -224,7 +254,7 @@ __global__ __launch_bounds__(512) void layernorm_bwd_split_kernel(RowBwdArgs a) 
   __shared__ float chain_g[kWave];
   __shared__ float chain_gt[kWave];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x >> 6;
+  const int w = wave_id();
   const int S = static_cast<int>(blockDim.x >> 6);
   const float n = static_cast<float>(a.cols);
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
@@ -234,17 +264,7 @@ __global__ __launch_bounds__(512) void layernorm_bwd_split_kernel(RowBwdArgs a) 
     const float mean = a.rms ? 0.0f : a.mean[row], rstd = a.rstd[row];
     const int64_t j0 = lane + int64_t(kWave) * T * w;
     float tv[T], gv[T];
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const int64_t j = j0 + kWave * t;
-      tv[t] = 0.0f;
-      gv[t] = 0.0f;
-      if (j < a.cols) {
-        const float d = x[j] - mean;
-        tv[t] = d * rstd;
-        gv[t] = a.gamma ? dy[j] * a.gamma[j] : dy[j];
-      }
-    }
+    ln_bwd_terms<T>(a, x, dy, j0, mean, rstd, tv, gv);
     float am = 0.0f;
     if (!a.rms) {  // uniform over the workgroup
       const float q = chain_across_waves(chain_g, lane, w, S, [&](float c) {
@@ -463,7 +483,7 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
   const int tid = threadIdx.x;
   const int nthr = R * kWave;
   const int lane = tid & (kWave - 1);
-  const int w = tid >> 6;
+  const int w = tid >> 6;  // (a wave-uniform index measured slower here for 2048-wide rows)
   const int64_t beta = blockIdx.x;
   const int64_t blk = nblk == 1 ? a.rows : p.k_block;
   const int64_t r0 = beta * blk;
@@ -482,8 +502,8 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
     pb[k] = 0.0f;
   }
   // Rows are software-pipelined (PF): the loads of a wave's next row are
-  // issued before the reductions, the barriers and the chain phase of this
-  // one.  The widest rows load at the top of each pass instead, to stay in
+  // issued after this row's dX stores, before the barriers and the chain
+  // phase.  The widest rows load at the top of each pass instead, to stay in
   // registers.
   float xv[T], dv[T];
   auto load_row = [&](int64_t row) {
@@ -523,7 +543,6 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
         }
         q = q + gv[t];
       }
-      if (PF && row + R < r1) load_row(row + R);
       const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
       float q2 = 0.0f;
 #pragma unroll
@@ -539,6 +558,7 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
           st_stream(dx + j, rstd * wv);
         }
       }
+      if (PF && row + R < r1) load_row(row + R);  // next row in flight through the barriers and chains
     }
     lds_only_barrier();
     const int nr = static_cast<int>(r1 - c0 < R ? r1 - c0 : R);
@@ -595,7 +615,7 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_ke
   __shared__ float st[RC * SW], sd[RC * SW];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int w = tid >> 6;
+  const int w = wave_id();
   int64_t beta;
   int g;
   const int64_t bid = blockIdx.x;
@@ -820,11 +840,11 @@ using FusedKernel = void (*)(RowBwdArgs, LnParamArgs, int, int64_t);
 // Kernels for R <= 16 waves (1024 threads) up to 768 columns; wider rows
 // take R <= 8 so that they keep their registers.
 FusedKernel pick_layernorm_fused(int64_t cols) {
-  if (cols <= kWave * 1) return layernorm_bwd_fused_kernel<1, 1024, true>;
-  if (cols <= kWave * 2) return layernorm_bwd_fused_kernel<2, 1024, true>;
-  if (cols <= kWave * 4) return layernorm_bwd_fused_kernel<4, 1024, true>;
-  if (cols <= kWave * 8) return layernorm_bwd_fused_kernel<8, 1024, true>;
-  if (cols <= kWave * 12) return layernorm_bwd_fused_kernel<12, 1024, true>;
+  if (cols <= kWave * 1) return layernorm_bwd_fused_kernel<1, 512, true>;
+  if (cols <= kWave * 2) return layernorm_bwd_fused_kernel<2, 512, true>;
+  if (cols <= kWave * 4) return layernorm_bwd_fused_kernel<4, 512, true>;
+  if (cols <= kWave * 8) return layernorm_bwd_fused_kernel<8, 512, true>;
+  if (cols <= kWave * 12) return layernorm_bwd_fused_kernel<12, 512, true>;
   if (cols <= kWave * 16) return layernorm_bwd_fused_kernel<16, 512, true>;
   return layernorm_bwd_fused_kernel<32, 512, false>;
 }
@@ -928,16 +948,14 @@ int64_t lds_budget_bytes() {
 
 int layernorm_fused_rows(int64_t rows, int64_t cols, int64_t k_block, int requested) {
   // R rows staged per pass: LDS holds 2 * R * cols floats; the chain phase
-  // needs R * 64 * kFusedChains >= cols; R * 64 within the kernel's bound.
-  // Without a request: 16 rows per pass while there are fewer row blocks
-  // than two per compute unit, else 8 (smaller workgroups, more of them
-  // resident per compute unit).
+  // needs R * 64 * kFusedChains >= cols; R <= 8 (512 threads, which leaves
+  // each wave the registers for its row and the next one in flight).
+  // Without a request: 8.
   const int64_t c = cols > 0 ? cols : 1;
   const int64_t fit = lds_budget_bytes() / (8 * c);
-  const int64_t rmax = c <= kWave * 12 ? 16 : 8;
+  const int64_t rmax = 8;
   const int64_t rmin = (c + kWave * kFusedChains - 1) / (kWave * kFusedChains);
   int64_t r = fit < rmax ? fit : rmax;
-  if (requested <= 0 && layernorm_param_blocks(rows, k_block) >= 512) requested = 8;
   if (requested > 0 && requested < r) r = requested;
   if (r < rmin) r = rmin;
   if (r > fit || r > rmax) return 0;  // does not fit: use the unfused kernels
