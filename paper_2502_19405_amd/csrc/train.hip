@@ -326,6 +326,20 @@ __global__ __launch_bounds__(64) void layernorm_bwd_generic_kernel(RowBwdArgs a)
 // LayerNorm parameter gradients.
 // ---------------------------------------------------------------------------
 
+// Workspace layout of the block partials: for each of the two arrays (dgamma,
+// then dbeta), the columns in tiles of kTile (the last one narrower), each
+// tile stored block-major ([block][column in tile]).  All partials of one
+// tile are one contiguous span, which the combine reads whole; the total is
+// 2 * blocks * cols floats.
+constexpr int kTile = 16;
+
+__device__ __forceinline__ int64_t ws_index(int arr, int64_t b, int64_t j, int64_t nblk,
+                                            int64_t cols) {
+  const int64_t t0 = j & ~int64_t(kTile - 1);
+  const int64_t tw = cols - t0 < kTile ? cols - t0 : kTile;
+  return (arr * cols + t0) * nblk + b * tw + (j - t0);
+}
+
 constexpr int kParamThreads = 256;
 
 __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
@@ -378,61 +392,71 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
     if (a.dgamma) a.dgamma[j] = pg;
     if (a.dbeta) a.dbeta[j] = pb;
   } else {
-    a.ws[beta * a.cols + j] = pg;
-    a.ws[(nblk + beta) * a.cols + j] = pb;
+    a.ws[ws_index(0, beta, j, nblk, a.cols)] = pg;
+    a.ws[ws_index(1, beta, j, nblk, a.cols)] = pb;
   }
 }
 
 // Left-to-right sum of the block partials, per column.  The chains are long
 // (one add per row block) and each add depends on the previous one, so the
-// operands must be at hand: a workgroup owns kCombCols columns, stages up to
-// kCombChunk blocks of both partial arrays in LDS chain-major ([chain][block],
-// rows padded so that 16-byte reads stay aligned and spread over the banks),
-// and then one lane per chain reads four consecutive partials per LDS read
-// and adds them in block order.  Chains past the last block are padded with
-// +0, which leaves a chain that started at +0 unchanged.
-constexpr int kCombThreads = 256;
-constexpr int kCombChunk = 1024;  // blocks per LDS pass
+// operands must be at hand: a workgroup owns COLS columns of one tile, all
+// its threads copy their partials for up to kCombChunk blocks (both arrays)
+// into LDS chain-major ([chain][block], rows padded so that 16-byte reads stay
+// aligned and spread over the banks), and then one lane per chain reads four
+// consecutive partials per LDS read and adds them in block order.  Chains past
+// the last block are padded with +0, which leaves a chain that started at +0
+// unchanged.  Whole tiles (COLS = kTile) read contiguous spans; with many
+// blocks quarter tiles (COLS = 4) put four times as many workgroups on the
+// loads, which bound the time there.
+constexpr int kCombChunk = 960;  // blocks per LDS pass: a multiple of 64 (pitch = 4 mod 64)
 
-// COLS columns per workgroup: few row blocks favour wide workgroups (fewer
-// of them), many blocks narrow ones (more loads in flight per chain).
-template <int COLS>
-__global__ __launch_bounds__(kCombThreads) void layernorm_param_combine_kernel(LnParamArgs a,
-                                                                            int64_t nblk,
-                                                                            int pitch) {
+template <int COLS, int NT, int MAXCHUNK>
+__global__ __launch_bounds__(NT) void layernorm_param_combine_kernel(LnParamArgs a, int64_t nblk,
+                                                                     int pitch) {
   constexpr int kChains = 2 * COLS;  // dgamma and dbeta of each column
-  extern __shared__ float buf[];     // [kChains][pitch]
+  // loads in flight per thread: a pass of MAXCHUNK blocks in one batch
+  constexpr int kBatch = (2 * MAXCHUNK * COLS + NT - 1) / NT;
+  static_assert(kTile % COLS == 0, "a workgroup's columns lie in one tile");
+  extern __shared__ float buf[];  // [kChains][pitch]
   const int tid = threadIdx.x;
-  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * COLS;
+  constexpr int kSub = kTile / COLS;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x / kSub) * kTile;
+  const int c0 = static_cast<int>(blockIdx.x % kSub) * COLS;  // first column within the tile
+  const int tw = static_cast<int>(a.cols - t0 < kTile ? a.cols - t0 : kTile);
   const int chunk = pitch - 4;  // blocks per pass (a multiple of 4)
   float acc = 0.0f;             // thread ch < kChains: chain ch
   const int ch = tid;
   for (int64_t b0 = 0; b0 < nblk; b0 += chunk) {
     const int nb = static_cast<int>(nblk - b0 < chunk ? nblk - b0 : chunk);
     const int nb4 = (nb + 3) & ~3;
-    // stage: thread (k, b1) loads chain k's blocks b1, b1 + R, ... (R block
-    // rows per pass), kBatch loads in flight per thread; consecutive threads
-    // take consecutive columns
-    {
-      constexpr int kRowsPerPass = kCombThreads / kChains;
-      constexpr int kBatch = 32;
-      const int k = tid % kChains, b1 = tid / kChains;
-      const int arr = k / COLS, c = k % COLS;
-      const bool col_ok = j0 + c < a.cols;
-      const float* src = a.ws + (arr * nblk + b0) * a.cols + j0 + c;
-      for (int base = 0; base < nb4; base += kRowsPerPass * kBatch) {
-        float v[kBatch];
+    // stage: element e of one array's share is (block e / COLS, column
+    // c0 + e % COLS); consecutive threads read consecutive columns.
+    const int span = nb * COLS;
+    for (int base = 0; base < 2 * span; base += NT * kBatch) {
+      float v[kBatch];
 #pragma unroll
-        for (int r = 0; r < kBatch; ++r) {
-          const int b = base + b1 + r * kRowsPerPass;
-          v[r] = (b < nb && col_ok) ? src[static_cast<int64_t>(b) * a.cols] : 0.0f;
-        }
+      for (int r = 0; r < kBatch; ++r) {
+        const int e2 = base + r * NT + tid;
+        const int arr = e2 >= span;
+        const int e = e2 - arr * span;
+        const int b = e / COLS, c = c0 + e % COLS;
+        v[r] = 0.0f;
+        if (e2 < 2 * span && c < tw) v[r] = a.ws[(arr * a.cols + t0) * nblk + (b0 + b) * tw + c];
+      }
 #pragma unroll
-        for (int r = 0; r < kBatch; ++r) {
-          const int b = base + b1 + r * kRowsPerPass;
-          if (b < nb4) buf[k * pitch + b] = v[r];
+      for (int r = 0; r < kBatch; ++r) {
+        const int e2 = base + r * NT + tid;
+        if (e2 < 2 * span) {
+          const int arr = e2 >= span;
+          const int e = e2 - arr * span;
+          buf[(arr * COLS + e % COLS) * pitch + e / COLS] = v[r];
         }
       }
+    }
+    // +0 past the last block of the pass, up to the next multiple of 4
+    if (tid < kChains * 4) {
+      const int b = nb + (tid & 3);
+      if (b < nb4) buf[(tid >> 2) * pitch + b] = 0.0f;
     }
     __syncthreads();
     if (ch < kChains) {
@@ -449,12 +473,12 @@ __global__ __launch_bounds__(kCombThreads) void layernorm_param_combine_kernel(L
     __syncthreads();
   }
   if (ch < kChains) {
-    const int arr = ch / COLS, c = ch % COLS;
-    if (j0 + c < a.cols) {
+    const int arr = ch / COLS, c = c0 + ch % COLS;
+    if (c < tw) {
       if (arr == 0) {
-        if (a.dgamma) a.dgamma[j0 + c] = acc;
+        if (a.dgamma) a.dgamma[t0 + c] = acc;
       } else {
-        if (a.dbeta) a.dbeta[j0 + c] = acc;
+        if (a.dbeta) a.dbeta[t0 + c] = acc;
       }
     }
   }
@@ -583,8 +607,8 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
         if (p.dgamma) p.dgamma[j] = pg[k];
         if (p.dbeta) p.dbeta[j] = pb[k];
       } else {
-        p.ws[beta * cols + j] = pg[k];
-        p.ws[(nblk + beta) * cols + j] = pb[k];
+        p.ws[ws_index(0, beta, j, nblk, cols)] = pg[k];
+        p.ws[ws_index(1, beta, j, nblk, cols)] = pb[k];
       }
     }
   }
@@ -692,8 +716,8 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_ke
       if (p.dgamma) p.dgamma[j] = pg;
       if (p.dbeta) p.dbeta[j] = pb;
     } else {
-      p.ws[beta * a.cols + j] = pg;
-      p.ws[(nblk + beta) * a.cols + j] = pb;
+      p.ws[ws_index(0, beta, j, nblk, a.cols)] = pg;
+      p.ws[ws_index(1, beta, j, nblk, a.cols)] = pb;
     }
   }
 }
@@ -911,17 +935,19 @@ int64_t layernorm_param_grid(int64_t rows, int64_t cols, int64_t k_block) {
 }
 
 hipError_t launch_layernorm_param_combine(const LnParamArgs& a, int64_t nblk, hipStream_t s) {
-  const int cols_per_group = nblk <= 256 ? 16 : 4;
-  const int64_t groups = (a.cols + cols_per_group - 1) / cols_per_group;
+  const int64_t tiles = (a.cols + kTile - 1) / kTile;
   const int64_t chunk = nblk < kCombChunk ? (nblk + 3) & ~int64_t(3) : kCombChunk;
   const int pitch = static_cast<int>(chunk) + 4;
-  const size_t lds = sizeof(float) * 2 * cols_per_group * static_cast<size_t>(pitch);
-  if (cols_per_group == 16)
-    hipLaunchKernelGGL(layernorm_param_combine_kernel<16>, dim3(static_cast<unsigned>(groups)),
-                       dim3(kCombThreads), lds, s, a, nblk, pitch);
-  else
-    hipLaunchKernelGGL(layernorm_param_combine_kernel<4>, dim3(static_cast<unsigned>(groups)),
-                       dim3(kCombThreads), lds, s, a, nblk, pitch);
+  if (nblk <= 256) {  // whole tiles
+    const size_t lds = sizeof(float) * 2 * kTile * static_cast<size_t>(pitch);
+    hipLaunchKernelGGL((layernorm_param_combine_kernel<kTile, 512, 256>),
+                       dim3(static_cast<unsigned>(tiles)), dim3(512), lds, s, a, nblk, pitch);
+  } else {  // quarter tiles
+    const size_t lds = sizeof(float) * 2 * 4 * static_cast<size_t>(pitch);
+    hipLaunchKernelGGL((layernorm_param_combine_kernel<4, 256, kCombChunk>),
+                       dim3(static_cast<unsigned>(tiles * (kTile / 4))), dim3(256), lds, s, a, nblk,
+                       pitch);
+  }
   return hipGetLastError();
 }
 

@@ -33,7 +33,8 @@ hipError_t launch_softmax_bwd_split(const RowBwdArgs& a, int S, hipStream_t s);
 hipError_t launch_layernorm_bwd_split(const RowBwdArgs& a, int S, hipStream_t s);
 
 // LayerNorm parameter gradients over rows, blocks of k_block rows (0 = one
-// block).  ws holds 2 * blocks * cols floats when there is more than one block.
+// block).  ws holds 2 * blocks * cols floats when there is more than one block
+// (block partials in column tiles, each tile block-major).
 struct LnParamArgs {
   int64_t rows, cols, k_block;
   const float* X; int64_t ldx;
