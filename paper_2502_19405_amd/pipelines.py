@@ -130,17 +130,30 @@ def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps
     mean, rstd = buf("mean", t), buf("rstd", t)
     Y = repops.layernorm_rows(H2, gamma, beta, eps=ln_eps, order=order, out=buf("Y", t, h),
                               mean_out=mean, rstd_out=rstd)
-    # backward
+    # backward.  Each layer's weight and bias gradients do not feed the input
+    # gradient, so they run on a second stream beside it: the weight-gradient
+    # products have few output tiles (hidden x ffn) and leave compute units
+    # free that the input-gradient chain fills.  Every call is deterministic
+    # and writes its own outputs, so the overlap changes no bit.
+    main = torch.cuda.current_stream(dev)
+    if "_side" not in b:
+        b["_side"] = torch.cuda.Stream(device=dev)  # default priority
+    side = b["_side"]
     dH2, _, _ = repops.layernorm_backward_rows(H2, dY, mean, rstd, gamma, order=order,
                                                dx_out=buf("dH2", t, h), dgamma_out=ggamma,
                                                dbeta_out=gbeta)
-    repops.matmul(G.t(), dH2, order=order, launch=gemm_launch, out=gW2)
-    repops.colsum_rows(dH2, order=order, out=gb2)
+    side.wait_stream(main)
+    with torch.cuda.stream(side):
+        repops.matmul(G.t(), dH2, order=order, launch=gemm_launch, out=gW2)
+        repops.colsum_rows(dH2, order=order, out=gb2)
     dG = repops.matmul(dH2, W2.t(), order=order, launch=gemm_launch, out=buf("dG", t, f))
     dH1 = repops.gelu_backward(H1, dG, order=order, out=dG)
-    repops.matmul(X.t(), dH1, order=order, launch=gemm_launch, out=gW1)
-    repops.colsum_rows(dH1, order=order, out=gb1)
+    side.wait_stream(main)
+    with torch.cuda.stream(side):
+        repops.matmul(X.t(), dH1, order=order, launch=gemm_launch, out=gW1)
+        repops.colsum_rows(dH1, order=order, out=gb1)
     dX = repops.matmul(dH1, W1.t(), order=order, launch=gemm_launch, out=buf("dX", t, h))
+    main.wait_stream(side)
     # optimizer
     state.step += 1
     repops.adam_step(state.param, state.grad, state.exp_avg, state.exp_avg_sq, lr, betas[0],
