@@ -32,8 +32,13 @@ def gpu_commit(rp, buf_u8, chunk):
 @pytest.mark.parametrize("chunk", [64, 1024, 4096, 100])
 def test_commit_sizes(rp, chunk):
     g = inputs.rng(950 + chunk)
+    # leaf counts around the 256 leaves one workgroup reduces, and (64-byte
+    # chunks) more than 512 x 256 leaves, so a level launch runs as well
     sizes = [0, 1, 3, 63, 64, 65, chunk - 1, chunk, chunk + 1, 2 * chunk, 3 * chunk + 7,
-             513 * chunk, 512 * chunk, 1025 * chunk - 3, 5000 * chunk + 1]
+             255 * chunk, 256 * chunk, 257 * chunk + 5, 513 * chunk, 512 * chunk,
+             1025 * chunk - 3, 5000 * chunk + 1]
+    if chunk == 64:
+        sizes.append((512 * 256 + 300) * chunk + 9)
     for n in sizes:
         if n < 0:
             continue
