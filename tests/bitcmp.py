@@ -36,7 +36,7 @@ def assert_bits_equal(got, want, what="", nan_equal=True):
     bad = mismatches(got, want, nan_equal)
     if bad.size:
         i = bad[0]
-        idx = np.unravel_index(i, got.shape)
+        idx = tuple(int(x) for x in np.unravel_index(i, got.shape))
         d = ulp_distance(got.ravel()[bad], want.ravel()[bad])
         raise AssertionError(
             f"{what}: {bad.size} of {got.size} outputs differ; first at {idx}: "
