@@ -11,9 +11,12 @@
 // LayerNorm parameter gradients: for column j, dgamma_j = sum over rows i of
 // dy_ij * t_ij and dbeta_j = sum of dy_ij, with blocks of k_block consecutive
 // rows, each block a sequential chain from +0 (fma for dgamma, add for dbeta),
-// block partials added left to right.  One thread per (block, column) forms
-// the block partials -- every chain is independent, so the grid is as wide as
-// blocks x columns -- and a second kernel adds them left to right per column.
+// block partials added left to right.  The partials are formed in the same
+// pass as the input gradient (one workgroup per row block staging rows in
+// LDS, or, with few blocks, a block's rows and column slices spread over
+// several workgroups), or on their own with one thread per (block, column)
+// -- every chain is independent -- and a second kernel adds them left to
+// right per column.
 // With a single block the first kernel writes the gradients directly (the left
 // to right sum of one partial P is +0 + P = P, since a chain started at +0 is
 // never -0).
@@ -861,8 +864,8 @@ hipError_t launch_split_bwd(SplitBwdKernel k, const RowBwdArgs& a, int S, hipStr
 
 using FusedKernel = void (*)(RowBwdArgs, LnParamArgs, int, int64_t);
 
-// Kernels for R <= 16 waves (1024 threads) up to 768 columns; wider rows
-// take R <= 8 so that they keep their registers.
+// Kernels for R <= 8 waves (512 threads); the widest rows (32 values per
+// lane) load each row at the top of its pass instead of one pass ahead.
 FusedKernel pick_layernorm_fused(int64_t cols) {
   if (cols <= kWave * 1) return layernorm_bwd_fused_kernel<1, 512, true>;
   if (cols <= kWave * 2) return layernorm_bwd_fused_kernel<2, 512, true>;
