@@ -357,29 +357,33 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
   const float* dp = a.dY + j;
   float pg = 0.0f, pb = 0.0f;
   int64_t i = i0;
-  // Eight rows per step: the loads are independent of the chains and issue
-  // together; the chains themselves advance one row at a time.
-  if (a.sum_only) {  // bias gradient: dY's column chains only
-    for (; i + 8 <= i1; i += 8) {
-      float dv[8];
+  // Rows in batches whose loads all issue before any arithmetic (one memory
+  // round trip per batch); the chains themselves advance one row at a time.
+  if (a.sum_only) {  // bias gradient: dY's column chains only, 32 rows a batch
+    constexpr int RB = 32;
+    for (; i + RB <= i1; i += RB) {
+      float dv[RB];
 #pragma unroll
-      for (int r = 0; r < 8; ++r) dv[r] = dp[(i + r) * a.lddy];
+      for (int r = 0; r < RB; ++r) dv[r] = dp[(i + r) * a.lddy];
 #pragma unroll
-      for (int r = 0; r < 8; ++r) pb = pb + dv[r];
+      for (int r = 0; r < RB; ++r) pb = pb + dv[r];
     }
     for (; i < i1; ++i) pb = pb + dp[i * a.lddy];
   }
-  for (; i + 8 <= i1; i += 8) {
-    float xv[8], dv[8];
+  constexpr int RB = 16;
+  for (; i + RB <= i1; i += RB) {
+    float xv[RB], dv[RB], mv[RB], rv[RB];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
+    for (int r = 0; r < RB; ++r) {
       xv[r] = xp[(i + r) * a.ldx];
       dv[r] = dp[(i + r) * a.lddy];
+      mv[r] = a.rms ? 0.0f : a.mean[i + r];
+      rv[r] = a.rstd[i + r];
     }
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const float d = xv[r] - (a.rms ? 0.0f : a.mean[i + r]);
-      const float t = d * a.rstd[i + r];
+    for (int r = 0; r < RB; ++r) {
+      const float d = xv[r] - mv[r];
+      const float t = d * rv[r];
       pg = __builtin_fmaf(dv[r], t, pg);
       pb = pb + dv[r];
     }
