@@ -147,12 +147,14 @@ def _rate(ms, nbytes=None, flops=None):
     return out
 
 
-def secondary(repops, steps):
+def secondary(repops, steps, streaming_only=False):
     """The other workloads, each timed with HIP events after warmup:
     row reductions and elementwise ops in GB/s of algorithmic bytes (each
     element read once and written once; causal softmax reads only the
     unmasked part), GEMM-shaped steps and the model-shaped pipelines in
-    TFLOP/s of 2*M*N*K."""
+    TFLOP/s of 2*M*N*K.  streaming_only keeps the bandwidth-bound operators
+    and the two copies, every call launched eagerly on one stream (no graph
+    replays, no GEMMs): the set the HBM byte counters are taken over."""
     import numpy as np
     import torch
     from paper_2502_19405_amd import inputs, pipelines
@@ -163,17 +165,17 @@ def secondary(repops, steps):
     g = inputs.rng(4)
 
     # 256^3 GEMM and 256 x 256 softmax (launch-bound sizes)
-    d = inputs.gemm256_softmax256()
-    A, B, S = t(d["A"]), t(d["B"]), t(d["S"])
-    C, P = torch.empty_like(A), torch.empty_like(S)
-    out["gemm_256"] = _rate(event_time_ms(lambda: repops.matmul(A, B, out=C), steps * 5),
-                            flops=2 * 256 ** 3)
-    out["gemm_256"].update(_graph_rate(graph_time_ms(lambda: repops.matmul(A, B, out=C)),
-                                       flops=2 * 256 ** 3))
-    out["softmax_256x256"] = _rate(event_time_ms(lambda: repops.softmax_rows(S, out=P), steps * 5),
-                                   nbytes=8 * 256 * 256)
-    out["softmax_256x256"].update(_graph_rate(graph_time_ms(lambda: repops.softmax_rows(S, out=P)),
-                                              nbytes=8 * 256 * 256))
+    d = {} if streaming_only else inputs.gemm256_softmax256()
+    if not streaming_only:
+        A, B, S = t(d["A"]), t(d["B"]), t(d["S"])
+        C, P = torch.empty_like(A), torch.empty_like(S)
+        out["gemm_256"] = _rate(event_time_ms(lambda: repops.matmul(A, B, out=C), steps * 5),
+                                flops=2 * 256 ** 3)
+        out["gemm_256"].update(_graph_rate(graph_time_ms(lambda: repops.matmul(A, B, out=C)),
+                                           flops=2 * 256 ** 3))
+        sm = lambda: repops.softmax_rows(S, out=P)  # noqa: E731
+        out["softmax_256x256"] = _rate(event_time_ms(sm, steps * 5), nbytes=8 * 256 * 256)
+        out["softmax_256x256"].update(_graph_rate(graph_time_ms(sm), nbytes=8 * 256 * 256))
 
     # causal softmax, Llama attention scores: 4 x 32 heads x 1024 rows of 1024
     T, rows = 1024, 4 * 32 * 1024
@@ -213,7 +215,7 @@ def secondary(repops, steps):
         Y = torch.empty_like(Z)
         ms = event_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y), steps)
         out[name] = _rate(ms, nbytes=4 * Z.numel() * 2)
-        if shape[0] == 4096:  # launch-bound: also without host launch gaps
+        if shape[0] == 4096 and not streaming_only:  # launch-bound: also without launch gaps
             out[name].update(_graph_rate(
                 graph_time_ms(lambda: repops.layernorm_rows(Z, gam, bet, out=Y)),
                 nbytes=4 * Z.numel() * 2))
@@ -232,7 +234,7 @@ def secondary(repops, steps):
         call = lambda: repops.layernorm_backward_rows(  # noqa: E731
             Z, dZ, mean, rstd, gam, dx_out=dX, dgamma_out=dg, dbeta_out=db, workspace=ws)
         out[name] = _rate(event_time_ms(call, steps), nbytes=4 * Z.numel() * 3)
-        if shape[0] == 4096:
+        if shape[0] == 4096 and not streaming_only:
             out[name].update(_graph_rate(graph_time_ms(call), nbytes=4 * Z.numel() * 3))
         del Z, dZ, dX, ws
     H = t(inputs.normal(g, (4096, 3072), var=0.31))
@@ -303,6 +305,19 @@ def secondary(repops, steps):
     out["commit_4096x14336"] = _rate(ms, nbytes=Wc.numel() * 4)
     del Wc, wsc
 
+    # streaming ceilings: a device-to-device copy of 512 MiB by torch's copy kernel
+    src = torch.empty(1 << 27, device=dev)
+    dst = torch.empty_like(src)
+    ms = event_time_ms(lambda: dst.copy_(src), steps)
+    out["copy_ceiling_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
+    # The library's own elementwise kernel with no arithmetic: the streaming
+    # rate the bandwidth-bound operators can reach.
+    ms = event_time_ms(lambda: repops.copy(src, out=dst), steps)
+    out["copy_repops_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
+    del src, dst
+    if streaming_only:
+        return out
+
     # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
     ms = event_time_ms(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet), steps)
@@ -353,16 +368,6 @@ def secondary(repops, steps):
     out["llama_dW_rank_share_4096x14336x1024"] = _rate(ms, flops=2 * 4096 * 14336 * 1024)
     del X, dY, W, gx, gw
 
-    # streaming ceilings: a device-to-device copy of 512 MiB by torch's copy kernel
-    src = torch.empty(1 << 27, device=dev)
-    dst = torch.empty_like(src)
-    ms = event_time_ms(lambda: dst.copy_(src), steps)
-    out["copy_ceiling_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
-    # The library's own elementwise kernel with no arithmetic: the streaming
-    # rate the bandwidth-bound operators can reach.
-    ms = event_time_ms(lambda: repops.copy(src, out=dst), steps)
-    out["copy_repops_512MiB"] = _rate(ms, nbytes=2 * 4 * src.numel())
-    del src, dst
     return out
 
 
@@ -377,6 +382,9 @@ def main():
                     help="auto | simple | tiled:I | mfma:I (mfma:0 is what auto picks here)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--streaming-only", action="store_true",
+                    help="secondary workloads: only the bandwidth-bound operators and copies, "
+                         "launched eagerly (for HBM byte counters)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -452,7 +460,7 @@ def main():
         torch.cuda.synchronize()
         result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_secondary:
-        result["secondary"] = secondary(repops, 20)
+        result["secondary"] = secondary(repops, 20, args.streaming_only)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(d, 2.0 * N * K)
     print(json.dumps(result), flush=True)

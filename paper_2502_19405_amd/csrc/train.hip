@@ -622,20 +622,93 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
 }
 
 // ---------------------------------------------------------------------------
-// LayerNorm backward, fused, for few row blocks: the G workgroups of a block
-// share its work.  Workgroup (beta, g) computes dX for its share of the
-// block's rows (whole rows, one wave each, as the wave kernel does) and the
-// chains of its column slice over all of the block's rows: chunks of rows are
-// loaded by all waves (t formed on the way) into LDS and one thread per
-// column advances its two chains through each chunk in row order, while the
-// next chunk's loads are in flight.  Every row is read twice (whole for dX,
-// by slices for the chains); the G workgroups of a block are placed on one
-// XCD so the second read finds the rows in that XCD's L2.  The rows are read
-// by workgroups other than the one writing their dX, so dX may not take the
-// place of X or dY here.
+// LayerNorm backward, fused, for few row blocks or rows too wide for the
+// one-workgroup-per-block kernel: the G workgroups of a block share its work.
+// Workgroup (beta, g) computes dX for its share of the block's rows (whole
+// rows, one wave each as the wave kernel does, or a group of waves each for
+// the widest) and the chains of its column slice over all of the block's
+// rows: chunks of rows are loaded by all waves (t formed on the way) into LDS
+// and one thread per column advances its two chains through each chunk in
+// row order, while the next chunk's loads are in flight.  Every row is read
+// twice (whole for dX, by slices for the chains); the G workgroups of a block
+// are placed on one XCD so the second read can find the rows in that XCD's L2
+// (with 4096-wide rows a 64-row block is 2 MB, and part of the second read
+// comes from further out).  The rows are read by workgroups other than the
+// one writing their dX, so dX may not take the place of X or dY here.
 // ---------------------------------------------------------------------------
 
 constexpr int kSplitWaves = 8;
+
+// dX of rows [d0, d1) by the kSplitWaves waves of a workgroup, S waves per
+// row and kSplitWaves / S rows at a time: wave h of a group (h < S) holds the
+// columns lane + 64 * (h * T + t), and each lane's chains pass from wave to
+// wave of the group in order through LDS, so the terms meet in the one-wave
+// order and the results are the same bits.  Every wave takes part in every
+// step (the steps hold workgroup barriers); a group past d1 works on row d0
+// and stores nothing.
+template <int T, int S>
+__device__ __forceinline__ void layernorm_bwd_rows_grouped(const RowBwdArgs& a, int64_t d0,
+                                                           int64_t d1, int lane, int w) {
+  constexpr int P = kSplitWaves / S;
+  __shared__ float chain_g[P * kWave], chain_gt[P * kWave];
+  const int h = w % S;
+  const int slot = (w / S) * kWave + lane;
+  const float n = static_cast<float>(a.cols);
+  auto group_chain = [&](float* ch, auto step) {
+#pragma unroll
+    for (int k = 0; k < S; ++k) {
+      if (h == k) ch[slot] = step(k > 0 ? ch[slot] : 0.0f);
+      __syncthreads();
+    }
+    return ch[slot];
+  };
+  for (int64_t base = d0; base < d1; base += P) {
+    const int64_t row = base + w / S;
+    const bool live = row < d1;
+    const int64_t rr = live ? row : d0;
+    const float* x = a.Y + rr * a.ldy;
+    const float* dy = a.dY + rr * a.lddy;
+    const float mean = a.rms ? 0.0f : a.mean[rr], rstd = a.rstd[rr];
+    const int64_t j0 = lane + int64_t(kWave) * T * h;
+    float tv[T], gv[T];
+    ln_bwd_terms<T>(a, x, dy, j0, mean, rstd, tv, gv);
+    float am = 0.0f;
+    if (!a.rms) {  // uniform over the workgroup
+      const float q = group_chain(chain_g, [&](float c) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) c = c + gv[t];  // past the row: +0
+        return c;
+      });
+      am = wave_tree_sum(q) / n;
+    }
+    const float q2 = group_chain(chain_gt, [&](float c) {
+#pragma unroll
+      for (int t = 0; t < T; ++t) c = __builtin_fmaf(gv[t], tv[t], c);
+      return c;
+    });
+    const float bm = wave_tree_sum(q2) / n;
+    if (live) {
+      float* dx = a.dX + row * a.lddx;
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int64_t j = j0 + kWave * t;
+        if (j < a.cols) {
+          const float u = gv[t] - am;
+          const float tb = tv[t] * bm;
+          st_stream(dx + j, rstd * (u - tb));
+        }
+      }
+    }
+    __syncthreads();  // chains read before the next rows
+  }
+}
+
+// The column-split kernel's dX rows: one wave per row up to 32 values per
+// lane; wider rows (up to 64 values per lane) shared by four waves of 16
+// values each, which leaves the registers for two workgroups per compute unit
+// (measured faster than one wave of 64 or two of 32; for 32 values per lane
+// one wave measured faster than two of 16).
+constexpr int kColsplitGroupT = 16;
 
 template <int T, int SWU>
 __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_kernel(
@@ -683,11 +756,18 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_ke
   };
   load_chunk(r0);
 
-  // dX for rows [d0, d1) of the block, one wave per row.
+  // dX for rows [d0, d1) of the block: one wave per row, or for wide rows a
+  // group of waves per row.
   const int64_t per = (r1 - r0 + G - 1) / G;
   const int64_t d0 = r0 + g * per;
   const int64_t d1 = (d0 + per < r1) ? d0 + per : r1;
-  for (int64_t row = d0 + w; row < d1; row += kSplitWaves) layernorm_bwd_row<T>(a, row, lane);
+  if constexpr (T > 32) {
+    static_assert(T % kColsplitGroupT == 0 && kSplitWaves % (T / kColsplitGroupT) == 0,
+                  "row groups must tile the workgroup");
+    layernorm_bwd_rows_grouped<kColsplitGroupT, T / kColsplitGroupT>(a, d0, d1, lane, w);
+  } else {
+    for (int64_t row = d0 + w; row < d1; row += kSplitWaves) layernorm_bwd_row<T>(a, row, lane);
+  }
 
   float pg = 0.0f, pb = 0.0f;
   for (int64_t i0 = r0; i0 < r1; i0 += RC) {
@@ -1015,15 +1095,18 @@ ColsplitKernel pick_colsplit_t(int64_t cols) {
   if (cols <= kWave * 4) return layernorm_bwd_colsplit_kernel<4, SWU>;
   if (cols <= kWave * 8) return layernorm_bwd_colsplit_kernel<8, SWU>;
   if (cols <= kWave * 12) return layernorm_bwd_colsplit_kernel<12, SWU>;
-  return layernorm_bwd_colsplit_kernel<16, SWU>;
+  if (cols <= kWave * 16) return layernorm_bwd_colsplit_kernel<16, SWU>;
+  if (cols <= kWave * 32) return layernorm_bwd_colsplit_kernel<32, SWU>;
+  return layernorm_bwd_colsplit_kernel<64, SWU>;
 }
 
 bool layernorm_colsplit_plan(int64_t rows, int64_t cols, int64_t k_block, ColsplitPlan* pl) {
-  // Few row blocks (fewer than one per compute unit) and rows a wave holds
-  // in registers; about 512 workgroups, slices of 16 to 256 columns.
-  if (rows < 1 || cols < 1 || cols > kWave * 16 || k_block < 1) return false;
+  // Rows a wave holds in registers, and few row blocks (fewer than one per
+  // compute unit) or rows too wide for the one-workgroup-per-block kernel's
+  // LDS stage; about 512 workgroups, slices of 16 to 256 columns.
+  if (rows < 1 || cols < 1 || cols > kWave * kMaxPerLane || k_block < 1) return false;
   const int64_t nblk = layernorm_param_blocks(rows, k_block);
-  if (nblk >= 256) return false;
+  if (nblk >= 256 && layernorm_fused_rows(rows, cols, k_block, 0) >= 1) return false;
   int64_t g0 = (512 + nblk - 1) / nblk;
   const int64_t gcol = (cols + kWave - 1) / kWave;
   if (g0 > gcol) g0 = gcol;

@@ -228,13 +228,18 @@ def test_layernorm_backward_distilbert_shape(rp):
 # Row-block counts on both sides of 256: with fewer, the automatic launch
 # spreads each block's rows and columns over several workgroups (block counts
 # with and without a multiple of 8, k_block 1 and k_block past the last row);
-# with more, one workgroup per block stages rows in LDS.  RMSNorm, and an
-# explicit wave launch on the same inputs.
+# with more, one workgroup per block stages rows in LDS, unless the rows are
+# too wide for its stage (over 2048 columns), when the blocks are spread as
+# with few.  Rows over 2048 columns take a pair of waves per row.  RMSNorm, and
+# an explicit wave launch on the same inputs.
 @pytest.mark.parametrize("rows,cols,k_block", [(512, 1024, 64), (1000, 96, 16), (2048, 300, 128),
                                                (130, 1000, 1), (777, 64, 4096), (4096, 17, 64),
                                                (8 * 64, 768, 64), (255 * 16 - 3, 200, 16),
                                                (110 * 64 - 5, 768, 64), (300, 200, 1),
-                                               (256 * 16 + 5, 96, 16), (256 * 64, 768, 64)])
+                                               (256 * 16 + 5, 96, 16), (256 * 64, 768, 64),
+                                               (4096, 2048, 64), (1000, 3000, 16),
+                                               (4096, 4096, 64), (258 * 16 - 5, 2100, 16),
+                                               (70, 4096, 4096)])
 def test_layernorm_backward_row_block_counts(rp, rows, cols, k_block):
     X, dY, mean, rstd, gamma = ln_case(rows + cols + k_block, rows, cols)
     order = rp.Order(k_block=k_block)
