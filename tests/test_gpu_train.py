@@ -206,6 +206,31 @@ def test_layernorm_backward_in_place_workspace_and_partial_requests(rp):
     assert_bits_equal(host(db), want[2], "params only dbeta")
 
 
+@pytest.mark.parametrize("cols", [1500, 2048, 3000, 4096])
+def test_layernorm_backward_in_place_wide_rows(rp, cols):
+    """Wide rows in place: the multi-workgroup kernel (other workgroups read
+    the rows dX replaces) must not be taken; the parameter gradients come
+    first, then dX over X or dY.  LayerNorm and RMSNorm, 3 and 70 row blocks."""
+    for rows in (150, 4470):
+        X, dY, mean, rstd, gamma = ln_case(cols + rows, rows, cols)
+        want = oracle.layernorm_backward_rows(X, dY, mean, rstd, gamma)
+        for which in ("dY", "X"):
+            announce("layernorm_backward in place wide", rows, cols, which)
+            x, d = dev(X), dev(dY)
+            dx, dg, db = rp.layernorm_backward_rows(x, d, dev(mean), dev(rstd), dev(gamma),
+                                                    dx_out=d if which == "dY" else x)
+            assert_bits_equal(host(dx), want[0], f"dX = {which} {rows}x{cols}")
+            assert_bits_equal(host(dg), want[1], f"dgamma, dX = {which} {rows}x{cols}")
+            assert_bits_equal(host(db), want[2], f"dbeta, dX = {which} {rows}x{cols}")
+        _, rstd2 = oracle.rmsnorm_rows(X, gamma, with_stats=True)
+        want = oracle.rmsnorm_backward_rows(X, dY, rstd2, gamma)
+        announce("rmsnorm_backward in place wide", rows, cols)
+        d = dev(dY)
+        dx, dg = rp.rmsnorm_backward_rows(dev(X), d, dev(rstd2), dev(gamma), dx_out=d)
+        assert_bits_equal(host(dx), want[0], f"rms dX = dY {rows}x{cols}")
+        assert_bits_equal(host(dg), want[1], f"rms dgamma, dX = dY {rows}x{cols}")
+
+
 def test_layernorm_backward_no_rows_gives_zero_parameter_gradients(rp):
     import torch
     announce("layernorm_backward rows=0")
