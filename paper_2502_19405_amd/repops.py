@@ -201,16 +201,21 @@ def _mat(t: torch.Tensor, name: str):
 
 
 _STRUCTS: dict = {}
+_DEFAULT_REF: list = []  # the default descriptor's reference, once built
 
 
 def _ord(order):
     """ctypes reference to the descriptor struct of `order` (default if None),
     built once per distinct descriptor."""
+    if order is None and _DEFAULT_REF:
+        return _DEFAULT_REF[0]
     o = order or _DEFAULT_ORDER
     r = _STRUCTS.get(o)
     if r is None:
         c = o.c()
         r = _STRUCTS[o] = (c, ctypes.byref(c))
+    if order is None:
+        _DEFAULT_REF.append(r[1])
     return r[1]
 
 
@@ -292,9 +297,10 @@ def bmm(A: torch.Tensor, B: torch.Tensor, alpha: float = 1.0, order: Order | Non
 
 
 def _rows(X: torch.Tensor, name: str):
-    if X.dim() != 2 or X.stride(1) != 1:
+    sh, st = X.shape, X.stride()
+    if len(sh) != 2 or st[1] != 1:
         raise ValueError(f"{name} must be a 2-D tensor with unit column stride")
-    return X.shape[0], X.shape[1], max(X.stride(0), X.shape[1], 1)
+    return sh[0], sh[1], max(st[0], sh[1], 1)
 
 
 def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = None,
