@@ -296,7 +296,8 @@ def secondary(repops, steps, streaming_only=False):
 
     # tensor commitment (SHA-256 Merkle tree, 1 KiB leaves) of a Llama-8B
     # feed-forward weight, 4096 x 14336 fp32: bytes read once; SHA-256 is
-    # integer-ALU bound (about 22.5 VALU instructions per byte)
+    # integer VALU work (about 30 instructions per byte with the tree levels),
+    # bound by the latency of each lane's dependent block chain
     Wc = t(inputs.normal(g, (4096, 14336), var=4e-4))
     dig = torch.empty(32, dtype=torch.uint8, device=dev)
     wsc = torch.empty(repops.commit_workspace(Wc.numel() * 4, 1024) // 4 + 1, dtype=torch.int32,
