@@ -1,0 +1,51 @@
+"""bench.py's host logic (CPU): the one-GPU refusal, launch-string parsing and
+the lookup of the headline kernel's HBM traffic from its counter summary."""
+import importlib.util
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    spec = importlib.util.spec_from_file_location("bench", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+@pytest.mark.parametrize("argv,env", [(["--gpus", "2"], {}), (["--gpus", "8"], {}),
+                                      ([], {"WORLD_SIZE": "2"})])
+def test_more_than_one_gpu_is_refused(argv, env):
+    e = dict(os.environ, **env)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv],
+                       capture_output=True, text=True, env=e, timeout=120)
+    assert r.returncode == 2, r.stderr
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_launch_strings(bench):
+    from paper_2502_19405_amd import repops
+    assert bench.parse_launch("auto", repops) is None
+    assert bench.parse_launch("", repops) is None
+    assert bench.parse_launch("simple", repops).kind == repops.LAUNCH_GEMM_SIMPLE
+    t = bench.parse_launch("tiled:2", repops)
+    assert (t.kind, t.p[0]) == (repops.LAUNCH_GEMM_TILED, 2)
+    m = bench.parse_launch("mfma", repops)
+    assert (m.kind, m.p[0]) == (repops.LAUNCH_GEMM_MFMA, 0)
+
+
+def test_traffic_comes_only_from_a_matching_counter_summary(bench, tmp_path, monkeypatch):
+    # The committed summary covers the committed kernel sources.
+    v = bench.measured_traffic("mfma:0")
+    assert v is not None and v > 50.3e6, v  # at least the algorithmic bytes
+    assert bench.measured_traffic("mfma:1") is None  # another kernel: no figure
+    # A source that differs from the one the counters were taken on voids it.
+    src = tmp_path / "gemm_mfma.hip"
+    src.write_bytes(open(bench.KERNEL_SOURCES[0], "rb").read() + b"\n")
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", [str(src), bench.KERNEL_SOURCES[1]])
+    assert bench.measured_traffic("mfma:0") is None
