@@ -180,7 +180,7 @@ repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch
                                 int64_t cols, uint32_t* kind, int* wpb,
                                 int64_t wave_max = repops::rows_wave_max_cols(),
                                 int* split = nullptr, int64_t (*split_max)(int) = nullptr,
-                                int auto_per_lane = 16) {
+                                int auto_per_lane = 16, int64_t auto_wave_cols = 1024) {
   const bool wave_order =
       order->row_width == 64 && order->row_combine == REPOPS_ROW_STRIDED_TREE;
   const bool wave_fits = cols <= wave_max;
@@ -190,7 +190,7 @@ repops_status_t row_launch_kind(const repops_order_t* order, const repops_launch
     if (launch && !launch_params_zero_from(launch, 0)) return REPOPS_ERR_LAUNCH;
     *kind = (wave_order && wave_fits) ? REPOPS_LAUNCH_ROWS_WAVE : REPOPS_LAUNCH_ROWS_GENERIC;
     if (wave_order && split && split_max) {
-      const int S = repops::auto_row_split(cols, auto_per_lane);
+      const int S = repops::auto_row_split(cols, auto_per_lane, auto_wave_cols);
       if (S > 1 && cols <= split_max(S)) {
         *kind = REPOPS_LAUNCH_ROWS_WAVE;
         *wpb = 1;
@@ -402,8 +402,10 @@ repops_status_t repops_softmax_rows(const repops_order_t* order, int64_t rows, i
   if (st != REPOPS_OK) return st;
   uint32_t kind;
   int wpb, split;
+  // One wave per row measured faster up to 2048 columns here (split rows
+  // beyond).
   st = row_launch_kind(order, launch, cols, &kind, &wpb, repops::rows_wave_max_cols(), &split,
-                       repops::rows_split_max_cols);
+                       repops::rows_split_max_cols, 16, 2048);
   if (st != REPOPS_OK || empty) return st;
   RowArgs a{};
   a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
@@ -498,9 +500,10 @@ repops_status_t repops_softmax_backward_rows(const repops_order_t* order, int64_
   uint32_t kind;
   int wpb;
   int split;
+  // One wave per row measured faster up to 4096 columns here.
   repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb,
                                        repops::rows_wave_max_cols(), &split,
-                                       repops::rows_split_max_cols, 8);
+                                       repops::rows_split_max_cols, 8, 4096);
   if (st != REPOPS_OK || empty) return st;
   if ((st = check_matrix(Y, rows, cols, ldy)) != REPOPS_OK) return st;
   if ((st = check_matrix(dY, rows, cols, lddy)) != REPOPS_OK) return st;
@@ -544,9 +547,10 @@ static repops_status_t norm_backward(
   if (rows > 0 && cols == 0) return REPOPS_ERR_SHAPE;
   uint32_t kind;
   int wpb, split;
+  // dX alone: one wave per row measured faster up to 2048 columns.
   repops_status_t st = row_launch_kind(order, launch, cols, &kind, &wpb,
                                        repops::rows_wave_max_cols(), &split,
-                                       repops::rows_split_max_cols);
+                                       repops::rows_split_max_cols, 16, 2048);
   if (st != REPOPS_OK) return st;
   const bool want_params = dgamma || dbeta;
   if (cols == 0 || (rows == 0 && !want_params) || (!dX && !want_params)) return REPOPS_OK;

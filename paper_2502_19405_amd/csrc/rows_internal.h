@@ -9,13 +9,16 @@
 namespace repops {
 
 // Waves per row that a wide row is split over when the launch leaves the
-// choice open: rows up to 1024 columns stay on one wave; wider rows get the
-// fewest waves (2, 4, 8) that leave at most `per_lane` values per lane (16,
-// or 8 for the softmax backward, which measured best there), or 8.
+// choice open: rows up to `wave_cols` columns stay on one wave (1024; the
+// callers pass what measured fastest for their operator: 2048 for the softmax
+// and the norm backward's input gradient, 4096 for the softmax backward);
+// wider rows get the fewest waves (2, 4, 8) that leave at most `per_lane`
+// values per lane (16, or 8 for the softmax backward, which measured best
+// there), or 8.
 // (Measured on 4096- and 8192-wide rows: 16 values per lane is within a few
 // percent of 8, 16 waves per row is far slower.)
-inline int auto_row_split(int64_t cols, int per_lane = 16) {
-  if (cols <= 1024) return 1;
+inline int auto_row_split(int64_t cols, int per_lane = 16, int64_t wave_cols = 1024) {
+  if (cols <= wave_cols) return 1;
   int S = 2;
   while (S < 8 && cols > int64_t(64) * per_lane * S) S *= 2;
   return S;
