@@ -13,8 +13,8 @@ namespace repops {
 // callers pass what measured fastest for their operator: 2048 for the softmax
 // and the norm backward's input gradient, 4096 for the softmax backward);
 // wider rows get the fewest waves (2, 4, 8) that leave at most `per_lane`
-// values per lane (16, or 8 for the softmax backward, which measured best
-// there), or 8.
+// values per lane (16, or 8 for the softmax backward and the RMSNorm, which
+// measured best there), or 8.
 // (Measured on 4096- and 8192-wide rows: 16 values per lane is within a few
 // percent of 8, 16 waves per row is far slower.)
 inline int auto_row_split(int64_t cols, int per_lane = 16, int64_t wave_cols = 1024) {
