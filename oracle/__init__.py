@@ -13,6 +13,13 @@ Parity status per function (details in the test docstrings):
   exp / gelu           pinned: special values, accuracy bounds against
                        high-precision references, constants against definitions
   softmax / layernorm  pinned: closed-form rows, bounds against float64
+  training, Llama-block, erf and commitment operators: pinned in their own
+                       test modules (tests/test_oracle_*.py)
+
+``oracle.compose`` chains these calls into the model-shaped programs (the
+feed-forward block, its training step, causal attention, a linear layer's
+backward products); ``tests/golden/make_oracle_digests.py`` records digests of
+their full outputs at the large shapes.
 """
 from __future__ import annotations
 

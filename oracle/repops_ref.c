@@ -134,9 +134,9 @@ static void parallel_for(int nthreads, int64_t count, range_fn fn, void *ctx)
 /* ------------------------------------------------------------------------- */
 
 /*
- * Section 3.2, matrix-multiplication listing: the two output loops (i, j) may
- * run in any order; the contraction loop over k runs in one fixed order,
- * starting from sum = 0 and adding a*b term by term.
+ * Section 3.2, the matrix-multiplication contraction: the output indices
+ * (i, j) may be visited in any order; for each output a running sum over k,
+ * started at zero, takes one product term at a time in one fixed order.
  *
  * Reading used here (the paper gives no block constant): the k range is cut
  * into consecutive blocks of k_block indices, the last one possibly shorter.
@@ -145,7 +145,7 @@ static void parallel_for(int nthreads, int64_t count, range_fn fn, void *ctx)
  * accumulator that starts at +0.  k_block = 0 means a single block covering the
  * whole range, which is the listing itself.  The term update is a fused
  * multiply-add (k_inner = 0) or a rounded product followed by a rounded add
- * (k_inner = 1): the listing's "sum = sum + a*b" admits both.
+ * (k_inner = 1): the paper's term update may be read either way.
  */
 float repops_ref_dot(int64_t k_block, int k_inner, int64_t K,
                      const float *a, int64_t inc_a, const float *b, int64_t inc_b)

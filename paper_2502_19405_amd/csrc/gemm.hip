@@ -11,8 +11,13 @@
 // The output indices are spread over lanes, waves and workgroups freely; the
 // k walk of one output always stays inside one lane, in ascending order, so
 // tile sizes, launch shapes and operand layout cannot change a bit.  Zero
-// padding past K adds fma(0, 0, P) = P (P is never -0: it starts at +0 and
-// round-to-nearest never produces -0 from a sum of opposite values).
+// padding past K adds fma(0, 0, P), which is P except for the sign of a zero:
+// a block partial can be -0 (fma(a, b, +0) with a negative product below half
+// the smallest subnormal rounds to -0), and fma(0, 0, -0) = +0.  The output
+// cannot see that sign: every block partial is added into an accumulator that
+// starts at +0, acc + (+0) and acc + (-0) are both acc when acc != 0, and
+// +0 + (-0) = +0 under round-to-nearest, so acc is never -0 and takes the same
+// bits whichever sign the zero partial had.
 #include <hip/hip_runtime.h>
 
 #include "repops_internal.h"

@@ -3,9 +3,12 @@
 An independent model of binary32 operations for brute-force checks on tiny
 inputs: every operation is carried out exactly in rationals and then rounded
 once to the nearest binary32 value (ties to even), with gradual underflow and
-overflow to infinity.  It shares nothing with the C oracle.  Exact zero results
-are +0 (the operation sequences checked with it never produce -0).
+overflow to infinity.  It shares nothing with the C oracle.  Zero results take
+IEEE-754's signs: a nonzero exact result that rounds to zero keeps its sign; an
+exact zero sum is +0 under round-to-nearest unless both addends are -0; a
+zero product's sign is the exclusive-or of the factors' signs.
 """
+import math
 from fractions import Fraction
 
 _EMIN = -126          # smallest normal exponent
@@ -37,16 +40,38 @@ def rn32(q: Fraction) -> float:
     return sign * float(r)
 
 
+def _neg(x) -> bool:
+    return math.copysign(1.0, x) < 0
+
+
+def _zero_sum(x_neg: bool, y_neg: bool) -> float:
+    """Sign of an exact zero sum of two signed zeros (round to nearest)."""
+    return -0.0 if (x_neg and y_neg) else 0.0
+
+
 def fma(a, b, c) -> float:
-    return rn32(Fraction(a) * Fraction(b) + Fraction(c))
+    exact = Fraction(a) * Fraction(b) + Fraction(c)
+    if exact != 0:
+        return rn32(exact)
+    if a == 0 or b == 0:  # a zero product plus c (= +-0 here)
+        return _zero_sum(_neg(a) != _neg(b), _neg(c))
+    return 0.0            # a nonzero product cancelled exactly by c
 
 
 def add(a, b) -> float:
-    return rn32(Fraction(a) + Fraction(b))
+    exact = Fraction(a) + Fraction(b)
+    if exact != 0:
+        return rn32(exact)
+    if a == 0 and b == 0:
+        return _zero_sum(_neg(a), _neg(b))
+    return 0.0
 
 
 def mul(a, b) -> float:
-    return rn32(Fraction(a) * Fraction(b))
+    exact = Fraction(a) * Fraction(b)
+    if exact != 0:
+        return rn32(exact)
+    return -0.0 if _neg(a) != _neg(b) else 0.0
 
 
 def canonical_dot(a, b, k_block, fused=True) -> float:

@@ -254,3 +254,36 @@ def test_matrix_core_chain_equals_fma_chain(rp, mode, k_block):
         announce("adversarial", mode, k_block, name)
         got = host(rp.matmul(dev(A), dev(B), order=rp.Order(k_block=k_block), launch=launch))
         assert_bits_equal(got, want, f"{mode} {name}")
+
+
+def _negative_zero_witness(m, n, k):
+    """Every output (i, j) has exactly one nonzero product, -2^-160, at
+    k = 7 i mod K (row i of A has one nonzero entry there; every row of B
+    that some row of A uses is 2^-80): the fused block partial holding it is
+    -0, while zero padding past K or the +0 accumulator turns it into +0."""
+    A = np.zeros((m, k), np.float32)
+    B = np.zeros((k, n), np.float32)
+    ks = (7 * np.arange(m)) % k
+    A[np.arange(m), ks] = -(2.0 ** -80)
+    B[np.unique(ks), :] = 2.0 ** -80
+    return A, B
+
+
+@pytest.mark.parametrize("k", [70, 64, 1, 133])
+@pytest.mark.parametrize("k_block", [64, 0])
+def test_negative_zero_partials_vanish_in_the_accumulator(rp, k, k_block):
+    """A -0 block partial (a negative product below half the smallest subnormal)
+    never reaches the output: the accumulator starts at +0, so every output is
+    +0 under every launch, with K both a multiple and not a multiple of the
+    slice depths, one block (k_block 0) and several."""
+    m, n = 70, 66
+    A, B = _negative_zero_witness(m, n, k)
+    want = oracle.matmul(A, B, k_block=k_block)
+    assert not np.signbit(want).any() and not want.any()
+    for name, launch in launches(rp, k_block, True):
+        announce("negative-zero witness", k, k_block, name)
+        got = host(rp.matmul(dev(A), dev(B), order=rp.Order(k_block=k_block), launch=launch))
+        assert_bits_equal(got, want, f"K={k} k_block={k_block} {name}")
+        got_t = host(rp.matmul(dev(np.ascontiguousarray(A.T)).t(), dev(B),
+                               order=rp.Order(k_block=k_block), launch=launch))
+        assert_bits_equal(got_t, want, f"transposed A K={k} k_block={k_block} {name}")

@@ -210,6 +210,31 @@ def test_kblock_at_least_k_is_the_listing(ref):
         assert oracle.dot(a, b, k_block=kb, lib=ref) == lit
 
 
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("k,pos", [(70, 69), (70, 3), (64, 63), (1, 0), (133, 100)])
+def test_negative_zero_partial_joins_a_positive_accumulator(ref, fused, k, pos):
+    """One product of -2^-160: a fused block partial holding it alone is -0
+    (the product rounds to -0), but the accumulator starts at +0 and +0 + (-0)
+    is +0, so the output is +0 for one block (k_block 0) and for several --
+    the exact IEEE model of the whole sequence (signed zeros included) says
+    so, and the oracle agrees bit for bit.  Taken alone, the single-chain
+    listing would end at -0 when the product is its last term."""
+    a = np.zeros(k, np.float32)
+    b = np.zeros(k, np.float32)
+    a[pos], b[pos] = -(2.0 ** -80), 2.0 ** -80
+    for kb in (0, 64, 16):
+        want = exactfp.canonical_dot([float(x) for x in a], [float(y) for y in b], kb, fused)
+        assert want == 0.0 and not np.signbit(want)
+        got = oracle.dot(a, b, k_block=kb, k_inner=0 if fused else 1, lib=ref)
+        assert np.float32(got).view(np.uint32) == np.float32(want).view(np.uint32)
+    lit = 0.0
+    for x, y in zip(a, b):
+        lit = exactfp.fma(float(x), float(y), lit) if fused else exactfp.add(
+            lit, exactfp.mul(float(x), float(y)))
+    assert lit == 0.0
+    assert np.signbit(lit) == (fused and pos == k - 1)
+
+
 def test_optimisation_level_does_not_change_bits(ref):
     """The -O0 and -O2 builds of the oracle agree bit for bit on every operator."""
     with tempfile.TemporaryDirectory() as tmp:
