@@ -17,9 +17,10 @@
 // several workgroups), or on their own with one thread per (block, column)
 // -- every chain is independent -- and a second kernel adds them left to
 // right per column.
-// With a single block the first kernel writes the gradients directly (the left
-// to right sum of one partial P is +0 + P = P, since a chain started at +0 is
-// never -0).
+// With a single block the first kernel writes the gradients directly as the
+// left-to-right sum of that one partial, +0 + P: a fused dgamma chain can end
+// at -0 (a negative product below half the smallest subnormal rounds to -0),
+// and the accumulator's +0 + (-0) = +0 must still be taken.
 #include <hip/hip_runtime.h>
 
 #include "rep_math.h"
@@ -66,8 +67,10 @@ __global__ __launch_bounds__(T > 32 ? 256 : 512) void softmax_bwd_wave_kernel(Ro
       yv[t] = y[j];
       dv[t] = dy[j];
     }
-    // A masked term is fma(+0, +0, q) = q: the chain never holds -0.
-    q = __builtin_fmaf(yv[t], dv[t], q);
+    // Masked and absent terms take no operation (as in the oracle's row
+    // order): the chain can hold -0 (a negative product below half the
+    // smallest subnormal), which fma(+0, +0, -0) = +0 would change.
+    if (j < valid) q = __builtin_fmaf(yv[t], dv[t], q);
   }
   const float s = wave_tree_sum(q);
   auto out = [&](int t, int64_t j) {
@@ -174,7 +177,8 @@ __device__ __forceinline__ void layernorm_bwd_row(const RowBwdArgs& a, int64_t r
   const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
   float q2 = 0.0f;
 #pragma unroll
-  for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);
+  for (int t = 0; t < T; ++t)  // terms past the row take no operation (the chain may hold -0)
+    if (lane + kWave * t < a.cols) q2 = __builtin_fmaf(gv[t], tv[t], q2);
   const float bm = wave_tree_sum(q2) / n;
   auto out = [&](int t) {
     const float u = gv[t] - am;
@@ -239,7 +243,8 @@ __global__ __launch_bounds__(512) void softmax_bwd_split_kernel(RowBwdArgs a) {
     }
     const float q = chain_across_waves(chain, lane, w, S, [&](float c) {
 #pragma unroll
-      for (int t = 0; t < T; ++t) c = __builtin_fmaf(yv[t], dv[t], c);  // masked: c
+      for (int t = 0; t < T; ++t)  // masked and absent terms: no operation (c may be -0)
+        if (lane + kWave * (s0 + t) < valid) c = __builtin_fmaf(yv[t], dv[t], c);
       return c;
     });
     const float sum = wave_tree_sum(q);
@@ -279,7 +284,8 @@ __global__ __launch_bounds__(512) void layernorm_bwd_split_kernel(RowBwdArgs a) 
     }
     const float q2 = chain_across_waves(chain_gt, lane, w, S, [&](float c) {
 #pragma unroll
-      for (int t = 0; t < T; ++t) c = __builtin_fmaf(gv[t], tv[t], c);
+      for (int t = 0; t < T; ++t)  // past the row: no operation (c may be -0)
+        if (j0 + kWave * t < a.cols) c = __builtin_fmaf(gv[t], tv[t], c);
       return c;
     });
     const float bm = wave_tree_sum(q2) / n;
@@ -396,8 +402,8 @@ __global__ __launch_bounds__(kParamThreads) void layernorm_param_partial_kernel(
     pb = pb + dv;
   }
   if (nblk == 1) {
-    if (a.dgamma) a.dgamma[j] = pg;
-    if (a.dbeta) a.dbeta[j] = pb;
+    if (a.dgamma) a.dgamma[j] = 0.0f + pg;  // the accumulator step: -0 becomes +0
+    if (a.dbeta) a.dbeta[j] = 0.0f + pb;
   } else {
     a.ws[ws_index(0, beta, j, nblk, a.cols)] = pg;
     a.ws[ws_index(1, beta, j, nblk, a.cols)] = pb;
@@ -577,7 +583,8 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
       const float am = a.rms ? 0.0f : wave_tree_sum(q) / n;
       float q2 = 0.0f;
 #pragma unroll
-      for (int t = 0; t < T; ++t) q2 = __builtin_fmaf(gv[t], tv[t], q2);
+      for (int t = 0; t < T; ++t)  // past the row: no operation (q2 may be -0)
+        if (lane + kWave * t < cols) q2 = __builtin_fmaf(gv[t], tv[t], q2);
       const float bm = wave_tree_sum(q2) / n;
 #pragma unroll
       for (int t = 0; t < T; ++t) {
@@ -611,8 +618,8 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
     const int64_t j = tid + static_cast<int64_t>(k) * nthr;
     if (j < cols) {
       if (nblk == 1) {
-        if (p.dgamma) p.dgamma[j] = pg[k];
-        if (p.dbeta) p.dbeta[j] = pb[k];
+        if (p.dgamma) p.dgamma[j] = 0.0f + pg[k];  // the accumulator step: -0 becomes +0
+        if (p.dbeta) p.dbeta[j] = 0.0f + pb[k];
       } else {
         p.ws[ws_index(0, beta, j, nblk, cols)] = pg[k];
         p.ws[ws_index(1, beta, j, nblk, cols)] = pb[k];
@@ -683,7 +690,8 @@ __device__ __forceinline__ void layernorm_bwd_rows_grouped(const RowBwdArgs& a, 
     }
     const float q2 = group_chain(chain_gt, [&](float c) {
 #pragma unroll
-      for (int t = 0; t < T; ++t) c = __builtin_fmaf(gv[t], tv[t], c);
+      for (int t = 0; t < T; ++t)  // past the row: no operation (c may be -0)
+        if (j0 + kWave * t < a.cols) c = __builtin_fmaf(gv[t], tv[t], c);
       return c;
     });
     const float bm = wave_tree_sum(q2) / n;
@@ -800,8 +808,8 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_ke
   if (tid < sw) {
     const int64_t j = c0 + tid;
     if (nblk == 1) {
-      if (p.dgamma) p.dgamma[j] = pg;
-      if (p.dbeta) p.dbeta[j] = pb;
+      if (p.dgamma) p.dgamma[j] = 0.0f + pg;  // the accumulator step: -0 becomes +0
+      if (p.dbeta) p.dbeta[j] = 0.0f + pb;
     } else {
       p.ws[ws_index(0, beta, j, nblk, a.cols)] = pg;
       p.ws[ws_index(1, beta, j, nblk, a.cols)] = pb;

@@ -411,3 +411,99 @@ def test_adam_misaligned_views(rp):
     rp.adam_step(pd, pad(gr), md, vd, 1e-3, weight_decay=0.01, step=3, decoupled=True)
     for got, w, what in zip((pd, md, vd), want, "pmv"):
         assert_bits_equal(host(got), w, f"misaligned {what}")
+
+
+# --------------------------------------------------------------------------
+# Signed zeros in the product chains.  fma(a, b, q) with a negative product
+# below half the smallest subnormal gives -0; masked and absent terms take no
+# operation in the row order, so a chain that holds -0 keeps it, and the row
+# sum of -0 chains is -0.  A kernel that padded absent terms with
+# fma(+0, +0, q) would turn those chains into +0 and change outputs that take
+# the sum's sign (dy = -0 minus the sum).  The parameter gradients' single
+# block is still added into the +0 accumulator (+0 + (-0) = +0).
+# --------------------------------------------------------------------------
+
+def _lane_terms(cols):
+    """Per column j: (t, number of terms of lane j mod 64)."""
+    j = np.arange(cols)
+    t = j // 64
+    n = (cols - (j % 64) + 63) // 64
+    return t, n
+
+
+def softmax_negzero_case(rows, cols, period):
+    """Y = 2^-140; dY = -2^-20 (products -2^-160 round to -0), except the last
+    term of every lane that has two or more, which is -0.0 (the product with
+    -0 keeps a -0 chain).  Causal rows get the pattern over their valid prefix."""
+    Y = np.full((rows, cols), 2.0 ** -140, np.float32)
+    dY = np.full((rows, cols), -(2.0 ** -20), np.float32)
+    for r in range(rows):
+        valid = cols if period == 0 else min(cols, r % period + 1)
+        t, n = _lane_terms(valid)
+        last = (t == n - 1) & (n >= 2)
+        dY[r, :valid][last] = -0.0
+    return Y, dY
+
+
+@pytest.mark.parametrize("cols,period", [(65, 0), (100, 0), (130, 0), (1000, 0), (2100, 0),
+                                         (3000, 0), (5000, 0), (300, 200), (1024, 1024)])
+def test_softmax_backward_negative_zero_chains(rp, cols, period):
+    rows = 40 if period == 0 else period
+    Y, dY = softmax_negzero_case(rows, cols, period)
+    want = oracle.softmax_backward_rows(Y, dY, causal_period=period)
+    # the witness bites: dy = -0 minus a -0 sum is +0 (a +0 sum would give -0)
+    full = min(cols, (rows - 1) % period + 1) if period else cols
+    r_full = rows - 1
+    cols_neg = np.nonzero(np.signbit(dY[r_full, :full]) & (dY[r_full, :full] == 0))[0]
+    assert cols_neg.size and not np.signbit(want[r_full, cols_neg]).any()
+    Yd, dYd = dev(Y), dev(dY)
+    for name, launch in row_launches(rp, cols=cols):
+        announce("softmax_backward -0 chains", cols, period, name)
+        got = host(rp.softmax_backward_rows(Yd, dYd, causal_period=period, launch=launch))
+        assert_bits_equal(got, want, f"{name} cols={cols} period={period}")
+
+
+def norm_negzero_case(rows, cols, rms):
+    """mean = 0, rstd = 1; per lane, terms in pairs (dy, x) = (+c, -tau) and
+    (-c, +tau) -- products -2^-151 that round to -0, and g sums that cancel to
+    +0 -- and, when a lane has an odd number of terms, a last term with
+    dy = -0, x = +tau (its dx is rstd * ((-0 - a) - t b) = +0 for a -0 sum b)."""
+    c, tau = 2.0 ** -81, 2.0 ** -70
+    t, n = _lane_terms(cols)
+    last = (n % 2 == 1) & (t == n - 1)
+    dy_row = np.where(t % 2 == 0, c, -c).astype(np.float32)
+    x_row = np.where(t % 2 == 0, -tau, tau).astype(np.float32)
+    dy_row[last] = -0.0
+    x_row[last] = tau
+    X = np.repeat(x_row[None], rows, 0)
+    dY = np.repeat(dy_row[None], rows, 0)
+    mean = np.zeros(rows, np.float32)
+    rstd = np.ones(rows, np.float32)
+    return X, dY, mean, rstd, last
+
+
+@pytest.mark.parametrize("rows", [50, 130])
+@pytest.mark.parametrize("cols", [150, 700, 1100, 2500, 4000])
+def test_layernorm_backward_negative_zero_chains(rp, rows, cols):
+    X, dY, mean, rstd, last = norm_negzero_case(rows, cols, False)
+    want = oracle.layernorm_backward_rows(X, dY, mean, rstd, None)
+    assert last.any() and not np.signbit(want[0][:, last]).any()
+    assert not np.signbit(want[1]).any()  # dgamma: -0 chains joined to +0
+    for name, launch in row_launches(rp, cols=cols):
+        announce("layernorm_backward -0 chains", rows, cols, name)
+        got = run_lnb(rp, X, dY, mean, rstd, None, launch=launch)
+        for a, b, what in zip(got, want, ("dX", "dgamma", "dbeta")):
+            assert_bits_equal(a, b, f"{name} {what} rows={rows} cols={cols}")
+
+
+@pytest.mark.parametrize("rows", [50, 130])
+@pytest.mark.parametrize("cols", [150, 1100, 4000])
+def test_rmsnorm_backward_negative_zero_chains(rp, rows, cols):
+    X, dY, _, rstd, last = norm_negzero_case(rows, cols, True)
+    want = oracle.rmsnorm_backward_rows(X, dY, rstd, None)
+    assert last.any() and not np.signbit(want[0][:, last]).any()
+    for name, launch in row_launches(rp, cols=cols):
+        announce("rmsnorm_backward -0 chains", rows, cols, name)
+        got = rp.rmsnorm_backward_rows(dev(X), dev(dY), dev(rstd), None, launch=launch)
+        for a, b, what in zip(got, want, ("dX", "dgamma")):
+            assert_bits_equal(host(a), b, f"{name} {what} rows={rows} cols={cols}")
