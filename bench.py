@@ -1,12 +1,18 @@
 """Benchmark of the reproducible fp32 operators on one MI355X.
 
-One step is one reproducible GEMM C = A.B + bias of the 2048^3 workload
-(A, B ~ U(-1,1), bias ~ U(-0.1,0.1), canonical 64-block k order), timed
-with HIP events on the stream the kernel runs on.  The same run also times the
-row reductions and GELU at their model shapes (secondary figures) and the CPU
-oracle on a bounded sample of the GEMM (cpu_baseline).  Prints one JSON line.
+One step is the backward pass of a Llama-shaped linear layer, the largest
+workload that fits one GPU: dX = dY.W^T (8192 x 4096, K = 14336) and
+dW = X^T.dY (4096 x 14336, K = 8192 tokens), 1.924 TFLOP per step, X ~ N(0,1),
+dY ~ N(0,1e-2), W ~ N(0,0.02^2), canonical 64-block k order.  Both products are
+timed with HIP events on the stream they run on, each kernel separately.  A
+fixed-duration clock ramp of the same products runs before the counted warmup
+(the matrix-core clocks need tens of milliseconds of sustained work to reach
+their steady state).  The same run times the other workloads (the 2048^3 GEMM,
+the row reductions and elementwise operators at their model shapes, the
+model-shaped pipelines) as secondary figures, and the CPU oracle on a bounded
+sample of the headline workload (cpu_baseline).  Prints one JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--launch tiled:1]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--launch mfma:0]
 """
 from __future__ import annotations
 
@@ -35,29 +41,35 @@ def parse_launch(spec, repops):
     return repops.Launch(kinds[kind], (int(idx or 0),))
 
 
-COUNTERS_MD = os.path.join(ROOT, "profiles", "gemm2048_bias_hbm_counters.md")
+COUNTERS_MD = os.path.join(ROOT, "profiles", "llama_linear_backward_hbm_counters.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2502_19405_amd", "csrc", f)
-                  for f in ("gemm_mfma.hip", "repops_internal.h")]
+                  for f in ("gemm_mfma.hip", "repops_internal.h", "api.cpp")]
 
 
-def measured_traffic(launch_spec):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when the summary does not cover this kernel as it now stands."""
+def kernel_source_sha256():
     import hashlib
-    if launch_spec != "mfma:0" or not os.path.exists(COUNTERS_MD):
-        return None
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(f, "rb") as fh:
             h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(launch_spec, product):
+    """HBM bytes per launch of one headline product ("dX" or "dW") from the
+    committed rocprofv3 counter summary, or None when the summary does not
+    cover this kernel as it now stands (other launch, changed sources)."""
+    if launch_spec not in ("auto", "mfma:0") or not os.path.exists(COUNTERS_MD):
+        return None
     fields = {}
     for line in open(COUNTERS_MD):
         key, eq, val = line.partition(" = ")
         if eq:
             fields[key.strip()] = val.strip()
-    if fields.get("kernel_source_sha256") != h.hexdigest():
+    if fields.get("kernel_source_sha256") != kernel_source_sha256():
         return None
-    return float(fields["traffic_bytes_per_launch"])
+    val = fields.get(f"traffic_bytes_per_launch_{product}")
+    return float(val) if val else None
 
 
 def event_time_ms(fn, reps, warmup=2):
@@ -105,30 +117,57 @@ def graph_time_ms(fn, calls=20, reps=10):
     return start.elapsed_time(stop) / (calls * reps)
 
 
-def cpu_baseline(d, flops_per_row_unit, target_s=12.0):
-    """The oracle, as it stands, on a bounded row sample of the same GEMM."""
-    import numpy as np
-    import oracle
-
-    threads = oracle.default_threads()
-    A, B, bias = d["A"], d["B"], d["bias"]
-    rows = 8
+def _timed_rows(fn, total_rows, target_s):
+    """Run fn(rows) on a growing row count until it takes about target_s (or
+    covers every row); returns (rows, seconds) of the last run."""
+    rows = 1
     while True:
         t0 = time.perf_counter()
-        oracle.matmul(np.ascontiguousarray(A[:rows]), B, bias, nthreads=threads)
+        fn(rows)
         dt = time.perf_counter() - t0
-        if dt > 1.0 or rows >= A.shape[0]:
+        if dt > target_s / 8 or rows >= total_rows:
             break
-        rows *= 2
-    if dt < target_s and rows < A.shape[0]:
-        rows = int(min(A.shape[0], max(rows, rows * target_s / max(dt, 1e-3))))
+        rows = min(total_rows, rows * 4)
+    if dt < target_s and rows < total_rows:
+        rows = int(min(total_rows, max(rows, rows * target_s / max(dt, 1e-3))))
         t0 = time.perf_counter()
-        oracle.matmul(np.ascontiguousarray(A[:rows]), B, bias, nthreads=threads)
+        fn(rows)
         dt = time.perf_counter() - t0
-    gflops = rows * flops_per_row_unit / dt / 1e9
-    return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of 2048 output rows of the 2048^3 GEMM (+bias), "
-                      f"{dt:.2f} s wall on {threads} threads"}
+    return rows, dt
+
+
+def cpu_baseline(d, target_s=12.0):
+    """The oracle, as it stands, on bounded samples: the headline's dX product
+    on leading rows of dY with every host thread, and single-threaded the
+    whole 256^3 GEMM and leading rows of the 2048^3 GEMM."""
+    import numpy as np
+    import oracle
+    from paper_2502_19405_amd import inputs
+
+    threads = oracle.default_threads()
+    dY, W = d["dY"], d["W"]
+    n, k = W.shape[0], W.shape[1]
+    rows, dt = _timed_rows(
+        lambda r: oracle.matmul(np.ascontiguousarray(dY[:r]), W, trans_b=True, nthreads=threads),
+        dY.shape[0], target_s)
+    gflops = rows * 2.0 * n * k / dt / 1e9
+    out = {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+           "sample": f"first {rows} of {dY.shape[0]} rows of dX = dY.W^T ({n} columns, K = {k}), "
+                     f"{dt:.2f} s wall on {threads} threads"}
+    one = {}
+    c1 = inputs.gemm256_softmax256()
+    t0 = time.perf_counter()
+    oracle.matmul(c1["A"], c1["B"], nthreads=1)
+    dt1 = time.perf_counter() - t0
+    one["gemm256"] = {"s": round(dt1, 3), "GFLOP/s": round(2 * 256 ** 3 / dt1 / 1e9, 3),
+                      "sample": "whole 256^3 GEMM"}
+    c2 = inputs.gemm2048_bias()
+    r2, dt2 = _timed_rows(lambda r: oracle.matmul(np.ascontiguousarray(c2["A"][:r]), c2["B"],
+                                                  c2["bias"], nthreads=1), 2048, 4.0)
+    one["gemm2048_bias"] = {"s": round(dt2, 3), "GFLOP/s": round(r2 * 2 * 2048 ** 2 / dt2 / 1e9, 3),
+                            "sample": f"first {r2} of 2048 output rows"}
+    out["single_thread"] = one
+    return out
 
 
 def _graph_rate(ms, nbytes=None, flops=None):
@@ -147,14 +186,16 @@ def _rate(ms, nbytes=None, flops=None):
     return out
 
 
-def secondary(repops, steps, streaming_only=False):
+def secondary(repops, steps, streaming_only=False, headline=None):
     """The other workloads, each timed with HIP events after warmup:
     row reductions and elementwise ops in GB/s of algorithmic bytes (each
     element read once and written once; causal softmax reads only the
     unmasked part), GEMM-shaped steps and the model-shaped pipelines in
     TFLOP/s of 2*M*N*K.  streaming_only keeps the bandwidth-bound operators
     and the two copies, every call launched eagerly on one stream (no graph
-    replays, no GEMMs): the set the HBM byte counters are taken over."""
+    replays, no GEMMs): the set the HBM byte counters are taken over.
+    headline: the headline's device tensors (X, dY, dW), reused for one
+    data-parallel rank's share of the dW product."""
     import numpy as np
     import torch
     from paper_2502_19405_amd import inputs, pipelines
@@ -176,6 +217,16 @@ def secondary(repops, steps, streaming_only=False):
         sm = lambda: repops.softmax_rows(S, out=P)  # noqa: E731
         out["softmax_256x256"] = _rate(event_time_ms(sm, steps * 5), nbytes=8 * 256 * 256)
         out["softmax_256x256"].update(_graph_rate(graph_time_ms(sm), nbytes=8 * 256 * 256))
+
+    # 2048^3 GEMM + bias (A, B ~ U(-1,1), bias ~ U(-0.1,0.1))
+    if not streaming_only:
+        c2 = inputs.gemm2048_bias()
+        A2, B2, bias2 = t(c2["A"]), t(c2["B"]), t(c2["bias"])
+        C2 = torch.empty((2048, 2048), device=dev)
+        out["gemm2048_bias"] = _rate(
+            event_time_ms(lambda: repops.matmul(A2, B2, bias2, out=C2), steps * 5, warmup=20),
+            flops=2 * 2048 ** 3)
+        del A2, B2, bias2, C2
 
     # causal softmax, Llama attention scores: 4 x 32 heads x 1024 rows of 1024
     T, rows = 1024, 4 * 32 * 1024
@@ -347,40 +398,49 @@ def secondary(repops, steps, streaming_only=False):
                                               K, 1024 * 4096, 128, 4096, 1, 0.08838835, S,
                                               32 * 1024 * 1024, 1024 * 1024, 1024), steps)
     out["bmm_qkT_4x32x1024x1024x128"] = _rate(ms, flops=2 * 4 * 32 * 1024 * 1024 * 128)
+    # causal: only the scores at or below the diagonal are ever read
+    out["bmm_qkT_4x32x1024x1024x128"]["causal_useful_TFLOP/s"] = round(
+        2 * 4 * 32 * 128 * (1024 * 1025 // 2) / ms / 1e9, 2)
     # PV: P [4*32*1024, 1024] times V's head columns, written in place into O
     P, V, O = bufs["P"], bufs["V"], bufs["O"]
     ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 128, 1024, P, 32 * 1024 * 1024,
                                               1024 * 1024, 1024, 0, V, 1024 * 4096, 128, 4096, 0,
                                               1.0, O, 1024 * 4096, 128, 4096), steps)
     out["bmm_pv_4x32x1024x128x1024"] = _rate(ms, flops=2 * 4 * 32 * 1024 * 128 * 1024)
+    # causal: row i of P has i + 1 nonzero probabilities
+    out["bmm_pv_4x32x1024x128x1024"]["causal_useful_TFLOP/s"] = round(
+        2 * 4 * 32 * 128 * (1024 * 1025 // 2) / ms / 1e9, 2)
     del X, Wq, Wk, Wv, Wo, bufs, Q, K, S, P, V, O
 
-    # Llama linear backward: dX = dY W^T, dW = X^T dY (8192 tokens, 4096 -> 14336)
-    d = inputs.llama_linear_backward()
-    X, dY, W = t(d["X"]), t(d["dY"]), t(d["W"])
-    gx = torch.empty((8192, 4096), device=dev)
-    gw = torch.empty((4096, 14336), device=dev)
-    ms = event_time_ms(lambda: pipelines.linear_backward(X, dY, W, out_dx=gx, out_dw=gw),
-                       max(steps // 4, 3))
-    out["llama_linear_backward"] = _rate(ms, flops=2 * 2 * 8192 * 4096 * 14336)
-    # one rank's share of dW under 8-way data parallelism: the same GEMM over
-    # 1024 of the 8192 tokens (the ordered cross-rank combine is not built)
-    ms = event_time_ms(lambda: repops.matmul(X[:1024].t(), dY[:1024], out=gw), steps)
-    out["llama_dW_rank_share_4096x14336x1024"] = _rate(ms, flops=2 * 4096 * 14336 * 1024)
-    del X, dY, W, gx, gw
+    # one rank's share of dW under 8-way data parallelism: the headline's dW
+    # product over 1024 of the 8192 tokens (the ordered cross-rank combine is
+    # not built)
+    if headline is not None:
+        X, dY, gw = headline["X"], headline["dY"], headline["dW"]
+        ms = event_time_ms(lambda: repops.matmul(X[:1024].t(), dY[:1024], out=gw), steps)
+        out["llama_dW_rank_share_4096x14336x1024"] = _rate(ms, flops=2 * 4096 * 14336 * 1024)
+        del X, dY, gw
 
     return out
+
+
+def input_digests(d):
+    import hashlib
+    import numpy as np
+    return {k: hashlib.sha256(np.ascontiguousarray(v).tobytes()).hexdigest() for k, v in d.items()}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # The clocks take about 40 ms of sustained matrix-core work to ramp up;
-    # 500 warmup steps (about 0.1 s) keep the ramp out of the timed region.
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=500)
-    ap.add_argument("--launch", default="mfma:0",
-                    help="auto | simple | tiled:I | mfma:I (mfma:0 is what auto picks here)")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    # The clocks take tens of milliseconds of sustained matrix-core work to
+    # reach their steady state; this ramp runs before the counted warmup and
+    # is not timed, so a small --warmup still measures steady clocks.
+    ap.add_argument("--ramp-ms", type=float, default=300.0)
+    ap.add_argument("--launch", default="auto",
+                    help="auto | simple | tiled:I | mfma:I (auto picks mfma:0 for both products)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--streaming-only", action="store_true",
@@ -395,63 +455,98 @@ def main():
               "exchange along their order-free dimensions, so a multi-GPU figure adds nothing "
               "here; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        print("--steps must be at least 1 and --warmup at least 0", file=sys.stderr)
+        sys.exit(2)
 
-    import numpy as np
     import torch
     from paper_2502_19405_amd import inputs, repops
 
     repops.load()
     dev = torch.device("cuda:0")
-    d = inputs.gemm2048_bias()
-    M = N = K = 2048
-    A = torch.from_numpy(d["A"]).to(dev)
-    B = torch.from_numpy(d["B"]).to(dev)
-    bias = torch.from_numpy(d["bias"]).to(dev)
-    C = torch.empty((M, N), device=dev)
+    d = inputs.llama_linear_backward()
+    digests = input_digests(d)
+    T, D_IN, D_OUT = d["X"].shape[0], d["X"].shape[1], d["W"].shape[1]
+    X = torch.from_numpy(d["X"]).to(dev)
+    dY = torch.from_numpy(d["dY"]).to(dev)
+    W = torch.from_numpy(d["W"]).to(dev)
+    dX = torch.empty((T, D_IN), device=dev)
+    dW = torch.empty((D_IN, D_OUT), device=dev)
     launch = parse_launch(args.launch, repops)
+    Wt, Xt = W.t(), X.t()
 
-    def step():
-        repops.matmul(A, B, bias, launch=launch, out=C)
+    def prod_dx():
+        repops.matmul(dY, Wt, launch=launch, out=dX)
 
-    for _ in range(args.warmup):
-        step()
+    def prod_dw():
+        repops.matmul(Xt, dY, launch=launch, out=dW)
+
+    # untimed clock ramp: the step repeated for a fixed wall-clock duration
     torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    stop.record()
+    ramp_steps = 0
+    while (time.perf_counter() - t0) * 1e3 < args.ramp_ms:
+        prod_dx()
+        prod_dw()
+        torch.cuda.synchronize()
+        ramp_steps += 1
+    ramp_ms = (time.perf_counter() - t0) * 1e3
+    for _ in range(args.warmup):
+        prod_dx()
+        prod_dw()
+    torch.cuda.synchronize()
+
+    # timed steps: an event before dX, between the two products and after dW
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(args.steps):
+        prod_dx()
+        ev[2 * i + 1].record()
+        prod_dw()
+        ev[2 * i + 2].record()
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
-    kernel_ms = start.elapsed_time(stop) / args.steps
-    flops = 2.0 * M * N * K
-    gflops = flops / (kernel_ms * 1e-3) / 1e9
-    achieved_tflops = gflops / 1e3
+    dx_ms = sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
+    dw_ms = sum(ev[2 * i + 1].elapsed_time(ev[2 * i + 2]) for i in range(args.steps)) / args.steps
+    step_ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    flops_each = 2.0 * T * D_IN * D_OUT
+    value_gflops = 2 * flops_each / (step_ms * 1e-3) / 1e9
 
-    # which unit bounds the kernel that ran: matrix cores or the vector ALU
-    mfma = launch is not None and launch.kind == repops.LAUNCH_GEMM_MFMA
+    mfma = launch is None or launch.kind == repops.LAUNCH_GEMM_MFMA
+    kernels = {}
+    for name, ms, shape in (("dX", dx_ms, f"{T}x{D_IN}, K={D_OUT}, W read transposed"),
+                            ("dW", dw_ms, f"{D_IN}x{D_OUT}, K={T}, X read transposed")):
+        tf = flops_each / (ms * 1e-3) / 1e12
+        kernels[name] = {"ms": round(ms, 4), "TFLOP/s": round(tf, 2),
+                         "frac": round(tf / FP32_VECTOR_PEAK_TFLOPS, 4), "shape": shape,
+                         "traffic": measured_traffic(args.launch, name)}
+    dom = "dX" if dx_ms >= dw_ms else "dW"  # the kernel that takes longer
     result = {
         "metric": METRIC,
-        "value": round(gflops, 1),
+        "value": round(value_gflops, 1),
         "unit": "GFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(kernel_ms, 5),
-        "wall_ms_per_step": round(wall_ms, 5),
+        "ms_per_step": round(step_ms, 4),
+        "wall_ms_per_step": round(wall_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "gemm2048_bias: C = A.B + bias, M=N=K=2048, A,B ~ U(-1,1), "
-                               "bias ~ U(-0.1,0.1), k_block 64, fma, left-to-right",
-                   "launch": args.launch or "auto", "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma" if mfma else "alu", "achieved": round(achieved_tflops, 3),
-                     "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved_tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(args.launch)},
+        "config": {"workload": f"llama_linear_backward: dX = dY.W^T and dW = X^T.dY, tokens {T}, "
+                               f"in {D_IN}, out {D_OUT}; X ~ N(0,1), dY ~ N(0,1e-2), "
+                               f"W ~ N(0,0.02^2); k_block 64, fma, left-to-right",
+                   "launch": args.launch, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma" if mfma else "alu", "kernel": dom,
+                     "achieved": kernels[dom]["TFLOP/s"], "peak": FP32_VECTOR_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": kernels[dom]["frac"],
+                     "traffic": kernels[dom]["traffic"]},
+        "kernels": kernels,
+        "clock_ramp": {"ms": round(ramp_ms, 1), "steps": ramp_steps},
+        "inputs_sha256": digests,
     }
     if args.calibrate_copy:
         src = torch.empty(64 << 20, device=dev)
@@ -461,9 +556,10 @@ def main():
         torch.cuda.synchronize()
         result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_secondary:
-        result["secondary"] = secondary(repops, 20, args.streaming_only)
+        result["secondary"] = secondary(repops, 20, args.streaming_only,
+                                        headline={"X": X, "dY": dY, "dW": dW})
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(d, 2.0 * N * K)
+        result["cpu_baseline"] = cpu_baseline(d)
     print(json.dumps(result), flush=True)
 
 

@@ -40,12 +40,28 @@ def test_launch_strings(bench):
 
 
 def test_traffic_comes_only_from_a_matching_counter_summary(bench, tmp_path, monkeypatch):
-    # The committed summary covers the committed kernel sources.
-    v = bench.measured_traffic("mfma:0")
-    assert v is not None and v > 50.3e6, v  # at least the algorithmic bytes
-    assert bench.measured_traffic("mfma:1") is None  # another kernel: no figure
+    summary = tmp_path / "counters.md"
+    summary.write_text("prose\n\ntraffic_bytes_per_launch_dX = 1234567\n"
+                       "traffic_bytes_per_launch_dW = 7654321\n"
+                       f"kernel_source_sha256 = {bench.kernel_source_sha256()}\n")
+    monkeypatch.setattr(bench, "COUNTERS_MD", str(summary))
+    assert bench.measured_traffic("auto", "dX") == 1234567.0
+    assert bench.measured_traffic("mfma:0", "dW") == 7654321.0
+    assert bench.measured_traffic("mfma:1", "dX") is None  # another kernel: no figure
     # A source that differs from the one the counters were taken on voids it.
     src = tmp_path / "gemm_mfma.hip"
     src.write_bytes(open(bench.KERNEL_SOURCES[0], "rb").read() + b"\n")
-    monkeypatch.setattr(bench, "KERNEL_SOURCES", [str(src), bench.KERNEL_SOURCES[1]])
-    assert bench.measured_traffic("mfma:0") is None
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", [str(src), *bench.KERNEL_SOURCES[1:]])
+    assert bench.measured_traffic("auto", "dX") is None
+
+
+def test_committed_counter_summary_parses(bench):
+    """The committed summary, when present, holds both products' figures (at
+    least their algorithmic bytes) -- or is stale, in which case bench.py
+    reports no traffic rather than a figure for other kernel sources."""
+    if not os.path.exists(bench.COUNTERS_MD):
+        pytest.skip("no counter summary committed")
+    for product, algorithmic in (("dX", 4 * (8192 * 14336 + 4096 * 14336 + 8192 * 4096)),
+                                 ("dW", 4 * (8192 * 4096 + 8192 * 14336 + 4096 * 14336))):
+        v = bench.measured_traffic("auto", product)
+        assert v is None or v >= algorithmic, (product, v)

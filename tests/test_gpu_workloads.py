@@ -1,15 +1,20 @@
 """GPU parity on the five workloads at full size (0 ULP).
 
-Where the oracle can take every output in seconds it does; at the large
-shapes it computes sampled outputs one by one (each from the original seeded
-inputs, never from a GPU result), and the launch configurations are compared
-with each other on every output.  Composite programs are checked end to end
-on rows (MLP) or on whole heads (attention) that the oracle recomputes from
-the original inputs.
+Every output of every workload is checked against the oracle: where the oracle
+takes them all in seconds (the 256^3 and 2048^3 GEMMs, the feed-forward block)
+it runs in the test; at the large shapes (the attention block, the linear
+layer's backward products, the feed-forward training step at 4096 tokens) the
+test compares SHA-256 digests of whole outputs with digests of the oracle's
+outputs stored by tests/golden/make_oracle_digests.py, and computes sampled
+outputs with the oracle one by one so that a mismatch is named.  Each workload
+runs under at least three launch configurations (matrix-core table entries and
+vector-FMA tiles): the first launch's outputs against the oracle, every other
+launch's outputs against the first one's on every element.
 """
 import numpy as np
 import pytest
 
+import digests
 import oracle
 from bitcmp import assert_bits_equal
 from gpu_util import announce, dev, host, same_bits
@@ -53,20 +58,14 @@ def test_gemm256_softmax256_full(rp):
 
 # ---------------------------------------------------------------- 2048^3 + bias
 
-def test_gemm2048_bias_sampled_and_cross_launch(rp):
+def test_gemm2048_bias_full_every_launch(rp):
     d = inputs.gemm2048_bias()
-    rows, cols = inputs.sample_indices(1, 4096, 2048, 2048)
-    want = oracle.matmul_at(d["A"], d["B"], rows, cols, bias=d["bias"])
+    announce("gemm2048 oracle (every output)")
+    want = oracle.matmul(d["A"], d["B"], d["bias"])
     dA, dB, dbias = dev(d["A"]), dev(d["B"]), dev(d["bias"])
-    ref = None
     for name, launch in gemm_launches(rp):
         announce("gemm2048", name)
-        C = rp.matmul(dA, dB, dbias, launch=launch)
-        assert_bits_equal(host(C)[rows, cols], want, name)
-        if ref is None:
-            ref = C
-        else:
-            assert same_bits(C, ref), f"{name} differs from the first launch configuration"
+        assert_bits_equal(host(rp.matmul(dA, dB, dbias, launch=launch)), want, name)
 
 
 def test_gemm2048_integer_exact(rp):
@@ -82,20 +81,66 @@ def test_gemm2048_integer_exact(rp):
 
 # ---------------------------------------------------------------- DistilBERT MLP
 
-def test_distilbert_mlp_rows_end_to_end(rp):
+def mlp_launches(rp):
+    """Matrix-core entries 0 (staged 128x128), 2 (register-staged), 5 (64x64)
+    and 7 (staged 256x128), and both vector-FMA tiles."""
+    return [(n, l) for n, l in gemm_launches(rp, include_simple=False)
+            if n.split(":")[0] in ("mfma0", "mfma2", "mfma5", "mfma7", "tiled0", "tiled1")]
+
+
+def test_distilbert_mlp_block_full_every_launch(rp):
     from paper_2502_19405_amd import pipelines
+    from oracle import compose
     d = inputs.distilbert_mlp()
-    announce("mlp pipeline")
-    out = pipelines.mlp_forward(dev(d["X"]), dev(d["W1"]), dev(d["b1"]), dev(d["W2"]),
-                                dev(d["b2"]), dev(d["gamma"]), dev(d["beta"]), keep=True)
-    rows = np.array([0, 1, 63, 64, 1000, 2047, 2048, 3333, 4094, 4095])
-    X = np.ascontiguousarray(d["X"][rows])
-    H1 = oracle.matmul(X, d["W1"], d["b1"])
-    G = oracle.gelu(H1)
-    H2 = oracle.matmul(G, d["W2"], d["b2"])
-    Y = oracle.layernorm_rows(H2, d["gamma"], d["beta"], eps=1e-5)
-    for key, want in (("H1", H1), ("G", G), ("H2", H2), ("Y", Y)):
-        assert_bits_equal(host(out[key])[rows], want, key)
+    announce("mlp oracle (every output)")
+    want = compose.mlp_forward(d["X"], d["W1"], d["b1"], d["W2"], d["b2"], d["gamma"], d["beta"])
+    args = [dev(d[k]) for k in ("X", "W1", "b1", "W2", "b2", "gamma", "beta")]
+    for name, launch in mlp_launches(rp):
+        announce("mlp pipeline", name)
+        out = pipelines.mlp_forward(*args, gemm_launch=launch, keep=True)
+        for key in ("H1", "G", "H2", "Y"):
+            assert_bits_equal(host(out[key]), want[key], f"{key} {name}")
+
+
+def test_distilbert_mlp_training_step_4096_tokens_every_launch(rp):
+    """Two whole training steps of the feed-forward block at 4096 tokens --
+    forward, every gradient (the dW products contract over the 4096 tokens,
+    the dX products over 3072 and 768 features), AdamW of all parameters --
+    equal the oracle's composition on every output (stored digests), under
+    four GEMM launch configurations."""
+    import torch
+    from paper_2502_19405_amd import pipelines
+    from oracle.compose import MLP_PARAM_NAMES
+    tokens = 4096
+    d = inputs.distilbert_mlp(tokens=tokens)
+    dYs = digests.train_step_gradients(tokens)
+    ins = dict(d)
+    ins.update({f"dY_step{i}": v for i, v in enumerate(dYs, start=1)})
+    want = digests.entry("mlp_train_step_4096", ins)
+    Xd = dev(d["X"])
+    ref = None
+    for name, launch in [(n, l) for n, l in mlp_launches(rp)
+                         if n.split(":")[0] in ("mfma0", "mfma5", "mfma7", "tiled1")]:
+        st = pipelines.MlpTrainState(*(dev(d[k]) for k in MLP_PARAM_NAMES))
+        outs = {}
+        for step, dY in enumerate(dYs, start=1):
+            announce("mlp train step 4096", name, step)
+            Yg, dXg = pipelines.mlp_train_step(st, Xd, dev(dY), gemm_launch=launch)
+            torch.cuda.synchronize()
+            outs[f"step{step}/Y"] = Yg.clone()
+            outs[f"step{step}/dX"] = dXg.clone()
+            for pn, gg, pg in zip(MLP_PARAM_NAMES, st.g, st.p):
+                outs[f"step{step}/grad_{pn}"] = gg.clone()
+                outs[f"step{step}/param_{pn}"] = pg.clone()
+            outs[f"step{step}/exp_avg"] = st.exp_avg.clone()
+            outs[f"step{step}/exp_avg_sq"] = st.exp_avg_sq.clone()
+        if ref is None:
+            for key, t in outs.items():
+                assert digests.sha256_of(host(t)) == want[key], f"{key} {name} differs from the oracle"
+            ref = outs
+        else:
+            for key, t in outs.items():
+                assert same_bits(t, ref[key]), f"{key} {name} differs from the first launch"
 
 
 def test_distilbert_shaped_gelu_and_layernorm_full(rp):
@@ -140,22 +185,40 @@ def test_llama_attention_heads_end_to_end(rp):
         assert_bits_equal(O[b * T:(b + 1) * T, cols], Oh, f"O[{b},{h}]")
 
 
-def test_llama_attention_projection_gemms_sampled(rp):
+def test_llama_attention_block_full_every_launch(rp):
+    """The whole attention block (Q, K, V projections, QK^T, causal softmax,
+    PV, output projection) at its full shape: every intermediate and the
+    output equal the oracle's composition (stored digests) under the first
+    launch configuration and equal that launch's bits under every other
+    matrix-core and vector-FMA launch; sampled projection outputs are also
+    recomputed by the oracle one by one."""
+    from paper_2502_19405_amd import pipelines
     d = inputs.llama_attention()
-    rows, cols = inputs.sample_indices(4, 1024, 4096, 4096)
-    dX = dev(d["X"])
-    for w in ("Wq", "Wo"):
-        want = oracle.matmul_at(d["X"], d[w], rows, cols)
-        for name, launch in gemm_launches(rp, include_simple=False):
-            announce("projection", w, name)
-            got = host(rp.matmul(dX, dev(d[w]), launch=launch))
-            assert_bits_equal(got[rows, cols], want, f"{w} {name}")
+    want = digests.entry("llama_attention", d)
+    args = [dev(d[k]) for k in ("X", "Wq", "Wk", "Wv", "Wo")]
+    rows, cols = inputs.sample_indices(4, 512, 4096, 4096)
+    samples = {"Q": oracle.matmul_at(d["X"], d["Wq"], rows, cols)}
+    ref = None
+    for name, launch in gemm_launches(rp, include_simple=False):
+        announce("attention block", name)
+        out = pipelines.attention_forward(*args, 4, 1024, 32, gemm_launch=launch, keep=True)
+        assert_bits_equal(host(out["Q"])[rows, cols], samples["Q"], f"Q samples {name}")
+        if ref is None:
+            for key in ("Q", "K", "V", "S", "P", "O", "out"):
+                assert digests.sha256_of(host(out[key])) == want[key], (
+                    f"{key} {name} differs from the oracle")
+            ref = out
+        else:
+            for key in ("Q", "K", "V", "S", "P", "O", "out"):
+                assert same_bits(out[key], ref[key]), f"{key} {name} differs from the first launch"
+        del out
 
 
 def test_llama_attention_score_bmm_and_softmax_full_shape(rp):
     """QK^T and PV at their full shapes (4 x 32 heads) on seeded operands of
-    the projections' distribution, sampled; causal softmax over all 131072 rows
-    of 1024, every output."""
+    the projections' distribution, sampled outputs against the oracle under
+    every matrix-core and vector-FMA launch; causal softmax over all 131072
+    rows of 1024, every output."""
     g = inputs.rng(44)
     B, T, D, H = 4, 1024, 4096, 32
     hd = D // H
@@ -179,6 +242,20 @@ def test_llama_attention_score_bmm_and_softmax_full_shape(rp):
         announce("causal softmax 131072x1024", launch)
         assert_bits_equal(host(rp.softmax_rows(dS, causal_period=T, launch=launch)), want_p,
                           str(launch))
+    # PV: the causal probabilities times V's head columns, written in place
+    # into O's head columns
+    V = inputs.normal(g, (B * T, D), var=1.64)
+    b0, b1, r, c = inputs.sample_indices(6, 2048, B, H, T, hd)
+    want_o = oracle.bmm_at_raw(B, H, T, hd, T, want_p.ravel(), H * T * T, T * T, T, 0,
+                               V.ravel(), T * D, hd, D, 0, 1.0, b0, b1, r, c)
+    dP, dV = dev(want_p), dev(V)
+    O = torch.empty((B * T, D), device="cuda:0")
+    for name, launch in gemm_launches(rp, include_simple=False):
+        announce("PV bmm", name)
+        rp.bmm_raw(B, H, T, hd, T, dP, H * T * T, T * T, T, 0, dV, T * D, hd, D, 0, 1.0,
+                   O, T * D, hd, D, launch=launch)
+        Oh = host(O).reshape(B, T, H, hd)
+        assert_bits_equal(Oh[b0, r, b1, c], want_o, name)
 
 
 # ---------------------------------------------------------------- Llama backward
@@ -188,11 +265,16 @@ def backward_data():
     return inputs.llama_linear_backward()
 
 
-def test_llama_linear_backward_sampled_across_tiles(rp, backward_data):
+def test_llama_linear_backward_full_every_launch(rp, backward_data):
+    """dX = dY W^T (K = 14336) and dW = X^T dY (K = 8192 tokens) at full size:
+    every output equals the oracle's (stored digests) under the first launch
+    and that launch's bits under every other matrix-core and vector-FMA
+    launch; sampled outputs are recomputed by the oracle one by one."""
     from paper_2502_19405_amd import pipelines
     d = backward_data
-    r1, c1 = inputs.sample_indices(6, 1024, 8192, 4096)
-    r2, c2 = inputs.sample_indices(7, 1024, 4096, 14336)
+    want = digests.entry("llama_linear_backward", d)
+    r1, c1 = inputs.sample_indices(6, 512, 8192, 4096)
+    r2, c2 = inputs.sample_indices(7, 512, 4096, 14336)
     want_dx = oracle.matmul_at(d["dY"], d["W"], r1, c1, trans_b=True)
     want_dw = oracle.matmul_at(d["X"], d["dY"], r2, c2, trans_a=True)
     dX_, dY_, W_ = dev(d["X"]), dev(d["dY"]), dev(d["W"])
@@ -200,9 +282,12 @@ def test_llama_linear_backward_sampled_across_tiles(rp, backward_data):
     for name, launch in gemm_launches(rp, include_simple=False):
         announce("linear backward", name)
         gx, gw = pipelines.linear_backward(dX_, dY_, W_, gemm_launch=launch)
-        assert_bits_equal(host(gx)[r1, c1], want_dx, f"dX {name}")
-        assert_bits_equal(host(gw)[r2, c2], want_dw, f"dW {name}")
+        assert_bits_equal(host(gx)[r1, c1], want_dx, f"dX samples {name}")
+        assert_bits_equal(host(gw)[r2, c2], want_dw, f"dW samples {name}")
         if ref is None:
+            assert digests.sha256_of(host(gx)) == want["dX"], f"dX {name} differs from the oracle"
+            assert digests.sha256_of(host(gw)) == want["dW"], f"dW {name} differs from the oracle"
             ref = (gx, gw)
         else:
-            assert same_bits(gx, ref[0]) and same_bits(gw, ref[1]), name
+            assert same_bits(gx, ref[0]), f"dX {name} differs from the first launch"
+            assert same_bits(gw, ref[1]), f"dW {name} differs from the first launch"
