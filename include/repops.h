@@ -48,7 +48,9 @@ enum {
     REPOPS_ERR_LAUNCH = 6, /* launch configuration invalid for this call */
     REPOPS_ERR_HIP = 7,    /* the HIP runtime rejected the kernel launch */
     REPOPS_ERR_VALUE = 8,  /* a scalar argument outside its domain */
-    REPOPS_ERR_WORKSPACE = 9 /* workspace NULL or smaller than the size the query returns */
+    REPOPS_ERR_WORKSPACE = 9, /* workspace NULL or smaller than the size the query returns */
+    REPOPS_ERR_SCRATCH = 10   /* the problem needs more than the fixed scratch of a
+                                 no-allocation entry point (REPOPS_NOALLOC_SCRATCH_BYTES) */
 };
 
 /*
@@ -298,6 +300,34 @@ repops_status_t repops_layernorm_backward_rows(
     const float *dY, int64_t lddy, const float *mean, const float *rstd, const float *gamma,
     float *dX, int64_t lddx, float *dgamma, float *dbeta, void *workspace,
     uint64_t workspace_bytes, const repops_launch_t *launch, void *hip_stream);
+
+/*
+ * repops_layernorm_backward_rows_noalloc -- repops_layernorm_backward_rows
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * operation, arguments, launch kinds and bits, with no workspace argument.
+ * The parameter gradients' block partials go to a fixed scratch array of
+ * REPOPS_NOALLOC_SCRATCH_BYTES in device memory, which every device the
+ * library runs on holds until the process ends; the call allocates and frees
+ * nothing.  Its device address is looked up (hipGetSymbolAddress) on the
+ * first call per device, with the caller's current device, which must be the
+ * device of hip_stream.
+ *   Limit: 2 * ceil(rows / k_block) * cols * 4 bytes (the workspace query's
+ *   size) at most REPOPS_NOALLOC_SCRATCH_BYTES, e.g. 65536 x 768 or
+ *   16384 x 4096 at k_block 64; beyond it REPOPS_ERR_SCRATCH, with nothing
+ *   enqueued.
+ *   Calls on one device share the scratch array: calls that overlap in time
+ *   on that device (on different streams, or from different host threads)
+ *   race and may give wrong parameter gradients; serialise them.  Every
+ *   partial a call reads is written earlier in the same call, so the contents
+ *   left by an earlier call never matter.
+ */
+#define REPOPS_NOALLOC_SCRATCH_BYTES (8ull << 20)
+repops_status_t repops_layernorm_backward_rows_noalloc(
+    const repops_order_t *order, int64_t rows, int64_t cols, const float *X, int64_t ldx,
+    const float *dY, int64_t lddy, const float *mean, const float *rstd, const float *gamma,
+    float *dX, int64_t lddx, float *dgamma, float *dbeta, const repops_launch_t *launch,
+    void *hip_stream);
 
 /*
  * repops_colsum_rows -- column sums over rows, the bias gradient of a linear

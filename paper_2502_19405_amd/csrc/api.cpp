@@ -334,6 +334,8 @@ const char* repops_status_str(repops_status_t s) {
     case REPOPS_ERR_HIP: return "HIP launch failed";
     case REPOPS_ERR_VALUE: return "invalid scalar argument";
     case REPOPS_ERR_WORKSPACE: return "workspace missing or too small";
+    case REPOPS_ERR_SCRATCH:
+      return "problem needs more scratch than the no-allocation entry point's fixed buffer holds";
     default: return "unknown status";
   }
 }
@@ -649,6 +651,24 @@ repops_status_t repops_layernorm_backward_rows(
     uint64_t workspace_bytes, const repops_launch_t* launch, void* hip_stream) {
   return norm_backward(false, order, rows, cols, X, ldx, dY, lddy, mean, rstd, gamma, dX, lddx,
                        dgamma, dbeta, workspace, workspace_bytes, launch, hip_stream);
+}
+
+repops_status_t repops_layernorm_backward_rows_noalloc(
+    const repops_order_t* order, int64_t rows, int64_t cols, const float* X, int64_t ldx,
+    const float* dY, int64_t lddy, const float* mean, const float* rstd, const float* gamma,
+    float* dX, int64_t lddx, float* dgamma, float* dbeta, const repops_launch_t* launch,
+    void* hip_stream) {
+  static_assert(REPOPS_NOALLOC_SCRATCH_BYTES == repops::kNoallocScratchBytes,
+                "the header states the scratch size");
+  uint64_t need = 0;
+  repops_status_t st = repops_layernorm_backward_workspace(order, rows, cols, &need);
+  if (st != REPOPS_OK) return st;
+  if (!dgamma && !dbeta) need = 0;
+  if (need > repops::kNoallocScratchBytes) return REPOPS_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (need > 0 && repops::noalloc_scratch(&ws) != hipSuccess) return REPOPS_ERR_HIP;
+  return norm_backward(false, order, rows, cols, X, ldx, dY, lddy, mean, rstd, gamma, dX, lddx,
+                       dgamma, dbeta, ws, need, launch, hip_stream);
 }
 
 repops_status_t repops_rmsnorm_backward_workspace(const repops_order_t* order, int64_t rows,

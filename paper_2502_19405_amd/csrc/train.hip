@@ -23,6 +23,8 @@
 // and the accumulator's +0 + (-0) = +0 must still be taken.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "rep_math.h"
 #include "repops_internal.h"
 #include "train_internal.h"
@@ -1161,6 +1163,41 @@ hipError_t launch_adam(int64_t n, float* p, const float* g, float* m, float* v,
   hipLaunchKernelGGL(adam_kernel, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0, s, n, p, g,
                      m, v, sc, vec ? 1 : 0);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fixed scratch for the LayerNorm backward entry point that allocates nothing
+// (repops_layernorm_backward_rows_noalloc): the block partials of the
+// parameter gradients go to this array instead of a caller's workspace.  Each
+// device holds its own copy for the life of the process.  In host code the
+// array's name only stands in for it, so the device address is looked up once
+// per device (with that device current) and kept; calls on one device share
+// the array.  Every partial the combine reads is written first in the same
+// call, so nothing needs clearing between calls.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[kNoallocScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace repops

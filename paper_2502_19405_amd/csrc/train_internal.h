@@ -63,6 +63,11 @@ bool layernorm_colsplit_plan(int64_t rows, int64_t cols, int64_t k_block, Colspl
 hipError_t launch_layernorm_bwd_colsplit(const RowBwdArgs& a, const LnParamArgs& p,
                                          const ColsplitPlan& pl, hipStream_t s);
 
+// Device address of the fixed scratch array (kNoallocScratchBytes) on the
+// current device, looked up once per device.
+constexpr uint64_t kNoallocScratchBytes = uint64_t(8) << 20;
+hipError_t noalloc_scratch(void** ptr);
+
 hipError_t launch_gelu_bwd(int64_t n, const float* x, const float* dy, float* dx, int threads,
                            int max_blocks, hipStream_t s, bool erf_form);
 

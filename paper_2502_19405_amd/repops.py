@@ -17,7 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librepops.so")
 
 (OK, ERR_NULL, ERR_SHAPE, ERR_STRIDE, ERR_ALIAS, ERR_ORDER, ERR_LAUNCH, ERR_HIP, ERR_VALUE,
- ERR_WORKSPACE) = range(10)
+ ERR_WORKSPACE, ERR_SCRATCH) = range(11)
+NOALLOC_SCRATCH_BYTES = 8 << 20  # REPOPS_NOALLOC_SCRATCH_BYTES
 K_FMA, K_MUL_ADD = 0, 1
 ROW_STRIDED_TREE, ROW_BLOCKED_LTR = 0, 1
 LAUNCH_AUTO = 0
@@ -99,6 +100,8 @@ _SIGNATURES = {
     "repops_layernorm_backward_workspace": (_i32, [_op, _i64, _i64, ctypes.POINTER(ctypes.c_uint64)]),
     "repops_layernorm_backward_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp,
                                               _vp, _i64, _vp, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
+    "repops_layernorm_backward_rows_noalloc": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _vp,
+                                                      _vp, _vp, _vp, _i64, _vp, _vp, _lp, _vp]),
     "repops_gelu_backward": (_i32, [_op, _i64, _vp, _vp, _vp, _lp, _vp]),
     "repops_colsum_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _vp, ctypes.c_uint64, _lp, _vp]),
     "repops_adam_step": (_i32, [_op, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32, _f32, _f32, _i64,
@@ -452,6 +455,38 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
         ptr(dbeta, "dbeta"), wptr, wbytes, _launch(launch), _stream(X))
     _check(rc, "repops_layernorm_backward_rows")
     return dx, dgamma, dbeta
+
+
+def layernorm_backward_rows_noalloc(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tensor,
+                                    rstd: torch.Tensor, gamma: torch.Tensor | None,
+                                    dx_out: torch.Tensor | None, dgamma_out: torch.Tensor | None,
+                                    dbeta_out: torch.Tensor | None, order: Order | None = None,
+                                    launch: Launch | None = None):
+    """repops_layernorm_backward_rows_noalloc: the LayerNorm backward into the
+    caller's outputs (any of them None to skip it), with the parameter
+    gradients' partials in the library's fixed scratch array -- nothing is
+    allocated here or in the library.  Calls that overlap on one device
+    race on the scratch array."""
+    rows, cols, ldx = _rows(X, "X")
+    r2, c2, lddy = _rows(dY, "dY")
+    if (r2, c2) != (rows, cols):
+        raise ValueError("X and dY shapes differ")
+    for t, name in ((mean, "mean"), (rstd, "rstd")):
+        if t.numel() != rows or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [{rows}] tensor")
+    for t, name in ((gamma, "gamma"), (dgamma_out, "dgamma_out"), (dbeta_out, "dbeta_out")):
+        if t is not None and (t.numel() != cols or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous [{cols}] tensor")
+    lddx = cols
+    if dx_out is not None:
+        _, _, lddx = _rows(dx_out, "dx_out")
+    ptr = lambda t, n: None if t is None else _dev(t, n)  # noqa: E731
+    rc = load().repops_layernorm_backward_rows_noalloc(
+        _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
+        _dev(mean, "mean"), _dev(rstd, "rstd"), ptr(gamma, "gamma"), ptr(dx_out, "dX"), lddx,
+        ptr(dgamma_out, "dgamma"), ptr(dbeta_out, "dbeta"), _launch(launch), _stream(X))
+    _check(rc, "repops_layernorm_backward_rows_noalloc")
+    return dx_out, dgamma_out, dbeta_out
 
 
 def colsum_rows(X: torch.Tensor, order: Order | None = None, out: torch.Tensor | None = None,

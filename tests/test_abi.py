@@ -245,6 +245,21 @@ def test_training_rejections(rp):
     assert adam(n=0, p=None, g=None, m=None, v=None) == rp.OK
     assert rp.status_str(rp.ERR_WORKSPACE).startswith("workspace")
 
+    # the no-allocation LayerNorm backward: its fixed scratch bounds the size
+    def nb(rows=64, cols=8, mean=FAKE_M, order=None, dg=FAKE_D):
+        return lib.repops_layernorm_backward_rows_noalloc(
+            order or o, rows, cols, FAKE_A, cols, FAKE_B, cols, mean, FAKE_R, None, FAKE_C, cols,
+            dg, None, None, None)
+    assert rp.NOALLOC_SCRATCH_BYTES == 8 << 20
+    assert nb(rows=262144, cols=768) == rp.ERR_SCRATCH     # 2 * 4096 * 768 * 4 B > 8 MiB
+    assert nb(rows=64 * 1366, cols=768) == rp.ERR_SCRATCH  # just over: 1366 blocks
+    assert nb(rows=64, mean=None) == rp.ERR_NULL           # one block: no scratch needed
+    assert nb(rows=64, dg=FAKE_C + 4) == rp.ERR_ALIAS
+    assert nb(cols=0) == rp.ERR_SHAPE
+    assert nb(order=_order(version=0)) == rp.ERR_ORDER
+    assert nb(rows=0, cols=8, dg=None) == rp.OK
+    assert "scratch" in rp.status_str(rp.ERR_SCRATCH)
+
 
 @no_gpu_only
 def test_llama_rejections(rp):
