@@ -192,6 +192,46 @@ static const float *col_of_b(const float *B, int64_t ldb, int trans_b, int64_t j
     return B + j;
 }
 
+/*
+ * Layout only: an operand whose k walk is strided in memory (A read
+ * transposed, B read as stored) is first copied into one contiguous vector per
+ * output row (of A) or output column (of B), so that every dot product reads
+ * memory with unit stride.  Values are copied unchanged and each output still
+ * takes its terms in ascending k, so the results are the same bits.  The copy
+ * covers batch0 x batch1 x count vectors of k elements: vector (b0, b1, r)
+ * holds the elements at src + b0 s0 + b1 s1 + r + kk inc, kk = 0 .. k-1.
+ */
+typedef struct {
+    const float *src; int64_t s0, s1, batch1, count, k, inc;
+    float *dst;
+} gather_ctx;
+
+static void gather_range(void *vctx, int64_t v0, int64_t v1)
+{
+    const gather_ctx *c = (const gather_ctx *)vctx;
+    for (int64_t v = v0; v < v1; ++v) {
+        const int64_t r = v % c->count, b = v / c->count;
+        const float *p = c->src + (b / c->batch1) * c->s0 + (b % c->batch1) * c->s1 + r;
+        float *d = c->dst + v * c->k;
+        for (int64_t kk = 0; kk < c->k; ++kk) d[kk] = p[kk * c->inc];
+    }
+}
+
+/* Contiguous copy of a strided operand, or NULL (then the strided operand is
+ * read in place: same values, same order, only slower). */
+static float *gather(const float *src, int64_t s0, int64_t s1, int64_t batch0, int64_t batch1,
+                     int64_t count, int64_t k, int64_t inc, int nthreads)
+{
+    const int64_t nvec = batch0 * batch1 * count;
+    if (nvec <= 0 || k <= 0 || (uint64_t)nvec > SIZE_MAX / sizeof(float) / (uint64_t)k)
+        return NULL;
+    float *dst = (float *)malloc((size_t)(nvec * k) * sizeof(float));
+    if (!dst) return NULL;
+    gather_ctx c = {src, s0, s1, batch1, count, k, inc, dst};
+    parallel_for(nthreads, nvec, gather_range, &c);
+    return dst;
+}
+
 /* Epilogue (paper silent; reading used here): the scale alpha multiplies the
  * finished contraction, then the bias is added, each one rounding. */
 typedef struct {
@@ -202,6 +242,7 @@ typedef struct {
     const float *B; int64_t ldb; int trans_b;
     const float *bias;
     float *C; int64_t ldc;
+    const float *Ag, *Bg;  /* contiguous copies (row i of A, column j of B) or NULL */
 } matmul_ctx;
 
 static void matmul_rows(void *vctx, int64_t i0, int64_t i1)
@@ -212,6 +253,8 @@ static void matmul_rows(void *vctx, int64_t i0, int64_t i1)
             int64_t ia, ib;
             const float *a = row_of_a(c->A, c->lda, c->trans_a, i, &ia);
             const float *b = col_of_b(c->B, c->ldb, c->trans_b, j, &ib);
+            if (c->Ag) { a = c->Ag + i * c->k; ia = 1; }
+            if (c->Bg) { b = c->Bg + j * c->k; ib = 1; }
             float v = repops_ref_dot(c->k_block, c->k_inner, c->k, a, ia, b, ib);
             if (c->bias) v = v + c->bias[j];
             c->C[i * c->ldc + j] = v;
@@ -227,8 +270,13 @@ int repops_ref_matmul(int64_t k_block, int k_inner, int64_t m, int64_t n, int64_
     if (check_order_k(k_block, k_inner) || m < 0 || n < 0 || k < 0) return -1;
     if (m == 0 || n == 0) return 0;
     if (!C || (k > 0 && (!A || !B))) return -2;
-    matmul_ctx c = {k_block, k_inner, n, k, A, lda, trans_a, B, ldb, trans_b, bias, C, ldc};
+    float *Ag = (k > 0 && trans_a) ? gather(A, 0, 0, 1, 1, m, k, lda, nthreads) : NULL;
+    float *Bg = (k > 0 && !trans_b) ? gather(B, 0, 0, 1, 1, n, k, ldb, nthreads) : NULL;
+    matmul_ctx c = {k_block, k_inner, n, k, A, lda, trans_a, B, ldb, trans_b, bias, C, ldc,
+                    Ag, Bg};
     parallel_for(nthreads, m, matmul_rows, &c);
+    free(Ag);
+    free(Bg);
     return 0;
 }
 
@@ -268,6 +316,7 @@ typedef struct {
     const float *B; int64_t sb0, sb1, ldb; int trans_b;
     float alpha;
     float *C; int64_t sc0, sc1, ldc;
+    const float *Ag, *Bg;  /* contiguous copies (per batch element: rows of A, columns of B) or NULL */
 } bmm_ctx;
 
 static float bmm_one(const bmm_ctx *c, int64_t b0, int64_t b1, int64_t i, int64_t j)
@@ -277,6 +326,9 @@ static float bmm_one(const bmm_ctx *c, int64_t b0, int64_t b1, int64_t i, int64_
     int64_t ia, ib;
     const float *a = row_of_a(Ab, c->lda, c->trans_a, i, &ia);
     const float *b = col_of_b(Bb, c->ldb, c->trans_b, j, &ib);
+    const int64_t bz = b0 * c->batch1 + b1;
+    if (c->Ag) { a = c->Ag + (bz * c->m + i) * c->k; ia = 1; }
+    if (c->Bg) { b = c->Bg + (bz * c->n + j) * c->k; ib = 1; }
     const float v = repops_ref_dot(c->k_block, c->k_inner, c->k, a, ia, b, ib);
     return v * c->alpha;
 }
@@ -303,9 +355,15 @@ int repops_ref_bmm(int64_t k_block, int k_inner, int64_t batch0, int64_t batch1,
     if (check_order_k(k_block, k_inner) || batch0 < 0 || batch1 < 0 || m < 0 || n < 0 || k < 0)
         return -1;
     if (batch0 == 0 || batch1 == 0 || m == 0 || n == 0) return 0;
+    float *Ag = (k > 0 && trans_a) ? gather(A, sa0, sa1, batch0, batch1, m, k, lda, nthreads)
+                                   : NULL;
+    float *Bg = (k > 0 && !trans_b) ? gather(B, sb0, sb1, batch0, batch1, n, k, ldb, nthreads)
+                                    : NULL;
     bmm_ctx c = {k_block, k_inner, batch1, m, n, k, A, sa0, sa1, lda, trans_a,
-                 B, sb0, sb1, ldb, trans_b, alpha, C, sc0, sc1, ldc};
+                 B, sb0, sb1, ldb, trans_b, alpha, C, sc0, sc1, ldc, Ag, Bg};
     parallel_for(nthreads, batch0 * batch1 * m, bmm_rows, &c);
+    free(Ag);
+    free(Bg);
     return 0;
 }
 
@@ -319,7 +377,7 @@ int repops_ref_bmm_at(int64_t k_block, int k_inner, int64_t batch0, int64_t batc
     if (check_order_k(k_block, k_inner) || batch0 < 0 || batch1 < 0 || m < 0 || n < 0 || k < 0)
         return -1;
     bmm_ctx c = {k_block, k_inner, batch1, m, n, k, A, sa0, sa1, lda, trans_a,
-                 B, sb0, sb1, ldb, trans_b, alpha, NULL, 0, 0, 0};
+                 B, sb0, sb1, ldb, trans_b, alpha, NULL, 0, 0, 0, NULL, NULL};
     fenv_t saved;
     fegetenv(&saved);
     install_ieee_env();
