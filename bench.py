@@ -88,6 +88,61 @@ def event_time_ms(fn, reps, warmup=2):
     return start.elapsed_time(stop) / reps
 
 
+class ClockSampler:
+    """Samples the GPU's current shader clock (the starred level of the
+    kernel driver's pp_dpm_sclk table) every few milliseconds in a background
+    thread; median() is None where the table is not readable or ambiguous."""
+
+    def __init__(self, period_s=0.01):
+        import glob
+        import threading
+        paths = glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")
+        self.path = paths[0] if len(paths) == 1 else None
+        self.samples, self.period, self._stop = [], period_s, threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        try:
+            for line in open(self.path):
+                if line.strip().endswith("*"):
+                    return int(line.split(":")[1].strip().rstrip("*").strip().lower().rstrip("mhz"))
+        except (OSError, ValueError, IndexError):
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = self._read()
+            if v:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.path:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self.path:
+            self._thread.join()
+
+    def median(self):
+        s = sorted(self.samples[len(self.samples) // 4:])  # past the first quarter
+        return s[len(s) // 2] if s else None
+
+
+def clock_ramp(fn, ms=150.0):
+    """Repeat fn for a fixed wall-clock duration (untimed) so that a
+    matrix-core workload is timed at steady clocks."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        fn()
+        torch.cuda.synchronize()
+
+
 def graph_time_ms(fn, calls=20, reps=10):
     """Average duration of fn() with `calls` of them captured in one HIP graph
     and the graph replayed `reps` times: the kernels' own time without host
@@ -223,6 +278,7 @@ def secondary(repops, steps, streaming_only=False, headline=None):
         c2 = inputs.gemm2048_bias()
         A2, B2, bias2 = t(c2["A"]), t(c2["B"]), t(c2["bias"])
         C2 = torch.empty((2048, 2048), device=dev)
+        clock_ramp(lambda: repops.matmul(A2, B2, bias2, out=C2))
         out["gemm2048_bias"] = _rate(
             event_time_ms(lambda: repops.matmul(A2, B2, bias2, out=C2), steps * 5, warmup=20),
             flops=2 * 2048 ** 3)
@@ -372,8 +428,13 @@ def secondary(repops, steps, streaming_only=False, headline=None):
 
     # DistilBERT feed-forward block: 4096 tokens, 768 -> 3072 -> 768, GELU, LayerNorm
     X, W1, W2, b1, b2 = (t(d[k]) for k in ("X", "W1", "W2", "b1", "b2"))
+    clock_ramp(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet))
     ms = event_time_ms(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet), steps)
     out["distilbert_mlp_block"] = _rate(ms, flops=2 * 2 * 4096 * 768 * 3072)
+    # the same block replayed from a HIP graph: the kernels without host launch gaps
+    out["distilbert_mlp_block"].update(_graph_rate(
+        graph_time_ms(lambda: pipelines.mlp_forward(X, W1, b1, W2, b2, gam, bet)),
+        flops=2 * 2 * 4096 * 768 * 3072))
     # one whole training step of the block: forward, every gradient, AdamW over
     # all 4.72 M parameters (six GEMMs of 2 * 4096 * 768 * 3072 flop each)
     st = pipelines.MlpTrainState(W1, b1, W2, b2, gam, bet)
@@ -381,6 +442,11 @@ def secondary(repops, steps, streaming_only=False, headline=None):
     sbufs = {}
     ms = event_time_ms(lambda: pipelines.mlp_train_step(st, X, dYb, bufs=sbufs), steps)
     out["distilbert_mlp_train_step"] = _rate(ms, flops=6 * 2 * 4096 * 768 * 3072)
+    # replayed from a HIP graph (the captured steps repeat one step's Adam
+    # scalars; the kernels and their sizes are those of every step)
+    out["distilbert_mlp_train_step"].update(_graph_rate(
+        graph_time_ms(lambda: pipelines.mlp_train_step(st, X, dYb, bufs=sbufs), calls=5),
+        flops=6 * 2 * 4096 * 768 * 3072))
     del X, W1, W2, b1, b2, st, dYb, sbufs
 
     # Llama attention block: 4 x 1024 tokens, d 4096, 32 heads
@@ -390,6 +456,7 @@ def secondary(repops, steps, streaming_only=False, headline=None):
     bufs["S"] = torch.empty((4, 32, 1024, 1024), device=dev)
     bufs["P"] = torch.empty((4 * 32 * 1024, 1024), device=dev)
     fl = 4 * 2 * 4096 ** 3 + 2 * 2 * 4 * 32 * 1024 * 1024 * 128
+    clock_ramp(lambda: pipelines.attention_forward(X, Wq, Wk, Wv, Wo, 4, 1024, 32, buffers=bufs))
     ms = event_time_ms(lambda: pipelines.attention_forward(X, Wq, Wk, Wv, Wo, 4, 1024, 32,
                                                            buffers=bufs), max(steps // 4, 3))
     out["llama_attention_block"] = _rate(ms, flops=fl)
@@ -498,14 +565,15 @@ def main():
 
     # timed steps: an event before dX, between the two products and after dW
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
-    t0 = time.perf_counter()
-    ev[0].record()
-    for i in range(args.steps):
-        prod_dx()
-        ev[2 * i + 1].record()
-        prod_dw()
-        ev[2 * i + 2].record()
-    torch.cuda.synchronize()
+    with ClockSampler() as clock:
+        t0 = time.perf_counter()
+        ev[0].record()
+        for i in range(args.steps):
+            prod_dx()
+            ev[2 * i + 1].record()
+            prod_dw()
+            ev[2 * i + 2].record()
+        torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
     dx_ms = sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
     dw_ms = sum(ev[2 * i + 1].elapsed_time(ev[2 * i + 2]) for i in range(args.steps)) / args.steps
@@ -545,6 +613,13 @@ def main():
                      "unit": "TFLOP/s", "frac": kernels[dom]["frac"],
                      "traffic": kernels[dom]["traffic"]},
         "kernels": kernels,
+        # the shader clock the chip held during the timed steps (the published
+        # peak assumes 2.4 GHz) and the slower product's fraction of the peak
+        # at that clock
+        "sustained_clock": ({"mhz": clock.median(),
+                             "frac_at_clock": round(kernels[dom]["TFLOP/s"] / (
+                                 FP32_VECTOR_PEAK_TFLOPS * clock.median() / 2400.0), 4)}
+                            if clock.median() else None),
         "clock_ramp": {"ms": round(ramp_ms, 1), "steps": ramp_steps},
         "inputs_sha256": digests,
     }

@@ -65,3 +65,17 @@ def test_committed_counter_summary_parses(bench):
                                  ("dW", 4 * (8192 * 4096 + 8192 * 14336 + 4096 * 14336))):
         v = bench.measured_traffic("auto", product)
         assert v is None or v >= algorithmic, (product, v)
+
+
+def test_clock_sampler_reads_the_starred_level(bench, tmp_path):
+    f = tmp_path / "pp_dpm_sclk"
+    f.write_text("0: 500Mhz\n1: 2187Mhz *\n2: 2400Mhz\n")
+    c = bench.ClockSampler()
+    c.path = str(f)
+    assert c._read() == 2187
+    c.samples = [2400, 2100, 2150, 2160, 2170]
+    assert c.median() == 2160  # the first quarter (ramp) is left out
+    f.write_text("0: 500Mhz\n")
+    assert c._read() is None
+    c.path = str(tmp_path / "missing")
+    assert c._read() is None
