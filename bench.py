@@ -479,6 +479,12 @@ def secondary(repops, steps, streaming_only=False, headline=None):
         2 * 4 * 32 * 128 * (1024 * 1025 // 2) / ms / 1e9, 2)
     del X, Wq, Wk, Wv, Wo, bufs, Q, K, S, P, V, O
 
+    # the headline's two products as one grouped launch (the pipeline's path)
+    if headline is not None:
+        X, dY, W, gx, gw = (headline[k] for k in ("X", "dY", "W", "dX", "dW"))
+        ms = event_time_ms(lambda: pipelines.linear_backward(X, dY, W, out_dx=gx, out_dw=gw), 5)
+        out["llama_linear_backward_grouped"] = _rate(ms, flops=2 * 2 * 8192 * 4096 * 14336)
+        del X, dY, W, gx, gw
     # one rank's share of dW under 8-way data parallelism: the headline's dW
     # product over 1024 of the 8192 tokens (the ordered cross-rank combine is
     # not built)
@@ -632,7 +638,7 @@ def main():
         result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_secondary:
         result["secondary"] = secondary(repops, 20, args.streaming_only,
-                                        headline={"X": X, "dY": dY, "dW": dW})
+                                        headline={"X": X, "dY": dY, "W": W, "dX": dX, "dW": dW})
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(d)
     print(json.dumps(result), flush=True)

@@ -167,6 +167,37 @@ repops_status_t repops_matmul(const repops_order_t *order, int64_t m, int64_t n,
  * multiplication).  Strides may be 0 for A and B; the C regions of different
  * batch elements must not overlap each other (not checked) nor A or B.
  */
+/*
+ * repops_matmul_grouped -- several independent products C_p = A_p.B_p (+ bias_p)
+ * in one call, Section 3.2 (matrix multiplication) as for repops_matmul: each
+ * product's outputs take exactly the bits repops_matmul gives for the same
+ * arguments.  The products run concurrently (one launch whose workgroups cover
+ * every product's output tiles, the products with the longest contraction
+ * first), so that products with few output tiles share the compute units:
+ * the weight and input gradients of a linear layer are the intended use.
+ *   count   0 .. REPOPS_MAX_GROUP products; descs: host array of count entries
+ *           (read during the call only; may be NULL when count = 0).
+ *   each desc's fields as repops_matmul's arguments.
+ *   No C_p may overlap its own operands or any other product's A, B, bias or C
+ *   (REPOPS_ERR_ALIAS).
+ *   launch  NULL or AUTO.  When every nonempty product has K > 0, K and k_block
+ *           multiples of 16, 16-byte aligned rows and the fused order, one
+ *           launch of the 128 x 128 matrix-core tile runs them all; otherwise the
+ *           products run one after another with repops_matmul's automatic
+ *           launch (the same bits either way).
+ */
+typedef struct repops_gemm_desc {
+    int64_t m, n, k;
+    const float *A; int64_t lda; int32_t trans_a;
+    const float *B; int64_t ldb; int32_t trans_b;
+    const float *bias;
+    float *C; int64_t ldc;
+} repops_gemm_desc_t;
+#define REPOPS_MAX_GROUP 8
+repops_status_t repops_matmul_grouped(const repops_order_t *order, int32_t count,
+                                      const repops_gemm_desc_t *descs,
+                                      const repops_launch_t *launch, void *hip_stream);
+
 repops_status_t repops_bmm(const repops_order_t *order, int64_t batch0, int64_t batch1,
                            int64_t m, int64_t n, int64_t k,
                            const float *A, int64_t sa0, int64_t sa1, int64_t lda, int32_t trans_a,

@@ -373,6 +373,94 @@ repops_status_t repops_matmul(const repops_order_t* order, int64_t m, int64_t n,
   return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
 }
 
+repops_status_t repops_matmul_grouped(const repops_order_t* order, int32_t count,
+                                      const repops_gemm_desc_t* descs,
+                                      const repops_launch_t* launch, void* hip_stream) {
+  static_assert(REPOPS_MAX_GROUP == repops::kMaxGroup, "one group size");
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (count < 0 || count > REPOPS_MAX_GROUP) return REPOPS_ERR_SHAPE;
+  if (count == 0) return REPOPS_OK;
+  if (!descs) return REPOPS_ERR_NULL;
+  if (launch && (launch->kind != REPOPS_LAUNCH_AUTO || !launch_params_zero_from(launch, 0)))
+    return REPOPS_ERR_LAUNCH;
+  GemmArgs g[REPOPS_MAX_GROUP];
+  bool live[REPOPS_MAX_GROUP];
+  for (int p = 0; p < count; ++p) {
+    const repops_gemm_desc_t& d = descs[p];
+    g[p] = GemmArgs{};
+    g[p].batch0 = 1; g[p].batch1 = 1; g[p].m = d.m; g[p].n = d.n; g[p].k = d.k;
+    g[p].A = d.A; g[p].lda = d.lda; g[p].ta = d.trans_a;
+    g[p].B = d.B; g[p].ldb = d.ldb; g[p].tb = d.trans_b;
+    g[p].C = d.C; g[p].ldc = d.ldc;
+    g[p].bias = d.bias; g[p].alpha = 1.0f; g[p].has_alpha = 0;
+    g[p].k_block = order->k_block;
+    g[p].fused = order->k_inner == REPOPS_K_FMA ? 1 : 0;
+    const repops_status_t st = check_operands(g[p]);
+    if (st != REPOPS_OK) return st;
+    live[p] = g[p].m > 0 && g[p].n > 0;
+  }
+  // The products run concurrently: no output may touch another product's
+  // operands or output.
+  for (int p = 0; p < count; ++p) {
+    if (!live[p]) continue;
+    const Extent ce = extent_of(g[p].C, 1, 0, 1, 0, g[p].m, g[p].n, g[p].ldc);
+    for (int q = 0; q < count; ++q) {
+      if (q == p || !live[q]) continue;
+      if (overlaps(ce, extent_of(g[q].C, 1, 0, 1, 0, g[q].m, g[q].n, g[q].ldc)))
+        return REPOPS_ERR_ALIAS;
+      if (g[q].k > 0) {
+        const Extent ae = g[q].ta ? extent_of(g[q].A, 1, 0, 1, 0, g[q].k, g[q].m, g[q].lda)
+                                  : extent_of(g[q].A, 1, 0, 1, 0, g[q].m, g[q].k, g[q].lda);
+        const Extent be = g[q].tb ? extent_of(g[q].B, 1, 0, 1, 0, g[q].n, g[q].k, g[q].ldb)
+                                  : extent_of(g[q].B, 1, 0, 1, 0, g[q].k, g[q].n, g[q].ldb);
+        if (overlaps(ce, ae) || overlaps(ce, be)) return REPOPS_ERR_ALIAS;
+      }
+      if (g[q].bias && overlaps(ce, extent_of(g[q].bias, 1, 0, 1, 0, 1, g[q].n, g[q].n)))
+        return REPOPS_ERR_ALIAS;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  bool one = order->k_inner == REPOPS_K_FMA && (order->k_block == 0 || order->k_block % 16 == 0);
+  int n_live = 0;
+  for (int p = 0; p < count; ++p) {
+    if (!live[p]) continue;
+    ++n_live;
+    one = one && g[p].k > 0 && repops::gemm_mfma_staged_ok(g[p], 0);
+  }
+  if (n_live == 0) return REPOPS_OK;
+  if (!one) {
+    for (int p = 0; p < count; ++p) {
+      if (!live[p]) continue;
+      const repops_status_t st = run_gemm(order, g[p], nullptr, s);
+      if (st != REPOPS_OK) return st;
+    }
+    return REPOPS_OK;
+  }
+  // One launch: the products with the longest contraction first, so that
+  // their tiles start first and the short ones fill the compute units behind
+  // them.
+  int idx[REPOPS_MAX_GROUP], n = 0;
+  for (int p = 0; p < count; ++p)
+    if (live[p]) idx[n++] = p;
+  for (int a = 1; a < n; ++a)
+    for (int b = a; b > 0 && g[idx[b]].k > g[idx[b - 1]].k; --b) {
+      const int t = idx[b]; idx[b] = idx[b - 1]; idx[b - 1] = t;
+    }
+  int bm, bn;
+  repops::gemm_mfma_tile(0, &bm, &bn);
+  repops::GroupArgs ga{};
+  ga.count = n;
+  ga.first[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    ga.g[i] = g[idx[i]];
+    ga.tiles_m[i] = (ga.g[i].m + bm - 1) / bm;
+    ga.tiles_n[i] = (ga.g[i].n + bn - 1) / bn;
+    ga.first[i + 1] = ga.first[i] + ga.tiles_m[i] * ga.tiles_n[i];
+  }
+  if (ga.first[n] > kMaxDim) return REPOPS_ERR_SHAPE;
+  return hip_status(repops::launch_gemm_mfma_grouped(ga, s));
+}
+
 repops_status_t repops_bmm(const repops_order_t* order, int64_t batch0, int64_t batch1, int64_t m,
                            int64_t n, int64_t k, const float* A, int64_t sa0, int64_t sa1,
                            int64_t lda, int32_t trans_a, const float* B, int64_t sb0, int64_t sb1,

@@ -307,7 +307,10 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB>
+// DUAL: a second set of block partials, so that each 64-deep block's adds into
+// acc are spread over the next block's matrix steps (the staged kernel uses it
+// where a wave owns one instruction tile).
+template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB, bool DUAL>
 struct StagedTile {
   static_assert(BK % 16 == 0, "k slices hold whole 16-step groups");
   static constexpr int NW = WM * WN;
@@ -579,13 +582,16 @@ struct StagedTile {
     // ring slots and the block boundaries known at compile time.
     constexpr int FSPB = BK <= 64 ? 64 / BK : 0;
     if (FSPB > 0 && NS % FSPB == 0 && spb == FSPB && nslices % NS == 0) {
-      if constexpr (IM * IN == 1 && FSPB == NS) {
-        // One instruction tile per wave leaves room for a second partial set:
-        // one ring turn is one k block, alternating between P and Q, and each
-        // block's partials join acc during the next block's first slice.  Q
-        // starts at +0, so the first block adds +0 to +0.
+      if constexpr (DUAL && FSPB == NS) {
+        // The second partial set: one ring turn is one k block, alternating
+        // between P and Q, and each block's partials join acc during the next
+        // block's first slice.  Q starts at +0, so the first block adds +0 to
+        // +0.
         v32f Q[IM][IN];
-        Q[0][0] = v32f{};
+#pragma unroll
+        for (int i = 0; i < IM; ++i)
+#pragma unroll
+          for (int j = 0; j < IN; ++j) Q[i][j] = v32f{};
         int s0 = 0;
         for (; s0 + 2 * NS <= nslices; s0 += 2 * NS) {
           turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
@@ -593,9 +599,15 @@ struct StagedTile {
         }
         if (s0 < nslices) {
           turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
-          acc[0][0] = acc[0][0] + P[0][0];
+#pragma unroll
+          for (int i = 0; i < IM; ++i)
+#pragma unroll
+            for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
         } else {
-          acc[0][0] = acc[0][0] + Q[0][0];
+#pragma unroll
+          for (int i = 0; i < IM; ++i)
+#pragma unroll
+            for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + Q[i][j];
         }
       } else {
         for (int s0 = 0; s0 < nslices; s0 += NS) {
@@ -658,7 +670,8 @@ struct StagedTile {
 template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool TA, bool TB>
 __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
     GemmArgs g, int64_t tiles_m, int64_t tiles_n, int64_t ntiles, int) {
-  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB>;
+  // one instruction tile per wave leaves registers for the second partial set
+  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB, (BM / WM / 32) * (BN / WN / 64) == 1>;
   __shared__ typename T::Smem sm;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     int64_t bz, tm, tn;
@@ -666,6 +679,33 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
     const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
     T::run(g, sm, b0, b1, tm * BM, tn * BN);
   }
+}
+
+// Several products in one launch with table entry 0's tile: workgroup t
+// finds its product p (first[p] <= t < first[p + 1]) and runs that product's
+// tile with the transposes it needs.  The four layouts' LDS forms have the
+// same size, so one allocation serves them all.  Every tile is the same
+// computation as in a launch of its own product, so the bits are the same.
+template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool DUAL>
+__global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_grouped_kernel(GroupArgs ga) {
+  using T00 = StagedTile<BM, BN, BK, WM, WN, NS, false, false, DUAL>;
+  using T01 = StagedTile<BM, BN, BK, WM, WN, NS, false, true, DUAL>;
+  using T10 = StagedTile<BM, BN, BK, WM, WN, NS, true, false, DUAL>;
+  using T11 = StagedTile<BM, BN, BK, WM, WN, NS, true, true, DUAL>;
+  static_assert(sizeof(typename T00::Smem) == sizeof(typename T11::Smem), "one LDS form size");
+  __shared__ typename T00::Smem sm;
+  const int64_t t = blockIdx.x;
+  int p = 0;
+  while (p + 1 < ga.count && t >= ga.first[p + 1]) ++p;
+  const GemmArgs& g = ga.g[p];
+  const int64_t ntiles = ga.first[p + 1] - ga.first[p];
+  int64_t bz, tm, tn;
+  tile_coords(t - ga.first[p], ntiles, ga.tiles_m[p], ga.tiles_n[p], &bz, &tm, &tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  if (!g.ta && !g.tb) T00::run(g, sm, 0, 0, m0, n0);
+  else if (!g.ta) T01::run(g, *reinterpret_cast<typename T01::Smem*>(&sm), 0, 0, m0, n0);
+  else if (!g.tb) T10::run(g, *reinterpret_cast<typename T10::Smem*>(&sm), 0, 0, m0, n0);
+  else T11::run(g, *reinterpret_cast<typename T11::Smem*>(&sm), 0, 0, m0, n0);
 }
 
 struct MfmaEntry {
@@ -721,6 +761,27 @@ bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0;
 int gemm_mfma_count() { return kMfmaCount; }
 const GemmConfig* gemm_mfma_config(int index) {
   return (index >= 0 && index < kMfmaCount) ? &kMfma[index].cfg : nullptr;
+}
+
+bool gemm_mfma_staged_ok(const GemmArgs& g, int index) {
+  const MfmaEntry& e = kMfma[index];
+  const bool vec_ok = aligned16(g.A) && g.lda % 4 == 0 && g.sa0 % 4 == 0 && g.sa1 % 4 == 0 &&
+                      aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
+  return e.staged[0] && vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
+         g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) && (g.tb || g.n % 4 == 0);
+}
+
+void gemm_mfma_tile(int index, int* bm, int* bn) {
+  *bm = kMfma[index].cfg.bm;
+  *bn = kMfma[index].cfg.bn;
+}
+
+hipError_t launch_gemm_mfma_grouped(const GroupArgs& ga, hipStream_t s) {
+  // table entry 0: 128 x 128 tiles, 8 waves, a 4-slot ring of 16-deep slices
+  const int64_t total = ga.first[ga.count];
+  hipLaunchKernelGGL((gemm_mfma_grouped_kernel<128, 128, 16, 4, 2, 4, 2, true>),
+                     dim3(static_cast<unsigned>(total)), dim3(512), 0, s, ga);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {

@@ -29,6 +29,21 @@ const GemmConfig* gemm_tiled_config(int index);
 int gemm_mfma_count();
 const GemmConfig* gemm_mfma_config(int index);
 
+// Several independent products in one launch of the default matrix-core tile
+// (table entry 0): problem p owns tiles [first[p], first[p + 1]).  Each
+// product must meet the staged kernel's conditions (gemm_mfma_staged_ok).
+constexpr int kMaxGroup = 8;
+struct GroupArgs {
+  GemmArgs g[kMaxGroup];
+  int64_t first[kMaxGroup + 1];
+  int64_t tiles_m[kMaxGroup], tiles_n[kMaxGroup];
+  int count;
+};
+bool gemm_mfma_staged_ok(const GemmArgs& g, int index);
+// Tile edge lengths of table entry `index` (for the grouped launch's tiles).
+void gemm_mfma_tile(int index, int* bm, int* bn);
+hipError_t launch_gemm_mfma_grouped(const GroupArgs& ga, hipStream_t s);
+
 hipError_t launch_gemm_simple(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_tiled(const GemmArgs& a, int index, hipStream_t s);
 hipError_t launch_gemm_mfma(const GemmArgs& a, int index, hipStream_t s);

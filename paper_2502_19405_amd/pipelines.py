@@ -45,9 +45,13 @@ def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_lau
     hd = d // heads
     alpha = attention_scale(hd)
     bufs = buffers or {}
-    Q = repops.matmul(X, Wq, order=order, launch=gemm_launch, out=bufs.get("Q"))
-    K = repops.matmul(X, Wk, order=order, launch=gemm_launch, out=bufs.get("K"))
-    V = repops.matmul(X, Wv, order=order, launch=gemm_launch, out=bufs.get("V"))
+    if gemm_launch is None:  # the three projections in one launch
+        Q, K, V = repops.matmul_grouped([(X, Wq, None, bufs.get("Q")), (X, Wk, None, bufs.get("K")),
+                                         (X, Wv, None, bufs.get("V"))], order=order)
+    else:
+        Q = repops.matmul(X, Wq, order=order, launch=gemm_launch, out=bufs.get("Q"))
+        K = repops.matmul(X, Wk, order=order, launch=gemm_launch, out=bufs.get("K"))
+        V = repops.matmul(X, Wv, order=order, launch=gemm_launch, out=bufs.get("V"))
     S = bufs.get("S")
     if S is None:
         S = torch.empty((batch, heads, seq, seq), dtype=torch.float32, device=X.device)
@@ -73,7 +77,12 @@ def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_lau
 
 def linear_backward(X, dY, W, order=None, gemm_launch=None, out_dx=None, out_dw=None):
     """Gradients of Y = X W: dX = dY W^T (contraction over the output
-    features) and dW = X^T dY (contraction over the tokens)."""
+    features) and dW = X^T dY (contraction over the tokens); one grouped launch
+    unless a launch configuration is given."""
+    if gemm_launch is None:
+        dX, dW = repops.matmul_grouped([(dY, W.t(), None, out_dx), (X.t(), dY, None, out_dw)],
+                                       order=order)
+        return dX, dW
     dX = repops.matmul(dY, W.t(), order=order, launch=gemm_launch, out=out_dx)
     dW = repops.matmul(X.t(), dY, order=order, launch=gemm_launch, out=out_dw)
     return dX, dW
@@ -130,30 +139,28 @@ def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps
     mean, rstd = buf("mean", t), buf("rstd", t)
     Y = repops.layernorm_rows(H2, gamma, beta, eps=ln_eps, order=order, out=buf("Y", t, h),
                               mean_out=mean, rstd_out=rstd)
-    # backward.  Each layer's weight and bias gradients do not feed the input
-    # gradient, so they run on a second stream beside it: the weight-gradient
-    # products have few output tiles (hidden x ffn) and leave compute units
-    # free that the input-gradient chain fills.  Every call is deterministic
-    # and writes its own outputs, so the overlap changes no bit.
-    main = torch.cuda.current_stream(dev)
-    if "_side" not in b:
-        b["_side"] = torch.cuda.Stream(device=dev)  # default priority
-    side = b["_side"]
+    # backward.  Each layer's weight gradient (few output tiles, a long
+    # contraction over the tokens) and its input gradient run as one grouped
+    # launch, so that the input gradient's tiles fill the compute units the
+    # weight gradient leaves free; every product keeps its own bits.
     dH2, _, _ = repops.layernorm_backward_rows(H2, dY, mean, rstd, gamma, order=order,
                                                dx_out=buf("dH2", t, h), dgamma_out=ggamma,
                                                dbeta_out=gbeta)
-    side.wait_stream(main)
-    with torch.cuda.stream(side):
+    if gemm_launch is None:
+        _, dG = repops.matmul_grouped([(G.t(), dH2, None, gW2), (dH2, W2.t(), None, buf("dG", t, f))],
+                                      order=order)
+    else:
         repops.matmul(G.t(), dH2, order=order, launch=gemm_launch, out=gW2)
-        repops.colsum_rows(dH2, order=order, out=gb2)
-    dG = repops.matmul(dH2, W2.t(), order=order, launch=gemm_launch, out=buf("dG", t, f))
+        dG = repops.matmul(dH2, W2.t(), order=order, launch=gemm_launch, out=buf("dG", t, f))
+    repops.colsum_rows(dH2, order=order, out=gb2)
     dH1 = repops.gelu_backward(H1, dG, order=order, out=dG)
-    side.wait_stream(main)
-    with torch.cuda.stream(side):
+    if gemm_launch is None:
+        _, dX = repops.matmul_grouped([(X.t(), dH1, None, gW1), (dH1, W1.t(), None, buf("dX", t, h))],
+                                      order=order)
+    else:
         repops.matmul(X.t(), dH1, order=order, launch=gemm_launch, out=gW1)
-        repops.colsum_rows(dH1, order=order, out=gb1)
-    dX = repops.matmul(dH1, W1.t(), order=order, launch=gemm_launch, out=buf("dX", t, h))
-    main.wait_stream(side)
+        dX = repops.matmul(dH1, W1.t(), order=order, launch=gemm_launch, out=buf("dX", t, h))
+    repops.colsum_rows(dH1, order=order, out=gb1)
     # optimizer
     state.step += 1
     repops.adam_step(state.param, state.grad, state.exp_avg, state.exp_avg_sq, lr, betas[0],

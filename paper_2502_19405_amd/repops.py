@@ -75,6 +75,15 @@ class RepopsError(RuntimeError):
         super().__init__(f"{what}: {status_str(code)} (code {code})")
 
 
+class GemmDescT(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int64), ("n", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("A", ctypes.c_void_p), ("lda", ctypes.c_int64), ("trans_a", ctypes.c_int32),
+                ("B", ctypes.c_void_p), ("ldb", ctypes.c_int64), ("trans_b", ctypes.c_int32),
+                ("bias", ctypes.c_void_p), ("C", ctypes.c_void_p), ("ldc", ctypes.c_int64)]
+
+
+MAX_GROUP = 8  # REPOPS_MAX_GROUP
+
 _lib = None
 _i64, _i32, _u32, _f32, _vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_void_p
 _op, _lp = ctypes.POINTER(OrderT), ctypes.POINTER(LaunchT)
@@ -87,6 +96,7 @@ _SIGNATURES = {
     "repops_gemm_config_name": (ctypes.c_char_p, [_u32, _u32]),
     "repops_matmul": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp, _vp,
                              _i64, _lp, _vp]),
+    "repops_matmul_grouped": (_i32, [_op, _i32, ctypes.POINTER(GemmDescT), _lp, _vp]),
     "repops_bmm": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
                           _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _lp, _vp]),
     "repops_softmax_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _lp, _vp]),
@@ -255,6 +265,38 @@ def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
                               _launch(launch), _stream(out))
     _check(rc, "repops_matmul")
     return out
+
+
+def matmul_grouped(products, order: Order | None = None) -> list:
+    """Several independent products in one call: products is a list of
+    (A, B, bias, out) with the meaning of matmul's arguments (bias and out may
+    be None); returns the outputs.  Every output has the bits matmul gives."""
+    if len(products) > MAX_GROUP:
+        raise ValueError(f"at most {MAX_GROUP} products per call")
+    descs = (GemmDescT * max(len(products), 1))()
+    outs = []
+    for d, (A, B, bias, out) in zip(descs, products):
+        pa, m, k, lda, ta = _mat(A, "A")
+        pb, k2, n, ldb, tb = _mat(B, "B")
+        if k != k2:
+            raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+        if out is None:
+            out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+        if out.shape != (m, n) or out.stride(1) != 1:
+            raise ValueError("out must be a row-major [m, n] tensor")
+        pbias = None
+        if bias is not None:
+            if bias.shape != (n,) or not bias.is_contiguous():
+                raise ValueError("bias must be a contiguous [n] tensor")
+            pbias = _dev(bias, "bias")
+        d.m, d.n, d.k = m, n, k
+        d.A, d.lda, d.trans_a, d.B, d.ldb, d.trans_b = pa, lda, ta, pb, ldb, tb
+        d.bias, d.C, d.ldc = pbias, _dev(out, "out"), max(out.stride(0), n, 1)
+        outs.append(out)
+    rc = load().repops_matmul_grouped(_ord(order), len(products), descs, None,
+                                      _stream(outs[0]) if outs else None)
+    _check(rc, "repops_matmul_grouped")
+    return outs
 
 
 def bmm_raw(batch0: int, batch1: int, m: int, n: int, k: int,

@@ -114,6 +114,35 @@ def test_matmul_rejections(rp):
 
 
 @no_gpu_only
+@no_gpu_only
+def test_matmul_grouped_rejections(rp):
+    lib = rp.load()
+    o = _order()
+    D = rp.GemmDescT
+
+    def desc(m=8, n=8, k=8, A=FAKE_A, lda=8, ta=0, B=FAKE_B, ldb=8, tb=0, bias=None, C=FAKE_C,
+             ldc=8):
+        return D(m, n, k, A, lda, ta, B, ldb, tb, bias, C, ldc)
+
+    def call(*ds, count=None, order=None, launch=None):
+        arr = (D * max(len(ds), 1))(*ds)
+        return lib.repops_matmul_grouped(order or o, len(ds) if count is None else count, arr,
+                                         launch, None)
+    assert lib.repops_matmul_grouped(o, 0, None, None, None) == rp.OK
+    assert lib.repops_matmul_grouped(o, 2, None, None, None) == rp.ERR_NULL
+    assert call(desc(), count=-1) == rp.ERR_SHAPE
+    assert call(*[desc(C=FAKE_C + 0x1000 * i) for i in range(9)]) == rp.ERR_SHAPE
+    assert call(desc(), order=_order(version=0)) == rp.ERR_ORDER
+    assert call(desc(), launch=ctypes.byref(rp.Launch(rp.LAUNCH_GEMM_MFMA, (0,)).c())) == \
+        rp.ERR_LAUNCH
+    assert call(desc(ldc=7)) == rp.ERR_STRIDE
+    assert call(desc(C=FAKE_A + 4)) == rp.ERR_ALIAS                  # over its own A
+    assert call(desc(), desc(C=FAKE_C + 16)) == rp.ERR_ALIAS         # two outputs overlap
+    assert call(desc(), desc(A=FAKE_C + 8, C=FAKE_D)) == rp.ERR_ALIAS  # reads another's output
+    assert call(desc(), desc(bias=FAKE_C + 4, C=FAKE_D)) == rp.ERR_ALIAS
+    assert call(desc(m=0), desc(n=0, C=FAKE_D)) == rp.OK               # nothing to compute
+
+
 def test_matmul_zero_sized_is_a_noop(rp):
     # nothing to write: succeeds without touching any pointer or the device
     assert _matmul(rp, m=0, A=None, B=None, C=None) == rp.OK

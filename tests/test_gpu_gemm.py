@@ -287,3 +287,56 @@ def test_negative_zero_partials_vanish_in_the_accumulator(rp, k, k_block):
         got_t = host(rp.matmul(dev(np.ascontiguousarray(A.T)).t(), dev(B),
                                order=rp.Order(k_block=k_block), launch=launch))
         assert_bits_equal(got_t, want, f"transposed A K={k} k_block={k_block} {name}")
+
+
+GROUP_CASES = [
+    # (m, n, k, trans_a, trans_b, bias) per product
+    [(300, 260, 512, 1, 0, False), (520, 300, 128, 0, 1, True)],      # one launch, mixed layouts
+    [(96, 80, 256, 0, 0, True), (200, 132, 48, 1, 1, False), (64, 64, 1024, 0, 1, False)],
+    [(65, 70, 130, 0, 0, True), (33, 17, 64, 1, 0, False)],           # K % 16 != 0: one by one
+    [(0, 10, 16, 0, 0, False), (40, 44, 0, 0, 0, True), (70, 72, 96, 0, 0, False)],  # empty ones
+]
+
+
+@pytest.mark.parametrize("case", range(len(GROUP_CASES)))
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (64, 1)])
+def test_matmul_grouped_equals_single_products(rp, case, k_block, k_inner):
+    """Every product of a grouped call has the bits of its own matmul call and
+    of the oracle -- in one launch (the staged tile) or one by one (other
+    shapes and orders)."""
+    g = inputs.rng(700 + case * 10 + k_block + k_inner)
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    prods, wants, hosts = [], [], []
+    for m, n, k, ta, tb, with_bias in GROUP_CASES[case]:
+        A = inputs.normal(g, (k, m) if ta else (m, k))
+        B = inputs.normal(g, (n, k) if tb else (k, n))
+        bias = inputs.uniform(g, (n,), -0.1, 0.1) if with_bias else None
+        wants.append(oracle.matmul(A, B, bias, trans_a=bool(ta), trans_b=bool(tb),
+                                   k_block=k_block, k_inner=k_inner))
+        dA, dB = dev(A), dev(B)
+        prods.append((dA.t() if ta else dA, dB.t() if tb else dB,
+                      None if bias is None else dev(bias), None))
+    announce("grouped matmul", case, k_block, k_inner)
+    outs = rp.matmul_grouped(prods, order=order)
+    for i, (out, want, p) in enumerate(zip(outs, wants, prods)):
+        assert_bits_equal(host(out), want, f"product {i} vs oracle")
+        single = rp.matmul(p[0], p[1], p[2], order=order)
+        assert same_bits(out, single), f"product {i} vs its own matmul"
+
+
+def test_matmul_grouped_training_step_shapes(rp):
+    """The feed-forward training step's gradient pairs at full size (weight
+    gradient, K = 4096 tokens, and input gradient), grouped, against their own
+    matmul calls on every output and the oracle on samples."""
+    g = inputs.rng(777)
+    G = inputs.normal(g, (4096, 3072), var=0.1)
+    dH = inputs.normal(g, (4096, 768), var=1e-4)
+    W2 = inputs.normal(g, (3072, 768), var=4e-4)
+    dG, dW, W = dev(G), dev(dH), dev(W2)
+    announce("grouped matmul dW2 + dG")
+    gw, gg = rp.matmul_grouped([(dG.t(), dW, None, None), (dW, W.t(), None, None)])
+    assert same_bits(gw, rp.matmul(dG.t(), dW)) and same_bits(gg, rp.matmul(dW, W.t()))
+    r, c = inputs.sample_indices(8, 512, 3072, 768)
+    assert_bits_equal(host(gw)[r, c], oracle.matmul_at(G, dH, r, c, trans_a=True), "dW2")
+    r, c = inputs.sample_indices(9, 512, 4096, 3072)
+    assert_bits_equal(host(gg)[r, c], oracle.matmul_at(dH, W2, r, c, trans_b=True), "dG")

@@ -106,8 +106,9 @@ def test_distilbert_mlp_training_step_4096_tokens_every_launch(rp):
     """Two whole training steps of the feed-forward block at 4096 tokens --
     forward, every gradient (the dW products contract over the 4096 tokens,
     the dX products over 3072 and 768 features), AdamW of all parameters --
-    equal the oracle's composition on every output (stored digests), under
-    four GEMM launch configurations."""
+    equal the oracle's composition on every output (stored digests), with the
+    automatic launches (gradient products grouped) and under four GEMM launch
+    configurations."""
     import torch
     from paper_2502_19405_amd import pipelines
     from oracle.compose import MLP_PARAM_NAMES
@@ -119,8 +120,9 @@ def test_distilbert_mlp_training_step_4096_tokens_every_launch(rp):
     want = digests.entry("mlp_train_step_4096", ins)
     Xd = dev(d["X"])
     ref = None
-    for name, launch in [(n, l) for n, l in mlp_launches(rp)
-                         if n.split(":")[0] in ("mfma0", "mfma5", "mfma7", "tiled1")]:
+    for name, launch in [("auto (grouped gradient products)", None)] + [
+            (n, l) for n, l in mlp_launches(rp)
+            if n.split(":")[0] in ("mfma0", "mfma5", "mfma7", "tiled1")]:
         st = pipelines.MlpTrainState(*(dev(d[k]) for k in MLP_PARAM_NAMES))
         outs = {}
         for step, dY in enumerate(dYs, start=1):
@@ -199,7 +201,8 @@ def test_llama_attention_block_full_every_launch(rp):
     rows, cols = inputs.sample_indices(4, 512, 4096, 4096)
     samples = {"Q": oracle.matmul_at(d["X"], d["Wq"], rows, cols)}
     ref = None
-    for name, launch in gemm_launches(rp, include_simple=False):
+    for name, launch in [("auto (grouped projections)", None)] + gemm_launches(
+            rp, include_simple=False):
         announce("attention block", name)
         out = pipelines.attention_forward(*args, 4, 1024, 32, gemm_launch=launch, keep=True)
         assert_bits_equal(host(out["Q"])[rows, cols], samples["Q"], f"Q samples {name}")
@@ -279,7 +282,7 @@ def test_llama_linear_backward_full_every_launch(rp, backward_data):
     want_dw = oracle.matmul_at(d["X"], d["dY"], r2, c2, trans_a=True)
     dX_, dY_, W_ = dev(d["X"]), dev(d["dY"]), dev(d["W"])
     ref = None
-    for name, launch in gemm_launches(rp, include_simple=False):
+    for name, launch in [("auto (grouped)", None)] + gemm_launches(rp, include_simple=False):
         announce("linear backward", name)
         gx, gw = pipelines.linear_backward(dX_, dY_, W_, gemm_launch=launch)
         assert_bits_equal(host(gx)[r1, c1], want_dx, f"dX samples {name}")
