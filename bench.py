@@ -468,6 +468,14 @@ def secondary(repops, steps, streaming_only=False, headline=None):
     # causal: only the scores at or below the diagonal are ever read
     out["bmm_qkT_4x32x1024x1024x128"]["causal_useful_TFLOP/s"] = round(
         2 * 4 * 32 * 128 * (1024 * 1025 // 2) / ms / 1e9, 2)
+    # the causal score product: only the tiles at or below each head's diagonal
+    ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 1024, 128, Q, 1024 * 4096, 128, 4096, 0,
+                                              K, 1024 * 4096, 128, 4096, 1, 0.08838835, S,
+                                              32 * 1024 * 1024, 1024 * 1024, 1024,
+                                              causal=repops.CAUSAL_OUTPUT), steps)
+    out["bmm_qkT_causal"] = _rate(ms, flops=2 * 4 * 32 * 128 * (1024 * 1025 // 2))
+    out["bmm_qkT_causal"]["dense_equivalent_TFLOP/s"] = round(
+        2 * 4 * 32 * 1024 * 1024 * 128 / ms / 1e9, 2)
     # PV: P [4*32*1024, 1024] times V's head columns, written in place into O
     P, V, O = bufs["P"], bufs["V"], bufs["O"]
     ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 128, 1024, P, 32 * 1024 * 1024,
@@ -477,6 +485,14 @@ def secondary(repops, steps, streaming_only=False, headline=None):
     # causal: row i of P has i + 1 nonzero probabilities
     out["bmm_pv_4x32x1024x128x1024"]["causal_useful_TFLOP/s"] = round(
         2 * 4 * 32 * 128 * (1024 * 1025 // 2) / ms / 1e9, 2)
+    # P's all-zero blocks skipped (the same bits)
+    ms = event_time_ms(lambda: repops.bmm_raw(4, 32, 1024, 128, 1024, P, 32 * 1024 * 1024,
+                                              1024 * 1024, 1024, 0, V, 1024 * 4096, 128, 4096, 0,
+                                              1.0, O, 1024 * 4096, 128, 4096,
+                                              causal=repops.CAUSAL_A), steps)
+    out["bmm_pv_causal"] = _rate(ms, flops=2 * 4 * 32 * 128 * (1024 * 1025 // 2))
+    out["bmm_pv_causal"]["dense_equivalent_TFLOP/s"] = round(
+        2 * 4 * 32 * 1024 * 128 * 1024 / ms / 1e9, 2)
     del X, Wq, Wk, Wv, Wo, bufs, Q, K, S, P, V, O
 
     # the headline's two products as one grouped launch (the pipeline's path)

@@ -206,6 +206,32 @@ repops_status_t repops_bmm(const repops_order_t *order, int64_t batch0, int64_t 
                            const repops_launch_t *launch, void *hip_stream);
 
 /*
+ * repops_bmm_causal -- repops_bmm for the causal attention products (Section
+ * 2.2's key-query and value products of a causal self-attention), with the
+ * same arguments plus a mask over each batch element's rows i, columns j and
+ * contraction index kk:
+ *   REPOPS_CAUSAL_OUTPUT  only the outputs with j <= i are wanted: they get
+ *       exactly repops_bmm's bits; outputs with j > i are unspecified (the
+ *       matrix-core kernels skip output tiles that lie wholly above the
+ *       diagonal and leave them unwritten).  For scores S = alpha Q K^T that a
+ *       causal softmax (causal_period = m) reads only at j <= i.
+ *   REPOPS_CAUSAL_A  the caller guarantees A[i][kk] is zero (either sign) for
+ *       kk > i and B is finite: every output gets exactly repops_bmm's bits.
+ *       The matrix-core kernels skip the k blocks of a row tile that hold only
+ *       such terms -- their block partials would be +0, which leaves the
+ *       accumulator unchanged.  For P V with P a causal softmax's output.
+ *   Any other mask value: REPOPS_ERR_VALUE.  Everything else as repops_bmm.
+ */
+#define REPOPS_CAUSAL_OUTPUT 1
+#define REPOPS_CAUSAL_A 2
+repops_status_t repops_bmm_causal(const repops_order_t *order, int64_t batch0, int64_t batch1,
+                                  int64_t m, int64_t n, int64_t k, const float *A, int64_t sa0,
+                                  int64_t sa1, int64_t lda, int32_t trans_a, const float *B,
+                                  int64_t sb0, int64_t sb1, int64_t ldb, int32_t trans_b,
+                                  float alpha, float *C, int64_t sc0, int64_t sc1, int64_t ldc,
+                                  int32_t mask, const repops_launch_t *launch, void *hip_stream);
+
+/*
  * repops_softmax_rows -- row softmax (an operator of the DistilBERT and Llama
  * programs of Section 4.2; order fixed by the descriptor):
  *     m = max over unmasked x_j;  e_j = exp_rep(x_j - m) (masked: +0);

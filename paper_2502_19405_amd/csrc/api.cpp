@@ -481,6 +481,28 @@ repops_status_t repops_bmm(const repops_order_t* order, int64_t batch0, int64_t 
   return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
 }
 
+repops_status_t repops_bmm_causal(const repops_order_t* order, int64_t batch0, int64_t batch1,
+                                  int64_t m, int64_t n, int64_t k, const float* A, int64_t sa0,
+                                  int64_t sa1, int64_t lda, int32_t trans_a, const float* B,
+                                  int64_t sb0, int64_t sb1, int64_t ldb, int32_t trans_b,
+                                  float alpha, float* C, int64_t sc0, int64_t sc1, int64_t ldc,
+                                  int32_t mask, const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  if (mask != REPOPS_CAUSAL_OUTPUT && mask != REPOPS_CAUSAL_A) return REPOPS_ERR_VALUE;
+  GemmArgs g{};
+  g.batch0 = batch0; g.batch1 = batch1; g.m = m; g.n = n; g.k = k;
+  g.A = A; g.sa0 = sa0; g.sa1 = sa1; g.lda = lda; g.ta = trans_a;
+  g.B = B; g.sb0 = sb0; g.sb1 = sb1; g.ldb = ldb; g.tb = trans_b;
+  g.C = C; g.sc0 = sc0; g.sc1 = sc1; g.ldc = ldc;
+  g.bias = nullptr; g.alpha = alpha; g.has_alpha = 1;
+  g.k_block = order->k_block;
+  g.causal = mask;
+  const repops_status_t st = check_operands(g);
+  if (st != REPOPS_OK) return st;
+  if (batch0 == 0 || batch1 == 0 || m == 0 || n == 0) return REPOPS_OK;
+  return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
+}
+
 repops_status_t repops_softmax_rows(const repops_order_t* order, int64_t rows, int64_t cols,
                                     const float* X, int64_t ldx, float* Y, int64_t ldy,
                                     int64_t causal_period, const repops_launch_t* launch,

@@ -56,6 +56,57 @@ __device__ __forceinline__ void tile_coords(int64_t t, int64_t ntiles, int64_t t
   *tn = in_group / gsize;
 }
 
+// Causal products (per batch element, row i, column j, contraction index kk).
+// causal == 1: only outputs with j <= i are wanted, so a tile whose first
+// column lies past its last row is skipped (its outputs are left unwritten).
+// causal == 2: A is zero at kk > i, so a row tile starting at m0 needs k only
+// up to the end of the k block holding row m0 + bm - 1's diagonal; every later
+// block is a chain of zero products, whose partial is +0 and leaves acc
+// unchanged (acc + (+0) = acc; acc is never -0), so skipping it keeps the bits.
+__device__ __forceinline__ bool tile_above_diagonal(const GemmArgs& g, int64_t m0, int bm,
+                                                    int64_t n0) {
+  return g.causal == 1 && n0 > m0 + bm - 1;
+}
+
+__device__ __forceinline__ int64_t k_extent(const GemmArgs& g, int64_t m0, int bm) {
+  if (g.causal != 2 || g.k_block <= 0) return g.k;
+  const int64_t end = (m0 + bm + g.k_block - 1) / g.k_block * g.k_block;
+  return end < g.k ? end : g.k;
+}
+
+// With causal == 1, square tiles and at least as many tile columns as rows,
+// the launch covers only the tiles at or below each batch element's diagonal
+// (tn <= tm): tile r of a batch element is the r-th of the lower triangle in
+// row order.
+__device__ __host__ __forceinline__ bool causal_triangle(int causal, int bm, int bn,
+                                                         int64_t tiles_m, int64_t tiles_n) {
+  return causal == 1 && bm == bn && tiles_n >= tiles_m;
+}
+
+// Tile of launch index t for any product: the lower triangle's tiles only (see
+// causal_triangle), or every tile with tile_coords -- row tiles in reverse order
+// when A is zero above its diagonal (causal == 2), so that the row tiles with
+// the longest contraction start first.
+__device__ __forceinline__ void tile_of(const GemmArgs& g, int bm, int bn, int64_t t,
+                                        int64_t ntiles, int64_t tiles_m, int64_t tiles_n,
+                                        int64_t* bz, int64_t* tm, int64_t* tn) {
+  if (causal_triangle(g.causal, bm, bn, tiles_m, tiles_n)) {
+    constexpr int64_t kXcd = 8;
+    if (ntiles % kXcd == 0) t = (t % kXcd) * (ntiles / kXcd) + t / kXcd;
+    const int64_t per = tiles_m * (tiles_m + 1) / 2;
+    *bz = t / per;
+    const int64_t r = t % per;
+    int64_t row = static_cast<int64_t>((sqrt(8.0 * static_cast<double>(r) + 1.0) - 1.0) / 2.0);
+    while ((row + 1) * (row + 2) / 2 <= r) ++row;
+    while (row * (row + 1) / 2 > r) --row;
+    *tm = row;
+    *tn = r - row * (row + 1) / 2;
+    return;
+  }
+  tile_coords(t, ntiles, tiles_m, tiles_n, bz, tm, tn);
+  if (g.causal == 2) *tm = tiles_m - 1 - *tm;
+}
+
 template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
 struct MfmaTile {
   static constexpr int NT = 64 * WM * WN;
@@ -184,7 +235,7 @@ struct MfmaTile {
     const int wave = tid >> 6;
     const int wm0 = (wave / WN) * TWM;
     const int wn0 = (wave % WN) * TWN;
-    const int64_t K = g.k;
+    const int64_t K = k_extent(g, m0, BM);
     const int64_t nslices = (K + BK - 1) / BK;
     const int64_t spb = g.k_block > 0 ? g.k_block / BK : (nslices > 0 ? nslices : 1);
     const float* A = g.A + b0 * g.sa0 + b1 * g.sa1;
@@ -246,9 +297,10 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_kernel(GemmArgs 
   __shared__ typename T::Smem sm;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     int64_t bz, tm, tn;
-    tile_coords(t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
+    tile_of(g, BM, BN, t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
     const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
     const int64_t m0 = tm * BM, n0 = tn * BN;
+    if (tile_above_diagonal(g, m0, BM, n0)) continue;  // uniform over the workgroup
     // Interior tiles (whole tile inside C, whole k slices, aligned rows) take
     // the path without per-element checks; the choice is uniform per tile.
     const bool interior = vec_ok && m0 + BM <= g.m && n0 + BN <= g.n && g.k % BK == 0;
@@ -553,7 +605,7 @@ struct StagedTile {
     const int wm0 = (wave / WN) * TWM;
     const int wn0 = (wave % WN) * TWN;
     // the host guarantees K / BK and k_block / BK fit in int
-    const int nslices = static_cast<int>(g.k / BK);
+    const int nslices = static_cast<int>(k_extent(g, m0, BM) / BK);
     const int spb = g.k_block > 0 ? static_cast<int>(g.k_block / BK) : (nslices > 0 ? nslices : 1);
     const Src src = sources(g, g.A + b0 * g.sa0 + b1 * g.sa1, g.B + b0 * g.sb0 + b1 * g.sb1, m0,
                             n0, wave, lane);
@@ -675,8 +727,9 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
   __shared__ typename T::Smem sm;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     int64_t bz, tm, tn;
-    tile_coords(t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
+    tile_of(g, BM, BN, t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
     const int64_t b1 = bz % g.batch1, b0 = bz / g.batch1;
+    if (tile_above_diagonal(g, tm * BM, BM, tn * BN)) continue;  // uniform over the workgroup
     T::run(g, sm, b0, b1, tm * BM, tn * BN);
   }
 }
@@ -788,7 +841,10 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
   const MfmaEntry& e = kMfma[index];
   const int64_t tiles_m = (g.m + e.cfg.bm - 1) / e.cfg.bm;
   const int64_t tiles_n = (g.n + e.cfg.bn - 1) / e.cfg.bn;
-  const int64_t ntiles = tiles_m * tiles_n * g.batch0 * g.batch1;
+  const int64_t per_batch = causal_triangle(g.causal, e.cfg.bm, e.cfg.bn, tiles_m, tiles_n)
+                                ? tiles_m * (tiles_m + 1) / 2
+                                : tiles_m * tiles_n;
+  const int64_t ntiles = per_batch * g.batch0 * g.batch1;
   const int64_t cap = int64_t(1) << 30;
   const unsigned grid = static_cast<unsigned>(ntiles < cap ? ntiles : cap);
   // float4 loads need 16-byte aligned rows and batch origins

@@ -16,6 +16,9 @@ struct GemmArgs {
   int has_alpha;      // 1: C = acc * alpha
   int64_t k_block;    // 0 = one block
   int fused;          // 1: fma chain, 0: rounded product then add
+  int causal;         // per batch element: 0 none; 1 outputs with j > i unspecified (the
+                      // matrix-core kernels skip tiles wholly above the diagonal); 2 A is
+                      // zero at kk > i (their kernels skip the all-zero k blocks)
 };
 
 struct GemmConfig {

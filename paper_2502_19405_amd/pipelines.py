@@ -33,14 +33,17 @@ def attention_scale(head_dim: int) -> float:
 
 
 def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_launch=None,
-                      keep=False, buffers=None):
+                      keep=False, buffers=None, causal_products=True):
     """Causal multi-head self-attention, fp32:
         Q, K, V = X Wq, X Wk, X Wv            [batch*seq, d]
         S[b,h]  = alpha * Q_h K_h^T            (bmm reading Q, K in place)
         P       = causal row softmax of S
         O_h     = P[b,h] V_h                   (written in place into [batch*seq, d])
         out     = O Wo
-    Heads are column blocks of width d/heads of the projections."""
+    Heads are column blocks of width d/heads of the projections.  With
+    causal_products the score product computes only the tiles the causal
+    softmax reads (S above the diagonal is left unspecified) and the value
+    product skips P's all-zero blocks; P and O keep their bits either way."""
     d = X.shape[1]
     hd = d // heads
     alpha = attention_scale(hd)
@@ -59,7 +62,8 @@ def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_lau
     repops.bmm_raw(batch, heads, seq, seq, hd,
                    Q, seq * d, hd, d, 0,
                    K, seq * d, hd, d, 1, alpha,
-                   S, heads * seq * seq, seq * seq, seq, order=order, launch=gemm_launch)
+                   S, heads * seq * seq, seq * seq, seq, order=order, launch=gemm_launch,
+                   causal=repops.CAUSAL_OUTPUT if causal_products else 0)
     P = repops.softmax_rows(S.view(batch * heads * seq, seq), causal_period=seq, order=order,
                             out=bufs.get("P"))
     O = bufs.get("O")
@@ -68,7 +72,8 @@ def attention_forward(X, Wq, Wk, Wv, Wo, batch, seq, heads, order=None, gemm_lau
     repops.bmm_raw(batch, heads, seq, hd, seq,
                    P, heads * seq * seq, seq * seq, seq, 0,
                    V, seq * d, hd, d, 0, 1.0,
-                   O, seq * d, hd, d, order=order, launch=gemm_launch)
+                   O, seq * d, hd, d, order=order, launch=gemm_launch,
+                   causal=repops.CAUSAL_A if causal_products else 0)
     out = repops.matmul(O, Wo, order=order, launch=gemm_launch, out=bufs.get("out"))
     if keep:
         return {"Q": Q, "K": K, "V": V, "S": S, "P": P, "O": O, "out": out}

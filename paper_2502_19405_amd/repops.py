@@ -83,6 +83,7 @@ class GemmDescT(ctypes.Structure):
 
 
 MAX_GROUP = 8  # REPOPS_MAX_GROUP
+CAUSAL_OUTPUT, CAUSAL_A = 1, 2  # repops_bmm_causal masks
 
 _lib = None
 _i64, _i32, _u32, _f32, _vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_void_p
@@ -97,6 +98,9 @@ _SIGNATURES = {
     "repops_matmul": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp, _vp,
                              _i64, _lp, _vp]),
     "repops_matmul_grouped": (_i32, [_op, _i32, ctypes.POINTER(GemmDescT), _lp, _vp]),
+    "repops_bmm_causal": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
+                                 _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _i32,
+                                 _lp, _vp]),
     "repops_bmm": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
                           _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _lp, _vp]),
     "repops_softmax_rows": (_i32, [_op, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _lp, _vp]),
@@ -304,9 +308,18 @@ def bmm_raw(batch0: int, batch1: int, m: int, n: int, k: int,
             B: torch.Tensor, sb0: int, sb1: int, ldb: int, trans_b: int, alpha: float,
             C: torch.Tensor, sc0: int, sc1: int, ldc: int,
             a_offset: int = 0, b_offset: int = 0, c_offset: int = 0,
-            order: Order | None = None, launch: Launch | None = None):
+            order: Order | None = None, launch: Launch | None = None, causal: int = 0):
     """The C-ABI bmm on raw element strides over the storage of A, B, C
-    (offsets in elements from each tensor's data pointer)."""
+    (offsets in elements from each tensor's data pointer).  causal: 0 for
+    repops_bmm, else repops_bmm_causal's mask (CAUSAL_OUTPUT, CAUSAL_A)."""
+    if causal:
+        rc = load().repops_bmm_causal(_ord(order), batch0, batch1, m, n, k,
+                                      _dev(A, "A") + 4 * a_offset, sa0, sa1, lda, trans_a,
+                                      _dev(B, "B") + 4 * b_offset, sb0, sb1, ldb, trans_b, alpha,
+                                      _dev(C, "C") + 4 * c_offset, sc0, sc1, ldc, causal,
+                                      _launch(launch), _stream(C))
+        _check(rc, "repops_bmm_causal")
+        return C
     rc = load().repops_bmm(_ord(order), batch0, batch1, m, n, k,
                            _dev(A, "A") + 4 * a_offset, sa0, sa1, lda, trans_a,
                            _dev(B, "B") + 4 * b_offset, sb0, sb1, ldb, trans_b, alpha,

@@ -10,8 +10,9 @@ little-endian bytes).  The GPU tests hash their own outputs and compare.
 
     python tests/golden/make_oracle_digests.py [workload ...]
 
-Workloads: llama_attention (4 x 1024 tokens, d 4096, 32 heads: Q, K, V, scores,
-probabilities, head outputs, output projection), llama_linear_backward (8192
+Workloads: llama_attention (4 x 1024 tokens, d 4096, 32 heads: Q, K, V, scores
+-- whole and with +0 above each head's diagonal --, probabilities, head outputs,
+output projection), llama_linear_backward (8192
 tokens, 4096 -> 14336: dX and dW), mlp_train_step_4096 (two training steps of
 the DistilBERT feed-forward block at 4096 tokens).
 """
@@ -58,10 +59,19 @@ def train_step_gradients(tokens, step_count=2):
     return [inputs.normal(g, (tokens, 768), var=1e-4) for _ in range(step_count)]
 
 
+def causal_lower(S):
+    """The scores at or below each head's diagonal, +0 above it (the part a
+    causal softmax reads)."""
+    T = S.shape[-1]
+    return np.where(np.tril(np.ones((T, T), bool)), S, np.float32(0.0)).astype(np.float32)
+
+
 def llama_attention():
     d = inputs.llama_attention()
     out = compose.attention_forward(d["X"], d["Wq"], d["Wk"], d["Wv"], d["Wo"], 4, 1024, 32)
-    return d, {k: sha256_of(v) for k, v in out.items()}
+    digests = {k: sha256_of(v) for k, v in out.items()}
+    digests["S_lower"] = sha256_of(causal_lower(out["S"]))
+    return d, digests
 
 
 def llama_linear_backward():

@@ -115,6 +115,21 @@ def test_matmul_rejections(rp):
 
 @no_gpu_only
 @no_gpu_only
+def test_bmm_causal_rejections(rp):
+    lib = rp.load()
+    o = _order()
+
+    def bc(mask=1, lda=8):
+        return lib.repops_bmm_causal(o, 1, 1, 8, 8, 8, FAKE_A, 64, 64, lda, 0, FAKE_B, 64, 64, 8,
+                                     1, 1.0, FAKE_C, 64, 64, 8, mask, None, None)
+    assert bc(mask=0) == rp.ERR_VALUE
+    assert bc(mask=3) == rp.ERR_VALUE
+    assert bc(lda=7) == rp.ERR_STRIDE
+    assert lib.repops_bmm_causal(o, 1, 1, 0, 8, 8, None, 0, 0, 8, 0, None, 0, 0, 8, 0, 1.0, None,
+                                 0, 0, 8, 2, None, None) == rp.OK
+
+
+@no_gpu_only
 def test_matmul_grouped_rejections(rp):
     lib = rp.load()
     o = _order()

@@ -340,3 +340,58 @@ def test_matmul_grouped_training_step_shapes(rp):
     assert_bits_equal(host(gw)[r, c], oracle.matmul_at(G, dH, r, c, trans_a=True), "dW2")
     r, c = inputs.sample_indices(9, 512, 4096, 3072)
     assert_bits_equal(host(gg)[r, c], oracle.matmul_at(dH, W2, r, c, trans_b=True), "dG")
+
+
+CAUSAL_SHAPES = [(1, 2, 300, 300, 64), (2, 3, 257, 257, 100), (1, 1, 1024, 1024, 128),
+                 (2, 2, 200, 130, 200)]
+
+
+@pytest.mark.parametrize("shape", CAUSAL_SHAPES)
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (32, 1)])
+def test_bmm_causal_output_lower_triangle(rp, shape, k_block, k_inner):
+    """REPOPS_CAUSAL_OUTPUT: every output with j <= i has repops_bmm's bits
+    (and the oracle's) under every launch; the rest is unspecified."""
+    b0, b1, m, n, k = shape
+    g = inputs.rng(900 + m + k + k_block)
+    A = inputs.normal(g, (b0, b1, m, k))
+    B = inputs.normal(g, (b0, b1, n, k))
+    want = oracle.bmm(A, B, alpha=0.125, trans_b=True, k_block=k_block, k_inner=k_inner)
+    lower = np.tril(np.ones((m, n), bool))
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    import torch
+    for name, launch in [("auto", None)] + launches(rp, k_block, k_inner == 0):
+        announce("bmm causal output", shape, k_block, k_inner, name)
+        C = torch.full((b0, b1, m, n), float("nan"), device="cuda:0")
+        rp.bmm_raw(b0, b1, m, n, k, dev(A), b1 * m * k, m * k, k, 0, dev(B), b1 * n * k, n * k, k,
+                   1, 0.125, C, b1 * m * n, m * n, n, order=order, launch=launch,
+                   causal=rp.CAUSAL_OUTPUT)
+        got = host(C)
+        assert_bits_equal(np.where(lower, got, 0), np.where(lower, want, 0), f"{shape} {name}")
+
+
+@pytest.mark.parametrize("shape", CAUSAL_SHAPES)
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (32, 1), (128, 0)])
+def test_bmm_causal_a_is_bitwise_bmm(rp, shape, k_block, k_inner):
+    """REPOPS_CAUSAL_A with A zero above its diagonal (as a causal softmax
+    leaves P, signed zeros included): every output equals repops_bmm and the
+    oracle bit for bit under every launch -- the skipped k blocks held only
+    zero products."""
+    b0, b1, m, n, k = shape
+    k = m  # P is square per batch element
+    g = inputs.rng(950 + m + k_block)
+    A = inputs.normal(g, (b0, b1, m, k))
+    upper = np.triu(np.ones((m, k), bool), 1)
+    A[..., upper] = 0.0
+    A[..., :, k - 1][..., :m - 1] = -0.0   # negative zeros above the diagonal too
+    A = np.ascontiguousarray(A, np.float32)
+    B = inputs.normal(g, (b0, b1, k, n))
+    want = oracle.bmm(A, B, k_block=k_block, k_inner=k_inner)
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    import torch
+    for name, launch in [("auto", None)] + launches(rp, k_block, k_inner == 0):
+        announce("bmm causal A", shape, k_block, k_inner, name)
+        C = torch.empty((b0, b1, m, n), device="cuda:0")
+        rp.bmm_raw(b0, b1, m, n, k, dev(A), b1 * m * k, m * k, k, 0, dev(B), b1 * k * n, k * n, n,
+                   0, 1.0, C, b1 * m * n, m * n, n, order=order, launch=launch,
+                   causal=rp.CAUSAL_A)
+        assert_bits_equal(host(C), want, f"{shape} {name}")
