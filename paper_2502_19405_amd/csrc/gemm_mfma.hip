@@ -96,9 +96,13 @@ __device__ __forceinline__ void tile_of(const GemmArgs& g, int bm, int bn, int64
     const int64_t per = tiles_m * (tiles_m + 1) / 2;
     *bz = t / per;
     const int64_t r = t % per;
-    int64_t row = static_cast<int64_t>((sqrt(8.0 * static_cast<double>(r) + 1.0) - 1.0) / 2.0);
-    while ((row + 1) * (row + 2) / 2 <= r) ++row;
-    while (row * (row + 1) / 2 > r) --row;
+    // the last row tile whose triangle starts at or before r (integer
+    // bisection; r < per, so it lies below tiles_m)
+    int64_t row = 0, hi = tiles_m - 1;
+    while (row < hi) {
+      const int64_t mid = (row + hi + 1) / 2;
+      if (mid * (mid + 1) / 2 <= r) row = mid; else hi = mid - 1;
+    }
     *tm = row;
     *tn = r - row * (row + 1) / 2;
     return;
