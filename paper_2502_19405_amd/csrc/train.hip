@@ -635,10 +635,11 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
 // one-workgroup-per-block kernel: the G workgroups of a block share its work.
 // Workgroup (beta, g) computes dX for its share of the block's rows (whole
 // rows, one wave each as the wave kernel does, or a group of waves each for
-// the widest) and the chains of its column slice over all of the block's
-// rows: chunks of rows are loaded by all waves (t formed on the way) into LDS
-// and one thread per column advances its two chains through each chunk in
-// row order, while the next chunk's loads are in flight.  Every row is read
+// the widest; the rows are dealt to the G workgroups in turn) and the chains
+// of its column slice over all of the block's rows: chunks of rows are loaded
+// by all waves (t formed on the way) into LDS and one thread per column
+// advances its two chains through each chunk in row order, while the next
+// chunk's loads are in flight.  Every row is read
 // twice (whole for dX, by slices for the chains); the G workgroups of a block
 // are placed on one XCD so the second read can find the rows in that XCD's L2
 // (with 4096-wide rows a 64-row block is 2 MB, and part of the second read
@@ -648,16 +649,18 @@ __global__ __launch_bounds__(MAXT) void layernorm_bwd_fused_kernel(RowBwdArgs a,
 
 constexpr int kSplitWaves = 8;
 
-// dX of rows [d0, d1) by the kSplitWaves waves of a workgroup, S waves per
-// row and kSplitWaves / S rows at a time: wave h of a group (h < S) holds the
-// columns lane + 64 * (h * T + t), and each lane's chains pass from wave to
-// wave of the group in order through LDS, so the terms meet in the one-wave
-// order and the results are the same bits.  Every wave takes part in every
-// step (the steps hold workgroup barriers); a group past d1 works on row d0
-// and stores nothing.
+// dX of the rows first + k * stride + q (k >= 0, q < P = kSplitWaves / S,
+// below end) by the kSplitWaves waves of a workgroup, S waves per row and P
+// rows at a time: wave h of a group (h < S) holds the columns
+// lane + 64 * (h * T + t), and each lane's chains pass from wave to wave of
+// the group in order through LDS, so the terms meet in the one-wave order and
+// the results are the same bits.  Every wave takes part in every step (the
+// steps hold workgroup barriers); a group past end works on row first and
+// stores nothing.
 template <int T, int S>
-__device__ __forceinline__ void layernorm_bwd_rows_grouped(const RowBwdArgs& a, int64_t d0,
-                                                           int64_t d1, int lane, int w) {
+__device__ __forceinline__ void layernorm_bwd_rows_grouped(const RowBwdArgs& a, int64_t first,
+                                                           int64_t stride, int64_t end, int lane,
+                                                           int w) {
   constexpr int P = kSplitWaves / S;
   __shared__ float chain_g[P * kWave], chain_gt[P * kWave];
   const int h = w % S;
@@ -671,10 +674,10 @@ __device__ __forceinline__ void layernorm_bwd_rows_grouped(const RowBwdArgs& a, 
     }
     return ch[slot];
   };
-  for (int64_t base = d0; base < d1; base += P) {
+  for (int64_t base = first; base < end; base += stride) {
     const int64_t row = base + w / S;
-    const bool live = row < d1;
-    const int64_t rr = live ? row : d0;
+    const bool live = row < end;
+    const int64_t rr = live ? row : first;
     const float* x = a.Y + rr * a.ldy;
     const float* dy = a.dY + rr * a.lddy;
     const float mean = a.rms ? 0.0f : a.mean[rr], rstd = a.rstd[rr];
@@ -766,17 +769,23 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void layernorm_bwd_colsplit_ke
   };
   load_chunk(r0);
 
-  // dX for rows [d0, d1) of the block: one wave per row, or for wide rows a
-  // group of waves per row.
-  const int64_t per = (r1 - r0 + G - 1) / G;
-  const int64_t d0 = r0 + g * per;
-  const int64_t d1 = (d0 + per < r1) ? d0 + per : r1;
+  // dX of the block's rows, dealt to its G workgroups in turn, P rows to a
+  // workgroup at a time (one wave per row, P = kSplitWaves, or for wide rows a
+  // group of waves per row): the workgroups go through the rows in the order
+  // the chains' chunks read them, so that the second read of a row tends to
+  // find it in L2.  (A chunk's dX just before its chains, which brings the
+  // two reads together, measured slower: each chunk then waits for its own
+  // rows.)
   if constexpr (T > 32) {
     static_assert(T % kColsplitGroupT == 0 && kSplitWaves % (T / kColsplitGroupT) == 0,
                   "row groups must tile the workgroup");
-    layernorm_bwd_rows_grouped<kColsplitGroupT, T / kColsplitGroupT>(a, d0, d1, lane, w);
+    constexpr int S = T / kColsplitGroupT, P = kSplitWaves / S;
+    layernorm_bwd_rows_grouped<kColsplitGroupT, S>(a, r0 + int64_t(g) * P, int64_t(P) * G, r1,
+                                                   lane, w);
   } else {
-    for (int64_t row = d0 + w; row < d1; row += kSplitWaves) layernorm_bwd_row<T>(a, row, lane);
+    const int64_t stride = int64_t(kSplitWaves) * G;
+    for (int64_t row = r0 + int64_t(g) * kSplitWaves + w; row < r1; row += stride)
+      layernorm_bwd_row<T>(a, row, lane);
   }
 
   float pg = 0.0f, pb = 0.0f;
