@@ -50,11 +50,19 @@ constexpr int kTopThreads = 256;
 
 __device__ __forceinline__ uint32_t rotr(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
 
-// Three-input XOR in one instruction: gfx950's three-input bitwise operation
-// with the parity truth table 0x96 (the compiler otherwise splits the Sigma /
-// sigma functions into two-input XORs).
+// SHA-256's three-input bitwise functions, each one gfx950 three-input bitwise
+// operation; the 8-bit table holds the output for input bits (a, b, c) at
+// bit 4a + 2b + c.  Parity (0x96) for the Sigma / sigma functions, majority
+// (0xE8), and choose -- b where a is set, else c -- (0xCA).  (The compiler
+// otherwise splits each into two-input operations.)
 __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
   return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+__device__ __forceinline__ uint32_t maj3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0xE8);
+}
+__device__ __forceinline__ uint32_t choose(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0xCA);
 }
 
 // The compression function on one block; W holds the block's 16 words and is
@@ -75,10 +83,10 @@ __device__ __forceinline__ void compress(uint32_t H[8], uint32_t W[16]) {
       W[t & 15] = w;
     }
     const uint32_t S1 = xor3(rotr(e, 6), rotr(e, 11), rotr(e, 25));
-    const uint32_t ch = (e & f) ^ (~e & g);
+    const uint32_t ch = choose(e, f, g);
     const uint32_t T1 = h + S1 + ch + kK[t] + w;
     const uint32_t S0 = xor3(rotr(a, 2), rotr(a, 13), rotr(a, 22));
-    const uint32_t maj = (a & b) ^ (a & c) ^ (b & c);
+    const uint32_t maj = maj3(a, b, c);
     const uint32_t T2 = S0 + maj;
     h = g;
     g = f;
