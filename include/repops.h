@@ -159,6 +159,23 @@ repops_status_t repops_matmul(const repops_order_t *order, int64_t m, int64_t n,
                               const repops_launch_t *launch, void *hip_stream);
 
 /*
+ * repops_matmul_gelu -- H = A.B (+ bias) and G = GELU(H), the feed-forward
+ * layer's first product and activation (Section 3.2's matrix multiplication,
+ * then Section 3.1's reproducible elementwise GELU, tanh form), in one pass:
+ * the threads that write an output of H also write its GELU into G.  H takes
+ * exactly the bits repops_matmul gives for the same arguments, and G exactly
+ * the bits repops_gelu gives for that H, under every launch descriptor.
+ *   Arguments as for repops_matmul, with H, ldh in the place of C, ldc.
+ *   G, ldg    [m x n] output, ldg >= n; must not overlap H, A, B or bias
+ *             (REPOPS_ERR_ALIAS); NULL is REPOPS_ERR_NULL unless m or n is 0.
+ */
+repops_status_t repops_matmul_gelu(const repops_order_t *order, int64_t m, int64_t n, int64_t k,
+                                   const float *A, int64_t lda, int32_t trans_a,
+                                   const float *B, int64_t ldb, int32_t trans_b,
+                                   const float *bias, float *H, int64_t ldh, float *G,
+                                   int64_t ldg, const repops_launch_t *launch, void *hip_stream);
+
+/*
  * repops_bmm -- batched product over (i0, i1) in [0,batch0) x [0,batch1), the
  * batched key-query and probability-value products of attention that Section
  * 2.2 decomposes into independent matrix products.  Batch element (i0, i1)

@@ -373,6 +373,38 @@ repops_status_t repops_matmul(const repops_order_t* order, int64_t m, int64_t n,
   return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
 }
 
+repops_status_t repops_matmul_gelu(const repops_order_t* order, int64_t m, int64_t n, int64_t k,
+                                   const float* A, int64_t lda, int32_t trans_a, const float* B,
+                                   int64_t ldb, int32_t trans_b, const float* bias, float* H,
+                                   int64_t ldh, float* G, int64_t ldg,
+                                   const repops_launch_t* launch, void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  GemmArgs g{};
+  g.batch0 = 1; g.batch1 = 1; g.m = m; g.n = n; g.k = k;
+  g.A = A; g.lda = lda; g.ta = trans_a;
+  g.B = B; g.ldb = ldb; g.tb = trans_b;
+  g.C = H; g.ldc = ldh;
+  g.G = G; g.ldg = ldg;
+  g.bias = bias; g.alpha = 1.0f; g.has_alpha = 0;
+  g.k_block = order->k_block;
+  const repops_status_t st = check_operands(g);
+  if (st != REPOPS_OK) return st;
+  if (m == 0 || n == 0) return REPOPS_OK;
+  if (!G) return REPOPS_ERR_NULL;
+  if (ldg < n) return REPOPS_ERR_STRIDE;
+  // G is written beside H by the same threads: it may touch no operand and
+  // not H.
+  const Extent ge = extent_of(G, 1, 0, 1, 0, m, n, ldg);
+  if (overlaps(ge, extent_of(H, 1, 0, 1, 0, m, n, ldh))) return REPOPS_ERR_ALIAS;
+  if (k > 0) {
+    const Extent ae = trans_a ? extent_of(A, 1, 0, 1, 0, k, m, lda) : extent_of(A, 1, 0, 1, 0, m, k, lda);
+    const Extent be = trans_b ? extent_of(B, 1, 0, 1, 0, n, k, ldb) : extent_of(B, 1, 0, 1, 0, k, n, ldb);
+    if (overlaps(ge, ae) || overlaps(ge, be)) return REPOPS_ERR_ALIAS;
+  }
+  if (bias && overlaps(ge, extent_of(bias, 1, 0, 1, 0, 1, n, n))) return REPOPS_ERR_ALIAS;
+  return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
+}
+
 repops_status_t repops_matmul_grouped(const repops_order_t* order, int32_t count,
                                       const repops_gemm_desc_t* descs,
                                       const repops_launch_t* launch, void* hip_stream) {

@@ -20,6 +20,7 @@
 // bits whichever sign the zero partial had.
 #include <hip/hip_runtime.h>
 
+#include "rep_math.h"
 #include "repops_internal.h"
 
 #pragma clang fp contract(off)
@@ -42,6 +43,15 @@ __device__ __forceinline__ float epilogue(const GemmArgs& g, float acc, int64_t 
   if (g.has_alpha) v = v * g.alpha;
   if (g.bias) v = v + g.bias[j];
   return v;
+}
+
+// Output (i, j) of one batch element (C and G already offset to it): the
+// value, and its GELU when the product carries a second output.
+__device__ __forceinline__ void store_out(const GemmArgs& g, float* C, float* G, int64_t i,
+                                          int64_t j, float acc) {
+  const float v = epilogue(g, acc, j);
+  C[i * g.ldc + j] = v;
+  if (G) G[i * g.ldg + j] = rep_gelu(v);
 }
 
 // ---------------------------------------------------------------------------
@@ -73,7 +83,8 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs g, int64_t ti
       for (int64_t kk = k0; kk < k1; ++kk) p = kstep<FUSED>(a[kk * ia], b[kk * ib], p);
       acc = acc + p;
     }
-    g.C[b0 * g.sc0 + b1 * g.sc1 + i * g.ldc + j] = epilogue(g, acc, j);
+    const int64_t co = b0 * g.sc0 + b1 * g.sc1;
+    store_out(g, g.C + co, g.G ? g.G + co : nullptr, i, j, acc);
   }
 }
 
@@ -187,6 +198,7 @@ __global__ __launch_bounds__((BM / TM) * (BN / TN)) void gemm_tiled_kernel(GemmA
     }
 
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
+    float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
       const int64_t i = m0 + ty * TM + r;
@@ -194,7 +206,7 @@ __global__ __launch_bounds__((BM / TM) * (BN / TN)) void gemm_tiled_kernel(GemmA
 #pragma unroll
       for (int c = 0; c < TN; ++c) {
         const int64_t j = n0 + tx * TN + c;
-        if (j < g.n) C[i * g.ldc + j] = epilogue(g, acc[r][c], j);
+        if (j < g.n) store_out(g, C, G, i, j, acc[r][c]);
       }
     }
   }

@@ -21,6 +21,7 @@
 // block starts from +0.
 #include <hip/hip_runtime.h>
 
+#include "rep_math.h"
 #include "repops_internal.h"
 
 #pragma clang fp contract(off)
@@ -35,6 +36,15 @@ __device__ __forceinline__ float epilogue(const GemmArgs& g, float acc, int64_t 
   if (g.has_alpha) v = v * g.alpha;
   if (g.bias) v = v + g.bias[j];
   return v;
+}
+
+// Output (i, j) of one batch element (C and G already offset to it): the
+// value, and its GELU when the product carries a second output.
+__device__ __forceinline__ void store_out(const GemmArgs& g, float* C, float* G, int64_t i,
+                                          int64_t j, float acc) {
+  const float v = epilogue(g, acc, j);
+  C[i * g.ldc + j] = v;
+  if (G) G[i * g.ldg + j] = rep_gelu(v);
 }
 
 // Map the launch-order tile index so that the tiles one XCD receives (the
@@ -278,6 +288,7 @@ struct MfmaTile {
     // r / 16 covers rows 32*(r/16) + [0, 32); inside it row
     // 8*((r%16)/4) + 4*(l/32) + r%4 and column l % 32.
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
+    float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int a = 0; a < IM; ++a)
 #pragma unroll
@@ -287,7 +298,7 @@ struct MfmaTile {
         for (int r = 0; r < 32; ++r) {
           const int row = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t i = m0 + wm0 + a * 64 + row;
-          if (!EDGE || (i < g.m && j < g.n)) C[i * g.ldc + j] = epilogue(g, acc[a][b][r], j);
+          if (!EDGE || (i < g.m && j < g.n)) store_out(g, C, G, i, j, acc[a][b][r]);
         }
       }
   }
@@ -710,6 +721,7 @@ struct StagedTile {
     // Accumulator layout (lane l, register r): block r / 16 holds columns
     // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
+    float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -718,7 +730,7 @@ struct StagedTile {
         for (int r = 0; r < 32; ++r) {
           const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
-          if (row < g.m && col < g.n) C[row * g.ldc + col] = epilogue(g, acc[i][j][r], col);
+          if (row < g.m && col < g.n) store_out(g, C, G, row, col, acc[i][j][r]);
         }
   }
 };

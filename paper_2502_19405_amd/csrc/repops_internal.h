@@ -11,6 +11,7 @@ struct GemmArgs {
   const float* A; int64_t sa0, sa1, lda; int ta;
   const float* B; int64_t sb0, sb1, ldb; int tb;
   float* C; int64_t sc0, sc1, ldc;
+  float* G; int64_t ldg;  // nullable: G = gelu(C) elementwise, batch offsets as C's
   const float* bias;  // nullable, [n]
   float alpha;
   int has_alpha;      // 1: C = acc * alpha

@@ -3,8 +3,10 @@
 Each function only chains C-ABI calls through the binding (no arithmetic of
 its own), in the shapes of the programs Verde's evaluation runs (Section 4.2):
 a DistilBERT feed-forward block, a Llama attention block and the backward
-products of a Llama linear layer.  Elementwise work is not fused into the
-GEMMs, so every intermediate keeps the bits of the operator that made it.
+products of a Llama linear layer.  The feed-forward GELU is produced by the
+first product's epilogue (repops_matmul_gelu), which gives the bits of the
+product and of the elementwise GELU taken separately; every other
+intermediate comes from its own operator call.
 """
 from __future__ import annotations
 
@@ -18,8 +20,7 @@ from . import repops
 def mlp_forward(X, W1, b1, W2, b2, gamma, beta, eps=1e-5, order=None, gemm_launch=None,
                 keep=False):
     """LayerNorm(gelu(X W1 + b1) W2 + b2): X [t, h], W1 [h, f], W2 [f, h]."""
-    H1 = repops.matmul(X, W1, b1, order=order, launch=gemm_launch)
-    G = repops.gelu(H1, order=order)
+    H1, G = repops.matmul_gelu(X, W1, b1, order=order, launch=gemm_launch)
     H2 = repops.matmul(G, W2, b2, order=order, launch=gemm_launch)
     Y = repops.layernorm_rows(H2, gamma, beta, eps=eps, order=order)
     if keep:
@@ -138,8 +139,8 @@ def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps
         return b[name]
 
     # forward (the LayerNorm statistics are the backward's saved tensors)
-    H1 = repops.matmul(X, W1, b1, order=order, launch=gemm_launch, out=buf("H1", t, f))
-    G = repops.gelu(H1, order=order, out=buf("G", t, f))
+    H1, G = repops.matmul_gelu(X, W1, b1, order=order, launch=gemm_launch, out=buf("H1", t, f),
+                               gelu_out=buf("G", t, f))
     H2 = repops.matmul(G, W2, b2, order=order, launch=gemm_launch, out=buf("H2", t, h))
     mean, rstd = buf("mean", t), buf("rstd", t)
     Y = repops.layernorm_rows(H2, gamma, beta, eps=ln_eps, order=order, out=buf("Y", t, h),

@@ -97,6 +97,8 @@ _SIGNATURES = {
     "repops_gemm_config_name": (ctypes.c_char_p, [_u32, _u32]),
     "repops_matmul": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp, _vp,
                              _i64, _lp, _vp]),
+    "repops_matmul_gelu": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp,
+                                  _vp, _i64, _vp, _i64, _lp, _vp]),
     "repops_matmul_grouped": (_i32, [_op, _i32, ctypes.POINTER(GemmDescT), _lp, _vp]),
     "repops_bmm_causal": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
                                  _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _i32,
@@ -269,6 +271,35 @@ def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
                               _launch(launch), _stream(out))
     _check(rc, "repops_matmul")
     return out
+
+
+def matmul_gelu(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
+                order: Order | None = None, launch: Launch | None = None,
+                out: torch.Tensor | None = None, gelu_out: torch.Tensor | None = None):
+    """(H, G) with H = A @ B (+ bias) and G = gelu(H) from one pass: H has the
+    bits matmul gives and G the bits gelu gives for that H."""
+    pa, m, k, lda, ta = _mat(A, "A")
+    pb, k2, n, ldb, tb = _mat(B, "B")
+    if k != k2:
+        raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    if gelu_out is None:
+        gelu_out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    for t, name in ((out, "out"), (gelu_out, "gelu_out")):
+        if t.shape != (m, n) or t.stride(1) != 1:
+            raise ValueError(f"{name} must be a row-major [m, n] tensor")
+    pbias = None
+    if bias is not None:
+        if bias.shape != (n,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous [n] tensor")
+        pbias = _dev(bias, "bias")
+    rc = load().repops_matmul_gelu(_ord(order), m, n, k, pa, lda, ta, pb, ldb, tb, pbias,
+                                   _dev(out, "out"), max(out.stride(0), n, 1),
+                                   _dev(gelu_out, "gelu_out"), max(gelu_out.stride(0), n, 1),
+                                   _launch(launch), _stream(out))
+    _check(rc, "repops_matmul_gelu")
+    return out, gelu_out
 
 
 def matmul_grouped(products, order: Order | None = None) -> list:

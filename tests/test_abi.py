@@ -114,7 +114,6 @@ def test_matmul_rejections(rp):
 
 
 @no_gpu_only
-@no_gpu_only
 def test_bmm_causal_rejections(rp):
     lib = rp.load()
     o = _order()
@@ -156,6 +155,31 @@ def test_matmul_grouped_rejections(rp):
     assert call(desc(), desc(A=FAKE_C + 8, C=FAKE_D)) == rp.ERR_ALIAS  # reads another's output
     assert call(desc(), desc(bias=FAKE_C + 4, C=FAKE_D)) == rp.ERR_ALIAS
     assert call(desc(m=0), desc(n=0, C=FAKE_D)) == rp.OK               # nothing to compute
+
+
+@no_gpu_only
+def test_matmul_gelu_rejections(rp):
+    lib = rp.load()
+    FAKE_G = 0x500000
+
+    def call(order=None, m=4, n=4, k=4, A=FAKE_A, lda=4, ta=0, B=FAKE_B, ldb=4, tb=0, bias=None,
+             H=FAKE_C, ldh=4, G=FAKE_G, ldg=4, launch=None):
+        return lib.repops_matmul_gelu(order or _order(), m, n, k, A, lda, ta, B, ldb, tb, bias, H,
+                                      ldh, G, ldg, launch, None)
+    assert call(order=_order(version=2)) == rp.ERR_ORDER
+    assert call(m=-1) == rp.ERR_SHAPE
+    assert call(H=None) == rp.ERR_NULL
+    assert call(G=None) == rp.ERR_NULL
+    assert call(ldh=3) == rp.ERR_STRIDE
+    assert call(ldg=3) == rp.ERR_STRIDE
+    assert call(H=FAKE_A + 8) == rp.ERR_ALIAS            # H over A (the matmul checks)
+    assert call(G=FAKE_C + 4) == rp.ERR_ALIAS            # G over H
+    assert call(G=FAKE_A + 60) == rp.ERR_ALIAS           # G over A's last element
+    assert call(G=FAKE_B) == rp.ERR_ALIAS                # G over B
+    assert call(bias=FAKE_G + 12) == rp.ERR_ALIAS        # bias inside G
+    assert call(launch=ctypes.byref(rp.Launch(7).c())) == rp.ERR_LAUNCH
+    # nothing to write: succeeds without touching any pointer or the device
+    assert call(m=0, A=None, B=None, H=None, G=None) == rp.OK
 
 
 def test_matmul_zero_sized_is_a_noop(rp):

@@ -55,6 +55,41 @@ ORDERS = [(64, 0), (0, 0), (128, 0), (64, 1), (32, 1)]
 
 
 @pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (64, 1)])
+def test_matmul_gelu_all_launches(rp, shape, k_block, k_inner):
+    # H = A.B + bias and G = gelu(H) from one pass: H the oracle's product, G
+    # the oracle's elementwise GELU of that product, under every launch and
+    # transposition; inputs scaled so that H spans GELU's curved part.
+    m, n, k = shape
+    g = inputs.rng(5 * m + n + 11 * k + k_block + k_inner)
+    A = (inputs.normal(g, (m, k)) * np.float32(1.5 / math.sqrt(max(k, 1)))).astype(np.float32)
+    B = inputs.normal(g, (k, n))
+    bias = inputs.uniform(g, (n,), -2.0, 2.0)
+    want_h = oracle.matmul(A, B, bias, k_block=k_block, k_inner=k_inner)
+    want_g = oracle.gelu(want_h)
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    dA, dB, dbias = dev(A), dev(B), dev(bias)
+    dAt, dBt = dev(np.ascontiguousarray(A.T)), dev(np.ascontiguousarray(B.T))
+    for name, launch in [("auto", None)] + launches(rp, k_block, k_inner == 0):
+        announce("matmul_gelu", shape, k_block, k_inner, name)
+        for ta, tb in ((0, 0), (1, 1)):
+            a = dAt.t() if ta else dA
+            b = dBt.t() if tb else dB
+            h, gl = rp.matmul_gelu(a, b, dbias, order=order, launch=launch)
+            assert_bits_equal(host(h), want_h, f"{name} H trans {ta}{tb}")
+            assert_bits_equal(host(gl), want_g, f"{name} G trans {ta}{tb}")
+    # no bias; padded output rows (ldh, ldg > n); the separate calls give the same bits
+    import torch
+    Hp = torch.full((m, n + 3), float("nan"), device=dA.device)
+    Gp = torch.full((m, n + 5), float("nan"), device=dA.device)
+    rp.matmul_gelu(dA, dB, None, order=order, out=Hp[:, :n], gelu_out=Gp[:, :n])
+    h_sep = rp.matmul(dA, dB, None, order=order)
+    assert same_bits(Hp[:, :n], h_sep)
+    assert same_bits(Gp[:, :n], rp.gelu(h_sep.contiguous(), order=order))
+    assert torch.isnan(Hp[:, n:]).all() and torch.isnan(Gp[:, n:]).all()
+
+
+@pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("k_block,k_inner", ORDERS)
 def test_matmul_small_all_launches(rp, shape, k_block, k_inner):
     m, n, k = shape
