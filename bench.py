@@ -72,20 +72,38 @@ def measured_traffic(launch_spec, product):
     return float(val) if val else None
 
 
-def event_time_ms(fn, reps, warmup=2):
+# Shortest timed region of a secondary workload (see event_time_ms); 0 keeps
+# every workload at exactly its given number of calls (the counter passes
+# count dispatches per workload).
+MIN_TIMED_MS = 2.0
+
+
+def event_time_ms(fn, reps, warmup=2, min_total_ms=None):
     """Average duration of fn() over reps launches, HIP events on the current
-    stream (the stream the library launches on)."""
+    stream (the stream the library launches on).  Calls of a few microseconds
+    are timed over enough launches to fill min_total_ms (MIN_TIMED_MS unless
+    given; the first, shorter timing then serves as further warmup), so that
+    the average is steady."""
     import torch
+    if min_total_ms is None:
+        min_total_ms = MIN_TIMED_MS
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(reps):
-        fn()
-    stop.record()
-    stop.synchronize()
-    return start.elapsed_time(stop) / reps
+
+    def timed(n):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(n):
+            fn()
+        stop.record()
+        stop.synchronize()
+        return start.elapsed_time(stop)
+    total = timed(reps)
+    if total < min_total_ms:
+        reps = min(int(reps * min_total_ms / max(total, 1e-3)) + 1, 20000)
+        total = timed(reps)
+    return total / reps
 
 
 class ClockSampler:
@@ -653,6 +671,9 @@ def main():
         torch.cuda.synchronize()
         result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_secondary:
+        global MIN_TIMED_MS
+        if args.streaming_only:
+            MIN_TIMED_MS = 0.0
         result["secondary"] = secondary(repops, 20, args.streaming_only,
                                         headline={"X": X, "dY": dY, "W": W, "dX": dX, "dW": dW})
     if not args.no_cpu_baseline:
