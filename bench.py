@@ -76,6 +76,10 @@ def measured_traffic(launch_spec, product):
 # every workload at exactly its given number of calls (the counter passes
 # count dispatches per workload).
 MIN_TIMED_MS = 2.0
+# Calls the last event_time_ms / graph_time_ms made (warmup and capture
+# included); _rate reports it, so a kernel trace of the run can be split into
+# workloads call for call.
+_LAUNCHED = [0]
 
 
 def event_time_ms(fn, reps, warmup=2, min_total_ms=None):
@@ -100,9 +104,11 @@ def event_time_ms(fn, reps, warmup=2, min_total_ms=None):
         stop.synchronize()
         return start.elapsed_time(stop)
     total = timed(reps)
+    _LAUNCHED[0] = warmup + reps
     if total < min_total_ms:
         reps = min(int(reps * min_total_ms / max(total, 1e-3)) + 1, 20000)
         total = timed(reps)
+        _LAUNCHED[0] += reps
     return total / reps
 
 
@@ -187,6 +193,7 @@ def graph_time_ms(fn, calls=20, reps=10):
         graph.replay()
     stop.record()
     stop.synchronize()
+    _LAUNCHED[0] = 2 + calls * (1 + reps)
     return start.elapsed_time(stop) / (calls * reps)
 
 
@@ -249,7 +256,7 @@ def _graph_rate(ms, nbytes=None, flops=None):
 
 
 def _rate(ms, nbytes=None, flops=None):
-    out = {"ms": round(ms, 4)}
+    out = {"ms": round(ms, 4), "launches": _LAUNCHED[0]}
     if nbytes is not None:
         gbps = nbytes / ms / 1e6
         out.update({"GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
