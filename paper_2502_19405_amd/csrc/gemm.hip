@@ -20,7 +20,7 @@
 // bits whichever sign the zero partial had.
 #include <hip/hip_runtime.h>
 
-#include "rep_math.h"
+#include "gemm_store.h"
 #include "repops_internal.h"
 
 #pragma clang fp contract(off)
@@ -36,22 +36,6 @@ __device__ __forceinline__ float kstep(float a, float b, float p) {
     const float prod = a * b;
     return p + prod;
   }
-}
-
-__device__ __forceinline__ float epilogue(const GemmArgs& g, float acc, int64_t j) {
-  float v = acc;
-  if (g.has_alpha) v = v * g.alpha;
-  if (g.bias) v = v + g.bias[j];
-  return v;
-}
-
-// Output (i, j) of one batch element (C and G already offset to it): the
-// value, and its GELU when the product carries a second output.
-__device__ __forceinline__ void store_out(const GemmArgs& g, float* C, float* G, int64_t i,
-                                          int64_t j, float acc) {
-  const float v = epilogue(g, acc, j);
-  C[i * g.ldc + j] = v;
-  if (G) G[i * g.ldg + j] = rep_gelu(v);
 }
 
 // ---------------------------------------------------------------------------
@@ -84,7 +68,7 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs g, int64_t ti
       acc = acc + p;
     }
     const int64_t co = b0 * g.sc0 + b1 * g.sc1;
-    store_out(g, g.C + co, g.G ? g.G + co : nullptr, i, j, acc);
+    gemm_store(g, g.C + co, g.G ? g.G + co : nullptr, i, j, acc);
   }
 }
 
@@ -206,7 +190,7 @@ __global__ __launch_bounds__((BM / TM) * (BN / TN)) void gemm_tiled_kernel(GemmA
 #pragma unroll
       for (int c = 0; c < TN; ++c) {
         const int64_t j = n0 + tx * TN + c;
-        if (j < g.n) store_out(g, C, G, i, j, acc[r][c]);
+        if (j < g.n) gemm_store(g, C, G, i, j, acc[r][c]);
       }
     }
   }

@@ -21,7 +21,7 @@
 // block starts from +0.
 #include <hip/hip_runtime.h>
 
-#include "rep_math.h"
+#include "gemm_store.h"
 #include "repops_internal.h"
 
 #pragma clang fp contract(off)
@@ -30,22 +30,6 @@ namespace repops {
 namespace {
 
 typedef float v32f __attribute__((ext_vector_type(32)));
-
-__device__ __forceinline__ float epilogue(const GemmArgs& g, float acc, int64_t j) {
-  float v = acc;
-  if (g.has_alpha) v = v * g.alpha;
-  if (g.bias) v = v + g.bias[j];
-  return v;
-}
-
-// Output (i, j) of one batch element (C and G already offset to it): the
-// value, and its GELU when the product carries a second output.
-__device__ __forceinline__ void store_out(const GemmArgs& g, float* C, float* G, int64_t i,
-                                          int64_t j, float acc) {
-  const float v = epilogue(g, acc, j);
-  C[i * g.ldc + j] = v;
-  if (G) G[i * g.ldg + j] = rep_gelu(v);
-}
 
 // Map the launch-order tile index so that the tiles one XCD receives (the
 // hardware deals workgroups round-robin over 8 XCDs) form a compact panel of
@@ -298,7 +282,7 @@ struct MfmaTile {
         for (int r = 0; r < 32; ++r) {
           const int row = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t i = m0 + wm0 + a * 64 + row;
-          if (!EDGE || (i < g.m && j < g.n)) store_out(g, C, G, i, j, acc[a][b][r]);
+          if (!EDGE || (i < g.m && j < g.n)) gemm_store(g, C, G, i, j, acc[a][b][r]);
         }
       }
   }
@@ -730,7 +714,7 @@ struct StagedTile {
         for (int r = 0; r < 32; ++r) {
           const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
-          if (row < g.m && col < g.n) store_out(g, C, G, row, col, acc[i][j][r]);
+          if (row < g.m && col < g.n) gemm_store(g, C, G, row, col, acc[i][j][r]);
         }
   }
 };
