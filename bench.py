@@ -43,7 +43,7 @@ def parse_launch(spec, repops):
 
 COUNTERS_MD = os.path.join(ROOT, "profiles", "llama_linear_backward_hbm_counters.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2502_19405_amd", "csrc", f)
-                  for f in ("gemm_mfma.hip", "repops_internal.h", "api.cpp")]
+                  for f in ("gemm_mfma.hip", "gemm_store.h", "repops_internal.h", "api.cpp")]
 
 
 def kernel_source_sha256():
