@@ -21,7 +21,7 @@ def declared_functions():
 @pytest.fixture(scope="module")
 def rp():
     if not os.path.exists(LIB):
-        pytest.fail("librepops.so is not built (run __graft_entry__.build())")
+        pytest.fail("librepops.so is not built (run python -m paper_2502_19405_amd.build)")
     from paper_2502_19405_amd import repops
     return repops
 
