@@ -80,6 +80,7 @@ MIN_TIMED_MS = 2.0
 # included); _rate reports it, so a kernel trace of the run can be split into
 # workloads call for call.
 _LAUNCHED = [0]
+_RAMPED = [0]  # untimed clock-ramp calls since the last _rate
 
 
 def event_time_ms(fn, reps, warmup=2, min_total_ms=None):
@@ -158,13 +159,15 @@ class ClockSampler:
 
 def clock_ramp(fn, ms=150.0):
     """Repeat fn for a fixed wall-clock duration (untimed) so that a
-    matrix-core workload is timed at steady clocks."""
+    matrix-core workload is timed at steady clocks; the calls are counted into
+    the next _rate figure."""
     import torch
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     while (time.perf_counter() - t0) * 1e3 < ms:
         fn()
         torch.cuda.synchronize()
+        _RAMPED[0] += 1
 
 
 def graph_time_ms(fn, calls=20, reps=10):
@@ -257,6 +260,9 @@ def _graph_rate(ms, nbytes=None, flops=None):
 
 def _rate(ms, nbytes=None, flops=None):
     out = {"ms": round(ms, 4), "launches": _LAUNCHED[0]}
+    if _RAMPED[0]:
+        out["ramp_launches"] = _RAMPED[0]
+        _RAMPED[0] = 0
     if nbytes is not None:
         gbps = nbytes / ms / 1e6
         out.update({"GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
