@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define REPOPS_ABI_VERSION 1u
+#define REPOPS_ABI_VERSION 2u
 
 typedef int32_t repops_status_t;
 enum {
@@ -185,18 +185,40 @@ repops_status_t repops_matmul_gelu(const repops_order_t *order, int64_t m, int64
  * batch elements must not overlap each other (not checked) nor A or B.
  */
 /*
+ * repops_matmul_gelu_backward -- C = GELU'(X) * (A.B), the input gradient of
+ * the feed-forward layer's GELU taken straight from the product that makes its
+ * output gradient (Section 3.2's matrix multiplication, then the reproducible
+ * GELU backward of Section 3.1's elementwise functions, as the training graph
+ * of Section 2.2 chains them): C[i][j] = RN(P[i][j] * gelu'(X[i][j])) with
+ * P the product repops_matmul gives and gelu' the tanh-form derivative, so C
+ * has exactly the bits of repops_matmul followed by repops_gelu_backward(X, P)
+ * under every launch descriptor.
+ *   Arguments as for repops_matmul without bias.
+ *   X, ldx    [m x n] forward input of the GELU, ldx >= n; C must not overlap
+ *             it (REPOPS_ERR_ALIAS); NULL is REPOPS_ERR_NULL unless m or n is 0.
+ */
+repops_status_t repops_matmul_gelu_backward(const repops_order_t *order, int64_t m, int64_t n,
+                                            int64_t k, const float *A, int64_t lda,
+                                            int32_t trans_a, const float *B, int64_t ldb,
+                                            int32_t trans_b, const float *X, int64_t ldx,
+                                            float *C, int64_t ldc, const repops_launch_t *launch,
+                                            void *hip_stream);
+
+/*
  * repops_matmul_grouped -- several independent products C_p = A_p.B_p (+ bias_p)
  * in one call, Section 3.2 (matrix multiplication) as for repops_matmul: each
  * product's outputs take exactly the bits repops_matmul gives for the same
- * arguments.  The products run concurrently (one launch whose workgroups cover
+ * arguments (repops_matmul_gelu_backward's where gelu_in is set).  The products run concurrently (one launch whose workgroups cover
  * every product's output tiles, the products with the longest contraction
  * first), so that products with few output tiles share the compute units:
  * the weight and input gradients of a linear layer are the intended use.
  *   count   0 .. REPOPS_MAX_GROUP products; descs: host array of count entries
  *           (read during the call only; may be NULL when count = 0).
- *   each desc's fields as repops_matmul's arguments.
- *   No C_p may overlap its own operands or any other product's A, B, bias or C
- *   (REPOPS_ERR_ALIAS).
+ *   each desc's fields as repops_matmul's arguments; gelu_in, ld_gelu_in: NULL
+ *           for a plain product, else the GELU input X of
+ *           repops_matmul_gelu_backward (then bias must be NULL).
+ *   No C_p may overlap its own operands or any other product's A, B, bias,
+ *   gelu_in or C (REPOPS_ERR_ALIAS).
  *   launch  NULL or AUTO.  When every nonempty product has K > 0, K and k_block
  *           multiples of 16, 16-byte aligned rows and the fused order, one
  *           launch of the 128 x 128 matrix-core tile runs them all; otherwise the
@@ -209,6 +231,7 @@ typedef struct repops_gemm_desc {
     const float *B; int64_t ldb; int32_t trans_b;
     const float *bias;
     float *C; int64_t ldc;
+    const float *gelu_in; int64_t ld_gelu_in;
 } repops_gemm_desc_t;
 #define REPOPS_MAX_GROUP 8
 repops_status_t repops_matmul_grouped(const repops_order_t *order, int32_t count,

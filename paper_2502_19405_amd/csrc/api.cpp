@@ -156,6 +156,18 @@ repops_status_t check_operands(const GemmArgs& g) {
   return REPOPS_OK;
 }
 
+// The GELU backward's forward input of a product (gelu_in): a [m x n] array
+// with its own leading dimension that the output may not touch; no bias.
+repops_status_t check_gelu_in(const GemmArgs& g) {
+  if (!g.gelu_in || g.m == 0 || g.n == 0) return REPOPS_OK;
+  if (g.bias) return REPOPS_ERR_VALUE;
+  if (g.ld_gelu_in < g.n) return REPOPS_ERR_STRIDE;
+  if (overlaps(extent_of(g.C, 1, 0, 1, 0, g.m, g.n, g.ldc),
+               extent_of(g.gelu_in, 1, 0, 1, 0, g.m, g.n, g.ld_gelu_in)))
+    return REPOPS_ERR_ALIAS;
+  return REPOPS_OK;
+}
+
 // Rows: Y may equal X exactly (same base, same leading dimension); any other
 // overlap is rejected.
 repops_status_t check_rows(int64_t rows, int64_t cols, const float* X, int64_t ldx, const float* Y,
@@ -405,6 +417,30 @@ repops_status_t repops_matmul_gelu(const repops_order_t* order, int64_t m, int64
   return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
 }
 
+repops_status_t repops_matmul_gelu_backward(const repops_order_t* order, int64_t m, int64_t n,
+                                            int64_t k, const float* A, int64_t lda,
+                                            int32_t trans_a, const float* B, int64_t ldb,
+                                            int32_t trans_b, const float* X, int64_t ldx,
+                                            float* C, int64_t ldc, const repops_launch_t* launch,
+                                            void* hip_stream) {
+  if (!order_valid(order)) return REPOPS_ERR_ORDER;
+  GemmArgs g{};
+  g.batch0 = 1; g.batch1 = 1; g.m = m; g.n = n; g.k = k;
+  g.A = A; g.lda = lda; g.ta = trans_a;
+  g.B = B; g.ldb = ldb; g.tb = trans_b;
+  g.C = C; g.ldc = ldc;
+  g.gelu_in = X; g.ld_gelu_in = ldx;
+  g.alpha = 1.0f; g.has_alpha = 0;
+  g.k_block = order->k_block;
+  repops_status_t st = check_operands(g);
+  if (st != REPOPS_OK) return st;
+  if (m == 0 || n == 0) return REPOPS_OK;
+  if (!X) return REPOPS_ERR_NULL;
+  st = check_gelu_in(g);
+  if (st != REPOPS_OK) return st;
+  return run_gemm(order, g, launch, static_cast<hipStream_t>(hip_stream));
+}
+
 repops_status_t repops_matmul_grouped(const repops_order_t* order, int32_t count,
                                       const repops_gemm_desc_t* descs,
                                       const repops_launch_t* launch, void* hip_stream) {
@@ -425,9 +461,11 @@ repops_status_t repops_matmul_grouped(const repops_order_t* order, int32_t count
     g[p].B = d.B; g[p].ldb = d.ldb; g[p].tb = d.trans_b;
     g[p].C = d.C; g[p].ldc = d.ldc;
     g[p].bias = d.bias; g[p].alpha = 1.0f; g[p].has_alpha = 0;
+    g[p].gelu_in = d.gelu_in; g[p].ld_gelu_in = d.ld_gelu_in;
     g[p].k_block = order->k_block;
     g[p].fused = order->k_inner == REPOPS_K_FMA ? 1 : 0;
-    const repops_status_t st = check_operands(g[p]);
+    repops_status_t st = check_operands(g[p]);
+    if (st == REPOPS_OK) st = check_gelu_in(g[p]);
     if (st != REPOPS_OK) return st;
     live[p] = g[p].m > 0 && g[p].n > 0;
   }
@@ -448,6 +486,9 @@ repops_status_t repops_matmul_grouped(const repops_order_t* order, int32_t count
         if (overlaps(ce, ae) || overlaps(ce, be)) return REPOPS_ERR_ALIAS;
       }
       if (g[q].bias && overlaps(ce, extent_of(g[q].bias, 1, 0, 1, 0, 1, g[q].n, g[q].n)))
+        return REPOPS_ERR_ALIAS;
+      if (g[q].gelu_in &&
+          overlaps(ce, extent_of(g[q].gelu_in, 1, 0, 1, 0, g[q].m, g[q].n, g[q].ld_gelu_in)))
         return REPOPS_ERR_ALIAS;
     }
   }

@@ -68,7 +68,8 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs g, int64_t ti
       acc = acc + p;
     }
     const int64_t co = b0 * g.sc0 + b1 * g.sc1;
-    gemm_store(g, g.C + co, g.G ? g.G + co : nullptr, i, j, acc);
+    gemm_store(g, g.C + co, g.G ? g.G + co : nullptr, g.gelu_in ? g.gelu_in + co : nullptr, i, j,
+               acc);
   }
 }
 
@@ -183,6 +184,7 @@ __global__ __launch_bounds__((BM / TM) * (BN / TN)) void gemm_tiled_kernel(GemmA
 
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
     float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
       const int64_t i = m0 + ty * TM + r;
@@ -190,7 +192,7 @@ __global__ __launch_bounds__((BM / TM) * (BN / TN)) void gemm_tiled_kernel(GemmA
 #pragma unroll
       for (int c = 0; c < TN; ++c) {
         const int64_t j = n0 + tx * TN + c;
-        if (j < g.n) gemm_store(g, C, G, i, j, acc[r][c]);
+        if (j < g.n) gemm_store(g, C, G, X, i, j, acc[r][c]);
       }
     }
   }

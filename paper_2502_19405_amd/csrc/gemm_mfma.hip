@@ -273,6 +273,7 @@ struct MfmaTile {
     // 8*((r%16)/4) + 4*(l/32) + r%4 and column l % 32.
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
     float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int a = 0; a < IM; ++a)
 #pragma unroll
@@ -282,7 +283,7 @@ struct MfmaTile {
         for (int r = 0; r < 32; ++r) {
           const int row = 32 * (r / 16) + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t i = m0 + wm0 + a * 64 + row;
-          if (!EDGE || (i < g.m && j < g.n)) gemm_store(g, C, G, i, j, acc[a][b][r]);
+          if (!EDGE || (i < g.m && j < g.n)) gemm_store(g, C, G, X, i, j, acc[a][b][r]);
         }
       }
   }
@@ -361,7 +362,11 @@ __device__ __forceinline__ void lds_barrier() {
 // DUAL: a second set of block partials, so that each 64-deep block's adds into
 // acc are spread over the next block's matrix steps (the staged kernel uses it
 // where a wave owns one instruction tile).
-template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB, bool DUAL>
+// GELU_OUT: the epilogue can write the GELU of the output (repops_matmul_gelu);
+// the grouped kernel, which never does, leaves that path out (with both GELU
+// paths its four tile forms together spilled registers).
+template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB, bool DUAL,
+          bool GELU_OUT = true>
 struct StagedTile {
   static_assert(BK % 16 == 0, "k slices hold whole 16-step groups");
   static constexpr int NW = WM * WN;
@@ -705,7 +710,8 @@ struct StagedTile {
     // Accumulator layout (lane l, register r): block r / 16 holds columns
     // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
-    float* G = g.G ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    float* G = (GELU_OUT && g.G) ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -714,7 +720,7 @@ struct StagedTile {
         for (int r = 0; r < 32; ++r) {
           const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
           const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
-          if (row < g.m && col < g.n) gemm_store(g, C, G, row, col, acc[i][j][r]);
+          if (row < g.m && col < g.n) gemm_store(g, C, G, X, row, col, acc[i][j][r]);
         }
   }
 };
@@ -741,10 +747,10 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
 // computation as in a launch of its own product, so the bits are the same.
 template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool DUAL>
 __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_grouped_kernel(GroupArgs ga) {
-  using T00 = StagedTile<BM, BN, BK, WM, WN, NS, false, false, DUAL>;
-  using T01 = StagedTile<BM, BN, BK, WM, WN, NS, false, true, DUAL>;
-  using T10 = StagedTile<BM, BN, BK, WM, WN, NS, true, false, DUAL>;
-  using T11 = StagedTile<BM, BN, BK, WM, WN, NS, true, true, DUAL>;
+  using T00 = StagedTile<BM, BN, BK, WM, WN, NS, false, false, DUAL, false>;
+  using T01 = StagedTile<BM, BN, BK, WM, WN, NS, false, true, DUAL, false>;
+  using T10 = StagedTile<BM, BN, BK, WM, WN, NS, true, false, DUAL, false>;
+  using T11 = StagedTile<BM, BN, BK, WM, WN, NS, true, true, DUAL, false>;
   static_assert(sizeof(typename T00::Smem) == sizeof(typename T11::Smem), "one LDS form size");
   __shared__ typename T00::Smem sm;
   const int64_t t = blockIdx.x;

@@ -1,9 +1,12 @@
 // The last operations of every GEMM kernel's output, shared by the vector and
 // matrix-core paths so that they cannot drift apart: the contraction's value
 // scaled by alpha (batched products) and plus bias[j] (matmul), each one
-// rounded operation, then the store -- and, for repops_matmul_gelu, the GELU
-// of the stored value into a second array (the same rep_gelu the elementwise
-// kernel runs, so both arrays have the bits of the separate calls).
+// rounded operation; for the GELU backward's product, times the GELU
+// derivative at the forward input (one rounded multiplication, as the
+// elementwise GELU backward takes it); then the store -- and, for
+// repops_matmul_gelu, the GELU of the stored value into a second array.  The
+// GELU functions are the ones the elementwise kernels run, so every array has
+// the bits of the separate calls.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -23,10 +26,12 @@ __device__ __forceinline__ float gemm_epilogue(const GemmArgs& g, float acc, int
   return v;
 }
 
-// Output (i, j) of one batch element (C and G already offset to it).
-__device__ __forceinline__ void gemm_store(const GemmArgs& g, float* C, float* G, int64_t i,
-                                           int64_t j, float acc) {
-  const float v = gemm_epilogue(g, acc, j);
+// Output (i, j) of one batch element (C, G and X, the GELU backward's
+// forward input, already offset to it; G and X nullable).
+__device__ __forceinline__ void gemm_store(const GemmArgs& g, float* C, float* G, const float* X,
+                                           int64_t i, int64_t j, float acc) {
+  float v = gemm_epilogue(g, acc, j);
+  if (X) v = v * rep_gelu_grad(X[i * g.ld_gelu_in + j]);
   C[i * g.ldc + j] = v;
   if (G) G[i * g.ldg + j] = rep_gelu(v);
 }

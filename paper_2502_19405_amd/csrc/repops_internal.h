@@ -12,6 +12,7 @@ struct GemmArgs {
   const float* B; int64_t sb0, sb1, ldb; int tb;
   float* C; int64_t sc0, sc1, ldc;
   float* G; int64_t ldg;  // nullable: G = gelu(C) elementwise, batch offsets as C's
+  const float* gelu_in; int64_t ld_gelu_in;  // nullable: C = value * gelu'(gelu_in), offsets as C's
   const float* bias;  // nullable, [n]
   float alpha;
   int has_alpha;      // 1: C = acc * alpha

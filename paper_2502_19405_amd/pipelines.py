@@ -4,8 +4,10 @@ Each function only chains C-ABI calls through the binding (no arithmetic of
 its own), in the shapes of the programs Verde's evaluation runs (Section 4.2):
 a DistilBERT feed-forward block, a Llama attention block and the backward
 products of a Llama linear layer.  The feed-forward GELU is produced by the
-first product's epilogue (repops_matmul_gelu), which gives the bits of the
-product and of the elementwise GELU taken separately; every other
+first product's epilogue (repops_matmul_gelu), and in the training step the
+GELU's input gradient by the epilogue of the product that makes its output
+gradient (repops_matmul_gelu_backward, grouped); both give the bits of the
+product and of the elementwise operator taken separately.  Every other
 intermediate comes from its own operator call.
 """
 from __future__ import annotations
@@ -152,14 +154,15 @@ def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps
     dH2, _, _ = repops.layernorm_backward_rows(H2, dY, mean, rstd, gamma, order=order,
                                                dx_out=buf("dH2", t, h), dgamma_out=ggamma,
                                                dbeta_out=gbeta)
+    # dH1 = gelu_backward(H1, dH2 W2^T) straight from the product's epilogue
     if gemm_launch is None:
-        _, dG = repops.matmul_grouped([(G.t(), dH2, None, gW2), (dH2, W2.t(), None, buf("dG", t, f))],
-                                      order=order)
+        _, dH1 = repops.matmul_grouped([(G.t(), dH2, None, gW2),
+                                        (dH2, W2.t(), None, buf("dH1", t, f), H1)], order=order)
     else:
         repops.matmul(G.t(), dH2, order=order, launch=gemm_launch, out=gW2)
-        dG = repops.matmul(dH2, W2.t(), order=order, launch=gemm_launch, out=buf("dG", t, f))
+        dH1 = repops.matmul_gelu_backward(dH2, W2.t(), H1, order=order, launch=gemm_launch,
+                                          out=buf("dH1", t, f))
     repops.colsum_rows(dH2, order=order, out=gb2)
-    dH1 = repops.gelu_backward(H1, dG, order=order, out=dG)
     if gemm_launch is None:
         _, dX = repops.matmul_grouped([(X.t(), dH1, None, gW1), (dH1, W1.t(), None, buf("dX", t, h))],
                                       order=order)

@@ -79,7 +79,8 @@ class GemmDescT(ctypes.Structure):
     _fields_ = [("m", ctypes.c_int64), ("n", ctypes.c_int64), ("k", ctypes.c_int64),
                 ("A", ctypes.c_void_p), ("lda", ctypes.c_int64), ("trans_a", ctypes.c_int32),
                 ("B", ctypes.c_void_p), ("ldb", ctypes.c_int64), ("trans_b", ctypes.c_int32),
-                ("bias", ctypes.c_void_p), ("C", ctypes.c_void_p), ("ldc", ctypes.c_int64)]
+                ("bias", ctypes.c_void_p), ("C", ctypes.c_void_p), ("ldc", ctypes.c_int64),
+                ("gelu_in", ctypes.c_void_p), ("ld_gelu_in", ctypes.c_int64)]
 
 
 MAX_GROUP = 8  # REPOPS_MAX_GROUP
@@ -99,6 +100,8 @@ _SIGNATURES = {
                              _i64, _lp, _vp]),
     "repops_matmul_gelu": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32, _vp,
                                   _vp, _i64, _vp, _i64, _lp, _vp]),
+    "repops_matmul_gelu_backward": (_i32, [_op, _i64, _i64, _i64, _vp, _i64, _i32, _vp, _i64, _i32,
+                                           _vp, _i64, _vp, _i64, _lp, _vp]),
     "repops_matmul_grouped": (_i32, [_op, _i32, ctypes.POINTER(GemmDescT), _lp, _vp]),
     "repops_bmm_causal": (_i32, [_op, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _i32,
                                  _vp, _i64, _i64, _i64, _i32, _f32, _vp, _i64, _i64, _i64, _i32,
@@ -302,15 +305,47 @@ def matmul_gelu(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = No
     return out, gelu_out
 
 
+def _gelu_in(X, m, n):
+    """(pointer, leading dimension) of a GELU backward's forward input."""
+    if X.dim() != 2 or tuple(X.shape) != (m, n) or X.stride(1) != 1:
+        raise ValueError(f"gelu_in must be a row-major [{m}, {n}] tensor")
+    return _dev(X, "gelu_in"), max(X.stride(0), n, 1)
+
+
+def matmul_gelu_backward(A: torch.Tensor, B: torch.Tensor, X: torch.Tensor,
+                         order: Order | None = None, launch: Launch | None = None,
+                         out: torch.Tensor | None = None) -> torch.Tensor:
+    """gelu_backward(X, A @ B) from one pass: the bits of matmul followed by
+    gelu_backward."""
+    pa, m, k, lda, ta = _mat(A, "A")
+    pb, k2, n, ldb, tb = _mat(B, "B")
+    if k != k2:
+        raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+    px, ldx = _gelu_in(X, m, n)
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    if out.shape != (m, n) or out.stride(1) != 1:
+        raise ValueError("out must be a row-major [m, n] tensor")
+    rc = load().repops_matmul_gelu_backward(_ord(order), m, n, k, pa, lda, ta, pb, ldb, tb, px,
+                                            ldx, _dev(out, "out"), max(out.stride(0), n, 1),
+                                            _launch(launch), _stream(out))
+    _check(rc, "repops_matmul_gelu_backward")
+    return out
+
+
 def matmul_grouped(products, order: Order | None = None) -> list:
     """Several independent products in one call: products is a list of
-    (A, B, bias, out) with the meaning of matmul's arguments (bias and out may
-    be None); returns the outputs.  Every output has the bits matmul gives."""
+    (A, B, bias, out) or (A, B, bias, out, gelu_in) with the meaning of matmul's
+    arguments (bias and out may be None) and of matmul_gelu_backward's X;
+    returns the outputs.  Every output has the bits matmul (or
+    matmul_gelu_backward) gives."""
     if len(products) > MAX_GROUP:
         raise ValueError(f"at most {MAX_GROUP} products per call")
     descs = (GemmDescT * max(len(products), 1))()
     outs = []
-    for d, (A, B, bias, out) in zip(descs, products):
+    for d, prod in zip(descs, products):
+        A, B, bias, out = prod[:4]
+        X = prod[4] if len(prod) > 4 else None
         pa, m, k, lda, ta = _mat(A, "A")
         pb, k2, n, ldb, tb = _mat(B, "B")
         if k != k2:
@@ -327,6 +362,8 @@ def matmul_grouped(products, order: Order | None = None) -> list:
         d.m, d.n, d.k = m, n, k
         d.A, d.lda, d.trans_a, d.B, d.ldb, d.trans_b = pa, lda, ta, pb, ldb, tb
         d.bias, d.C, d.ldc = pbias, _dev(out, "out"), max(out.stride(0), n, 1)
+        if X is not None:
+            d.gelu_in, d.ld_gelu_in = _gelu_in(X, m, n)
         outs.append(out)
     rc = load().repops_matmul_grouped(_ord(order), len(products), descs, None,
                                       _stream(outs[0]) if outs else None)

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_function(rp):
 
 def test_version_default_order_and_status_strings(rp):
     lib = rp.load()
-    assert lib.repops_abi_version() == 1
+    assert lib.repops_abi_version() == 2
     o = rp.OrderT()
     lib.repops_order_default(ctypes.byref(o))
     assert (o.version, o.k_block, o.k_inner, o.k_combine, o.row_width, o.row_combine) == (
@@ -180,6 +180,39 @@ def test_matmul_gelu_rejections(rp):
     assert call(launch=ctypes.byref(rp.Launch(7).c())) == rp.ERR_LAUNCH
     # nothing to write: succeeds without touching any pointer or the device
     assert call(m=0, A=None, B=None, H=None, G=None) == rp.OK
+
+
+@no_gpu_only
+def test_matmul_gelu_backward_rejections(rp):
+    lib = rp.load()
+    FAKE_X = 0x500000
+
+    def call(order=None, m=4, n=4, k=4, A=FAKE_A, lda=4, ta=0, B=FAKE_B, ldb=4, tb=0, X=FAKE_X,
+             ldx=4, C=FAKE_C, ldc=4, launch=None):
+        return lib.repops_matmul_gelu_backward(order or _order(), m, n, k, A, lda, ta, B, ldb, tb,
+                                               X, ldx, C, ldc, launch, None)
+    assert call(order=_order(version=2)) == rp.ERR_ORDER
+    assert call(m=-1) == rp.ERR_SHAPE
+    assert call(C=None) == rp.ERR_NULL
+    assert call(X=None) == rp.ERR_NULL
+    assert call(ldx=3) == rp.ERR_STRIDE
+    assert call(C=FAKE_X + 8) == rp.ERR_ALIAS            # C over X
+    assert call(C=FAKE_B + 60) == rp.ERR_ALIAS           # C over B (the matmul checks)
+    assert call(launch=ctypes.byref(rp.Launch(7).c())) == rp.ERR_LAUNCH
+    assert call(m=0, A=None, B=None, X=None, C=None) == rp.OK
+    # the grouped form: gelu_in per product
+    D = rp.GemmDescT
+
+    def desc(bias=None, C=FAKE_C, gelu_in=FAKE_X, ld_gelu_in=8):
+        return D(8, 8, 8, FAKE_A, 8, 0, FAKE_B, 8, 0, bias, C, 8, gelu_in, ld_gelu_in)
+
+    def grouped(*ds):
+        arr = (D * len(ds))(*ds)
+        return lib.repops_matmul_grouped(_order(), len(ds), arr, None, None)
+    assert grouped(desc(ld_gelu_in=7)) == rp.ERR_STRIDE
+    assert grouped(desc(bias=0x600000)) == rp.ERR_VALUE          # no bias with gelu_in
+    assert grouped(desc(C=FAKE_X + 16)) == rp.ERR_ALIAS          # C over its own gelu_in
+    assert grouped(desc(), desc(C=FAKE_X + 16, gelu_in=None)) == rp.ERR_ALIAS  # over another's
 
 
 def test_matmul_zero_sized_is_a_noop(rp):

@@ -90,6 +90,44 @@ def test_matmul_gelu_all_launches(rp, shape, k_block, k_inner):
 
 
 @pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("k_block,k_inner", [(64, 0), (0, 0), (64, 1)])
+def test_matmul_gelu_backward_all_launches(rp, shape, k_block, k_inner):
+    # C = gelu_backward(X, A.B) from one pass: the oracle's product, then the
+    # oracle's GELU backward with that product as dy, under every launch and
+    # transposition; alone and as one product of a grouped call
+    m, n, k = shape
+    g = inputs.rng(7 * m + 3 * n + 13 * k + k_block + k_inner)
+    A = inputs.normal(g, (m, k))
+    B = (inputs.normal(g, (k, n)) * np.float32(0.1)).astype(np.float32)
+    X = inputs.uniform(g, (m, n), -4.0, 4.0)
+    want = oracle.gelu_backward(X, oracle.matmul(A, B, k_block=k_block, k_inner=k_inner))
+    order = rp.Order(k_block=k_block, k_inner=k_inner)
+    dA, dB, dX = dev(A), dev(B), dev(X)
+    dAt, dBt = dev(np.ascontiguousarray(A.T)), dev(np.ascontiguousarray(B.T))
+    for name, launch in [("auto", None)] + launches(rp, k_block, k_inner == 0):
+        announce("matmul_gelu_backward", shape, k_block, k_inner, name)
+        for ta, tb in ((0, 0), (1, 1)):
+            a = dAt.t() if ta else dA
+            b = dBt.t() if tb else dB
+            got = rp.matmul_gelu_backward(a, b, dX, order=order, launch=launch)
+            assert_bits_equal(host(got), want, f"{name} trans {ta}{tb}")
+    import torch
+    # the forward input in a padded view, and the separate calls give the same bits
+    Xp = torch.full((m, n + 7), float("nan"), device=dA.device)
+    Xp[:, :n] = dX
+    got = rp.matmul_gelu_backward(dA, dB, Xp[:, :n], order=order)
+    p = rp.matmul(dA, dB, order=order)
+    assert same_bits(got, rp.gelu_backward(dX, p, order=order))
+    # grouped beside a plain product: each with its own bits
+    other = dev(inputs.normal(g, (k, 2 * n + 1)))
+    announce("grouped gelu_backward", shape, k_block, k_inner)
+    plain, gb = rp.matmul_grouped([(dA, other, None, None), (dA, dB, None, None, dX)],
+                                  order=order)
+    assert same_bits(plain, rp.matmul(dA, other, order=order))
+    assert_bits_equal(host(gb), want, f"grouped {shape}")
+
+
+@pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("k_block,k_inner", ORDERS)
 def test_matmul_small_all_launches(rp, shape, k_block, k_inner):
     m, n, k = shape
