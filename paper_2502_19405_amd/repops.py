@@ -186,12 +186,24 @@ def _check(rc: int, what: str):
         raise RepopsError(rc, what)
 
 
+_F32 = torch.float32
+
+
 def _dev(t: torch.Tensor, name: str):
-    if t.dtype != torch.float32:
+    if t.dtype is not _F32:
         raise TypeError(f"{name} must be float32")
     if not t.is_cuda:
         raise TypeError(f"{name} must be a device tensor")
     return t.data_ptr()
+
+
+def _vec(t, name: str, size: int):
+    """Pointer of an optional contiguous [size] float32 device vector."""
+    if t is None:
+        return None
+    if t.numel() != size or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous [{size}] tensor")
+    return _dev(t, name)
 
 
 try:  # the raw handle of the current stream, without building a Stream object
@@ -435,9 +447,9 @@ def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = 
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
     _, _, ldy = _rows(out, "out")
-    rc = load().repops_softmax_rows(_ord(order), rows, cols,
-                                    _dev(X, "X"), ldx, _dev(out, "out"), ldy, causal_period,
-                                    _launch(launch), _stream(out))
+    rc = (_lib or load()).repops_softmax_rows(_ord(order), rows, cols, _dev(X, "X"), ldx,
+                                              _dev(out, "out"), ldy, causal_period,
+                                              _launch(launch), _stream(out))
     _check(rc, "repops_softmax_rows")
     return out
 
@@ -451,19 +463,11 @@ def layernorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None,
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
     _, _, ldy = _rows(out, "out")
-    ptrs = []
-    for t, name, size in ((gamma, "gamma", cols), (beta, "beta", cols), (mean_out, "mean_out", rows),
-                          (rstd_out, "rstd_out", rows)):
-        if t is None:
-            ptrs.append(None)
-            continue
-        if t.numel() != size or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous [{size}] tensor")
-        ptrs.append(_dev(t, name))
-    rc = load().repops_layernorm_rows(_ord(order), rows, cols,
-                                      _dev(X, "X"), ldx, ptrs[0], ptrs[1], float(eps),
-                                      _dev(out, "out"), ldy, ptrs[2], ptrs[3], _launch(launch),
-                                      _stream(out))
+    rc = (_lib or load()).repops_layernorm_rows(
+        _ord(order), rows, cols, _dev(X, "X"), ldx, _vec(gamma, "gamma", cols),
+        _vec(beta, "beta", cols), float(eps), _dev(out, "out"), ldy,
+        _vec(mean_out, "mean_out", rows),
+        _vec(rstd_out, "rstd_out", rows), _launch(launch), _stream(out))
     _check(rc, "repops_layernorm_rows")
     return out
 
