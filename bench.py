@@ -170,12 +170,17 @@ def clock_ramp(fn, ms=150.0):
         _RAMPED[0] += 1
 
 
+GRAPHS = True  # False (--no-graphs): no graph-replayed figures
+
+
 def graph_time_ms(fn, calls=20, reps=10):
     """Average duration of fn() with `calls` of them captured in one HIP graph
     and the graph replayed `reps` times: the kernels' own time without host
     launch gaps (none of the library's calls allocates or clears memory, so
-    they capture as they run)."""
+    they capture as they run).  None when GRAPHS is off."""
     import torch
+    if not GRAPHS:
+        return None
     fn()
     torch.cuda.synchronize()
     side = torch.cuda.Stream()
@@ -254,7 +259,10 @@ def cpu_baseline(d, target_s=12.0):
 
 
 def _graph_rate(ms, nbytes=None, flops=None):
-    """The same figures for graph-replayed calls, keys prefixed graph_."""
+    """The same figures for graph-replayed calls, keys prefixed graph_ (none
+    without a measurement)."""
+    if ms is None:
+        return {}
     return {"graph_" + k: v for k, v in _rate(ms, nbytes, flops).items()}
 
 
@@ -559,6 +567,8 @@ def main():
     # reach their steady state; this ramp runs before the counted warmup and
     # is not timed, so a small --warmup still measures steady clocks.
     ap.add_argument("--ramp-ms", type=float, default=300.0)
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="leave out the graph-replayed secondary figures (counter passes)")
     ap.add_argument("--launch", default="auto",
                     help="auto | simple | tiled:I | mfma:I (auto picks mfma:0 for both products)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -684,9 +694,10 @@ def main():
         torch.cuda.synchronize()
         result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_secondary:
-        global MIN_TIMED_MS
+        global MIN_TIMED_MS, GRAPHS
         if args.streaming_only:
             MIN_TIMED_MS = 0.0
+        GRAPHS = not args.no_graphs
         result["secondary"] = secondary(repops, 20, args.streaming_only,
                                         headline={"X": X, "dY": dY, "W": W, "dX": dX, "dW": dW})
     if not args.no_cpu_baseline:
