@@ -99,6 +99,7 @@ repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_
     int mfma_pref = 0;                                  // 128 x 128 tiles, 8 waves, ring
     if (outputs <= (int64_t(1) << 20)) mfma_pref = 5;   // small outputs: 64 x 64 tiles
     else if (g.k <= 256) mfma_pref = 2;                 // short k: register-staged slices
+    else if (g.causal == 2) mfma_pref = 8;              // causal A: 64-row tiles
     if (!mfma_ok(repops::gemm_mfma_config(mfma_pref))) mfma_pref = 0;
     const int tiled_pref = outputs >= (int64_t(1) << 22) ? 1 : 0;
     if (mfma_ok(repops::gemm_mfma_config(mfma_pref))) {

@@ -810,6 +810,10 @@ const MfmaEntry kMfma[] = {
     REPOPS_MFMA(64, 64, 32, 1, 2, 2),               // 5: small outputs
     REPOPS_STAGED(128, 128, 32, 4, 2, 4, 2, 2, 4),  // 6
     REPOPS_STAGED(256, 128, 16, 4, 2, 4, 2, 4, 2),  // 7
+    // 8: products whose A is zero above its diagonal (causal probabilities x
+    // values): 64-row tiles end their contraction closer to their diagonal, and
+    // three workgroups per CU overlap one tile's loads and stores with another's
+    REPOPS_STAGED(64, 128, 16, 2, 2, 4, 3, 1, 4),
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
