@@ -176,15 +176,6 @@ repops_status_t repops_matmul_gelu(const repops_order_t *order, int64_t m, int64
                                    int64_t ldg, const repops_launch_t *launch, void *hip_stream);
 
 /*
- * repops_bmm -- batched product over (i0, i1) in [0,batch0) x [0,batch1), the
- * batched key-query and probability-value products of attention that Section
- * 2.2 decomposes into independent matrix products.  Batch element (i0, i1)
- * reads A + i0*sa0 + i1*sa1 and B + i0*sb0 + i1*sb1 with the matmul layout
- * rules, and writes C + i0*sc0 + i1*sc1:  C[i][j] = acc * alpha (one rounded
- * multiplication).  Strides may be 0 for A and B; the C regions of different
- * batch elements must not overlap each other (not checked) nor A or B.
- */
-/*
  * repops_matmul_gelu_backward -- C = GELU'(X) * (A.B), the input gradient of
  * the feed-forward layer's GELU taken straight from the product that makes its
  * output gradient (Section 3.2's matrix multiplication, then the reproducible
@@ -238,6 +229,21 @@ repops_status_t repops_matmul_grouped(const repops_order_t *order, int32_t count
                                       const repops_gemm_desc_t *descs,
                                       const repops_launch_t *launch, void *hip_stream);
 
+/*
+ * repops_bmm -- batched product over (i0, i1) in [0,batch0) x [0,batch1), the
+ * batched key-query and probability-value products of attention that Section
+ * 2.2 decomposes into independent matrix products.  Batch element (i0, i1)
+ * reads A + i0*sa0 + i1*sa1 and B + i0*sb0 + i1*sb1 with the matmul layout
+ * rules, and writes C + i0*sc0 + i1*sc1:  C[i][j] = acc * alpha (one rounded
+ * multiplication).  Strides may be 0 for A and B.  C may not overlap A or B
+ * (REPOPS_ERR_ALIAS), and no two of its elements may share an address
+ * (REPOPS_ERR_STRIDE), checked by a sufficient condition: taking the
+ * dimensions batch0, batch1, m (stride ldc) and n (stride 1) that have more
+ * than one element in increasing order of |stride|, each stride must exceed
+ * the span of the ones before it -- every permutation of a dense array, such
+ * as heads interleaved within the rows of a [tokens x heads*dim] output,
+ * passes.
+ */
 repops_status_t repops_bmm(const repops_order_t *order, int64_t batch0, int64_t batch1,
                            int64_t m, int64_t n, int64_t k,
                            const float *A, int64_t sa0, int64_t sa1, int64_t lda, int32_t trans_a,

@@ -65,6 +65,37 @@ Extent extent_of(const float* p, int64_t b0, int64_t s0, int64_t b1, int64_t s1,
 
 bool overlaps(Extent a, Extent b) { return a.lo < b.hi && b.lo < a.hi; }
 
+// True when no two elements of a [b0][b1][rows][cols] array with element
+// strides (s0, s1, ld, 1) share an address: taking the dimensions of more than
+// one element in increasing order of |stride|, each must step past the span of
+// the ones before it.  A sufficient condition (every permutation of a dense
+// array passes); an output that fails it would have two batch elements write
+// one address in an unspecified order.
+bool elements_disjoint(int64_t b0, int64_t s0, int64_t b1, int64_t s1, int64_t rows, int64_t ld,
+                       int64_t cols) {
+  struct Dim {
+    uint64_t size, stride;
+  };
+  auto mag = [](int64_t s) { return s < 0 ? 0 - static_cast<uint64_t>(s) : static_cast<uint64_t>(s); };
+  Dim d[4] = {{static_cast<uint64_t>(cols), 1},
+              {static_cast<uint64_t>(rows), mag(ld)},
+              {static_cast<uint64_t>(b1), mag(s1)},
+              {static_cast<uint64_t>(b0), mag(s0)}};
+  for (int i = 1; i < 4; ++i)
+    for (int j = i; j > 0 && d[j].stride < d[j - 1].stride; --j) {
+      const Dim t = d[j];
+      d[j] = d[j - 1];
+      d[j - 1] = t;
+    }
+  unsigned __int128 span = 0;  // offsets the dimensions taken so far reach
+  for (const Dim& x : d) {
+    if (x.size <= 1) continue;
+    if (x.stride <= span) return false;
+    span += static_cast<unsigned __int128>(x.size - 1) * x.stride;
+  }
+  return true;
+}
+
 repops_status_t hip_status(hipError_t e) { return e == hipSuccess ? REPOPS_OK : REPOPS_ERR_HIP; }
 
 repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_launch_t* launch,
@@ -138,6 +169,8 @@ repops_status_t check_operands(const GemmArgs& g) {
   if (!g.C) return REPOPS_ERR_NULL;
   if (g.k > 0 && (!g.A || !g.B)) return REPOPS_ERR_NULL;
   if (g.ldc < g.n || g.ldc < 1) return REPOPS_ERR_STRIDE;
+  if (!elements_disjoint(g.batch0, g.sc0, g.batch1, g.sc1, g.m, g.ldc, g.n))
+    return REPOPS_ERR_STRIDE;
   if (g.k > 0) {
     if (g.lda < (g.ta ? g.m : g.k)) return REPOPS_ERR_STRIDE;
     if (g.ldb < (g.tb ? g.k : g.n)) return REPOPS_ERR_STRIDE;

@@ -206,6 +206,16 @@ def _vec(t, name: str, size: int):
     return _dev(t, name)
 
 
+def _workspace(t):
+    """(pointer, bytes) of a caller's workspace: any contiguous device tensor,
+    whose size the library checks against what the call needs."""
+    if t is None:
+        return None, 0
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor")
+    return t.data_ptr(), t.numel() * t.element_size()
+
+
 try:  # the raw handle of the current stream, without building a Stream object
     _raw_stream = torch._C._cuda_getCurrentRawStream
 except AttributeError:  # pragma: no cover - older torch
@@ -274,15 +284,14 @@ def matmul(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = None,
         raise ValueError(f"inner dimensions differ: {k} vs {k2}")
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
-    if out.shape != (m, n) or out.stride(1) != 1:
-        raise ValueError("out must be a row-major [m, n] tensor")
+    ldc = _rows_as(out, m, n, "out")
     pbias = None
     if bias is not None:
         if bias.shape != (n,) or not bias.is_contiguous():
             raise ValueError("bias must be a contiguous [n] tensor")
         pbias = _dev(bias, "bias")
     rc = load().repops_matmul(_ord(order), m, n, k, pa, lda, ta,
-                              pb, ldb, tb, pbias, _dev(out, "out"), max(out.stride(0), n, 1),
+                              pb, ldb, tb, pbias, _dev(out, "out"), ldc,
                               _launch(launch), _stream(out))
     _check(rc, "repops_matmul")
     return out
@@ -301,17 +310,15 @@ def matmul_gelu(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = No
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
     if gelu_out is None:
         gelu_out = torch.empty((m, n), dtype=torch.float32, device=A.device)
-    for t, name in ((out, "out"), (gelu_out, "gelu_out")):
-        if t.shape != (m, n) or t.stride(1) != 1:
-            raise ValueError(f"{name} must be a row-major [m, n] tensor")
+    ldh = _rows_as(out, m, n, "out")
+    ldg = _rows_as(gelu_out, m, n, "gelu_out")
     pbias = None
     if bias is not None:
         if bias.shape != (n,) or not bias.is_contiguous():
             raise ValueError("bias must be a contiguous [n] tensor")
         pbias = _dev(bias, "bias")
     rc = load().repops_matmul_gelu(_ord(order), m, n, k, pa, lda, ta, pb, ldb, tb, pbias,
-                                   _dev(out, "out"), max(out.stride(0), n, 1),
-                                   _dev(gelu_out, "gelu_out"), max(gelu_out.stride(0), n, 1),
+                                   _dev(out, "out"), ldh, _dev(gelu_out, "gelu_out"), ldg,
                                    _launch(launch), _stream(out))
     _check(rc, "repops_matmul_gelu")
     return out, gelu_out
@@ -319,9 +326,8 @@ def matmul_gelu(A: torch.Tensor, B: torch.Tensor, bias: torch.Tensor | None = No
 
 def _gelu_in(X, m, n):
     """(pointer, leading dimension) of a GELU backward's forward input."""
-    if X.dim() != 2 or tuple(X.shape) != (m, n) or X.stride(1) != 1:
-        raise ValueError(f"gelu_in must be a row-major [{m}, {n}] tensor")
-    return _dev(X, "gelu_in"), max(X.stride(0), n, 1)
+    ld = _rows_as(X, m, n, "gelu_in")
+    return _dev(X, "gelu_in"), ld
 
 
 def matmul_gelu_backward(A: torch.Tensor, B: torch.Tensor, X: torch.Tensor,
@@ -336,10 +342,9 @@ def matmul_gelu_backward(A: torch.Tensor, B: torch.Tensor, X: torch.Tensor,
     px, ldx = _gelu_in(X, m, n)
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
-    if out.shape != (m, n) or out.stride(1) != 1:
-        raise ValueError("out must be a row-major [m, n] tensor")
+    ldc = _rows_as(out, m, n, "out")
     rc = load().repops_matmul_gelu_backward(_ord(order), m, n, k, pa, lda, ta, pb, ldb, tb, px,
-                                            ldx, _dev(out, "out"), max(out.stride(0), n, 1),
+                                            ldx, _dev(out, "out"), ldc,
                                             _launch(launch), _stream(out))
     _check(rc, "repops_matmul_gelu_backward")
     return out
@@ -364,8 +369,7 @@ def matmul_grouped(products, order: Order | None = None) -> list:
             raise ValueError(f"inner dimensions differ: {k} vs {k2}")
         if out is None:
             out = torch.empty((m, n), dtype=torch.float32, device=A.device)
-        if out.shape != (m, n) or out.stride(1) != 1:
-            raise ValueError("out must be a row-major [m, n] tensor")
+        ldc = _rows_as(out, m, n, "out")
         pbias = None
         if bias is not None:
             if bias.shape != (n,) or not bias.is_contiguous():
@@ -373,7 +377,7 @@ def matmul_grouped(products, order: Order | None = None) -> list:
             pbias = _dev(bias, "bias")
         d.m, d.n, d.k = m, n, k
         d.A, d.lda, d.trans_a, d.B, d.ldb, d.trans_b = pa, lda, ta, pb, ldb, tb
-        d.bias, d.C, d.ldc = pbias, _dev(out, "out"), max(out.stride(0), n, 1)
+        d.bias, d.C, d.ldc = pbias, _dev(out, "out"), ldc
         if X is not None:
             d.gelu_in, d.ld_gelu_in = _gelu_in(X, m, n)
         outs.append(out)
@@ -414,31 +418,48 @@ def bmm(A: torch.Tensor, B: torch.Tensor, alpha: float = 1.0, order: Order | Non
     whose last two dimensions are row-major or transposed views."""
     if A.dim() != 4 or B.dim() != 4:
         raise ValueError("bmm takes 4-D tensors [batch0, batch1, rows, cols]")
-    b0, b1 = A.shape[:2]
+    b0, b1, m, k = A.shape
+    n = B.shape[3]
     if tuple(B.shape[:2]) != (b0, b1):
         raise ValueError("batch dimensions differ")
-    _, m, k, lda, ta = _mat(A[0, 0], "A")
-    _, k2, n, ldb, tb = _mat(B[0, 0], "B")
-    if k != k2:
-        raise ValueError(f"inner dimensions differ: {k} vs {k2}")
+    if B.shape[2] != k:
+        raise ValueError(f"inner dimensions differ: {k} vs {B.shape[2]}")
     if out is None:
         out = torch.empty((b0, b1, m, n), dtype=torch.float32, device=A.device)
-    if out.stride(3) != 1:
-        raise ValueError("out must be row-major in its last two dimensions")
+    if out.dim() != 4 or tuple(out.shape) != (b0, b1, m, n) or out.stride(3) != 1:
+        raise ValueError(f"out must be a [{b0}, {b1}, {m}, {n}] tensor, row-major in its last two "
+                         "dimensions")
+    if b0 == 0 or b1 == 0:
+        return out
+    _, _, _, lda, ta = _mat(A[0, 0], "A")
+    _, _, _, ldb, tb = _mat(B[0, 0], "B")
     rc = load().repops_bmm(_ord(order), b0, b1, m, n, k,
                            _dev(A, "A"), A.stride(0), A.stride(1), lda, ta,
                            _dev(B, "B"), B.stride(0), B.stride(1), ldb, tb, float(alpha),
                            _dev(out, "out"), out.stride(0), out.stride(1),
-                           max(out.stride(2), n, 1), _launch(launch), _stream(out))
+                           out.stride(2) if m > 1 else max(n, 1), _launch(launch), _stream(out))
     _check(rc, "repops_bmm")
     return out
 
 
 def _rows(X: torch.Tensor, name: str):
+    """(rows, cols, ld) of a 2-D tensor with unit column stride.  ld is the row
+    stride as it stands, so rows that overlap (a row stride below cols, as in an
+    expanded view) reach the library, which rejects them; a single row's stride
+    is never used and passes as cols."""
     sh, st = X.shape, X.stride()
     if len(sh) != 2 or st[1] != 1:
         raise ValueError(f"{name} must be a 2-D tensor with unit column stride")
-    return sh[0], sh[1], max(st[0], sh[1], 1)
+    return sh[0], sh[1], st[0] if sh[0] > 1 else max(sh[1], 1)
+
+
+def _rows_as(t: torch.Tensor, rows: int, cols: int, name: str) -> int:
+    """Row stride of a 2-D tensor with unit column stride that must be exactly
+    [rows, cols] (the library writes or reads that many rows through it)."""
+    r, c, ld = _rows(t, name)
+    if r != rows or c != cols:
+        raise ValueError(f"{name} must be [{rows}, {cols}] (got [{r}, {c}])")
+    return ld
 
 
 def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = None,
@@ -446,7 +467,7 @@ def softmax_rows(X: torch.Tensor, causal_period: int = 0, order: Order | None = 
     rows, cols, ldx = _rows(X, "X")
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
-    _, _, ldy = _rows(out, "out")
+    ldy = _rows_as(out, rows, cols, "out")
     rc = (_lib or load()).repops_softmax_rows(_ord(order), rows, cols, _dev(X, "X"), ldx,
                                               _dev(out, "out"), ldy, causal_period,
                                               _launch(launch), _stream(out))
@@ -462,7 +483,7 @@ def layernorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None,
     rows, cols, ldx = _rows(X, "X")
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
-    _, _, ldy = _rows(out, "out")
+    ldy = _rows_as(out, rows, cols, "out")
     rc = (_lib or load()).repops_layernorm_rows(
         _ord(order), rows, cols, _dev(X, "X"), ldx, _vec(gamma, "gamma", cols),
         _vec(beta, "beta", cols), float(eps), _dev(out, "out"), ldy,
@@ -515,7 +536,7 @@ def softmax_backward_rows(Y: torch.Tensor, dY: torch.Tensor, causal_period: int 
         raise ValueError("Y and dY shapes differ")
     if out is None:
         out = torch.empty_like(Y, memory_format=torch.contiguous_format)
-    _, _, lddx = _rows(out, "out")
+    lddx = _rows_as(out, rows, cols, "out")
     rc = load().repops_softmax_backward_rows(
         _ord(order), rows, cols, _dev(Y, "Y"), ldy,
         _dev(dY, "dY"), lddy, _dev(out, "out"), lddx, causal_period, _launch(launch), _stream(out))
@@ -559,7 +580,7 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
     lddx = cols
     if need_dx:
         dx = dx_out if dx_out is not None else torch.empty_like(X, memory_format=torch.contiguous_format)
-        _, _, lddx = _rows(dx, "dx_out")
+        lddx = _rows_as(dx, rows, cols, "dx_out")
     wptr, wbytes = None, 0
     if need_params:
         dgamma = dgamma_out if dgamma_out is not None else torch.empty(cols, dtype=torch.float32,
@@ -573,8 +594,7 @@ def layernorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, mean: torch.Tenso
             need = layernorm_backward_workspace(rows, cols, order)
             if need:
                 workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
-        if workspace is not None:
-            wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
+        wptr, wbytes = _workspace(workspace)
     ptr = lambda t, n: None if t is None else _dev(t, n)  # noqa: E731
     rc = load().repops_layernorm_backward_rows(
         _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
@@ -606,7 +626,7 @@ def layernorm_backward_rows_noalloc(X: torch.Tensor, dY: torch.Tensor, mean: tor
             raise ValueError(f"{name} must be a contiguous [{cols}] tensor")
     lddx = cols
     if dx_out is not None:
-        _, _, lddx = _rows(dx_out, "dx_out")
+        lddx = _rows_as(dx_out, rows, cols, "dx_out")
     ptr = lambda t, n: None if t is None else _dev(t, n)  # noqa: E731
     rc = load().repops_layernorm_backward_rows_noalloc(
         _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy,
@@ -627,9 +647,8 @@ def colsum_rows(X: torch.Tensor, order: Order | None = None, out: torch.Tensor |
         need = layernorm_backward_workspace(rows, cols, order)
         if need:
             workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
-    if workspace is not None:
-        wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
-    rc = load().repops_colsum_rows(_ord(order), rows, cols, X.data_ptr() if rows else None, ldx,
+    wptr, wbytes = _workspace(workspace)
+    rc = load().repops_colsum_rows(_ord(order), rows, cols, _dev(X, "X") if rows else None, ldx,
                                    _flat(out, cols, "out"), wptr, wbytes, None, _stream(out))
     _check(rc, "repops_colsum_rows")
     return out
@@ -729,12 +748,15 @@ def rope(X: torch.Tensor, heads: int, head_dim: int, inv_freq: torch.Tensor,
         raise ValueError("X is narrower than heads * head_dim")
     if out is None:
         out = torch.empty((rows, heads * head_dim), dtype=torch.float32, device=X.device)
-    if out.dim() != 2 or out.stride(1) != 1:
-        raise ValueError("out must be a 2-D tensor with unit column stride")
+    if (out.dim() != 2 or out.stride(1) != 1 or out.shape[0] != rows
+            or out.shape[1] < heads * head_dim):
+        raise ValueError(f"out must be a 2-D tensor with unit column stride, {rows} rows and at "
+                         f"least {heads * head_dim} columns")
     pinv = _flat(inv_freq, head_dim // 2, "inv_freq")
     rc = load().repops_rope(_ord(order), rows, heads, head_dim, _dev(X, "X"),
-                            max(X.stride(0), 1), pinv, position_period, position_offset,
-                            1 if inverse else 0, _dev(out, "out"), max(out.stride(0), 1),
+                            X.stride(0) if rows > 1 else X.shape[1], pinv, position_period,
+                            position_offset, 1 if inverse else 0, _dev(out, "out"),
+                            out.stride(0) if rows > 1 else out.shape[1],
                             _launch(launch), _stream(X))
     _check(rc, "repops_rope")
     return out
@@ -747,7 +769,7 @@ def rmsnorm_rows(X: torch.Tensor, gamma: torch.Tensor | None = None, eps: float 
     rows, cols, ldx = _rows(X, "X")
     if out is None:
         out = torch.empty_like(X, memory_format=torch.contiguous_format)
-    _, _, ldy = _rows(out, "out")
+    ldy = _rows_as(out, rows, cols, "out")
     pg = None if gamma is None else _flat(gamma, cols, "gamma")
     pr = None if rstd_out is None else _flat(rstd_out, rows, "rstd_out")
     rc = load().repops_rmsnorm_rows(_ord(order), rows, cols, _dev(X, "X"), ldx, pg, float(eps),
@@ -781,7 +803,7 @@ def rmsnorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, rstd: torch.Tensor,
     lddx = cols
     if need_dx:
         dx = dx_out if dx_out is not None else torch.empty_like(X, memory_format=torch.contiguous_format)
-        _, _, lddx = _rows(dx, "dx_out")
+        lddx = _rows_as(dx, rows, cols, "dx_out")
     wptr, wbytes = None, 0
     if need_dgamma:
         dgamma = dgamma_out if dgamma_out is not None else torch.empty(cols, dtype=torch.float32,
@@ -790,8 +812,7 @@ def rmsnorm_backward_rows(X: torch.Tensor, dY: torch.Tensor, rstd: torch.Tensor,
             need = rmsnorm_backward_workspace(rows, cols, order)
             if need:
                 workspace = torch.empty(need // 4, dtype=torch.float32, device=X.device)
-        if workspace is not None:
-            wptr, wbytes = _dev(workspace, "workspace"), workspace.numel() * 4
+        wptr, wbytes = _workspace(workspace)
     rc = load().repops_rmsnorm_backward_rows(
         _ord(order), rows, cols, _dev(X, "X"), ldx, _dev(dY, "dY"), lddy, prs, pg,
         None if dx is None else _dev(dx, "dX"), lddx,
@@ -852,11 +873,14 @@ def commit(t: torch.Tensor, chunk_bytes: int = 1024, digest: torch.Tensor | None
     nbytes = t.numel() * t.element_size()
     if digest is None:
         digest = torch.empty(32, dtype=torch.uint8, device=t.device)
+    if (not digest.is_cuda or not digest.is_contiguous()
+            or digest.numel() * digest.element_size() < 32):
+        raise ValueError("digest must be a contiguous device tensor of at least 32 bytes")
     if workspace is None:
         need = commit_workspace(nbytes, chunk_bytes)
         workspace = torch.empty(max(need // 4, 1), dtype=torch.int32, device=t.device)
+    wptr, wbytes = _workspace(workspace)
     rc = load().repops_commit(t.data_ptr() if nbytes else None, nbytes, chunk_bytes,
-                              digest.data_ptr(), workspace.data_ptr(),
-                              workspace.numel() * workspace.element_size(), None, _stream(t))
+                              digest.data_ptr(), wptr, wbytes, None, _stream(t))
     _check(rc, "repops_commit")
     return digest

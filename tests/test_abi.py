@@ -236,6 +236,18 @@ def test_bmm_rejections(rp):
     assert call(C=FAKE_A + 4 * 90) == rp.ERR_ALIAS
     assert call(ldb=3) == rp.ERR_STRIDE
     assert call(b1=0, A=None, B=None, C=None) == rp.OK
+    # no two output elements may share an address: batch strides 0 or shorter
+    # than a batch element's span are rejected...
+    assert call(sc1=0) == rp.ERR_STRIDE
+    assert call(sc1=15) == rp.ERR_STRIDE      # a 4 x 4 element with ldc 4 spans 16
+    assert call(sc0=40) == rp.ERR_STRIDE      # b1 = 3 elements of 16 span 48
+    assert call(sc0=-16, sc1=16) == rp.ERR_STRIDE
+    # ...while interleaved dense layouts pass that check and reach the alias
+    # check after it: heads within rows ([b0][m][b1][n]: sc0 48, sc1 4, ldc 12)
+    # and batch dimensions in either order
+    for sc0, sc1, ldc in ((48, 4, 12), (16, 32, 4), (4, 96, 12)):
+        assert call(sc0=sc0, sc1=sc1, ldc=ldc, C=FAKE_A + 4 * 8) == rp.ERR_ALIAS, (sc0, sc1, ldc)
+    assert call(sc0=48, sc1=3, ldc=12, C=FAKE_A + 4 * 8) == rp.ERR_STRIDE
 
 
 @no_gpu_only
@@ -433,6 +445,39 @@ def test_commit_rejections(rp):
     assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_W + 2, 1 << 20, None, None) == rp.ERR_STRIDE
     wave = ctypes.byref(rp.Launch(rp.LAUNCH_ROWS_WAVE, (4,)).c())
     assert c(FAKE_A, 4096, 1024, FAKE_C, FAKE_W, 1 << 20, wave, None) == rp.ERR_LAUNCH
+
+
+def test_binding_passes_row_strides_and_checks_output_shapes(rp):
+    # the binding hands the library a tensor's own row stride (rows that
+    # overlap, as in an expanded view, are then rejected there, not widened),
+    # and every output must have exactly the shape the call writes: both
+    # checks run before any pointer is taken, so host tensors show them here
+    import torch
+    X = torch.zeros(4, 8)
+    assert rp._rows(X, "X") == (4, 8, 8)
+    assert rp._rows(torch.zeros(8).expand(4, 8), "X") == (4, 8, 0)
+    assert rp._rows(torch.zeros(40)[:8].view(1, 8), "X") == (1, 8, 8)
+    assert rp._rows(torch.zeros(4, 12)[:, 2:10], "X") == (4, 8, 12)
+    with pytest.raises(ValueError, match="unit column stride"):
+        rp._rows(torch.zeros(8, 4).t(), "X")
+    assert rp._rows_as(torch.zeros(4, 12)[:, :8], 4, 8, "out") == 12
+    with pytest.raises(ValueError, match=r"must be \[4, 8\]"):
+        rp._rows_as(torch.zeros(3, 8), 4, 8, "out")
+    short, narrow = torch.zeros(3, 8), torch.zeros(4, 7)
+    for bad in (short, narrow):
+        for call in (lambda: rp.softmax_rows(X, out=bad),
+                     lambda: rp.layernorm_rows(X, out=bad),
+                     lambda: rp.rmsnorm_rows(X, out=bad),
+                     lambda: rp.softmax_backward_rows(X, X, out=bad)):
+            with pytest.raises(ValueError):
+                call()
+    with pytest.raises(ValueError, match="rows"):
+        rp.rope(X, 2, 4, torch.zeros(2), out=short)
+    with pytest.raises(ValueError, match="out must be"):
+        rp.bmm(torch.zeros(2, 3, 4, 5), torch.zeros(2, 3, 5, 6), out=torch.zeros(1, 3, 4, 6))
+    # a caller's workspace must be device memory the library may fill contiguously
+    with pytest.raises(ValueError, match="workspace"):
+        rp._workspace(torch.zeros(16))
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
