@@ -299,7 +299,8 @@ repops_status_t repops_softmax_rows(const repops_order_t *order, int64_t rows, i
  *   sqrt and the division are correctly rounded.  gamma / beta may be NULL:
  *   the operation is skipped (y = t, t + beta or t * gamma), which differs from
  *   passing ones / zeros in the sign of zero.  mean_out / rstd_out: NULL or
- *   [rows].  cols must be >= 1.  In-place as for softmax.
+ *   [rows]; neither may overlap X, Y, gamma, beta or the other
+ *   (REPOPS_ERR_ALIAS).  cols must be >= 1.  In-place as for softmax.
  */
 repops_status_t repops_layernorm_rows(const repops_order_t *order, int64_t rows, int64_t cols,
                                       const float *X, int64_t ldx, const float *gamma,

@@ -657,6 +657,17 @@ repops_status_t repops_layernorm_rows(const repops_order_t* order, int64_t rows,
   const Extent ye = extent_of(Y, 1, 0, 1, 0, rows, cols, ldy);
   if (gamma && overlaps(ye, extent_of(gamma, 1, 0, 1, 0, 1, cols, cols))) return REPOPS_ERR_ALIAS;
   if (beta && overlaps(ye, extent_of(beta, 1, 0, 1, 0, 1, cols, cols))) return REPOPS_ERR_ALIAS;
+  // the row statistics touch no input, not Y and not each other
+  const Extent xe = extent_of(X, 1, 0, 1, 0, rows, cols, ldx);
+  for (const float* stat : {static_cast<const float*>(mean_out), static_cast<const float*>(rstd_out)}) {
+    if (!stat) continue;
+    const Extent se = vec_extent(stat, rows);
+    if (overlaps(se, ye) || overlaps(se, xe) || (gamma && overlaps(se, vec_extent(gamma, cols))) ||
+        (beta && overlaps(se, vec_extent(beta, cols))))
+      return REPOPS_ERR_ALIAS;
+  }
+  if (mean_out && rstd_out && overlaps(vec_extent(mean_out, rows), vec_extent(rstd_out, rows)))
+    return REPOPS_ERR_ALIAS;
   RowArgs a{};
   a.rows = rows; a.cols = cols; a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy;
   a.W = static_cast<int>(order->row_width);

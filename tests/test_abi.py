@@ -284,6 +284,14 @@ def test_rows_and_elementwise_rejections(rp):
                                      None, None) == rp.ERR_SHAPE
     assert lib.repops_layernorm_rows(o, 4, 8, FAKE_A, 8, FAKE_C + 4, None, 1e-5, FAKE_C, 8, None,
                                      None, None, None) == rp.ERR_ALIAS
+    # the row statistics may touch no input, not Y and not each other (X and Y
+    # are 4 x 8 floats, gamma 8 floats, each statistic 4 floats)
+    for gamma, mean, rstd in ((None, FAKE_A + 8, None),        # inside X
+                              (None, None, FAKE_C + 64),       # inside Y
+                              (None, FAKE_B, FAKE_B + 8),      # mean and rstd overlap
+                              (FAKE_B, FAKE_B + 16, None)):    # inside gamma
+        assert lib.repops_layernorm_rows(o, 4, 8, FAKE_A, 8, gamma, None, 1e-5, FAKE_C, 8, mean,
+                                         rstd, None, None) == rp.ERR_ALIAS, (gamma, mean, rstd)
     assert lib.repops_gelu(o, -1, FAKE_A, FAKE_C, None, None) == rp.ERR_SHAPE
     assert lib.repops_gelu(o, 8, FAKE_A, FAKE_A + 4, None, None) == rp.ERR_ALIAS
     assert lib.repops_exp(o, 8, None, FAKE_C, None, None) == rp.ERR_NULL
