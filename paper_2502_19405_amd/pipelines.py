@@ -136,9 +136,11 @@ def mlp_train_step(state: MlpTrainState, X, dY, lr=1e-4, betas=(0.9, 0.999), eps
     b = bufs if bufs is not None else {}
 
     def buf(name, *shape):
-        if name not in b:
-            b[name] = torch.empty(shape, dtype=torch.float32, device=dev)
-        return b[name]
+        # reused across steps while the shape stays; replaced when it changes
+        t_ = b.get(name)
+        if t_ is None or tuple(t_.shape) != shape or t_.device != dev:
+            t_ = b[name] = torch.empty(shape, dtype=torch.float32, device=dev)
+        return t_
 
     # forward (the LayerNorm statistics are the backward's saved tensors)
     H1, G = repops.matmul_gelu(X, W1, b1, order=order, launch=gemm_launch, out=buf("H1", t, f),
