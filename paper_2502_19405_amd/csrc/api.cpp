@@ -128,9 +128,17 @@ repops_status_t run_gemm(const repops_order_t* order, GemmArgs& g, const repops_
     // order; the simple path for block lengths no tile divides.
     const int64_t outputs = g.m * g.n * g.batch0 * g.batch1;
     int mfma_pref = 0;                                  // 128 x 128 tiles, 8 waves, ring
-    if (outputs <= (int64_t(1) << 20)) mfma_pref = 5;   // small outputs: 64 x 64 tiles
-    else if (g.k <= 256) mfma_pref = 2;                 // short k: register-staged slices
-    else if (g.causal == 2) mfma_pref = 8;              // causal A: 64-row tiles
+    if (outputs <= (int64_t(1) << 20)) {
+      mfma_pref = 5;                                    // small outputs: 64 x 64 tiles
+    } else if (g.k <= 256) {
+      // short k: the persistent ring form where each compute unit takes at
+      // least four tiles in turn, else register-staged slices
+      int cus = 0;
+      const int64_t ring = repops::gemm_mfma_ring_tiles(g, 9, &cus);
+      mfma_pref = cus > 0 && ring >= 4 * static_cast<int64_t>(cus) ? 9 : 2;
+    } else if (g.causal == 2) {
+      mfma_pref = 8;                                    // causal A: 64-row tiles
+    }
     if (!mfma_ok(repops::gemm_mfma_config(mfma_pref))) mfma_pref = 0;
     const int tiled_pref = outputs >= (int64_t(1) << 22) ? 1 : 0;
     if (mfma_ok(repops::gemm_mfma_config(mfma_pref))) {

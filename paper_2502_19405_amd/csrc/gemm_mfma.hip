@@ -366,7 +366,7 @@ __device__ __forceinline__ void lds_barrier() {
 // the grouped kernel, which never does, leaves that path out (with both GELU
 // paths its four tile forms together spilled registers).
 template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB, bool DUAL,
-          bool GELU_OUT = true>
+          bool GELU_OUT = true, bool RING = false>
 struct StagedTile {
   static_assert(BK % 16 == 0, "k slices hold whole 16-step groups");
   static constexpr int NW = WM * WN;
@@ -533,9 +533,9 @@ struct StagedTile {
   // register set) is spread in small shares between this slice's matrix
   // steps, where it costs no matrix-unit time.
   template <bool OPEN, bool FAST, bool ADD = false>
-  __device__ static void slice(Smem& sm, const Src& src, int s, int nslices, int slot, int nslot,
-                               int lane, int wave, int wm0, int wn0, Pack (&pk)[2],
-                               v32f (&P)[IM][IN], v32f (&acc)[IM][IN],
+  __device__ static void slice(Smem& sm, const Src& src, const Src& nsrc, int nlim, int s,
+                               int nslices, int slot, int nslot, int lane, int wave, int wm0,
+                               int wn0, Pack (&pk)[2], v32f (&P)[IM][IN], v32f (&acc)[IM][IN],
                                const v32f (&done)[IM][IN]) {
     constexpr int QN = BK / 4;
     constexpr int STEPS = 4 * IM * IN;
@@ -552,7 +552,24 @@ struct StagedTile {
       } else if (FAST) {
         wait_vmcnt<(NS - 2) * PER>();
         lds_barrier();
-        issue_slice(sm, src, s + NS < nslices ? s + NS : nslices - 1, slot, wave);
+        if constexpr (RING) {
+          // Past this tile's last slice the freed slot takes slice
+          // s + NS - nslices (at most nlim) of the tile nsrc describes: the
+          // next tile's first slices, or this tile's again (loads never read
+          // as data).
+          const bool here = s + NS < nslices;
+          const int past = s + NS - nslices < nlim ? s + NS - nslices : nlim;
+          Src pick;
+#pragma unroll
+          for (int u = 0; u < AU; ++u) pick.a[u] = here ? src.a[u] : nsrc.a[u];
+#pragma unroll
+          for (int u = 0; u < BU; ++u) pick.b[u] = here ? src.b[u] : nsrc.b[u];
+          pick.astep = src.astep;
+          pick.bstep = src.bstep;
+          issue_slice(sm, pick, here ? s + NS : past, slot, wave);
+        } else {
+          issue_slice(sm, src, s + NS < nslices ? s + NS : nslices - 1, slot, wave);
+        }
         read_pack(sm.a[nslot], sm.b[nslot], lane, wm0, wn0, 0, pk[0]);
       } else if (s + 1 < nslices) {
         const int later = nslices - 2 - s;  // slices after s + 1, capped by the ring
@@ -587,18 +604,75 @@ struct StagedTile {
   // One turn of the ring (NS slices, one k block) of the fast path,
   // accumulating the block in X while the previous block's partials in Y join
   // acc during the first slice.
-  __device__ static void turn(Smem& sm, const Src& src, int s0, int nslices, int lane, int wave,
-                              int wm0, int wn0, Pack (&pk)[2], v32f (&X)[IM][IN],
-                              v32f (&acc)[IM][IN], const v32f (&Y)[IM][IN]) {
+  __device__ static void turn(Smem& sm, const Src& src, const Src& nsrc, int nlim, int s0,
+                              int nslices, int lane, int wave, int wm0, int wn0, Pack (&pk)[2],
+                              v32f (&X)[IM][IN], v32f (&acc)[IM][IN], const v32f (&Y)[IM][IN]) {
 #pragma unroll
     for (int t = 0; t < NS; ++t) {
       if (t == 0)
-        slice<true, true, true>(sm, src, s0, nslices, 0, 1 % NS, lane, wave, wm0, wn0, pk, X,
-                                acc, Y);
+        slice<true, true, true>(sm, src, nsrc, nlim, s0, nslices, 0, 1 % NS, lane, wave, wm0,
+                                wn0, pk, X, acc, Y);
       else
-        slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0, pk,
-                           X, acc, Y);
+        slice<false, true>(sm, src, nsrc, nlim, s0 + t, nslices, t, (t + 1) % NS, lane, wave,
+                           wm0, wn0, pk, X, acc, Y);
     }
+  }
+
+  // The fast path with the second partial set over one tile's nslices slices
+  // (a whole number of ring turns, one k block each): the ring holds slices
+  // 0 .. NS - 1 and pk[0] the first group of slice 0.  acc receives the tile's
+  // accumulators; past the last slice the ring is refilled from nsrc (see
+  // slice), and pk[0] then holds the first group of that tile's slice 0.
+  __device__ static void dual_fast(Smem& sm, const Src& src, const Src& nsrc, int nlim,
+                                   int nslices, int lane, int wave, int wm0, int wn0,
+                                   Pack (&pk)[2], v32f (&acc)[IM][IN]) {
+    // Q starts at +0, so the first block adds +0 to +0.
+    v32f P[IM][IN], Q[IM][IN];
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < IN; ++j) {
+        P[i][j] = v32f{};
+        Q[i][j] = v32f{};
+        acc[i][j] = v32f{};
+      }
+    int s0 = 0;
+    for (; s0 + 2 * NS <= nslices; s0 += 2 * NS) {
+      turn(sm, src, nsrc, nlim, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
+      turn(sm, src, nsrc, nlim, s0 + NS, nslices, lane, wave, wm0, wn0, pk, Q, acc, P);
+    }
+    if (s0 < nslices) {
+      turn(sm, src, nsrc, nlim, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
+    } else {
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + Q[i][j];
+    }
+  }
+
+  // Accumulator layout (lane l, register r): block r / 16 holds columns
+  // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
+  __device__ static void store_tile(const GemmArgs& g, int64_t b0, int64_t b1, int64_t m0,
+                                    int64_t n0, int lane, int wm0, int wn0,
+                                    const v32f (&acc)[IM][IN]) {
+    float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
+    float* G = (GELU_OUT && g.G) ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int j = 0; j < IN; ++j)
+#pragma unroll
+        for (int r = 0; r < 32; ++r) {
+          const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
+          const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
+          if (row < g.m && col < g.n) gemm_store(g, C, G, X, row, col, acc[i][j][r]);
+        }
   }
 
   __device__ static void run(const GemmArgs& g, Smem& sm, int64_t b0, int64_t b1, int64_t m0,
@@ -641,40 +715,18 @@ struct StagedTile {
       if constexpr (DUAL && FSPB == NS) {
         // The second partial set: one ring turn is one k block, alternating
         // between P and Q, and each block's partials join acc during the next
-        // block's first slice.  Q starts at +0, so the first block adds +0 to
-        // +0.
-        v32f Q[IM][IN];
-#pragma unroll
-        for (int i = 0; i < IM; ++i)
-#pragma unroll
-          for (int j = 0; j < IN; ++j) Q[i][j] = v32f{};
-        int s0 = 0;
-        for (; s0 + 2 * NS <= nslices; s0 += 2 * NS) {
-          turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
-          turn(sm, src, s0 + NS, nslices, lane, wave, wm0, wn0, pk, Q, acc, P);
-        }
-        if (s0 < nslices) {
-          turn(sm, src, s0, nslices, lane, wave, wm0, wn0, pk, P, acc, Q);
-#pragma unroll
-          for (int i = 0; i < IM; ++i)
-#pragma unroll
-            for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + P[i][j];
-        } else {
-#pragma unroll
-          for (int i = 0; i < IM; ++i)
-#pragma unroll
-            for (int j = 0; j < IN; ++j) acc[i][j] = acc[i][j] + Q[i][j];
-        }
+        // block's first slice.
+        dual_fast(sm, src, src, nslices - 1, nslices, lane, wave, wm0, wn0, pk, acc);
       } else {
         for (int s0 = 0; s0 < nslices; s0 += NS) {
 #pragma unroll
           for (int t = 0; t < NS; ++t) {
             if (t % FSPB == 0)
-              slice<true, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0, wn0,
-                                pk, P, acc, P);
+              slice<true, true>(sm, src, src, nslices - 1, s0 + t, nslices, t, (t + 1) % NS,
+                                lane, wave, wm0, wn0, pk, P, acc, P);
             else
-              slice<false, true>(sm, src, s0 + t, nslices, t, (t + 1) % NS, lane, wave, wm0,
-                                 wn0, pk, P, acc, P);
+              slice<false, true>(sm, src, src, nslices - 1, s0 + t, nslices, t, (t + 1) % NS,
+                                 lane, wave, wm0, wn0, pk, P, acc, P);
             if (t % FSPB == FSPB - 1) {
 #pragma unroll
               for (int i = 0; i < IM; ++i)
@@ -690,11 +742,11 @@ struct StagedTile {
       for (int s = 0; s < nslices; ++s) {
         const int nslot = slot + 1 == NS ? 0 : slot + 1;
         if (pos == 0)
-          slice<true, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P, acc,
-                             P);
+          slice<true, false>(sm, src, src, 0, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk,
+                             P, acc, P);
         else
-          slice<false, false>(sm, src, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk, P, acc,
-                              P);
+          slice<false, false>(sm, src, src, 0, s, nslices, slot, nslot, lane, wave, wm0, wn0, pk,
+                              P, acc, P);
         if (++pos == spb || s + 1 == nslices) {
           pos = 0;
 #pragma unroll
@@ -706,22 +758,74 @@ struct StagedTile {
       }
     }
     __syncthreads();
+    store_tile(g, b0, b1, m0, n0, lane, wm0, wn0, acc);
+  }
 
-    // Accumulator layout (lane l, register r): block r / 16 holds columns
-    // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
-    float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
-    float* G = (GELU_OUT && g.G) ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
-    const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+  // Launch index t's batch element and tile origin.
+  __device__ static void locate(const GemmArgs& g, int64_t t, int64_t ntiles, int64_t tiles_m,
+                                int64_t tiles_n, int64_t* b0, int64_t* b1, int64_t* m0,
+                                int64_t* n0) {
+    int64_t bz, tm, tn;
+    tile_of(g, BM, BN, t, ntiles, tiles_m, tiles_n, &bz, &tm, &tn);
+    *b1 = bz % g.batch1;
+    *b0 = bz / g.batch1;
+    *m0 = tm * BM;
+    *n0 = tn * BN;
+  }
+
+  __device__ static Src sources_of(const GemmArgs& g, int64_t b0, int64_t b1, int64_t m0,
+                                   int64_t n0, int wave, int lane) {
+    return sources(g, g.A + b0 * g.sa0 + b1 * g.sa1, g.B + b0 * g.sb0 + b1 * g.sb1, m0, n0, wave,
+                   lane);
+  }
+
+  // Launch indices blockIdx.x, + gridDim.x, ... in one workgroup, the ring
+  // running on from each tile into the next: the last ring turn of a tile
+  // loads the next tile's first NS slices into the slots it frees and its last
+  // slice publishes the next tile's first one, so the next tile starts on
+  // operands already in LDS while this tile's stores drain.  (The next tile's
+  // first waits then also cover those stores: vector-memory operations
+  // complete in issue order.)  Every tile takes the fast path with the second
+  // partial set and the same slice count: K and k_block make whole ring turns
+  // of one k block each, and no tile is skipped or cut short (the host checks).
+  __device__ static void run_ring(const GemmArgs& g, Smem& sm, int64_t tiles_m, int64_t tiles_n,
+                                  int64_t ntiles) {
+    static_assert(DUAL && RING, "the ring form runs the fast path with the second partial set");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm0 = (wave / WN) * TWM;
+    const int wn0 = (wave % WN) * TWN;
+    const int nslices = static_cast<int>(g.k / BK);
+    int64_t t = blockIdx.x;
+    int64_t b0, b1, m0, n0;
+    locate(g, t, ntiles, tiles_m, tiles_n, &b0, &b1, &m0, &n0);
+    Src src = sources_of(g, b0, b1, m0, n0, wave, lane);
+    // the first tile's prologue, as in run()
+    Pack pk[2];
 #pragma unroll
-    for (int i = 0; i < IM; ++i)
-#pragma unroll
-      for (int j = 0; j < IN; ++j)
-#pragma unroll
-        for (int r = 0; r < 32; ++r) {
-          const int64_t row = m0 + wm0 + i * 32 + 8 * ((r % 16) / 4) + 4 * (lane / 32) + (r % 4);
-          const int64_t col = n0 + wn0 + j * 64 + 32 * (r / 16) + (lane & 31);
-          if (row < g.m && col < g.n) gemm_store(g, C, G, X, row, col, acc[i][j][r]);
-        }
+    for (int s = 0; s < NS; ++s) issue_slice(sm, src, s, s, wave);
+    wait_landed<NS - 1>(NS - 1);
+    lds_barrier();
+    read_pack(sm.a[0], sm.b[0], lane, wm0, wn0, 0, pk[0]);
+    for (;;) {
+      const int64_t tn = t + gridDim.x;
+      const bool more = tn < ntiles;  // uniform over the workgroup
+      int64_t nb0 = b0, nb1 = b1, nm0 = m0, nn0 = n0;
+      if (more) locate(g, tn, ntiles, tiles_m, tiles_n, &nb0, &nb1, &nm0, &nn0);
+      const Src nsrc = more ? sources_of(g, nb0, nb1, nm0, nn0, wave, lane) : src;
+      v32f acc[IM][IN];
+      dual_fast(sm, src, nsrc, nslices - 1, nslices, lane, wave, wm0, wn0, pk, acc);
+      store_tile(g, b0, b1, m0, n0, lane, wm0, wn0, acc);
+      if (!more) break;
+      t = tn;
+      b0 = nb0;
+      b1 = nb1;
+      m0 = nm0;
+      n0 = nn0;
+      src = nsrc;
+    }
+    wait_vmcnt<0>();  // the re-loads past the last tile
   }
 };
 
@@ -738,6 +842,16 @@ __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
     if (tile_above_diagonal(g, tm * BM, BM, tn * BN)) continue;  // uniform over the workgroup
     T::run(g, sm, b0, b1, tm * BM, tn * BN);
   }
+}
+
+// The persistent form of a staged tile (StagedTile::run_ring); the host
+// launches about one workgroup per compute unit.
+template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool TA, bool TB>
+__global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_ring_kernel(
+    GemmArgs g, int64_t tiles_m, int64_t tiles_n, int64_t ntiles, int) {
+  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB, true, true, true>;
+  __shared__ typename T::Smem sm;
+  T::run_ring(g, sm, tiles_m, tiles_n, ntiles);
 }
 
 // Several products in one launch with table entry 0's tile: workgroup t
@@ -774,6 +888,9 @@ struct MfmaEntry {
   // staged variant of the same tile shape (nullptr: none); needs K % 16 == 0
   // and 16-byte aligned rows
   void (*staged[4])(GemmArgs, int64_t, int64_t, int64_t, int);
+  // persistent form of the staged tile with the ring running across tiles
+  // (nullptr: none); taken where every tile makes whole ring turns
+  void (*ring[4])(GemmArgs, int64_t, int64_t, int64_t, int);
 };
 
 // MINW: waves per SIMD the register allocation must leave room for.
@@ -784,6 +901,7 @@ struct MfmaEntry {
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, true>,                                  \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, false>,                                  \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>},                                  \
+   {nullptr, nullptr, nullptr, nullptr},                                                      \
    {nullptr, nullptr, nullptr, nullptr}}
 
 // MINW: waves per SIMD the register allocation must leave room for; FWM x FWN:
@@ -799,7 +917,26 @@ struct MfmaEntry {
    {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                      \
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                       \
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>},                       \
+   {nullptr, nullptr, nullptr, nullptr}}
+
+// A staged tile with its persistent ring form as well (one instruction tile
+// per wave: the second partial set).
+#define REPOPS_RING(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN)                                  \
+  {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW "/s" #NS "/ring", BM, BN, BK},            \
+   64 * WM * WN,                                                                              \
+   {gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, false>,                               \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, true>,                                \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, false>,                                \
+    gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, true>},                                \
+   {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                      \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                       \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>},                       \
+   {gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                        \
+    gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                         \
+    gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                         \
+    gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
 
 const MfmaEntry kMfma[] = {
     REPOPS_STAGED(128, 128, 16, 4, 2, 4, 2, 2, 4),  // 0: default for large outputs
@@ -814,6 +951,8 @@ const MfmaEntry kMfma[] = {
     // values): 64-row tiles end their contraction closer to their diagonal, and
     // three workgroups per CU overlap one tile's loads and stores with another's
     REPOPS_STAGED(64, 128, 16, 2, 2, 4, 3, 1, 4),
+    // 9: entry 0's tile, persistent, its ring running on into the next tile
+    REPOPS_RING(128, 128, 16, 4, 2, 4, 2, 2, 4),
 };
 constexpr int kMfmaCount = sizeof(kMfma) / sizeof(kMfma[0]);
 
@@ -832,6 +971,32 @@ bool gemm_mfma_staged_ok(const GemmArgs& g, int index) {
                       aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
   return e.staged[0] && vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
          g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) && (g.tb || g.n % 4 == 0);
+}
+
+// Tiles of a launch that the ring form of entry `index` can take, else 0: every
+// tile makes whole ring turns of one 64-deep k block each (16-deep slices,
+// four slots) over the same K, the staged kernel's layout rules hold, and no
+// tile is skipped or cut short.  *cus receives the device's compute units; the
+// launch takes the ring form when the tiles outnumber them.
+int64_t gemm_mfma_ring_tiles(const GemmArgs& g, int index, int* cus) {
+  const MfmaEntry& e = kMfma[index];
+  *cus = 0;
+  if (!e.ring[0] || e.cfg.bk != 16 || g.k <= 0 || g.k_block != 64 || g.k % 64 != 0 ||
+      !gemm_mfma_staged_ok(g, index))
+    return 0;
+  const int64_t tiles_m = (g.m + e.cfg.bm - 1) / e.cfg.bm;
+  const int64_t tiles_n = (g.n + e.cfg.bn - 1) / e.cfg.bn;
+  const bool tri = causal_triangle(g.causal, e.cfg.bm, e.cfg.bn, tiles_m, tiles_n);
+  if (g.causal != 0 && !tri) return 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      *cus <= 0) {
+    *cus = 0;
+    return 0;
+  }
+  const int64_t per_batch = tri ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
+  return per_batch * g.batch0 * g.batch1;
 }
 
 void gemm_mfma_tile(int index, int* bm, int* bn) {
@@ -866,8 +1031,14 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
   const bool staged_ok = vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
                          g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) &&
                          (g.tb || g.n % 4 == 0);
+  unsigned blocks = grid;
   if (e.staged[0] && staged_ok) kernel = e.staged[g.ta * 2 + g.tb];
-  hipLaunchKernelGGL(kernel, dim3(grid), dim3(e.threads), 0, s, g, tiles_m, tiles_n, ntiles,
+  int cus = 0;
+  if (gemm_mfma_ring_tiles(g, index, &cus) > cus) {
+    kernel = e.ring[g.ta * 2 + g.tb];
+    blocks = static_cast<unsigned>(cus);
+  }
+  hipLaunchKernelGGL(kernel, dim3(blocks), dim3(e.threads), 0, s, g, tiles_m, tiles_n, ntiles,
                      vec_ok);
   return hipGetLastError();
 }

@@ -45,6 +45,10 @@ struct GroupArgs {
   int count;
 };
 bool gemm_mfma_staged_ok(const GemmArgs& g, int index);
+// Tiles the persistent ring form of matrix-core entry `index` would take for
+// this product (0 when it cannot); *cus receives the device's compute units,
+// and the launch takes the ring form when the tiles outnumber them.
+int64_t gemm_mfma_ring_tiles(const GemmArgs& g, int index, int* cus);
 // Tile edge lengths of table entry `index` (for the grouped launch's tiles).
 void gemm_mfma_tile(int index, int* bm, int* bn);
 hipError_t launch_gemm_mfma_grouped(const GroupArgs& ga, hipStream_t s);
