@@ -365,8 +365,12 @@ __device__ __forceinline__ void lds_barrier() {
 // GELU_OUT: the epilogue can write the GELU of the output (repops_matmul_gelu);
 // the grouped kernel, which never does, leaves that path out (with both GELU
 // paths its four tile forms together spilled registers).
+// EPI: interior tiles take the specialised stores (store_plain); without it every
+// output goes through the checked loop -- the form kept for products with no
+// scale, bias or GELU array, whose kernels the added store code would otherwise
+// change (register assignment and the schedule of the matrix loop).
 template <int BM, int BN, int BK, int WM, int WN, int NS, bool TA, bool TB, bool DUAL,
-          bool GELU_OUT = true, bool RING = false>
+          bool GELU_OUT = true, bool RING = false, bool EPI = true>
 struct StagedTile {
   static_assert(BK % 16 == 0, "k slices hold whole 16-step groups");
   static constexpr int NW = WM * WN;
@@ -657,12 +661,73 @@ struct StagedTile {
 
   // Accumulator layout (lane l, register r): block r / 16 holds columns
   // 32*(r/16) + (l % 32), row 8*((r%16)/4) + 4*(l/32) + r%4.
+  // An interior tile's stores: the scale, the bias and the GELU arrays resolved
+  // once per tile (a lane's bias values read once), one address per output row
+  // and array, no bounds checks; the operations are gemm_store's, in its order.
+  template <bool ALPHA, bool BIAS, bool GOUT, bool XIN>
+  __device__ static void store_plain(const GemmArgs& g, float* C, float* G, const float* X,
+                                     int64_t m0, int64_t n0, int lane, int wm0, int wn0,
+                                     const v32f (&acc)[IM][IN]) {
+    const int64_t r0 = m0 + wm0 + 4 * (lane / 32);
+    const int64_t c0 = n0 + wn0 + (lane & 31);
+    float bj[IN][2];
+#pragma unroll
+    for (int j = 0; j < IN; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) bj[j][h] = BIAS ? g.bias[c0 + j * 64 + 32 * h] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < IM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int64_t row = r0 + i * 32 + 8 * q + r4;
+          float* pc = C + row * g.ldc + c0;
+          float* pg = GOUT ? G + row * g.ldg + c0 : nullptr;
+          const float* px = XIN ? X + row * g.ld_gelu_in + c0 : nullptr;
+#pragma unroll
+          for (int j = 0; j < IN; ++j)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int o = j * 64 + 32 * h;
+              float v = gemm_scale_bias<ALPHA, BIAS>(acc[i][j][16 * h + 4 * q + r4], g.alpha,
+                                                     bj[j][h]);
+              if constexpr (XIN) v = v * rep_gelu_grad(px[o]);
+              pc[o] = v;
+              if constexpr (GOUT) pg[o] = rep_gelu(v);
+            }
+        }
+  }
+
   __device__ static void store_tile(const GemmArgs& g, int64_t b0, int64_t b1, int64_t m0,
                                     int64_t n0, int lane, int wm0, int wn0,
                                     const v32f (&acc)[IM][IN]) {
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
     float* G = (GELU_OUT && g.G) ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
     const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
+    if (EPI && m0 + BM <= g.m && n0 + BN <= g.n) {  // interior tile (uniform over the workgroup)
+      if (!G && !X) {
+        if (g.has_alpha) {
+          if (g.bias) store_plain<true, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else store_plain<true, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+        } else {
+          if (g.bias) store_plain<false, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else store_plain<false, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+        }
+        return;
+      }
+      if constexpr (GELU_OUT) {  // the forward product's GELU (no scale)
+        if (G && !X && !g.has_alpha) {
+          if (g.bias) store_plain<false, true, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else store_plain<false, false, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          return;
+        }
+      }
+      if (X && !G && !g.has_alpha && !g.bias) {  // the GELU backward's product
+        store_plain<false, false, false, true>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+        return;
+      }
+    }
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -829,11 +894,12 @@ struct StagedTile {
   }
 };
 
-template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool TA, bool TB>
+template <int BM, int BN, int BK, int WM, int WN, int NS, int MINW, bool TA, bool TB, bool EPI>
 __global__ __launch_bounds__(64 * WM * WN, MINW) void gemm_mfma_staged_kernel(
     GemmArgs g, int64_t tiles_m, int64_t tiles_n, int64_t ntiles, int) {
   // one instruction tile per wave leaves registers for the second partial set
-  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB, (BM / WM / 32) * (BN / WN / 64) == 1>;
+  using T = StagedTile<BM, BN, BK, WM, WN, NS, TA, TB, (BM / WM / 32) * (BN / WN / 64) == 1,
+                       true, false, EPI>;
   __shared__ typename T::Smem sm;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     int64_t bz, tm, tn;
@@ -886,8 +952,9 @@ struct MfmaEntry {
   int threads;
   void (*kernel[4])(GemmArgs, int64_t, int64_t, int64_t, int);  // [ta * 2 + tb]
   // staged variant of the same tile shape (nullptr: none); needs K % 16 == 0
-  // and 16-byte aligned rows
-  void (*staged[4])(GemmArgs, int64_t, int64_t, int64_t, int);
+  // and 16-byte aligned rows.  [0]: for products with no scale, bias or GELU
+  // array; [1]: for the others (the specialised interior stores)
+  void (*staged[2][4])(GemmArgs, int64_t, int64_t, int64_t, int);
   // persistent form of the staged tile with the ring running across tiles
   // (nullptr: none); taken where every tile makes whole ring turns
   void (*ring[4])(GemmArgs, int64_t, int64_t, int64_t, int);
@@ -901,23 +968,32 @@ struct MfmaEntry {
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, false, true>,                                  \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, false>,                                  \
     gemm_mfma_kernel<BM, BN, BK, WM, WN, MINW, true, true>},                                  \
-   {nullptr, nullptr, nullptr, nullptr},                                                      \
+   {{nullptr, nullptr, nullptr, nullptr}, {nullptr, nullptr, nullptr, nullptr}},              \
    {nullptr, nullptr, nullptr, nullptr}}
+
+// The staged kernels of a tile: [0] with the plain epilogue where PLAIN_EPI is
+// false (the same kernels as [1] otherwise), [1] with the specialised stores.
+#define REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, PLAIN_EPI)                       \
+  {{gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false, PLAIN_EPI>,          \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true, PLAIN_EPI>,           \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false, PLAIN_EPI>,           \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true, PLAIN_EPI>},           \
+   {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false, true>,               \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true, true>,                \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false, true>,                \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true, true>}}
 
 // MINW: waves per SIMD the register allocation must leave room for; FWM x FWN:
 // the wave grid of the register-staged fallback of the same tile (as many
 // waves, each owning whole 64 x 32 instruction tiles).
-#define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN)                                \
+#define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN, PLAIN_EPI)                     \
   {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW "/s" #NS, BM, BN, BK},                    \
    64 * WM * WN,                                                                              \
    {gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, false>,                               \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, true>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, false>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, true>},                                \
-   {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                      \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                       \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>},                       \
+   REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, PLAIN_EPI),                            \
    {nullptr, nullptr, nullptr, nullptr}}
 
 // A staged tile with its persistent ring form as well (one instruction tile
@@ -929,28 +1005,25 @@ struct MfmaEntry {
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, true>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, false>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, true>},                                \
-   {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                      \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                       \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                       \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>},                       \
+   REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, false),                                \
    {gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false>,                        \
     gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true>,                         \
     gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false>,                         \
     gemm_mfma_ring_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true>}}
 
 const MfmaEntry kMfma[] = {
-    REPOPS_STAGED(128, 128, 16, 4, 2, 4, 2, 2, 4),  // 0: default for large outputs
-    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2),  // 1: one wave per SIMD
-    REPOPS_MFMA(128, 128, 16, 2, 2, 2),             // 2: short k (attention scores)
-    REPOPS_STAGED(128, 128, 32, 2, 2, 4, 1, 2, 2),  // 3
-    REPOPS_STAGED(256, 128, 16, 4, 2, 3, 1, 4, 2),  // 4
-    REPOPS_MFMA(64, 64, 32, 1, 2, 2),               // 5: small outputs
-    REPOPS_STAGED(128, 128, 32, 4, 2, 4, 2, 2, 4),  // 6
-    REPOPS_STAGED(256, 128, 16, 4, 2, 4, 2, 4, 2),  // 7
+    REPOPS_STAGED(128, 128, 16, 4, 2, 4, 2, 2, 4, false),  // 0: default for large outputs
+    REPOPS_STAGED(128, 128, 16, 2, 2, 4, 2, 2, 2, true),   // 1: one wave per SIMD
+    REPOPS_MFMA(128, 128, 16, 2, 2, 2),                    // 2: short k, few tiles
+    REPOPS_STAGED(128, 128, 32, 2, 2, 4, 1, 2, 2, true),   // 3
+    REPOPS_STAGED(256, 128, 16, 4, 2, 3, 1, 4, 2, true),   // 4
+    REPOPS_MFMA(64, 64, 32, 1, 2, 2),                      // 5: small outputs
+    REPOPS_STAGED(128, 128, 32, 4, 2, 4, 2, 2, 4, true),   // 6
+    REPOPS_STAGED(256, 128, 16, 4, 2, 4, 2, 4, 2, true),   // 7
     // 8: products whose A is zero above its diagonal (causal probabilities x
     // values): 64-row tiles end their contraction closer to their diagonal, and
     // three workgroups per CU overlap one tile's loads and stores with another's
-    REPOPS_STAGED(64, 128, 16, 2, 2, 4, 3, 1, 4),
+    REPOPS_STAGED(64, 128, 16, 2, 2, 4, 3, 1, 4, true),
     // 9: entry 0's tile, persistent, its ring running on into the next tile
     REPOPS_RING(128, 128, 16, 4, 2, 4, 2, 2, 4),
 };
@@ -969,7 +1042,7 @@ bool gemm_mfma_staged_ok(const GemmArgs& g, int index) {
   const MfmaEntry& e = kMfma[index];
   const bool vec_ok = aligned16(g.A) && g.lda % 4 == 0 && g.sa0 % 4 == 0 && g.sa1 % 4 == 0 &&
                       aligned16(g.B) && g.ldb % 4 == 0 && g.sb0 % 4 == 0 && g.sb1 % 4 == 0;
-  return e.staged[0] && vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
+  return e.staged[1][0] && vec_ok && g.k % e.cfg.bk == 0 && g.k / e.cfg.bk <= INT32_MAX &&
          g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) && (g.tb || g.n % 4 == 0);
 }
 
@@ -1032,7 +1105,9 @@ hipError_t launch_gemm_mfma(const GemmArgs& g, int index, hipStream_t s) {
                          g.k_block / e.cfg.bk <= INT32_MAX && (!g.ta || g.m % 4 == 0) &&
                          (g.tb || g.n % 4 == 0);
   unsigned blocks = grid;
-  if (e.staged[0] && staged_ok) kernel = e.staged[g.ta * 2 + g.tb];
+  // the specialised stores where the product has a scale, a bias or a GELU array
+  const int epi = (g.has_alpha || g.bias || g.G || g.gelu_in) ? 1 : 0;
+  if (e.staged[1][0] && staged_ok) kernel = e.staged[epi][g.ta * 2 + g.tb];
   int cus = 0;
   if (gemm_mfma_ring_tiles(g, index, &cus) > cus) {
     kernel = e.ring[g.ta * 2 + g.tb];

@@ -19,6 +19,16 @@
 
 namespace repops {
 
+// The epilogue's arithmetic with the scale and the bias value at hand (the
+// same rounded operations, in the same order, as gemm_epilogue).
+template <bool ALPHA, bool BIAS>
+__device__ __forceinline__ float gemm_scale_bias(float acc, float alpha, float bias_j) {
+  float v = acc;
+  if constexpr (ALPHA) v = v * alpha;
+  if constexpr (BIAS) v = v + bias_j;
+  return v;
+}
+
 __device__ __forceinline__ float gemm_epilogue(const GemmArgs& g, float acc, int64_t j) {
   float v = acc;
   if (g.has_alpha) v = v * g.alpha;
