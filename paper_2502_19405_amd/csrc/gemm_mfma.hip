@@ -705,21 +705,28 @@ struct StagedTile {
     float* C = g.C + b0 * g.sc0 + b1 * g.sc1;
     float* G = (GELU_OUT && g.G) ? g.G + b0 * g.sc0 + b1 * g.sc1 : nullptr;
     const float* X = g.gelu_in ? g.gelu_in + b0 * g.sc0 + b1 * g.sc1 : nullptr;
-    if (EPI && m0 + BM <= g.m && n0 + BN <= g.n) {  // interior tile (uniform over the workgroup)
+    // interior tile (uniform over the workgroup)
+    if (EPI && m0 + BM <= g.m && n0 + BN <= g.n) {
       if (!G && !X) {
         if (g.has_alpha) {
-          if (g.bias) store_plain<true, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
-          else store_plain<true, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          if (g.bias)
+            store_plain<true, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else
+            store_plain<true, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
         } else {
-          if (g.bias) store_plain<false, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
-          else store_plain<false, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          if (g.bias)
+            store_plain<false, true, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else
+            store_plain<false, false, false, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
         }
         return;
       }
       if constexpr (GELU_OUT) {  // the forward product's GELU (no scale)
         if (G && !X && !g.has_alpha) {
-          if (g.bias) store_plain<false, true, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
-          else store_plain<false, false, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          if (g.bias)
+            store_plain<false, true, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
+          else
+            store_plain<false, false, true, false>(g, C, G, X, m0, n0, lane, wm0, wn0, acc);
           return;
         }
       }
@@ -971,13 +978,14 @@ struct MfmaEntry {
    {{nullptr, nullptr, nullptr, nullptr}, {nullptr, nullptr, nullptr, nullptr}},              \
    {nullptr, nullptr, nullptr, nullptr}}
 
-// The staged kernels of a tile: [0] with the plain epilogue where PLAIN_EPI is
-// false (the same kernels as [1] otherwise), [1] with the specialised stores.
-#define REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, PLAIN_EPI)                       \
-  {{gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false, PLAIN_EPI>,          \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true, PLAIN_EPI>,           \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false, PLAIN_EPI>,           \
-    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true, PLAIN_EPI>},           \
+// The staged kernels of a tile: [1] with the specialised interior stores; [0]
+// with EPI = EPI0 -- false keeps a form whose every output takes the checked
+// loop, true makes [0] the same kernels as [1].
+#define REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, EPI0)                            \
+  {{gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false, EPI0>,               \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true, EPI0>,                \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false, EPI0>,                \
+    gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, true, EPI0>},                \
    {gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, false, true>,               \
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, false, true, true>,                \
     gemm_mfma_staged_kernel<BM, BN, BK, WM, WN, NS, MINW, true, false, true>,                \
@@ -986,14 +994,14 @@ struct MfmaEntry {
 // MINW: waves per SIMD the register allocation must leave room for; FWM x FWN:
 // the wave grid of the register-staged fallback of the same tile (as many
 // waves, each owning whole 64 x 32 instruction tiles).
-#define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN, PLAIN_EPI)                     \
+#define REPOPS_STAGED(BM, BN, BK, WM, WN, NS, MINW, FWM, FWN, EPI0)                          \
   {{#BM "x" #BN "x" #BK "/w" #WM "x" #WN "/o" #MINW "/s" #NS, BM, BN, BK},                    \
    64 * WM * WN,                                                                              \
    {gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, false>,                               \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, false, true>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, false>,                                \
     gemm_mfma_kernel<BM, BN, BK, FWM, FWN, MINW, true, true>},                                \
-   REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, PLAIN_EPI),                            \
+   REPOPS_STAGED_KERNELS(BM, BN, BK, WM, WN, NS, MINW, EPI0),                                 \
    {nullptr, nullptr, nullptr, nullptr}}
 
 // A staged tile with its persistent ring form as well (one instruction tile
