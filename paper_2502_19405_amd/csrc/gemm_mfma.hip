@@ -675,6 +675,25 @@ struct StagedTile {
     for (int j = 0; j < IN; ++j)
 #pragma unroll
       for (int h = 0; h < 2; ++h) bj[j][h] = BIAS ? g.bias[c0 + j * 64 + 32 * h] : 0.0f;
+    // The GELU inputs of all the lane's outputs are loaded before any store:
+    // the compiler cannot see that X and C do not overlap (the host rejects
+    // overlap), so loads written after earlier rows' stores would stay after
+    // them, and each row would wait out a memory round trip.
+    float xv[XIN ? IM : 1][4][4][IN][2];
+    if constexpr (XIN) {
+#pragma unroll
+      for (int i = 0; i < IM; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const float* px = X + (r0 + i * 32 + 8 * q + r4) * g.ld_gelu_in + c0;
+#pragma unroll
+            for (int j = 0; j < IN; ++j)
+#pragma unroll
+              for (int h = 0; h < 2; ++h) xv[i][q][r4][j][h] = px[j * 64 + 32 * h];
+          }
+    }
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -684,7 +703,6 @@ struct StagedTile {
           const int64_t row = r0 + i * 32 + 8 * q + r4;
           float* pc = C + row * g.ldc + c0;
           float* pg = GOUT ? G + row * g.ldg + c0 : nullptr;
-          const float* px = XIN ? X + row * g.ld_gelu_in + c0 : nullptr;
 #pragma unroll
           for (int j = 0; j < IN; ++j)
 #pragma unroll
@@ -692,7 +710,7 @@ struct StagedTile {
               const int o = j * 64 + 32 * h;
               float v = gemm_scale_bias<ALPHA, BIAS>(acc[i][j][16 * h + 4 * q + r4], g.alpha,
                                                      bj[j][h]);
-              if constexpr (XIN) v = v * rep_gelu_grad(px[o]);
+              if constexpr (XIN) v = v * rep_gelu_grad(xv[i][q][r4][j][h]);
               pc[o] = v;
               if constexpr (GOUT) pg[o] = rep_gelu(v);
             }
