@@ -711,8 +711,13 @@ struct StagedTile {
               float v = gemm_scale_bias<ALPHA, BIAS>(acc[i][j][16 * h + 4 * q + r4], g.alpha,
                                                      bj[j][h]);
               if constexpr (XIN) v = v * rep_gelu_grad(xv[i][q][r4][j][h]);
-              pc[o] = v;
-              if constexpr (GOUT) pg[o] = rep_gelu(v);
+              if constexpr (RING) {  // streamed: see run_ring
+                __builtin_nontemporal_store(v, pc + o);
+                if constexpr (GOUT) __builtin_nontemporal_store(rep_gelu(v), pg + o);
+              } else {
+                pc[o] = v;
+                if constexpr (GOUT) pg[o] = rep_gelu(v);
+              }
             }
         }
   }
@@ -875,7 +880,10 @@ struct StagedTile {
   // slice publishes the next tile's first one, so the next tile starts on
   // operands already in LDS while this tile's stores drain.  (The next tile's
   // first waits then also cover those stores: vector-memory operations
-  // complete in issue order.)  Every tile takes the fast path with the second
+  // complete in issue order.)  An interior tile's stores are non-temporal:
+  // with short contractions (the attention scores) a round of tiles writes
+  // about as much as it reads, and cached output lines would push out of L2
+  // the operand panels that the neighbouring tiles are reading.  Every tile takes the fast path with the second
   // partial set and the same slice count: K and k_block make whole ring turns
   // of one k block each, and no tile is skipped or cut short (the host checks).
   __device__ static void run_ring(const GemmArgs& g, Smem& sm, int64_t tiles_m, int64_t tiles_n,
