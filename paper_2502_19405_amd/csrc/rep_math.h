@@ -184,21 +184,21 @@ __device__ __forceinline__ float rep_exp_neg_sq(float x, float c) {
   return rep_exp(a) * rep_exp(b);
 }
 
-// exp(z^2) erfc(z) for z >= 0.5.  Both intervals run one degree-12 Horner
-// chain: the second interval's coefficients are preceded by four zeros, which
-// keeps the chain at +0 until its own leading coefficient, so the result is
-// that of its degree-8 chain bit for bit.
+// exp(z^2) erfc(z) for z >= 0.5: each interval's Horner chain from its
+// leading coefficient.  Every lane evaluates both (straight-line code, the
+// coefficients as instruction literals) and keeps the one for its interval.
 __device__ __forceinline__ float rep_erfc_scaled(float z) {
   const bool lo = z < 2.5f;
   const float t = 1.0f / (1.0f + z);
-  const float s = lo ? z - 1.5f : (t - 0.1875f) * 9.5f;
-  float p = lo ? kErfcA[12] : 0.0f;
+  const float sa = z - 1.5f;
+  const float sb = (t - 0.1875f) * 9.5f;
+  float pa = kErfcA[12];
 #pragma unroll
-  for (int j = 11; j >= 0; --j) {
-    const float c = lo ? kErfcA[j] : (j <= 8 ? kErfcB[j] : 0.0f);
-    p = __builtin_fmaf(p, s, c);
-  }
-  return p;
+  for (int j = 11; j >= 0; --j) pa = __builtin_fmaf(pa, sa, kErfcA[j]);
+  float pb = kErfcB[8];
+#pragma unroll
+  for (int j = 7; j >= 0; --j) pb = __builtin_fmaf(pb, sb, kErfcB[j]);
+  return lo ? pa : pb;
 }
 
 __device__ __forceinline__ float rep_erf(float x) {
