@@ -127,3 +127,54 @@ def test_ring_equals_entry0_on_the_feed_forward_shapes(rp):
         r = rp.matmul(a, b, launch=ring_launch(rp))
         e = rp.matmul(a, b, launch=rp.Launch(rp.LAUNCH_GEMM_MFMA, (0,)))
         assert torch.equal(r.view(torch.int32), e.view(torch.int32)), name
+
+
+def test_ring_under_graph_replay(rp):
+    # The dense and lower-triangle score products of the bmm test above in the
+    # ring form, captured in one HIP graph: every replay (with eager work and a
+    # synchronisation between replays) gives the eager bits, and those are
+    # the oracle's.
+    import torch
+    b0, b1, s, k = 4, 8, 512, 128
+    g = inputs.rng(9500)
+    Q = inputs.normal(g, (b0, b1, s, k))
+    K = inputs.normal(g, (b0, b1, s, k))
+    alpha = float(np.float32(1.0 / np.sqrt(k)))
+    want = oracle.bmm(Q, K, alpha=alpha, trans_b=True)
+    dQ, dK = dev(Q), dev(K)
+    dense = torch.empty((b0, b1, s, s), device="cuda:0")
+    tri = torch.empty((b0, b1, s, s), device="cuda:0")
+
+    def calls():
+        for out, causal in ((dense, 0), (tri, rp.CAUSAL_OUTPUT)):
+            rp.bmm_raw(b0, b1, s, s, k, dQ, b1 * s * k, s * k, k, 0, dK, b1 * s * k, s * k, k, 1,
+                       alpha, out, b1 * s * s, s * s, s, launch=ring_launch(rp), causal=causal)
+
+    lower = torch.tril(torch.ones((s, s), dtype=torch.bool, device="cuda:0"))
+    announce("ring graph", "eager")
+    calls()
+    torch.cuda.synchronize()
+    eager_dense = host(dense).copy()
+    eager_tri = host(torch.where(lower, tri, torch.zeros_like(tri))).copy()
+    assert_bits_equal(eager_dense, want, "ring eager dense scores")
+    assert_bits_equal(eager_tri, np.where(np.tril(np.ones((s, s), bool)), want, np.float32(0)),
+                      "ring eager lower-triangle scores")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        calls()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        calls()
+    for rep in range(3):
+        announce("ring graph", "replay", rep)
+        dense.fill_(float("nan"))
+        tri.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert_bits_equal(host(dense), eager_dense, f"ring graph dense replay {rep}")
+        got_tri = host(torch.where(lower, tri, torch.zeros_like(tri)))
+        assert_bits_equal(got_tri, eager_tri, f"ring graph lower-triangle replay {rep}")
