@@ -7,8 +7,9 @@ compute units, so these shapes have a few hundred tiles: each workgroup then
 takes several tiles in turn, and the last ring turn of each tile loads the next
 tile's first slices.  Covered: an odd and an even number of ring turns per
 tile, ragged row and column edges, every transposition, bias, the GELU and
-GELU-backward epilogues, batched products, and the lower-triangle score
-product of causal attention.  Shapes the ring form declines (K not a multiple
+GELU-backward epilogues, batched products, the lower-triangle score product
+of causal attention, and replays of both score products captured in a HIP
+graph.  Shapes the ring form declines (K not a multiple
 of 64, other block lengths, few tiles) run entry 0's kernels and are covered by
 the other GEMM tests, which run every table entry.
 """
