@@ -883,9 +883,10 @@ struct StagedTile {
   // complete in issue order.)  An interior tile's stores are non-temporal:
   // with short contractions (the attention scores) a round of tiles writes
   // about as much as it reads, and cached output lines would push out of L2
-  // the operand panels that the neighbouring tiles are reading.  Every tile takes the fast path with the second
-  // partial set and the same slice count: K and k_block make whole ring turns
-  // of one k block each, and no tile is skipped or cut short (the host checks).
+  // the operand panels that the neighbouring tiles are reading.  Every tile
+  // takes the fast path with the second partial set and the same slice count:
+  // K and k_block make whole ring turns of one k block each, and no tile is
+  // skipped or cut short (the host checks).
   __device__ static void run_ring(const GemmArgs& g, Smem& sm, int64_t tiles_m, int64_t tiles_n,
                                   int64_t ntiles) {
     static_assert(DUAL && RING, "the ring form runs the fast path with the second partial set");
